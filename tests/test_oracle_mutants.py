@@ -1,0 +1,106 @@
+"""The pins must catch plausible mistakes in the oracle.
+
+Each case plants one mistake in a private copy of oracle.c (dropped bias, sign
+error, transposed weight operand, missing ReLU or clamp, off-by-one in a loop,
+fp32 accumulation, wrong bias index), builds it on the CPU, and checks that the
+battery of independent pins rejects it.  The committed oracle must pass the
+same battery.
+"""
+
+import json
+import math
+import os
+import shutil
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import brute
+from workloads import Layer, dense_to_csr, integer_shadow, make_config, tiny_random
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+_ACC_BLOCK = """        for (int64_t t = 0; t < cur_len; ++t) {
+            const int32_t i = cur_col[t];
+            const double y = (double)cur_val[t];
+            for (int64_t e = W->row_ptr[i]; e < W->row_ptr[i + 1]; ++e)
+                acc[W->col[e]] += y * (double)W->val[e];
+        }"""
+
+_TRANSPOSED = """        for (int64_t t = 0; t < cur_len; ++t) {
+            const int32_t i = cur_col[t];
+            const double y = (double)cur_val[t];
+            for (int64_t j2 = 0; j2 < n; ++j2)
+                for (int64_t e = W->row_ptr[j2]; e < W->row_ptr[j2 + 1]; ++e)
+                    if (W->col[e] == i) acc[j2] += y * (double)W->val[e];
+        }"""
+
+MUTANTS = {
+    "drop_bias": ("double z = acc[j] + (double)W->bias[j];", "double z = acc[j];"),
+    "sign": ("acc[W->col[e]] += y * (double)W->val[e];", "acc[W->col[e]] -= y * (double)W->val[e];"),
+    "transposed_W": (_ACC_BLOCK, _TRANSPOSED),
+    "no_relu": ("if (z < 0.0) z = 0.0;", ""),
+    "no_clamp": ("if (z > job->ymax) z = job->ymax;", ""),
+    "skip_last_weight": ("e < W->row_ptr[i + 1]; ++e)\n                acc",
+                         "e + 1 < W->row_ptr[i + 1]; ++e)\n                acc"),
+    "skip_first_input": ("for (int64_t t = 0; t < cur_len; ++t) {\n            const int32_t i",
+                         "for (int64_t t = 1; t < cur_len; ++t) {\n            const int32_t i"),
+    "fp32_accumulate": ("acc[W->col[e]] += y * (double)W->val[e];",
+                        "acc[W->col[e]] = (float)(acc[W->col[e]] + (float)(y * (double)W->val[e]));"),
+    "bias_index": ("(double)W->bias[j];\n            if (z < 0.0)", "(double)W->bias[0];\n            if (z < 0.0)"),
+    "keep_zero": ("if (f != 0.0f) {", "if (f != 0.0f || j == 0) {"),
+}
+
+
+def battery(lib):
+    """Independent pins; returns the names of those that fail."""
+    failed = []
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    W = np.array(g["W"], np.float32)
+    rp, c, v = dense_to_csr(W)
+    lay = [Layer(rp, c, v, np.array(g["b"], np.float32))] * 2
+    y0 = dense_to_csr(np.array(g["Y0"], np.float32))
+    try:
+        out = oracle.forward(3, lay, math.inf, y0, lib=lib)
+        if not np.array_equal(oracle.csr_to_dense(out, 3), np.array(g["Y2"], np.float32)):
+            failed.append("hand")
+        out = oracle.forward(3, lay, 8.0, y0, lib=lib)
+        if not np.array_equal(oracle.csr_to_dense(out, 3), np.array(g["ymax8_Y2"], np.float32)):
+            failed.append("hand_clamp")
+        for seed in (1, 2):
+            p = tiny_random(seed, 17, 3, 4, w_density=0.4, y_density=0.8)
+            got = oracle.forward(17, p.layers, math.inf, p.y0_csr, lib=lib)
+            if not np.all(got[2] != 0):
+                failed.append("no_stored_zeros")
+            want = brute.dense_forward(oracle.csr_to_dense(p.y0_csr, 17), [l.to_dense(17) for l in p.layers],
+                                       [l.bias for l in p.layers])
+            if oracle.csr_to_dense(got, 17).tobytes() != want.tobytes():
+                failed.append(f"brute{seed}")
+        q = integer_shadow(make_config(3, n=256, L=2, batch=6))
+        Yi = oracle.csr_to_dense(q.y0_csr, 256).astype(np.int64)
+        for l in q.layers:
+            Yi = np.clip(Yi @ l.to_dense(256).astype(np.int64) + l.bias.astype(np.int64), 0, 1000)
+        got = oracle.forward(256, q.layers, q.ymax, q.y0_csr, lib=lib)
+        if not np.array_equal(oracle.csr_to_dense(got, 256), Yi.astype(np.float32)):
+            failed.append("integer_shadow")
+    except ValueError:
+        failed.append("error")
+    return failed
+
+
+def test_committed_oracle_passes_battery():
+    assert battery(oracle.load()) == []
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = open(os.path.join(os.path.dirname(oracle.__file__), "oracle.c")).read()
+    old, new = MUTANTS[name]
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    path = tmp_path / "mutant.c"
+    path.write_text(src.replace(old, new))
+    lib = oracle.load(oracle.build(str(tmp_path / "libmutant.so"), str(path)))
+    assert battery(lib), f"mutant {name} passed every pin"

@@ -1,0 +1,276 @@
+"""Pins for the CPU oracle: hand-worked examples, brute force, closed forms and invariants.
+
+None of these re-types the oracle's formula: each compares it with something
+the mathematics fixes independently (a worked example, a dense brute-force
+loop, a library matmul in an exact or linear regime, a structural invariant).
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import brute
+from workloads import Layer, dense_to_csr, integer_shadow, make_config, tiny_random
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _layers_from_dense(Ws, bs):
+    out = []
+    for W, b in zip(Ws, bs):
+        W = np.asarray(W, dtype=np.float32)
+        rp, c, v = dense_to_csr(W)
+        out.append(Layer(rp, c, v, np.asarray(b, dtype=np.float32)))
+    return out
+
+
+def _run(n, layers, ymax, Y0, **kw):
+    return oracle.csr_to_dense(oracle.forward(n, layers, ymax, dense_to_csr(np.asarray(Y0, np.float32)), **kw), n)
+
+
+# --------------------------------------------------------------------------- worked examples
+
+
+def test_hand_example_two_layers():
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    n = g["n"]
+    layers = _layers_from_dense([g["W"]] * 2, [g["b"]] * 2)
+    y1 = _run(n, layers[:1], math.inf, g["Y0"])
+    assert np.array_equal(y1, np.array(g["Y1"], np.float32))
+    y2 = _run(n, layers, math.inf, g["Y0"])
+    assert np.array_equal(y2, np.array(g["Y2"], np.float32))
+
+
+def test_hand_example_csr_and_zero_pruning():
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    layers = _layers_from_dense([g["W"]], [g["b"]])
+    rp, c, v = oracle.forward(g["n"], layers, math.inf, dense_to_csr(np.array(g["Y0"], np.float32)))
+    assert rp.tolist() == g["Y1_csr"]["row_ptr"]
+    assert c.tolist() == g["Y1_csr"]["col"]
+    assert v.tolist() == g["Y1_csr"]["val"]
+
+
+def test_hand_example_clamp():
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    layers = _layers_from_dense([g["W"]] * 2, [g["b"]] * 2)
+    assert np.array_equal(_run(3, layers[:1], 8.0, g["Y0"]), np.array(g["ymax8_Y1"], np.float32))
+    assert np.array_equal(_run(3, layers, 8.0, g["Y0"]), np.array(g["ymax8_Y2"], np.float32))
+
+
+def test_hand_example_intermediates_by_brute_force():
+    """The companion loops reproduce the hand-worked intermediate products too."""
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    z = brute.mxm(g["Y0"], g["W"], brute.S1)
+    assert z == [[float(x) for x in r] for r in g["Y0W"]]
+    zb = [[a + b for a, b in zip(r, g["b"])] for r in z]
+    assert zb == [[float(x) for x in r] for r in g["Y0W_plus_b"]]
+
+
+def test_maxplus_example():
+    g = json.load(open(os.path.join(GOLDEN, "maxplus_example.json")))
+    f = lambda M: [[-math.inf if v is None else float(v) for v in r] for r in M]
+    assert brute.mxm(f(g["A"]), f(g["B"]), brute.S2) == f(g["C"])
+
+
+def test_semiring_zero_is_identity_and_annihilator():
+    """Sec. II.E: a (+) 0 = a and a (x) 0 = 0 for S1 (0) and S2 (-inf)."""
+    for sr in (brute.S1, brute.S2):
+        for a in (-3.5, 0.0, 2.25, 7.0):
+            assert sr.add(a, sr.zero) == a
+            assert sr.mul(a, sr.zero) == sr.zero
+            assert sr.mul(a, sr.one) == a
+
+
+# --------------------------------------------------------------------------- brute force
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_oracle_equals_dense_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 24))
+    L = int(rng.integers(1, 4))
+    batch = int(rng.integers(1, 6))
+    ymax = [math.inf, 0.75, 3.0][seed % 3]
+    p = tiny_random(seed, n, L, batch, w_density=float(rng.uniform(0.05, 0.9)),
+                    y_density=float(rng.uniform(0.1, 1.0)), explicit_zeros=bool(seed % 2), ymax=ymax)
+    got = oracle.csr_to_dense(oracle.forward(n, p.layers, ymax, p.y0_csr), n)
+    want = brute.dense_forward(oracle.csr_to_dense(p.y0_csr, n), [l.to_dense(n) for l in p.layers],
+                               [l.bias for l in p.layers], ymax)
+    assert got.tobytes() == want.tobytes()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_fig4_listing_equals_brute_force(seed):
+    """The two-semiring rewrite (Sec. III) in the paper's orientation equals the plain definition."""
+    rng = np.random.default_rng(100 + seed)
+    n, L, batch = int(rng.integers(2, 12)), int(rng.integers(1, 4)), int(rng.integers(1, 5))
+    p = tiny_random(100 + seed, n, L, batch, w_density=0.5, y_density=0.7)
+    Y0 = oracle.csr_to_dense(p.y0_csr, n)
+    Ws = [l.to_dense(n) for l in p.layers]
+    bs = [l.bias for l in p.layers]
+    lit = brute.fig4_forward(Y0.tolist(), [w.tolist() for w in Ws], [b.tolist() for b in bs])
+    assert lit.tobytes() == brute.dense_forward(Y0, Ws, bs).tobytes()
+    got = oracle.csr_to_dense(oracle.forward(n, p.layers, math.inf, p.y0_csr), n)
+    assert got.tobytes() == lit.tobytes()
+
+
+def test_layer_ranges_compose():
+    p = tiny_random(7, 20, 4, 5, w_density=0.4)
+    full = oracle.forward(20, p.layers, math.inf, p.y0_csr)
+    mid = oracle.forward(20, p.layers, math.inf, p.y0_csr, k0=0, k1=2)
+    rest = oracle.forward(20, p.layers, math.inf, mid, k0=2, k1=4)
+    for a, b in zip(full, rest):
+        assert np.array_equal(a, b)
+    same = oracle.forward(20, p.layers, math.inf, p.y0_csr, k0=1, k1=1)
+    for a, b in zip(same, p.y0_csr):
+        assert np.array_equal(a, b)
+
+
+# --------------------------------------------------------------------------- closed forms
+
+
+def test_linear_regime_is_chain_product():
+    """b = 0, W >= 0, Y >= 0: h is the identity, so Y_L = Y_0 W_0 ... W_{L-1} (Sec. III remark on linear h)."""
+    rng = np.random.default_rng(5)
+    n, L, batch = 40, 4, 6
+    layers, dense = [], []
+    for k in range(L):
+        W = (rng.random((n, n)) < 0.2) * rng.uniform(0.0, 0.6, (n, n))
+        W = W.astype(np.float32)
+        dense.append(W.astype(np.float64))
+        rp, c, v = dense_to_csr(W)
+        layers.append(Layer(rp, c, v, np.zeros(n, np.float32)))
+    Y0 = rng.random((batch, n)).astype(np.float32)
+    got = _run(n, layers, math.inf, Y0).astype(np.float64)
+    want = Y0.astype(np.float64)
+    for W in dense:
+        want = want @ W
+    # one fp32 rounding per layer: relative error below L * 2^-24 up to the condition (all terms >= 0)
+    np.testing.assert_allclose(got, want, rtol=L * 2.0 ** -23, atol=0)
+
+
+def test_affine_regime_is_matmul_plus_bias():
+    """b >= max |Y W|: nothing is clipped, so Y_1 = Y W + b exactly up to the final fp32 rounding."""
+    rng = np.random.default_rng(6)
+    n, batch = 32, 8
+    W = ((rng.random((n, n)) < 0.3) * rng.uniform(-1, 1, (n, n))).astype(np.float32)
+    Y0 = rng.uniform(-1, 1, (batch, n)).astype(np.float32)
+    z = Y0.astype(np.float64) @ W.astype(np.float64)
+    b = np.full(n, np.abs(z).max() + 1.0, np.float32)
+    rp, c, v = dense_to_csr(W)
+    got = _run(n, [Layer(rp, c, v, b)], math.inf, Y0)
+    want = (z + b.astype(np.float64)).astype(np.float32)
+    assert np.max(np.abs(got.view(np.int32) - want.view(np.int32))) <= 1  # at most one ulp (summation order)
+
+
+def test_identity_input_reads_back_weights():
+    """Y_0 = I (batch = n) gives row i of Y_1 = h(W(i,:) + b): pins the orientation Y W (not W Y)."""
+    p = tiny_random(11, 30, 1, 1, w_density=0.3)
+    n = 30
+    l = p.layers[0]
+    got = _run(n, p.layers, math.inf, np.eye(n, dtype=np.float32))
+    Wd = l.to_dense(n).astype(np.float64)
+    want = np.maximum(Wd + l.bias.astype(np.float64), 0.0).astype(np.float32)
+    assert got.tobytes() == want.tobytes()
+
+
+def test_permutation_weights_permute_columns():
+    rng = np.random.default_rng(12)
+    n, batch = 25, 4
+    perm = rng.permutation(n)
+    W = np.zeros((n, n), np.float32)
+    W[np.arange(n), perm] = 1.0
+    rp, c, v = dense_to_csr(W)
+    Y0 = rng.random((batch, n)).astype(np.float32)
+    got = _run(n, [Layer(rp, c, v, np.zeros(n, np.float32))], math.inf, Y0)
+    want = np.zeros_like(Y0)
+    want[:, perm] = Y0
+    assert got.tobytes() == want.tobytes()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_integer_shadow_matches_exact_integer_arithmetic(cfg):
+    """Integer-valued inputs: every partial sum is exact, so numpy int64 matmul + bias + clip is the answer."""
+    small = {1: dict(n=96, L=3, batch=7), 2: dict(n=128, L=3, batch=9), 3: dict(n=256, L=3, batch=11),
+             4: dict(n=2048, L=3, batch=13, window=256), 5: dict(n=1024, L=3, batch=5, block=256)}[cfg]
+    p = make_config(cfg, 0.1 if cfg == 2 else None, **small)
+    q = integer_shadow(p)
+    n = q.n
+    Y = q.y0_dense if q.y0_dense is not None else oracle.csr_to_dense(q.y0_csr, n)
+    Yi = Y.astype(np.int64)
+    for l in q.layers:
+        Yi = np.clip(Yi @ l.to_dense(n).astype(np.int64) + l.bias.astype(np.int64), 0, int(q.ymax))
+    got = oracle.csr_to_dense(oracle.forward(n, q.layers, q.ymax, q.y0_as_csr()), n)
+    assert np.array_equal(got, Yi.astype(np.float32))
+
+
+def test_deep_sparse_layer0_closed_form():
+    """All weights 1/16 and binary inputs: z = c/16 + b with c an integer count (one rounding only)."""
+    p = make_config(4, n=4096, L=1, batch=64, window=512)
+    n = p.n
+    l = p.layers[0]
+    Y = oracle.csr_to_dense(p.y0_csr, n)
+    c = (Y.astype(np.int64) @ (l.to_dense(n) != 0).astype(np.int64)).astype(np.float64)
+    want = np.minimum(np.maximum(c / 16.0 + np.float64(np.float32(-0.3)), 0.0), 32.0).astype(np.float32)
+    got = oracle.csr_to_dense(oracle.forward(n, p.layers, p.ymax, p.y0_csr), n)
+    assert got.tobytes() == want.tobytes()
+    # c = 5 is the first survivor: 5/16 - 0.3 rounds to the same fp32 whichever way it is evaluated
+    assert np.float32(5 / 16 + np.float64(np.float32(-0.3))) == np.float32(np.float32(5 / 16) + np.float32(-0.3))
+
+
+# --------------------------------------------------------------------------- invariants
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_invariants(seed):
+    n, L, batch = 60, 5, 10
+    ymax = 2.0 if seed % 2 else math.inf
+    p = tiny_random(200 + seed, n, L, batch, w_density=0.15, y_density=0.3, bias_lo=-0.4, bias_hi=0.0,
+                    ymax=ymax)
+    # zero rows
+    rp, c, v = p.y0_csr
+    keep = np.ones(batch, bool)
+    keep[::3] = False  # make every third sample an all-zero row
+    Y0 = oracle.csr_to_dense(p.y0_csr, n) * keep[:, None]
+    csr = dense_to_csr(Y0)
+    out, trace = oracle.forward(n, p.layers, ymax, csr, trace=True)
+    Y = oracle.csr_to_dense(out, n)
+    assert np.all(Y >= 0) and np.all(Y <= ymax)
+    assert np.all(out[2] != 0)  # no stored zeros
+    assert np.all(Y[~keep] == 0)  # b <= 0: zero rows stay zero
+    assert trace[-1] == out[0][-1]
+    # b <= 0: every stored entry has a structural product path
+    struct = (Y0 != 0).astype(np.int64)
+    for l in p.layers:
+        struct = ((struct @ (l.to_dense(n) != 0).astype(np.int64)) > 0).astype(np.int64)
+    assert np.all(struct[Y != 0] == 1)
+    # sorted, unique columns per row
+    for r in range(batch):
+        cols = out[1][out[0][r]:out[0][r + 1]]
+        assert np.all(np.diff(cols) > 0)
+
+
+def test_preact_consistent_with_forward():
+    p = tiny_random(31, 50, 1, 6, w_density=0.3)
+    z, s = oracle.preact(50, p.layers[0], p.y0_csr)
+    out = oracle.csr_to_dense(oracle.forward(50, p.layers, math.inf, p.y0_csr), 50)
+    assert out.tobytes() == np.maximum(z, 0.0).astype(np.float32).tobytes()
+    assert np.all(s >= np.abs(z) - 1e-12)
+
+
+def test_rejects_bad_input():
+    p = tiny_random(3, 10, 1, 2)
+    l = p.layers[0]
+    bad = Layer(l.row_ptr, np.where(l.col == l.col.max(), 10, l.col).astype(np.int32), l.val, l.bias)
+    with pytest.raises(ValueError):
+        oracle.forward(10, [bad], math.inf, p.y0_csr)
+    rp, c, v = p.y0_csr
+    if len(c) >= 2 and rp[1] - rp[0] >= 2:
+        c2 = c.copy()
+        c2[0], c2[1] = c2[1], c2[0]
+        with pytest.raises(ValueError):
+            oracle.forward(10, [l], math.inf, (rp, c2, v))
