@@ -1,0 +1,156 @@
+/*
+ * sdnn.h -- C ABI of the MI355X sparse DNN forward-pass library (libsdnn.so).
+ *
+ * The library computes the inference step of a ReLU deep neural network,
+ *
+ *     Y_{k+1} = h(Y_k W_k + 1 b_k^T),   h(x) = min(max(x, 0), ymax),
+ *
+ * for k = k0 .. k1-1 (Kepner et al., arXiv:1708.02937, Sec. III, batched
+ * inference equation and ReLU; Sec. IV, Fig. 4: the function dnn(Y, W, B, L)
+ * whose loop body is one matrix multiply over the +.x semiring followed by an
+ * element-wise + (max.+ multiply) with the bias and an element-wise max (max.+
+ * add) with zero).  The paper writes the product as W_k Y_k with Y stored
+ * neurons x batch; this ABI takes Y batch x n (one sample per row) and W_k
+ * n_in x n_out, i.e. the transposes of the paper's operands.  ymax = +INFINITY
+ * gives the paper's plain ReLU.  The bias is added at every position, as the
+ * dense equation states.
+ *
+ * Arithmetic: inputs and outputs are fp32.  The sparse paths form every product
+ * exactly and accumulate in fp64, add the bias and apply h in fp64, and round
+ * once to fp32 per layer; the dense-W path (the comparison arm for the paper's
+ * sparse-versus-dense experiment, Sec. V) does the same on the fp64 matrix
+ * cores.  Output entries equal to zero are not stored in CSR results (Sec. II,
+ * 0-element).
+ *
+ * Conventions for every call:
+ *   - Pointers named in comments as "device" must point to memory on the
+ *     current HIP device; "host" pointers to host memory.  The library never
+ *     frees memory it did not allocate.
+ *   - CSR matrices use int64 row_ptr (rows + 1 entries, row_ptr[0] = 0),
+ *     int32 column indices strictly increasing within a row, fp32 values.
+ *   - Work is enqueued on the net's HIP stream and is asynchronous unless the
+ *     description says the call synchronises.
+ *   - No call aborts or throws; each returns an sdnn_status.  On error,
+ *     sdnn_last_error() returns a thread-local text with the detail and the
+ *     net stays usable.
+ *   - A net must be used from one host thread at a time.
+ */
+#ifndef SDNN_H
+#define SDNN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SDNN_OK = 0,
+    SDNN_ERR_NULL_POINTER = 1,       /* a required pointer is NULL */
+    SDNN_ERR_INVALID_VALUE = 2,      /* bad size or count, non-finite weight or bias, ymax not > 0 */
+    SDNN_ERR_INVALID_INDEX = 3,      /* CSR structure: row_ptr not monotone or not ending at nnz, a
+                                        column out of [0, n), unsorted or repeated within a row */
+    SDNN_ERR_DIMENSION_MISMATCH = 4, /* layer range outside [0, L] or batch / nnz inconsistent */
+    SDNN_ERR_INVALID_OBJECT = 5,     /* NULL net, layer not set, dense arm not built */
+    SDNN_ERR_WORKSPACE_TOO_SMALL = 6,/* ws_bytes below sdnn_workspace_size() */
+    SDNN_ERR_OUT_OF_MEMORY = 7,      /* device allocation by the library failed */
+    SDNN_ERR_DEVICE = 8,             /* a HIP call failed; detail in sdnn_last_error() */
+    SDNN_ERR_UNSUPPORTED = 9         /* a size this build does not handle (see the message) */
+} sdnn_status;
+
+/* Which product a dense-Y forward uses for Y_k W_k. */
+enum {
+    SDNN_ARM_SPARSE = 0, /* CSR W_k: each output neuron gathers its fan-in (row-per-wavefront SpMM) */
+    SDNN_ARM_DENSE = 1   /* dense W_k with explicit zeros on the matrix cores (Sec. V dense baseline) */
+};
+
+typedef struct sdnn_net_s *sdnn_net;
+
+/*
+ * Create a net of L layers of width n (every layer is n x n, Sec. IV: all
+ * layers have the same number of neurons).  ymax > 0 is the clamp of h
+ * (+INFINITY for plain ReLU).  `stream` is a hipStream_t (NULL = the default
+ * stream).  *net receives a host handle owned by the caller; release it with
+ * sdnn_net_free.  Checks the device is a gfx950 part.
+ * Errors: NULL_POINTER, INVALID_VALUE (n < 1, n > 2^31-1, L < 0, ymax <= 0 or NaN), DEVICE.
+ */
+sdnn_status sdnn_net_create(sdnn_net *net, int64_t n, int32_t L, float ymax, void *stream);
+
+/* Replace the stream later work is enqueued on. */
+sdnn_status sdnn_net_set_stream(sdnn_net net, void *stream);
+
+/*
+ * Set layer k (0 <= k < L) from a CSR W_k (n_in x n_out, row i = fan-out of
+ * input neuron i, Sec. IV: CSR weights) and bias b_k[n] (Sec. III: b_k is
+ * replicated over the batch).  All four arrays are device memory that the
+ * caller keeps alive and unchanged until the net is freed or the layer is set
+ * again.  The call validates the CSR and the values on the device, builds the
+ * library-owned fan-in (transposed) copy used by the dense-Y path, and
+ * synchronises the net's stream once.  Fan-in lists longer than 8192 are
+ * rejected with UNSUPPORTED.
+ * Errors: INVALID_OBJECT, NULL_POINTER (nnz > 0 and col/val NULL), INVALID_VALUE
+ * (nnz < 0 or >= 2^31, non-finite value), INVALID_INDEX, UNSUPPORTED, OUT_OF_MEMORY, DEVICE.
+ */
+sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64_t *row_ptr,
+                               const int32_t *col_idx, const float *val, const float *bias);
+
+/*
+ * Build, for every layer that is set, a library-owned dense copy of W_k with
+ * explicit zeros (n*n values each, held in fp64, Sec. V.B: the dense version
+ * stores zeros explicitly) for SDNN_ARM_DENSE.  Synchronises once.
+ * Errors: INVALID_OBJECT (a layer not set), OUT_OF_MEMORY, DEVICE.
+ */
+sdnn_status sdnn_net_build_dense(sdnn_net net);
+
+/*
+ * Bytes of device workspace a forward call over `batch` samples needs:
+ * y_is_csr = 0 for sdnn_forward_dense, 1 for sdnn_forward_csr.
+ * Errors: INVALID_OBJECT, NULL_POINTER, INVALID_VALUE (batch < 0).
+ */
+sdnn_status sdnn_workspace_size(sdnn_net net, int64_t batch, int32_t y_is_csr, int64_t *bytes);
+
+/*
+ * Layers [k0, k1) on a dense batch: Y_in and Y_out are device fp32 arrays of
+ * batch x n, row-major (sample-major).  Y_out receives Y_{k1}; it may alias
+ * Y_in.  ws is device memory of at least sdnn_workspace_size(net, batch, 0)
+ * bytes that the call may overwrite.  Asynchronous on the net's stream; no
+ * host synchronisation.  k0 == k1 copies Y_in to Y_out.
+ * Errors: INVALID_OBJECT, NULL_POINTER, DIMENSION_MISMATCH, INVALID_VALUE (arm),
+ * WORKSPACE_TOO_SMALL, DEVICE.
+ */
+sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const float *Y_in,
+                               float *Y_out, void *ws, int64_t ws_bytes, int32_t arm);
+
+/*
+ * Layers [k0, k1) on a CSR batch Y_in = (y_row_ptr[batch+1], y_col, y_val),
+ * device arrays, columns strictly increasing within a row (not checked; the
+ * result is undefined otherwise).  y_col and y_val may be NULL when every row
+ * is empty.  Row extents outside [0, nnz] and column indices outside [0, n)
+ * are detected on the device and reported as INVALID_INDEX (the offending
+ * entries are skipped, so no access leaves the arrays).  The result Y_{k1} is written in CSR with
+ * no stored zeros: out_row_ptr (device, batch + 1 int64, caller-owned)
+ * receives the row pointers; *out_col and *out_val (host pointers to receive
+ * device addresses) point into ws and stay valid until ws is reused; *out_nnz
+ * (host) receives nnz(Y_{k1}).  ws is device memory of at least
+ * sdnn_workspace_size(net, batch, 1) bytes.  Synchronises the net's stream
+ * once, at the end, to read the nnz.
+ * Errors: INVALID_OBJECT, NULL_POINTER, DIMENSION_MISMATCH, INVALID_INDEX, WORKSPACE_TOO_SMALL, DEVICE.
+ */
+sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const int64_t *y_row_ptr,
+                             const int32_t *y_col, const float *y_val, void *ws, int64_t ws_bytes,
+                             int64_t *out_row_ptr, int32_t **out_col, float **out_val, int64_t *out_nnz);
+
+/* Free the net and the device memory the library allocated for it (synchronises its stream). */
+sdnn_status sdnn_net_free(sdnn_net net);
+
+/* Static text for a status code. */
+const char *sdnn_status_string(sdnn_status status);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char *sdnn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SDNN_H */

@@ -1,0 +1,409 @@
+// Host runtime behind the C ABI of include/sdnn.h: argument checks, layer set-up, workspace carving and
+// the layer loop of the forward pass (the loop of the paper's dnn() function, Fig. 4, Sec. IV), with every
+// layer's work enqueued on the net's HIP stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "sdnn.h"
+
+using sdnn::Edge;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+sdnn_status fail(sdnn_status s, const std::string &msg) {
+    g_last_error = msg;
+    return s;
+}
+
+sdnn_status fail_hip(hipError_t e, const char *what) {
+    return fail(SDNN_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define SDNN_HIP(call)                                      \
+    do {                                                    \
+        hipError_t e_ = (call);                             \
+        if (e_ != hipSuccess) return fail_hip(e_, #call);   \
+    } while (0)
+
+struct Layer {
+    bool set = false;
+    int64_t nnz = 0;
+    const int64_t *row_ptr = nullptr;  // caller-owned fan-out CSR and bias
+    const int32_t *col = nullptr;
+    const float *val = nullptr;
+    const float *bias = nullptr;
+    bool bias_nonpos = true;
+    Edge *w_pack = nullptr;    // fan-out entries packed as (column, weight)
+    int64_t *fan_ptr = nullptr;  // fan-in CSR (W_k^T)
+    Edge *fan = nullptr;
+    double *dense_wt = nullptr;  // n x n, W_k^T row-major in fp64, for the dense arm
+};
+
+template <typename T>
+void dfree(T *&p) {
+    if (p) (void)hipFree((void *)p);
+    p = nullptr;
+}
+
+void release(Layer &l) {
+    dfree(l.w_pack);
+    dfree(l.fan_ptr);
+    dfree(l.fan);
+    dfree(l.dense_wt);
+    l = Layer();
+}
+
+template <typename T>
+sdnn_status dalloc(T **p, size_t count, const char *what) {
+    *p = nullptr;
+    if (count == 0) count = 1;
+    hipError_t e = hipMalloc((void **)p, count * sizeof(T));
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        *p = nullptr;
+        return fail(SDNN_ERR_OUT_OF_MEMORY, std::string("hipMalloc failed for ") + what);
+    }
+    return SDNN_OK;
+}
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Workspace of a CSR forward: two slot buffers (count[batch], col[batch*n], val[batch*n]) and a scan area.
+struct CsrWs {
+    int32_t *cnt[2];
+    int32_t *col[2];
+    float *val[2];
+    int64_t *scan_tmp;
+    size_t bytes;
+};
+
+CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
+    CsrWs w{};
+    char *p = (char *)base;
+    size_t off = 0;
+    const size_t slots = (size_t)batch * (size_t)n;
+    for (int b = 0; b < 2; ++b) {
+        w.cnt[b] = (int32_t *)(p + off);
+        off = align_up(off + (size_t)batch * sizeof(int32_t));
+        w.col[b] = (int32_t *)(p + off);
+        off = align_up(off + slots * sizeof(int32_t));
+        w.val[b] = (float *)(p + off);
+        off = align_up(off + slots * sizeof(float));
+    }
+    w.scan_tmp = (int64_t *)(p + off);
+    off = align_up(off + (size_t)sdnn::scan_tmp_elems(batch) * sizeof(int64_t));
+    w.bytes = off;
+    return w;
+}
+
+size_t dense_ws_bytes(int64_t n, int64_t batch) { return 2 * align_up((size_t)n * (size_t)batch * sizeof(float)); }
+
+}  // namespace
+
+struct sdnn_net_s {
+    int64_t n = 0;
+    int32_t L = 0;
+    double ymax = INFINITY;
+    hipStream_t stream = nullptr;
+    int device = 0;
+    std::vector<Layer> layers;
+    uint32_t *d_flags = nullptr;
+    int32_t *d_int = nullptr;
+};
+
+extern "C" {
+
+const char *sdnn_status_string(sdnn_status s) {
+    switch (s) {
+        case SDNN_OK: return "SDNN_OK";
+        case SDNN_ERR_NULL_POINTER: return "SDNN_ERR_NULL_POINTER";
+        case SDNN_ERR_INVALID_VALUE: return "SDNN_ERR_INVALID_VALUE";
+        case SDNN_ERR_INVALID_INDEX: return "SDNN_ERR_INVALID_INDEX";
+        case SDNN_ERR_DIMENSION_MISMATCH: return "SDNN_ERR_DIMENSION_MISMATCH";
+        case SDNN_ERR_INVALID_OBJECT: return "SDNN_ERR_INVALID_OBJECT";
+        case SDNN_ERR_WORKSPACE_TOO_SMALL: return "SDNN_ERR_WORKSPACE_TOO_SMALL";
+        case SDNN_ERR_OUT_OF_MEMORY: return "SDNN_ERR_OUT_OF_MEMORY";
+        case SDNN_ERR_DEVICE: return "SDNN_ERR_DEVICE";
+        case SDNN_ERR_UNSUPPORTED: return "SDNN_ERR_UNSUPPORTED";
+    }
+    return "SDNN_ERR_UNKNOWN";
+}
+
+const char *sdnn_last_error(void) { return g_last_error.c_str(); }
+
+sdnn_status sdnn_net_create(sdnn_net *out, int64_t n, int32_t L, float ymax, void *stream) {
+    g_last_error.clear();
+    if (!out) return fail(SDNN_ERR_NULL_POINTER, "net is NULL");
+    *out = nullptr;
+    if (n < 1 || n > 0x7fffffffLL) return fail(SDNN_ERR_INVALID_VALUE, "n must be in [1, 2^31-1]");
+    if (L < 0) return fail(SDNN_ERR_INVALID_VALUE, "L must be >= 0");
+    if (!(ymax > 0.0f)) return fail(SDNN_ERR_INVALID_VALUE, "ymax must be > 0 (INFINITY for plain ReLU)");
+    int dev = 0;
+    SDNN_HIP(hipGetDevice(&dev));
+    hipDeviceProp_t prop;
+    SDNN_HIP(hipGetDeviceProperties(&prop, dev));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(SDNN_ERR_UNSUPPORTED, std::string("built for gfx950, device is ") + prop.gcnArchName);
+    sdnn_net net = new (std::nothrow) sdnn_net_s();
+    if (!net) return fail(SDNN_ERR_OUT_OF_MEMORY, "host allocation failed");
+    net->n = n;
+    net->L = L;
+    net->ymax = (double)ymax;
+    net->stream = (hipStream_t)stream;
+    net->device = dev;
+    net->layers.resize((size_t)L);
+    sdnn_status st = dalloc(&net->d_flags, 4, "flags");
+    if (st == SDNN_OK) st = dalloc(&net->d_int, 4, "scratch");
+    if (st != SDNN_OK) {
+        dfree(net->d_flags);
+        dfree(net->d_int);
+        delete net;
+        return st;
+    }
+    *out = net;
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_net_set_stream(sdnn_net net, void *stream) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    net->stream = (hipStream_t)stream;
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64_t *row_ptr, const int32_t *col_idx,
+                               const float *val, const float *bias) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    if (k < 0 || k >= net->L) return fail(SDNN_ERR_DIMENSION_MISMATCH, "layer index outside [0, L)");
+    if (!row_ptr || !bias) return fail(SDNN_ERR_NULL_POINTER, "row_ptr and bias are required");
+    if (nnz < 0 || nnz > 0x7fffffffLL) return fail(SDNN_ERR_INVALID_VALUE, "nnz must be in [0, 2^31-1]");
+    if (nnz > 0 && (!col_idx || !val)) return fail(SDNN_ERR_NULL_POINTER, "col_idx and val are required when nnz > 0");
+    const int64_t n = net->n;
+    hipStream_t s = net->stream;
+
+    // 1. validate on the device
+    SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
+    SDNN_HIP(sdnn::launch_validate_layer(n, nnz, row_ptr, col_idx, val, bias, net->d_flags, s));
+    uint32_t flags = 0;
+    SDNN_HIP(hipMemcpyAsync(&flags, net->d_flags, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    SDNN_HIP(hipStreamSynchronize(s));
+    if (flags & 1u)
+        return fail(SDNN_ERR_INVALID_INDEX,
+                    "W_k is not valid CSR (row_ptr monotone from 0 to nnz, columns in [0,n) strictly increasing)");
+    if (flags & 2u) return fail(SDNN_ERR_INVALID_VALUE, "W_k or b_k holds a non-finite value");
+
+    // 2. derived copies
+    Layer nl;
+    nl.set = true;
+    nl.nnz = nnz;
+    nl.row_ptr = row_ptr;
+    nl.col = col_idx;
+    nl.val = val;
+    nl.bias = bias;
+    nl.bias_nonpos = (flags & 4u) == 0;
+    int32_t *counts = nullptr;
+    int64_t *tmp = nullptr;
+    sdnn_status st = SDNN_OK;
+    auto cleanup = [&](sdnn_status r) {
+        dfree(counts);
+        dfree(tmp);
+        if (r != SDNN_OK) release(nl);
+        return r;
+    };
+    if ((st = dalloc(&nl.w_pack, (size_t)nnz, "packed W_k")) != SDNN_OK) return cleanup(st);
+    if ((st = dalloc(&nl.fan_ptr, (size_t)n + 1, "fan-in pointers")) != SDNN_OK) return cleanup(st);
+    if ((st = dalloc(&nl.fan, (size_t)nnz, "fan-in lists")) != SDNN_OK) return cleanup(st);
+    if ((st = dalloc(&counts, (size_t)n, "fan-in counts")) != SDNN_OK) return cleanup(st);
+    if ((st = dalloc(&tmp, (size_t)sdnn::scan_tmp_elems(n), "scan scratch")) != SDNN_OK) return cleanup(st);
+
+    hipError_t e;
+#define SETUP_HIP(call)                                            \
+    do {                                                           \
+        e = (call);                                                \
+        if (e != hipSuccess) return cleanup(fail_hip(e, #call));   \
+    } while (0)
+    SETUP_HIP(sdnn::launch_pack_edges(nnz, col_idx, val, nl.w_pack, s));
+    SETUP_HIP(hipMemsetAsync(counts, 0, (size_t)n * sizeof(int32_t), s));
+    SETUP_HIP(sdnn::launch_fanin_counts(nnz, col_idx, counts, s));
+    SETUP_HIP(sdnn::launch_exclusive_scan_i32_to_i64(n, counts, nl.fan_ptr, tmp, s));
+    SETUP_HIP(hipMemsetAsync(counts, 0, (size_t)n * sizeof(int32_t), s));
+    SETUP_HIP(sdnn::launch_fanin_scatter(n, row_ptr, col_idx, val, nl.fan_ptr, counts, nl.fan, s));
+    SETUP_HIP(hipMemsetAsync(net->d_int, 0, sizeof(int32_t), s));
+    SETUP_HIP(sdnn::launch_max_segment(n, nl.fan_ptr, net->d_int, s));
+    int32_t max_fanin = 0;
+    SETUP_HIP(hipMemcpyAsync(&max_fanin, net->d_int, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    SETUP_HIP(hipStreamSynchronize(s));
+    if (max_fanin > 8192) {
+        char msg[128];
+        std::snprintf(msg, sizeof msg, "a fan-in list has %d entries; at most 8192 are supported", max_fanin);
+        return cleanup(fail(SDNN_ERR_UNSUPPORTED, msg));
+    }
+    SETUP_HIP(sdnn::launch_fanin_sort(n, max_fanin, nl.fan_ptr, nl.fan, s));
+    SETUP_HIP(hipStreamSynchronize(s));
+#undef SETUP_HIP
+    cleanup(SDNN_OK);
+    Layer &slot = net->layers[(size_t)k];
+    release(slot);  // the stream was synchronised above, so nothing still reads the old copies
+    slot = nl;
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_net_build_dense(sdnn_net net) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    const int64_t n = net->n;
+    for (int32_t k = 0; k < net->L; ++k) {
+        Layer &l = net->layers[(size_t)k];
+        if (!l.set) return fail(SDNN_ERR_INVALID_OBJECT, "every layer must be set before build_dense");
+        if (l.dense_wt) continue;
+        sdnn_status st = dalloc(&l.dense_wt, (size_t)n * (size_t)n, "dense W_k");
+        if (st != SDNN_OK) return st;
+        hipError_t e = sdnn::launch_dense_from_fanin(n, l.fan_ptr, l.fan, l.dense_wt, net->stream);
+        if (e != hipSuccess) return fail_hip(e, "launch_dense_from_fanin");
+    }
+    SDNN_HIP(hipStreamSynchronize(net->stream));
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_workspace_size(sdnn_net net, int64_t batch, int32_t y_is_csr, int64_t *bytes) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    if (!bytes) return fail(SDNN_ERR_NULL_POINTER, "bytes is NULL");
+    if (batch < 0) return fail(SDNN_ERR_INVALID_VALUE, "batch must be >= 0");
+    *bytes = y_is_csr ? (int64_t)carve_csr(nullptr, net->n, batch).bytes : (int64_t)dense_ws_bytes(net->n, batch);
+    return SDNN_OK;
+}
+
+static sdnn_status check_range(sdnn_net net, int32_t k0, int32_t k1) {
+    if (k0 < 0 || k1 < k0 || k1 > net->L) return fail(SDNN_ERR_DIMENSION_MISMATCH, "need 0 <= k0 <= k1 <= L");
+    for (int32_t k = k0; k < k1; ++k)
+        if (!net->layers[(size_t)k].set) return fail(SDNN_ERR_INVALID_OBJECT, "a layer in [k0, k1) is not set");
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const float *Y_in, float *Y_out,
+                               void *ws, int64_t ws_bytes, int32_t arm) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    sdnn_status st = check_range(net, k0, k1);
+    if (st != SDNN_OK) return st;
+    if (batch < 0) return fail(SDNN_ERR_DIMENSION_MISMATCH, "batch must be >= 0");
+    if (arm != SDNN_ARM_SPARSE && arm != SDNN_ARM_DENSE) return fail(SDNN_ERR_INVALID_VALUE, "unknown arm");
+    if (batch == 0) return SDNN_OK;
+    if (!Y_in || !Y_out) return fail(SDNN_ERR_NULL_POINTER, "Y_in and Y_out are required");
+    const int64_t n = net->n;
+    hipStream_t s = net->stream;
+    if (k0 == k1) {
+        if (Y_out != Y_in)
+            SDNN_HIP(hipMemcpyAsync(Y_out, Y_in, (size_t)batch * (size_t)n * sizeof(float), hipMemcpyDeviceToDevice, s));
+        return SDNN_OK;
+    }
+    if (!ws) return fail(SDNN_ERR_NULL_POINTER, "ws is required");
+    if (ws_bytes < (int64_t)dense_ws_bytes(n, batch))
+        return fail(SDNN_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than sdnn_workspace_size(net, batch, 0)");
+    if (arm == SDNN_ARM_DENSE)
+        for (int32_t k = k0; k < k1; ++k)
+            if (!net->layers[(size_t)k].dense_wt)
+                return fail(SDNN_ERR_INVALID_OBJECT, "dense arm requested before sdnn_net_build_dense");
+    float *buf[2];
+    buf[0] = (float *)ws;
+    buf[1] = (float *)((char *)ws + align_up((size_t)n * (size_t)batch * sizeof(float)));
+    SDNN_HIP(sdnn::launch_transpose(Y_in, buf[0], batch, n, s));  // batch x n -> n x batch
+    int cur = 0;
+    for (int32_t k = k0; k < k1; ++k) {
+        const Layer &l = net->layers[(size_t)k];
+        if (arm == SDNN_ARM_SPARSE)
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.bias, net->ymax, buf[cur], buf[cur ^ 1], s));
+        else
+            SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, l.dense_wt, l.bias, net->ymax, buf[cur], buf[cur ^ 1], s));
+        cur ^= 1;
+    }
+    SDNN_HIP(sdnn::launch_transpose(buf[cur], Y_out, n, batch, s));  // n x batch -> batch x n
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const int64_t *y_row_ptr,
+                             const int32_t *y_col, const float *y_val, void *ws, int64_t ws_bytes,
+                             int64_t *out_row_ptr, int32_t **out_col, float **out_val, int64_t *out_nnz) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    sdnn_status st = check_range(net, k0, k1);
+    if (st != SDNN_OK) return st;
+    if (batch < 0 || batch > 0x7fffffffLL) return fail(SDNN_ERR_DIMENSION_MISMATCH, "batch must be in [0, 2^31-1]");
+    if (!y_row_ptr || !out_row_ptr || !out_col || !out_val || !out_nnz)
+        return fail(SDNN_ERR_NULL_POINTER, "y_row_ptr and the four outputs are required");
+    if (!ws) return fail(SDNN_ERR_NULL_POINTER, "ws is required");
+    const int64_t n = net->n;
+    hipStream_t s = net->stream;
+    CsrWs w = carve_csr(ws, n, batch);
+    if (ws_bytes < (int64_t)w.bytes)
+        return fail(SDNN_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than sdnn_workspace_size(net, batch, 1)");
+    if (k0 == k1) {  // identity: copy the input CSR into the workspace
+        int64_t in_nnz = 0;
+        SDNN_HIP(hipMemcpyAsync(&in_nnz, y_row_ptr + batch, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        SDNN_HIP(hipStreamSynchronize(s));
+        if (in_nnz < 0 || in_nnz > batch * n)
+            return fail(SDNN_ERR_DIMENSION_MISMATCH, "y_row_ptr[batch] outside [0, batch*n]");
+        if (in_nnz > 0 && (!y_col || !y_val)) return fail(SDNN_ERR_NULL_POINTER, "y_col and y_val are required");
+        SDNN_HIP(hipMemcpyAsync(out_row_ptr, y_row_ptr, (size_t)(batch + 1) * sizeof(int64_t), hipMemcpyDeviceToDevice, s));
+        if (in_nnz > 0) {
+            SDNN_HIP(hipMemcpyAsync(w.col[0], y_col, (size_t)in_nnz * sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+            SDNN_HIP(hipMemcpyAsync(w.val[0], y_val, (size_t)in_nnz * sizeof(float), hipMemcpyDeviceToDevice, s));
+        }
+        SDNN_HIP(hipStreamSynchronize(s));
+        *out_col = w.col[0];
+        *out_val = w.val[0];
+        *out_nnz = in_nnz;
+        return SDNN_OK;
+    }
+    SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
+
+    int cur = 0;
+    for (int32_t k = k0; k < k1; ++k) {
+        const Layer &l = net->layers[(size_t)k];
+        const bool first = k == k0;
+        SDNN_HIP(sdnn::launch_spgemm_layer(n, batch, first ? y_row_ptr : nullptr, first ? nullptr : w.cnt[cur ^ 1],
+                                           first ? y_col : w.col[cur ^ 1], first ? y_val : w.val[cur ^ 1], l.row_ptr,
+                                           l.w_pack, l.bias, l.bias_nonpos ? 1 : 0, net->ymax, w.cnt[cur], w.col[cur],
+                                           w.val[cur], net->d_flags, s));
+        cur ^= 1;
+    }
+    const int last = cur ^ 1;  // buffer holding Y_{k1} in slots
+    SDNN_HIP(sdnn::launch_exclusive_scan_i32_to_i64(batch, w.cnt[last], out_row_ptr, w.scan_tmp, s));
+    SDNN_HIP(sdnn::launch_compact_rows(n, batch, w.cnt[last], out_row_ptr, w.col[last], w.val[last], w.col[cur],
+                                       w.val[cur], s));
+    int64_t nnz = 0;
+    uint32_t flags = 0;
+    SDNN_HIP(hipMemcpyAsync(&nnz, out_row_ptr + batch, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    SDNN_HIP(hipMemcpyAsync(&flags, net->d_flags, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    SDNN_HIP(hipStreamSynchronize(s));
+    if (flags & 1u)
+        return fail(SDNN_ERR_INVALID_INDEX, "Y_in is not valid CSR (row extents or column indices out of range)");
+    *out_col = w.col[cur];
+    *out_val = w.val[cur];
+    *out_nnz = nnz;
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_net_free(sdnn_net net) {
+    g_last_error.clear();
+    if (!net) return SDNN_OK;
+    (void)hipStreamSynchronize(net->stream);
+    for (Layer &l : net->layers) release(l);
+    dfree(net->d_flags);
+    dfree(net->d_int);
+    delete net;
+    return SDNN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,64 @@
+// Shared definitions of the HIP library (kernels and host runtime).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sdnn {
+
+// A weight entry packed for one 64-bit load: the other end of the edge and its fp32 value.
+struct __align__(8) Edge {
+    int32_t idx;
+    float w;
+};
+
+constexpr int kWave = 64;
+
+// Wave-local exclusive count of set bits below this lane in a 64-bit ballot.
+__device__ __forceinline__ int lane_rank(uint64_t mask) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+// h(z) = min(max(z, 0), ymax) in fp64, then one round-to-nearest-even to fp32.
+__device__ __forceinline__ float activate(double z, double ymax) {
+    if (z < 0.0) z = 0.0;
+    if (z > ymax) z = ymax;
+    return (float)z;
+}
+
+// ---------------------------------------------------------------- launchers (defined in the .hip files)
+
+// setup.hip
+hipError_t launch_validate_layer(int64_t n, int64_t nnz, const int64_t *row_ptr, const int32_t *col,
+                                 const float *val, const float *bias, uint32_t *flags, hipStream_t s);
+hipError_t launch_fanin_counts(int64_t nnz, const int32_t *col, int32_t *counts, hipStream_t s);
+hipError_t launch_exclusive_scan_i32_to_i64(int64_t count, const int32_t *in, int64_t *out, int64_t *tmp,
+                                            hipStream_t s);
+int64_t scan_tmp_elems(int64_t count);
+hipError_t launch_fanin_scatter(int64_t n, const int64_t *row_ptr, const int32_t *col, const float *val,
+                                const int64_t *fan_ptr, int32_t *cursor, Edge *fan, hipStream_t s);
+hipError_t launch_fanin_sort(int64_t n, int32_t max_len, const int64_t *fan_ptr, Edge *fan, hipStream_t s);
+hipError_t launch_max_segment(int64_t n, const int64_t *ptr, int32_t *out, hipStream_t s);
+hipError_t launch_pack_edges(int64_t nnz, const int32_t *col, const float *val, Edge *out, hipStream_t s);
+
+// spmm.hip
+hipError_t launch_transpose(const float *in, float *out, int64_t rows, int64_t cols, hipStream_t s);
+hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan, const float *bias,
+                             double ymax, const float *yt, float *zt, hipStream_t s);
+
+// gemm.hip
+hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *wt, hipStream_t s);
+hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, const double *wt, const float *bias, double ymax,
+                                   const float *yt, float *zt, hipStream_t s);
+
+// spgemm.hip
+size_t spgemm_lds_bytes(int64_t n);
+hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
+                               const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const Edge *w,
+                               const float *bias, int bias_nonpos, double ymax, int32_t *out_cnt, int32_t *out_col,
+                               float *out_val, uint32_t *err, hipStream_t s);
+hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, const int64_t *row_ptr,
+                               const int32_t *in_col, const float *in_val, int32_t *out_col, float *out_val,
+                               hipStream_t s);
+
+}  // namespace sdnn

@@ -1,0 +1,273 @@
+"""GPU results against the oracle, through the C ABI (binding in paper_1708_02937_amd).
+
+Tolerance and pattern rule: see tests/parity.py (|g - o| <= 1e-6 + 1e-5 |o|; pattern equal
+except entries at the ReLU threshold within the fp32 rounding allowance; integer-valued
+problems bit for bit).
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+from tests import parity
+from workloads import Layer, csr_rows, dense_to_csr, integer_shadow, make_config, tiny_random
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sd():
+    import torch
+
+    import paper_1708_02937_amd as sd
+
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return sd
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def run_dense(sd, p, arm, y0=None):
+    import torch
+
+    net = sd.net_from_problem(p, dense=(arm == sd.SDNN_ARM_DENSE))
+    y = torch.from_numpy(p.y0_dense if y0 is None else y0).cuda()
+    out = net.forward_dense(y, arm=arm).cpu().numpy()
+    net.free()
+    return out
+
+
+def run_csr(sd, p, y0=None, k0=0, k1=None):
+    net = sd.net_from_problem(p)
+    rp, c, v = net.forward_csr(*(p.y0_as_csr() if y0 is None else y0), k0=k0, k1=k1)
+    res = (rp.cpu().numpy(), c.cpu().numpy(), v.cpu().numpy())
+    net.free()
+    return res
+
+
+ARMS = ["sparse", "dense"]
+
+
+def _arm(sd, name):
+    return sd.SDNN_ARM_SPARSE if name == "sparse" else sd.SDNN_ARM_DENSE
+
+
+# ------------------------------------------------------------------------------------------ small shapes
+
+TINY = [(1, 1, 1, 1), (2, 7, 2, 3), (3, 63, 2, 64), (4, 64, 3, 65), (5, 65, 2, 130), (6, 200, 3, 257),
+        (7, 333, 2, 129), (8, 130, 1, 2048)]
+
+
+@pytest.mark.parametrize("arm", ARMS)
+@pytest.mark.parametrize("seed,n,L,batch", TINY)
+def test_tiny_dense_batch(sd, arm, seed, n, L, batch):
+    ymax = [math.inf, 1.5][seed % 2]
+    p = tiny_random(seed, n, L, batch, w_density=0.2, y_density=0.6, dense_input=True, ymax=ymax,
+                    explicit_zeros=seed % 3 == 0)
+    _say("tiny dense", arm, seed, n, L, batch)
+    out = run_dense(sd, p, _arm(sd, arm))
+    parity.compare(p, dense_to_csr(out))
+
+
+@pytest.mark.parametrize("seed,n,L,batch", TINY + [(9, 5000, 2, 17), (10, 17000, 2, 9), (11, 40000, 1, 5)])
+def test_tiny_csr_batch(sd, seed, n, L, batch):
+    p = tiny_random(seed, n, L, batch, w_density=min(0.3, 8.0 / n + 0.001), y_density=0.3,
+                    bias_lo=-0.3, bias_hi=0.05 if seed % 2 else 0.0, ymax=[math.inf, 2.0][seed % 2],
+                    explicit_zeros=seed % 3 == 0)
+    _say("tiny csr", seed, n, L, batch)
+    parity.compare(p, run_csr(sd, p))
+
+
+@pytest.mark.parametrize("cfg,kw", [
+    (1, dict(n=1024, L=4, batch=64)), (2, dict(n=512, L=3, batch=200)), (3, dict(n=2048, L=3, batch=100)),
+    (4, dict(n=20000, L=3, batch=50, window=1024)), (5, dict(n=20480, L=2, batch=12, block=4096))])
+def test_integer_shadows_bit_exact(sd, cfg, kw):
+    p = integer_shadow(make_config(cfg, 0.1 if cfg == 2 else None, **kw))
+    _say("integer shadow", cfg, kw)
+    if p.y0_dense is not None:
+        for arm in ARMS:
+            parity.compare(p, dense_to_csr(run_dense(sd, p, _arm(sd, arm))), exact=True)
+    parity.compare(p, run_csr(sd, p), exact=True)
+
+
+# ------------------------------------------------------------------------------------------ the workloads
+
+
+@pytest.mark.parametrize("arm", ARMS)
+def test_config1_full(sd, arm):
+    p = make_config(1)
+    _say("config 1", arm)
+    st = parity.compare(p, dense_to_csr(run_dense(sd, p, _arm(sd, arm))))
+    assert st["entries"] > 0
+
+
+def test_config1_csr_path(sd):
+    p = make_config(1)
+    _say("config 1 csr")
+    parity.compare(p, run_csr(sd, p))
+
+
+@pytest.mark.parametrize("d", [0.5, 0.1, 0.01, 0.001])
+def test_config2_sparse_arm_sampled(sd, d):
+    p = make_config(2, d)
+    _say("config 2 sparse arm", d)
+    out = run_dense(sd, p, sd.SDNN_ARM_SPARSE)
+    rows = np.random.default_rng(0).choice(p.batch, 12 if d >= 0.1 else 48, replace=False)
+    parity.compare(p, dense_to_csr(out[rows]), rows=rows)
+
+
+@pytest.mark.parametrize("d", [0.5, 0.01])
+def test_config2_dense_arm_sampled(sd, d):
+    p = make_config(2, d)
+    _say("config 2 dense arm", d)
+    out = run_dense(sd, p, sd.SDNN_ARM_DENSE)
+    rows = np.random.default_rng(1).choice(p.batch, 12, replace=False)
+    parity.compare(p, dense_to_csr(out[rows]), rows=rows)
+
+
+def test_config3_scaled_full_compare(sd):
+    p = make_config(3, n=4096, L=6, batch=300)
+    _say("config 3 scaled")
+    parity.compare(p, run_csr(sd, p))
+
+
+def test_config3_full_size_sampled(sd):
+    p = make_config(3)
+    _say("config 3 full size")
+    rp, c, v = run_csr(sd, p)
+    rows = np.random.default_rng(2).choice(p.batch, 10, replace=False)
+    parity.compare(p, csr_rows((rp, c, v), rows), rows=rows)
+
+
+def test_config4_scaled(sd):
+    p = make_config(4, n=32768, L=6, batch=400)
+    _say("config 4 scaled")
+    parity.compare(p, run_csr(sd, p))
+
+
+def test_config5_scaled(sd):
+    p = make_config(5, n=32768, L=3, batch=24)
+    _say("config 5 scaled")
+    parity.compare(p, run_csr(sd, p))
+
+
+# ------------------------------------------------------------------------------------------ structure
+
+
+def test_identity_input_reads_back_weights(sd):
+    """Y_0 = I gives row i of Y_1 = h(W(i,:) + b): pins the Y W orientation on both paths."""
+    p = tiny_random(21, 150, 1, 150, w_density=0.1)
+    eye = np.eye(150, dtype=np.float32)
+    p.y0_dense = eye
+    want = np.maximum(p.layers[0].to_dense(150).astype(np.float64) + p.layers[0].bias, 0).astype(np.float32)
+    for arm in ARMS:
+        assert run_dense(sd, p, _arm(sd, arm)).tobytes() == want.tobytes()
+    got = parity.to_dense(run_csr(sd, p, y0=dense_to_csr(eye)), 150)
+    assert got.tobytes() == want.tobytes()
+
+
+def test_run_twice_identical(sd):
+    p = make_config(3, n=4096, L=4, batch=128)
+    a, b = run_csr(sd, p), run_csr(sd, p)
+    for x, y in zip(a, b):
+        assert x.tobytes() == y.tobytes()
+    q = make_config(2, 0.1, L=3, batch=256)
+    assert run_dense(sd, q, sd.SDNN_ARM_SPARSE).tobytes() == run_dense(sd, q, sd.SDNN_ARM_SPARSE).tobytes()
+
+
+def test_layer_ranges_compose(sd):
+    import torch
+
+    p = make_config(3, n=2048, L=5, batch=64)
+    net = sd.net_from_problem(p)
+    full = [x.cpu().numpy() for x in net.forward_csr(*p.y0_csr)]
+    mid = [x.clone() for x in net.forward_csr(*p.y0_csr, k0=0, k1=2)]
+    rest = [x.cpu().numpy() for x in net.forward_csr(*mid, k0=2, k1=5)]
+    for x, y in zip(full, rest):
+        assert x.tobytes() == y.tobytes()
+    same = [x.cpu().numpy() for x in net.forward_csr(*p.y0_csr, k0=3, k1=3)]
+    for x, y in zip(same, p.y0_csr):
+        assert x.tobytes() == y.tobytes()
+    q = make_config(2, 0.01, n=512, L=4, batch=128)
+    net2 = sd.net_from_problem(q)
+    y = torch.from_numpy(q.y0_dense).cuda()
+    a = net2.forward_dense(y).cpu().numpy()
+    b = net2.forward_dense(net2.forward_dense(y, k0=0, k1=1), k0=1, k1=4).cpu().numpy()
+    assert a.tobytes() == b.tobytes()
+    assert net2.forward_dense(y, k0=2, k1=2).cpu().numpy().tobytes() == q.y0_dense.tobytes()
+    net.free()
+    net2.free()
+
+
+def test_degenerate_cases(sd):
+    import torch
+
+    n = 100
+    empty = Layer(np.zeros(n + 1, np.int64), np.zeros(0, np.int32), np.zeros(0, np.float32),
+                  np.linspace(-0.5, 0.5, n).astype(np.float32))
+    p = tiny_random(3, n, 2, 10, dense_input=True)
+    p.layers[1] = empty
+    want = np.maximum(empty.bias.astype(np.float64), 0).astype(np.float32)
+    for arm in ARMS:
+        out = run_dense(sd, p, _arm(sd, arm))
+        assert out.tobytes() == np.tile(want, (10, 1)).tobytes()
+    # batch 0 and empty input rows
+    net = sd.net_from_problem(p)
+    y = torch.zeros((0, n), device="cuda")
+    assert net.forward_dense(y).shape == (0, n)
+    rp = np.zeros(5, np.int64)
+    out = net.forward_csr(rp, np.zeros(0, np.int32), np.zeros(0, np.float32))
+    p.y0_dense, p.y0_csr = None, (rp, np.zeros(0, np.int32), np.zeros(0, np.float32))
+    parity.compare(p, [x.cpu().numpy() for x in out])  # empty samples: h(b) propagates
+    net.free()
+
+
+def test_errors_leave_net_usable(sd):
+    import torch
+
+    p = tiny_random(4, 50, 2, 6, w_density=0.2, dense_input=True)
+    net = sd.Net(50, 2)
+    l = p.layers[0]
+    bad_cols = l.col.copy()
+    r = int(np.argmax(np.diff(l.row_ptr) >= 2))
+    a = l.row_ptr[r]
+    bad_cols[a], bad_cols[a + 1] = bad_cols[a + 1], bad_cols[a]  # unsorted row
+    with pytest.raises(sd.SdnnError) as e:
+        net.set_layer(0, l.row_ptr, bad_cols, l.val, l.bias)
+    assert e.value.status == 3
+    with pytest.raises(sd.SdnnError) as e:
+        net.set_layer(0, l.row_ptr, np.where(l.col == l.col.max(), 50, l.col).astype(np.int32), l.val, l.bias)
+    assert e.value.status == 3
+    bad_rp = l.row_ptr.copy()
+    bad_rp[-1] += 1
+    with pytest.raises(sd.SdnnError) as e:
+        net.set_layer(0, bad_rp, l.col, l.val, l.bias)
+    assert e.value.status == 3
+    nanb = l.bias.copy()
+    nanb[3] = np.nan
+    with pytest.raises(sd.SdnnError) as e:
+        net.set_layer(0, l.row_ptr, l.col, l.val, nanb)
+    assert e.value.status == 2
+    y = torch.from_numpy(p.y0_dense).cuda()
+    with pytest.raises(sd.SdnnError) as e:  # layers not set
+        net.forward_dense(y)
+    assert e.value.status == 5
+    for k, lk in enumerate(p.layers):
+        net.set_layer(k, lk.row_ptr, lk.col, lk.val, lk.bias)
+    with pytest.raises(sd.SdnnError) as e:  # dense arm before build_dense
+        net.forward_dense(y, arm=sd.SDNN_ARM_DENSE)
+    assert e.value.status == 5
+    ws = torch.empty(16, dtype=torch.uint8, device="cuda")
+    out = torch.empty_like(y)
+    with pytest.raises(sd.SdnnError) as e:
+        sd.sdnn_forward_dense(net.handle, 0, 2, 6, y, out, ws, 16, 0)
+    assert e.value.status == 6
+    with pytest.raises(sd.SdnnError) as e:
+        sd.sdnn_forward_dense(net.handle, 1, 3, 6, y, out, ws, 16, 0)
+    assert e.value.status == 4
+    got = net.forward_dense(y).cpu().numpy()  # still usable
+    parity.compare(p, dense_to_csr(got))
+    net.free()

@@ -1,0 +1,79 @@
+"""The C-ABI library loads and exports what include/sdnn.h declares; host-side argument checks.
+
+These run without a GPU: no call here reaches a kernel.
+"""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sdnn.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sdnn_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for want in ["sdnn_net_create", "sdnn_net_set_layer", "sdnn_net_build_dense", "sdnn_workspace_size",
+                 "sdnn_forward_dense", "sdnn_forward_csr", "sdnn_net_free", "sdnn_status_string",
+                 "sdnn_last_error", "sdnn_net_set_stream"]:
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_1708_02937_amd as sd
+
+    lib = ctypes.CDLL(sd.LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_uses_the_c_names():
+    import paper_1708_02937_amd as sd
+
+    for n in _declared():
+        assert callable(getattr(sd, n)), n
+
+
+def test_status_strings():
+    import paper_1708_02937_amd as sd
+
+    for code, name in sd.STATUS_NAMES.items():
+        assert sd.sdnn_status_string(code) == name
+    assert sd.sdnn_status_string(1234) == "SDNN_ERR_UNKNOWN"
+
+
+def test_host_side_argument_errors():
+    import paper_1708_02937_amd as sd
+
+    lib = sd.lib
+    assert lib.sdnn_net_create(None, 8, 1, 1.0, None) == 1  # NULL out pointer
+    h = ctypes.c_void_p()
+    assert lib.sdnn_net_create(ctypes.byref(h), 0, 1, 1.0, None) == 2  # n < 1
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, -1, 1.0, None) == 2  # L < 0
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, 0.0, None) == 2  # ymax <= 0
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, float("nan"), None) == 2
+    out = ctypes.c_int64()
+    assert lib.sdnn_workspace_size(None, 4, 0, ctypes.byref(out)) == 5  # NULL net
+    assert lib.sdnn_net_set_layer(None, 0, 0, None, None, None, None) == 5
+    assert lib.sdnn_forward_dense(None, 0, 1, 1, None, None, None, 0, 0) == 5
+    assert lib.sdnn_net_free(None) == 0
+    assert "ymax" in sd.sdnn_last_error() or sd.sdnn_last_error() == ""
+
+
+def test_oracle_and_library_share_no_code():
+    """The oracle is a separate C file built by gcc; the library's sources never include or name it."""
+    csrc = os.path.join(ROOT, "paper_1708_02937_amd")
+    for dirpath, _, files in os.walk(csrc):
+        for f in files:
+            if f.endswith((".hip", ".cpp", ".h", ".py")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.lower(), f

@@ -84,6 +84,9 @@ def battery(lib):
         got = oracle.forward(256, q.layers, q.ymax, q.y0_csr, lib=lib)
         if not np.array_equal(oracle.csr_to_dense(got, 256), Yi.astype(np.float32)):
             failed.append("integer_shadow")
+        want = dense_to_csr(Yi.astype(np.float32))  # canonical CSR of the exact answer
+        if not (np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])):
+            failed.append("integer_shadow_pattern")
     except ValueError:
         failed.append("error")
     return failed
