@@ -1,0 +1,297 @@
+"""Benchmark: edges/s of the sparse DNN forward pass on one MI355X.
+
+Default workload (the density sweep, n = 4096, L = 16, batch = 1024, fp32 storage): one step is one
+forward pass of all L layers through the CSR (sparse-W) path at each of the four weight densities
+{50%, 10%, 1%, 0.1%}; value = sum over the sweep of batch * nnz(W_k) * L divided by the step time.
+Inputs are resident in HBM before timing starts.  Besides the headline line it measures the dense-W
+arm at every density (the paper's sparse-versus-dense comparison, Sec. V) and reports the crossover
+density, the roofline of the dominant kernel, and the CPU oracle on a bounded sample as a baseline.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..5]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "edges/sec (batch × nnz(W_k) × L / time) at 1 MI355X; achieved HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+FP64_VECTOR_TFLOPS = 78.6  # MI355X fp64 vector peak: the sparse kernels multiply-add in fp64
+FP64_MATRIX_TFLOPS = 78.6  # MI355X fp64 matrix-core peak (dense-W arm)
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def _src_hash(*names):
+    h = hashlib.sha256()
+    for nm in names:
+        with open(os.path.join(ROOT, "paper_1708_02937_amd", "csrc", nm), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def _pmc_traffic(kernel_tag: str, src_names):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, or None when the kernel source
+    changed since the counters were taken (the summary records a hash of the sources it measured)."""
+    path = os.path.join(PROFILES, f"{kernel_tag}_pmc.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#")):
+                k, v = line.split(":", 1)
+                rec[k.strip()] = v.strip()
+    if rec.get("source_hash") != _src_hash(*src_names):
+        return None
+    return int(rec["hbm_bytes_per_launch"]) if "hbm_bytes_per_launch" in rec else None
+
+
+# ----------------------------------------------------------------------------------- timing helpers
+
+
+def _events(torch):
+    return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+
+def time_calls(torch, fn, reps: int) -> float:
+    """Average milliseconds per call of fn(), timed with HIP events on the current stream."""
+    a, b = _events(torch)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+# ----------------------------------------------------------------------------------- the sweep
+
+
+def spmm_algorithmic(n, batch, nnz):
+    """Algorithmic bytes and flops of one dense-Y CSR layer launch (one layer, all samples).
+
+    bytes: read Y^T (4 n batch) + fan-in lists (8 nnz) + list pointers (8 (n+1)) + bias (4 n),
+    write Y_{k+1}^T (4 n batch).  flops: 2 per product, batch * nnz products.
+    """
+    return 8 * n * batch + 8 * nnz + 8 * (n + 1) + 4 * n, 2.0 * batch * nnz
+
+
+def run_sweep(args, torch, sd):
+    from workloads import make_config
+
+    densities = [float(x) for x in args.densities.split(",")]
+    nets, ys, outs, probs = [], [], [], []
+    for d in densities:
+        t0 = time.time()
+        p = make_config(2, d)
+        net = sd.net_from_problem(p)
+        nets.append(net)
+        probs.append(p)
+        ys.append(torch.from_numpy(p.y0_dense).cuda())
+        outs.append(torch.empty_like(ys[-1]))
+        net.workspace(p.batch, 0)
+        log(f"density {d}: nnz/layer {p.layers[0].nnz}, set-up {time.time() - t0:.1f}s")
+
+    def step():
+        for net, y, o in zip(nets, ys, outs):
+            net.forward_dense(y, out=o)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    a, b = _events(torch)
+    t_wall = time.perf_counter()
+    a.record()
+    for _ in range(args.steps):
+        step()
+    b.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = a.elapsed_time(b) / args.steps
+    edges = sum(p.edges() for p in probs)
+    value = edges / (ms_step / 1e3)
+    log(f"step {ms_step:.3f} ms (wall {1e3 * t_wall / args.steps:.3f} ms), {value:.4g} edges/s")
+
+    # per-density forward time and the per-launch time of the layer kernel
+    sweep = {}
+    per_launch = {}
+    reps = max(3, args.steps)
+    for d, net, y, o, p in zip(densities, nets, ys, outs, probs):
+        t_full = time_calls(torch, lambda: net.forward_dense(y, out=o), reps)
+        t_one = time_calls(torch, lambda: net.forward_dense(y, k0=0, k1=1, out=o), reps * 4)
+        launch = (t_full - t_one) / (p.L - 1)  # the two transposes cancel; what is left is L-1 layer launches
+        per_launch[d] = launch
+        sweep[f"{d:g}"] = {"sparse_ms": round(t_full, 4), "sparse_edges_per_s": p.edges() / (t_full / 1e3),
+                           "layer_launch_ms": round(launch, 5), "nnz_per_layer": int(p.layers[0].nnz)}
+
+    # dense-W arm (matrix cores) at every density, one density at a time (n*n fp64 per layer)
+    if not args.no_dense:
+        for d, net, y, o, p in zip(densities, nets, ys, outs, probs):
+            net.build_dense()
+            t_dense = time_calls(torch, lambda: net.forward_dense(y, out=o, arm=sd.SDNN_ARM_DENSE), max(2, reps // 2))
+            sweep[f"{d:g}"]["dense_ms"] = round(t_dense, 4)
+            # release the dense copies by re-uploading the layer set (drops dense_wt)
+            for k, l in enumerate(p.layers):
+                net.set_layer(k, l.row_ptr, l.col, l.val, l.bias)
+            torch.cuda.synchronize()
+
+    crossover = None
+    pts = sorted((d, v["sparse_ms"], v.get("dense_ms")) for d, v in
+                 ((float(k), v) for k, v in sweep.items()) if v.get("dense_ms"))
+    for (d0, s0, q0), (d1, s1, q1) in zip(pts, pts[1:]):
+        r0, r1 = math.log(s0 / q0), math.log(s1 / q1)
+        if r0 <= 0 <= r1 and r1 != r0:  # sparse faster at d0, slower at d1
+            t = -r0 / (r1 - r0)
+            crossover = math.exp(math.log(d0) + t * (math.log(d1) - math.log(d0)))
+    # dominant kernel: the layer launch with the largest share of the step
+    dom = max(densities, key=lambda d: per_launch[d])
+    p = probs[densities.index(dom)]
+    nnz_avg = sum(l.nnz for l in p.layers) / p.L
+    byt, flops = spmm_algorithmic(p.n, p.batch, nnz_avg)
+    t_s = per_launch[dom] / 1e3
+    intensity = flops / byt
+    if intensity > FP64_VECTOR_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+        roof = {"bound": "alu", "achieved": round(flops / t_s / 1e12, 3), "peak": FP64_VECTOR_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(byt / t_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = _pmc_traffic(f"spmm_fanin_d{dom:g}", ["spmm.hip", "common.h"])
+    roof["kernel"] = "spmm_fanin_kernel"
+    roof["per_launch_ms"] = round(per_launch[dom], 5)
+    roof["density"] = dom
+    roof["algorithmic_bytes_per_launch"] = int(byt)
+    roof["algorithmic_flops_per_launch"] = flops
+    for net in nets:
+        net.free()
+    cfg = {"workload": "density-sweep n=4096 L=16 batch=1024 d=" + "/".join(f"{d:g}" for d in densities)
+                       + " (CSR sparse-W path; fp32 storage, fp64 accumulate)",
+           "n": 4096, "L": 16, "batch": 1024, "densities": densities}
+    return dict(value=value, ms_step=ms_step, edges=edges, sweep=sweep, crossover=crossover, roofline=roof,
+                config=cfg, probs=probs, densities=densities)
+
+
+def cpu_baseline(args, probs, densities):
+    """Oracle on the host cores: the first R samples of every density, all L layers."""
+    import oracle
+    from workloads import csr_rows
+
+    rows = args.cpu_rows
+    threads = oracle.default_threads()
+    edges = 0
+    t_total = 0.0
+    for d, p in zip(densities, probs):
+        y = csr_rows(p.y0_as_csr(), np.arange(rows))
+        t0 = time.perf_counter()
+        oracle.forward(p.n, p.layers, p.ymax, y, threads=threads)
+        t_total += time.perf_counter() - t0
+        edges += rows * sum(l.nnz for l in p.layers)
+    return {"value": edges / t_total, "unit": "edges/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {min(rows, probs[0].batch)} of {probs[0].batch} samples at each density, all {probs[0].L} layers "
+                      f"({t_total:.1f} s of CPU work)", "seconds": round(t_total, 2),
+            "cpu": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+# ----------------------------------------------------------------------------------- other workloads
+
+
+def run_csr_config(args, torch, sd):
+    """Configs 3-5 (sparse Y through the SpGEMM path) and config 1, one forward per step."""
+    from workloads import make_config
+
+    p = make_config(args.config)
+    net = sd.net_from_problem(p)
+    if p.y0_csr is not None:
+        y = tuple(torch.from_numpy(a).cuda() for a in p.y0_csr)
+        fn = lambda: net.forward_csr(*y)
+    else:
+        y = torch.from_numpy(p.y0_dense).cuda()
+        o = torch.empty_like(y)
+        fn = lambda: net.forward_dense(y, out=o)
+    for _ in range(args.warmup):
+        fn()
+    ms = time_calls(torch, fn, args.steps)
+    net.free()
+    cfg = {"workload": f"{p.name} n={p.n} L={p.L} batch={p.batch}", "n": p.n, "L": p.L, "batch": p.batch}
+    return dict(value=p.edges() / (ms / 1e3), ms_step=ms, config=cfg, roofline=None, sweep=None, crossover=None)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--densities", default="0.5,0.1,0.01,0.001")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense-W arm")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES bytes 5 times (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (batch rows would shard "
+              "across GPUs with no per-layer exchange; see the design notes). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1708_02937_amd as sd
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    if args.copy_probe:
+        src = torch.ones(args.copy_probe // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": args.copy_probe}), flush=True)
+        return
+    if args.config == 2:
+        r = run_sweep(args, torch, sd)
+    else:
+        r = run_csr_config(args, torch, sd)
+    out = {
+        "metric": METRIC, "value": r["value"], "unit": "edges/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(r["ms_step"], 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic", "config": r["config"],
+        "roofline": r["roofline"],
+    }
+    if r.get("sweep"):
+        out["sweep"] = r["sweep"]
+        out["crossover_density"] = r["crossover"]
+    if args.config == 2 and not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args, r["probs"], r["densities"])
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
