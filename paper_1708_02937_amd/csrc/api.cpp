@@ -44,6 +44,7 @@ struct Layer {
     Edge *w_pack = nullptr;    // fan-out entries packed as (column, weight)
     int64_t *fan_ptr = nullptr;  // fan-in CSR (W_k^T)
     Edge *fan = nullptr;
+    int32_t *tile_ptr = nullptr;  // where each fan-in list crosses each 128-input tile (high fan-in only)
     double *dense_wt = nullptr;  // n x n, W_k^T row-major in fp64, for the dense arm
 };
 
@@ -57,6 +58,7 @@ void release(Layer &l) {
     dfree(l.w_pack);
     dfree(l.fan_ptr);
     dfree(l.fan);
+    dfree(l.tile_ptr);
     dfree(l.dense_wt);
     l = Layer();
 }
@@ -249,6 +251,11 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
         return cleanup(fail(SDNN_ERR_UNSUPPORTED, msg));
     }
     SETUP_HIP(sdnn::launch_fanin_sort(n, max_fanin, nl.fan_ptr, nl.fan, s));
+    if (sdnn::spmm_wants_tiles(n, nnz)) {
+        if ((st = dalloc(&nl.tile_ptr, (size_t)n * (size_t)(sdnn::spmm_tile_count(n) + 1), "tile pointers")) != SDNN_OK)
+            return cleanup(st);
+        SETUP_HIP(sdnn::launch_spmm_tile_ptr(n, nl.fan_ptr, nl.fan, nl.tile_ptr, s));
+    }
     SETUP_HIP(hipStreamSynchronize(s));
 #undef SETUP_HIP
     cleanup(SDNN_OK);
@@ -323,7 +330,8 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
     for (int32_t k = k0; k < k1; ++k) {
         const Layer &l = net->layers[(size_t)k];
         if (arm == SDNN_ARM_SPARSE)
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.bias, net->ymax, buf[cur], buf[cur ^ 1], s));
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_ptr, l.bias, net->ymax, buf[cur],
+                                             buf[cur ^ 1], s));
         else
             SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, l.dense_wt, l.bias, net->ymax, buf[cur], buf[cur ^ 1], s));
         cur ^= 1;

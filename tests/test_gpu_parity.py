@@ -72,6 +72,19 @@ def test_tiny_dense_batch(sd, arm, seed, n, L, batch):
     parity.compare(p, dense_to_csr(out))
 
 
+@pytest.mark.parametrize("seed,n,L,batch,d", [(31, 1100, 2, 128, 0.97), (32, 1100, 2, 260, 0.95),
+                                              (33, 2000, 2, 1028, 0.6), (34, 1500, 1, 516, 0.75)])
+def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
+    """Average fan-in >= 1024 selects the LDS-tiled product; ragged n and batch exercise its edges."""
+    p = tiny_random(seed, n, L, batch, w_density=d, y_density=0.7, dense_input=True,
+                    ymax=[math.inf, 3.0][seed % 2], bias_lo=-1.0, bias_hi=1.0)
+    _say("high fan-in", seed, n, L, batch, d)
+    parity.compare(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE)))
+    q = integer_shadow(p)
+    q.y0_dense = np.where(p.y0_dense != 0, q.y0_dense if q.y0_dense is not None else 1, 0).astype(np.float32)
+    parity.compare(q, dense_to_csr(run_dense(sd, q, sd.SDNN_ARM_SPARSE)), exact=True)
+
+
 @pytest.mark.parametrize("seed,n,L,batch", TINY + [(9, 5000, 2, 17), (10, 17000, 2, 9), (11, 40000, 1, 5)])
 def test_tiny_csr_batch(sd, seed, n, L, batch):
     p = tiny_random(seed, n, L, batch, w_density=min(0.3, 8.0 / n + 0.001), y_density=0.3,
