@@ -41,6 +41,7 @@ struct Layer {
     const float *val = nullptr;
     const float *bias = nullptr;
     bool bias_nonpos = true;
+    int64_t pos_bias = 0;      // neurons with b_j > 0
     Edge *w_pack = nullptr;    // fan-out entries packed as (column, weight)
     int64_t *fan_ptr = nullptr;  // fan-in CSR (W_k^T)
     Edge *fan = nullptr;
@@ -194,11 +195,12 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     hipStream_t s = net->stream;
 
     // 1. validate on the device
-    SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
+    SDNN_HIP(hipMemsetAsync(net->d_flags, 0, 2 * sizeof(uint32_t), s));
     SDNN_HIP(sdnn::launch_validate_layer(n, nnz, row_ptr, col_idx, val, bias, net->d_flags, s));
-    uint32_t flags = 0;
-    SDNN_HIP(hipMemcpyAsync(&flags, net->d_flags, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    uint32_t fl[2] = {0, 0};
+    SDNN_HIP(hipMemcpyAsync(fl, net->d_flags, 2 * sizeof(uint32_t), hipMemcpyDeviceToHost, s));
     SDNN_HIP(hipStreamSynchronize(s));
+    const uint32_t flags = fl[0];
     if (flags & 1u)
         return fail(SDNN_ERR_INVALID_INDEX,
                     "W_k is not valid CSR (row_ptr monotone from 0 to nnz, columns in [0,n) strictly increasing)");
@@ -213,6 +215,7 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     nl.val = val;
     nl.bias = bias;
     nl.bias_nonpos = (flags & 4u) == 0;
+    nl.pos_bias = (int64_t)fl[1];
     int32_t *counts = nullptr;
     int64_t *tmp = nullptr;
     sdnn_status st = SDNN_OK;
@@ -376,8 +379,19 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     }
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
 
-    int cur = 0;
-    for (int32_t k = k0; k < k1; ++k) {
+    // Activation format per layer.  While outputs are sparse they stay as slot rows (row-wise SpGEMM).
+    // A layer whose bias is positive on at least a quarter of the neurons gives every such neuron
+    // h(b_j) > 0 in every sample that does not push it below zero, so its output is dense: from the
+    // first such layer on, activations are kept dense and neuron-major and each layer gathers over
+    // fan-in lists (the dense-Y product), and the result is packed back into rows at the end.
+    int32_t kd = k1;
+    for (int32_t k = k0; k < k1; ++k)
+        if (4 * net->layers[(size_t)k].pos_bias >= n) {
+            kd = k;
+            break;
+        }
+    int cur = 0;  // slot buffer that receives the next sparse layer's output
+    for (int32_t k = k0; k < kd; ++k) {
         const Layer &l = net->layers[(size_t)k];
         const bool first = k == k0;
         SDNN_HIP(sdnn::launch_spgemm_layer(n, batch, first ? y_row_ptr : nullptr, first ? nullptr : w.cnt[cur ^ 1],
@@ -386,10 +400,32 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
                                            w.val[cur], net->d_flags, s));
         cur ^= 1;
     }
-    const int last = cur ^ 1;  // buffer holding Y_{k1} in slots
+    int last, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
+    if (kd < k1) {
+        const bool from_user = kd == k0;
+        const int db = from_user ? 0 : cur;  // the input rows (if any) sit in buffer cur ^ 1
+        float *dense[2] = {reinterpret_cast<float *>(w.col[db]), w.val[db]};  // two n x batch fp32 buffers
+        SDNN_HIP(sdnn::launch_densify(n, batch, from_user ? y_row_ptr : nullptr, from_user ? nullptr : w.cnt[cur ^ 1],
+                                      from_user ? y_col : w.col[cur ^ 1], from_user ? y_val : w.val[cur ^ 1],
+                                      dense[0], net->d_flags, s));
+        int dc = 0;
+        for (int32_t k = kd; k < k1; ++k) {
+            const Layer &l = net->layers[(size_t)k];
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_ptr, l.bias, net->ymax, dense[dc],
+                                             dense[dc ^ 1], s));
+            dc ^= 1;
+        }
+        SDNN_HIP(sdnn::launch_transpose(dense[dc], dense[dc ^ 1], n, batch, s));  // -> batch x n
+        SDNN_HIP(sdnn::launch_dense_to_slots(n, batch, dense[dc ^ 1], w.cnt[db ^ 1], w.col[db ^ 1], w.val[db ^ 1], s));
+        last = db ^ 1;
+        outb = db;
+    } else {
+        last = cur ^ 1;
+        outb = cur;
+    }
     SDNN_HIP(sdnn::launch_exclusive_scan_i32_to_i64(batch, w.cnt[last], out_row_ptr, w.scan_tmp, s));
-    SDNN_HIP(sdnn::launch_compact_rows(n, batch, w.cnt[last], out_row_ptr, w.col[last], w.val[last], w.col[cur],
-                                       w.val[cur], s));
+    SDNN_HIP(sdnn::launch_compact_rows(n, batch, w.cnt[last], out_row_ptr, w.col[last], w.val[last], w.col[outb],
+                                       w.val[outb], s));
     int64_t nnz = 0;
     uint32_t flags = 0;
     SDNN_HIP(hipMemcpyAsync(&nnz, out_row_ptr + batch, sizeof(int64_t), hipMemcpyDeviceToHost, s));
@@ -397,8 +433,8 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     SDNN_HIP(hipStreamSynchronize(s));
     if (flags & 1u)
         return fail(SDNN_ERR_INVALID_INDEX, "Y_in is not valid CSR (row extents or column indices out of range)");
-    *out_col = w.col[cur];
-    *out_val = w.val[cur];
+    *out_col = w.col[outb];
+    *out_val = w.val[outb];
     *out_nnz = nnz;
     return SDNN_OK;
 }

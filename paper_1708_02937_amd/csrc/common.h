@@ -61,6 +61,10 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const Edge *w,
                                const float *bias, int bias_nonpos, double ymax, int32_t *out_cnt, int32_t *out_col,
                                float *out_val, uint32_t *err, hipStream_t s);
+hipError_t launch_densify(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
+                          const int32_t *in_col, const float *in_val, float *yt, uint32_t *err, hipStream_t s);
+hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,
+                                 float *out_val, hipStream_t s);
 hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, const int64_t *row_ptr,
                                const int32_t *in_col, const float *in_val, int32_t *out_col, float *out_val,
                                hipStream_t s);

@@ -38,7 +38,10 @@ __global__ void validate_layer_kernel(int64_t n, int64_t nnz, const int64_t *__r
     }
     const float bi = bias[i];
     if (!isfinite(bi)) f |= kFlagValue;
-    if (bi > 0.0f) f |= kFlagPosBias;
+    if (bi > 0.0f) {
+        f |= kFlagPosBias;
+        atomicAdd(&flags[1], 1u);  // number of neurons with a positive bias
+    }
     if (f) atomicOr(flags, f);
 }
 

@@ -141,6 +141,20 @@ def test_config2_dense_arm_sampled(sd, d):
     parity.compare(p, dense_to_csr(out[rows]), rows=rows)
 
 
+@pytest.mark.parametrize("sparse_layers", [0, 1, 2, 3])
+def test_csr_path_switches_to_dense_activations(sd, sparse_layers):
+    """Layers with mostly positive bias move the CSR path to dense activations; switch after 0..3 layers."""
+    p = tiny_random(40 + sparse_layers, 700, 4, 37, w_density=0.02, y_density=0.05, bias_lo=-0.2, bias_hi=0.0)
+    for k in range(sparse_layers, p.L):
+        p.layers[k].bias = np.full(p.n, 0.02, np.float32)
+    _say("format switch", sparse_layers)
+    parity.compare(p, run_csr(sd, p))
+    q = integer_shadow(p)
+    for k in range(sparse_layers, p.L):
+        q.layers[k].bias = np.ones(p.n, np.float32)
+    parity.compare(q, run_csr(sd, q), exact=True)
+
+
 def test_config3_scaled_full_compare(sd):
     p = make_config(3, n=4096, L=6, batch=300)
     _say("config 3 scaled")
@@ -159,6 +173,22 @@ def test_config4_scaled(sd):
     p = make_config(4, n=32768, L=6, batch=400)
     _say("config 4 scaled")
     parity.compare(p, run_csr(sd, p))
+
+
+def test_config4_full_size_sampled(sd):
+    p = make_config(4)
+    _say("config 4 full size")
+    rp, c, v = run_csr(sd, p)
+    rows = np.random.default_rng(3).choice(p.batch, 24, replace=False)
+    parity.compare(p, csr_rows((rp, c, v), rows), rows=rows)
+
+
+def test_config5_full_size_sampled(sd):
+    p = make_config(5)
+    _say("config 5 full size")
+    rp, c, v = run_csr(sd, p)
+    rows = np.random.default_rng(4).choice(p.batch, 6, replace=False)
+    parity.compare(p, csr_rows((rp, c, v), rows), rows=rows)
 
 
 def test_config5_scaled(sd):

@@ -144,13 +144,19 @@ def _bernoulli_positions(rng: np.random.Generator, total: int, p: float) -> np.n
 
 
 def _bernoulli_csr(rng, rows: int, cols: int, p: float):
-    pos = _bernoulli_positions(rng, rows * cols, p)
-    r = pos // cols
-    c = (pos - r * cols).astype(np.int32)
-    counts = np.bincount(r, minlength=rows).astype(np.int64)
+    """CSR pattern of a rows x cols Bernoulli(p) matrix, drawn in blocks of rows (about 4M trials each,
+    which keeps the temporaries small; a Bernoulli process restarted at block boundaries is still one)."""
+    block = max(1, min(rows, (1 << 22) // max(1, cols)))
+    cols_out, counts = [], np.zeros(rows, dtype=np.int64)
+    for r0 in range(0, rows, block):
+        nr = min(block, rows - r0)
+        pos = _bernoulli_positions(rng, nr * cols, p)
+        r = pos // cols
+        cols_out.append((pos - r * cols).astype(np.int32))
+        counts[r0:r0 + nr] = np.bincount(r, minlength=nr)
     row_ptr = np.zeros(rows + 1, dtype=np.int64)
     np.cumsum(counts, out=row_ptr[1:])
-    return row_ptr, c
+    return row_ptr, (np.concatenate(cols_out) if cols_out else np.zeros(0, np.int32))
 
 
 def _distinct_per_row(rng, rows: int, k: int, width: int) -> np.ndarray:
