@@ -45,7 +45,8 @@ struct Layer {
     Edge *w_pack = nullptr;    // fan-out entries packed as (column, weight)
     int64_t *fan_ptr = nullptr;  // fan-in CSR (W_k^T)
     Edge *fan = nullptr;
-    int32_t *tile_ptr = nullptr;  // where each fan-in list crosses each 128-input tile (high fan-in only)
+    int32_t *tile_ptr = nullptr;  // where each fan-in list crosses each input tile (high fan-in only)
+    int32_t *w_seg = nullptr;     // where each fan-out row crosses each accumulator window (wide layers only)
     double *dense_wt = nullptr;  // n x n, W_k^T row-major in fp64, for the dense arm
 };
 
@@ -60,6 +61,7 @@ void release(Layer &l) {
     dfree(l.fan_ptr);
     dfree(l.fan);
     dfree(l.tile_ptr);
+    dfree(l.w_seg);
     dfree(l.dense_wt);
     l = Layer();
 }
@@ -121,6 +123,8 @@ struct sdnn_net_s {
     std::vector<Layer> layers;
     uint32_t *d_flags = nullptr;
     int32_t *d_int = nullptr;
+    unsigned long long *d_work = nullptr;  // one work counter per layer of a forward call
+    int num_cu = 256;
 };
 
 extern "C" {
@@ -163,12 +167,15 @@ sdnn_status sdnn_net_create(sdnn_net *out, int64_t n, int32_t L, float ymax, voi
     net->ymax = (double)ymax;
     net->stream = (hipStream_t)stream;
     net->device = dev;
+    net->num_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
     net->layers.resize((size_t)L);
     sdnn_status st = dalloc(&net->d_flags, 4, "flags");
     if (st == SDNN_OK) st = dalloc(&net->d_int, 4, "scratch");
+    if (st == SDNN_OK) st = dalloc(&net->d_work, (size_t)(L > 0 ? L : 1), "work counters");
     if (st != SDNN_OK) {
         dfree(net->d_flags);
         dfree(net->d_int);
+        dfree(net->d_work);
         delete net;
         return st;
     }
@@ -254,6 +261,11 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
         return cleanup(fail(SDNN_ERR_UNSUPPORTED, msg));
     }
     SETUP_HIP(sdnn::launch_fanin_sort(n, max_fanin, nl.fan_ptr, nl.fan, s));
+    if (sdnn::spgemm_wants_window_index(n)) {
+        if ((st = dalloc(&nl.w_seg, (size_t)n * (size_t)(sdnn::spgemm_windows(n) + 1), "window offsets")) != SDNN_OK)
+            return cleanup(st);
+        SETUP_HIP(sdnn::launch_window_seg(n, row_ptr, col_idx, nl.w_seg, s));
+    }
     if (sdnn::spmm_wants_tiles(n, nnz)) {
         if ((st = dalloc(&nl.tile_ptr, (size_t)n * (size_t)(sdnn::spmm_tile_count(n) + 1), "tile pointers")) != SDNN_OK)
             return cleanup(st);
@@ -378,6 +390,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         return SDNN_OK;
     }
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
+    SDNN_HIP(hipMemsetAsync(net->d_work, 0, (size_t)(k1 - k0) * sizeof(unsigned long long), s));
 
     // Activation format per layer.  While outputs are sparse they stay as slot rows (row-wise SpGEMM).
     // A layer whose bias is positive on at least a quarter of the neurons gives every such neuron
@@ -396,8 +409,9 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         const bool first = k == k0;
         SDNN_HIP(sdnn::launch_spgemm_layer(n, batch, first ? y_row_ptr : nullptr, first ? nullptr : w.cnt[cur ^ 1],
                                            first ? y_col : w.col[cur ^ 1], first ? y_val : w.val[cur ^ 1], l.row_ptr,
-                                           l.w_pack, l.bias, l.bias_nonpos ? 1 : 0, net->ymax, w.cnt[cur], w.col[cur],
-                                           w.val[cur], net->d_flags, s));
+                                           l.w_seg, l.w_pack, l.nnz, l.bias, l.bias_nonpos ? 1 : 0, net->ymax,
+                                           w.cnt[cur], w.col[cur], w.val[cur], net->d_flags, net->d_work + (k - k0),
+                                           net->num_cu, s));
         cur ^= 1;
     }
     int last, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
@@ -446,6 +460,7 @@ sdnn_status sdnn_net_free(sdnn_net net) {
     for (Layer &l : net->layers) release(l);
     dfree(net->d_flags);
     dfree(net->d_int);
+    dfree(net->d_work);
     delete net;
     return SDNN_OK;
 }

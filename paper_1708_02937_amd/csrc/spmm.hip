@@ -8,9 +8,9 @@
 // accumulators from a coalesced load of row i of Y^T.  The epilogue adds b_j, applies h and rounds once
 // to fp32 (the element-wise max.+ steps of Fig. 4, fused so Y_k W_k never reaches memory).
 //
-// XCD-aware launch: workgroups are dealt round-robin to the 8 XCDs, so the batch chunk is taken from
-// blockIdx % chunks; with 8 chunks every XCD touches only its own n x 64V slice of Y^T, which stays in
-// that XCD's L2 while all output neurons gather from it.
+// XCD-aware launch: workgroups are dealt round-robin to the 8 XCDs, so the batch chunk follows from
+// blockIdx % 8.  Each XCD owns every eighth chunk and works through its chunks one at a time, so the
+// rows of Y^T that its current output neurons gather stay in that XCD's L2.
 #include "common.h"
 
 namespace sdnn {
@@ -75,8 +75,19 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
                                                          float *__restrict__ zt) {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int64_t c = blockIdx.x % chunks;
-    const int64_t j = (int64_t)(blockIdx.x / chunks) * 4 + wave;
+    int64_t c, g;
+    if (chunks % 8 == 0) {
+        // chunk-major per XCD: XCD x works through chunks x, x+8, ... one at a time, every neuron group
+        // of a chunk before the next, so the input rows its current neurons gather stay in its L2
+        const int64_t groups = (n + 3) / 4;
+        const int64_t local = blockIdx.x / 8;
+        c = (blockIdx.x % 8) + 8 * (local / groups);
+        g = local % groups;
+    } else {
+        c = blockIdx.x % chunks;
+        g = blockIdx.x / chunks;
+    }
+    const int64_t j = g * 4 + wave;
     if (j >= n) return;
     const int64_t col = c * (64 * V) + (int64_t)lane * V;
     const bool active = col < batch;       // batch is a multiple of V, so col < batch => col + V <= batch
