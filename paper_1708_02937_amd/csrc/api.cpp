@@ -47,7 +47,7 @@ struct Layer {
     Edge *fan = nullptr;
     int32_t *tile_ptr = nullptr;  // where each fan-in list crosses each input tile (high fan-in only)
     int32_t *w_seg = nullptr;     // where each fan-out row crosses each accumulator window (wide layers only)
-    double *dense_wt = nullptr;  // n x n, W_k^T row-major in fp64, for the dense arm
+    double *dense_wt = nullptr;  // n x n, W_k row-major in fp64 (zeros explicit), for the dense arm
 };
 
 template <typename T>
