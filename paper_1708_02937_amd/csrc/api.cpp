@@ -45,7 +45,7 @@ struct Layer {
     Edge *w_pack = nullptr;    // fan-out entries packed as (column, weight)
     int64_t *fan_ptr = nullptr;  // fan-in CSR (W_k^T)
     Edge *fan = nullptr;
-    int32_t *tile_ptr = nullptr;  // where each fan-in list crosses each input tile (high fan-in only)
+    uint16_t *tile_mask = nullptr;  // which rows of each 16-row input tile each fan-in list holds (high fan-in only)
     int32_t *w_seg = nullptr;     // where each fan-out row crosses each accumulator window (wide layers only)
     double *dense_wt = nullptr;  // n x n, W_k row-major in fp64 (zeros explicit), for the dense arm
 };
@@ -60,7 +60,7 @@ void release(Layer &l) {
     dfree(l.w_pack);
     dfree(l.fan_ptr);
     dfree(l.fan);
-    dfree(l.tile_ptr);
+    dfree(l.tile_mask);
     dfree(l.w_seg);
     dfree(l.dense_wt);
     l = Layer();
@@ -267,9 +267,9 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
         SETUP_HIP(sdnn::launch_window_seg(n, row_ptr, col_idx, nl.w_seg, s));
     }
     if (sdnn::spmm_wants_tiles(n, nnz)) {
-        if ((st = dalloc(&nl.tile_ptr, (size_t)n * (size_t)(sdnn::spmm_tile_count(n) + 1), "tile pointers")) != SDNN_OK)
+        if ((st = dalloc(&nl.tile_mask, sdnn::spmm_tile_mask_elems(n), "tile masks")) != SDNN_OK)
             return cleanup(st);
-        SETUP_HIP(sdnn::launch_spmm_tile_ptr(n, nl.fan_ptr, nl.fan, nl.tile_ptr, s));
+        SETUP_HIP(sdnn::launch_spmm_tile_mask(n, nl.fan_ptr, nl.fan, nl.tile_mask, s));
     }
     SETUP_HIP(hipStreamSynchronize(s));
 #undef SETUP_HIP
@@ -345,7 +345,7 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
     for (int32_t k = k0; k < k1; ++k) {
         const Layer &l = net->layers[(size_t)k];
         if (arm == SDNN_ARM_SPARSE)
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_ptr, l.bias, net->ymax, buf[cur],
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax, buf[cur],
                                              buf[cur ^ 1], s));
         else
             SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, l.dense_wt, l.bias, net->ymax, buf[cur], buf[cur ^ 1], s));
@@ -425,7 +425,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         int dc = 0;
         for (int32_t k = kd; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_ptr, l.bias, net->ymax, dense[dc],
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax, dense[dc],
                                              dense[dc ^ 1], s));
             dc ^= 1;
         }

@@ -44,10 +44,12 @@ hipError_t launch_pack_edges(int64_t nnz, const int32_t *col, const float *val, 
 // spmm.hip
 hipError_t launch_transpose(const float *in, float *out, int64_t rows, int64_t cols, hipStream_t s);
 int spmm_tile_count(int64_t n);
+size_t spmm_tile_mask_elems(int64_t n);
 bool spmm_wants_tiles(int64_t n, int64_t nnz);
-hipError_t launch_spmm_tile_ptr(int64_t n, const int64_t *fan_ptr, const Edge *fan, int32_t *tile_ptr, hipStream_t s);
+hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *fan, uint16_t *tile_mask,
+                                 hipStream_t s);
 hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
-                             const int32_t *tile_ptr, const float *bias, double ymax, const float *yt, float *zt,
+                             const uint16_t *tile_mask, const float *bias, double ymax, const float *yt, float *zt,
                              hipStream_t s);
 
 // gemm.hip

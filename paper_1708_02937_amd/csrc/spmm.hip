@@ -138,49 +138,55 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
     store_v<V>(zt + j * batch + col, out);
 }
 
-// High fan-in variant: the same product with the gathered rows of Y^T served from LDS.
+// High fan-in variant: the same product with the gathered rows of Y^T served from LDS and each row read once
+// per wave for all of the wave's neurons that use it.
 //
-// A workgroup (4 wave64s) owns 32 output neurons (8 per wave) and a chunk of 256 batch columns.  Input
-// neurons are walked in tiles of 16 rows.  For every tile the workgroup stages the 16 x 256 slab of Y^T
-// in LDS, widened to fp64 once at staging (32 KiB), the tile's segment of each of its 32 fan-in lists
-// (tile_ptr says where each list crosses each tile boundary) and the segment lengths.  Everything is
-// double-buffered: the global loads for tile t+1 are issued before tile t is multiplied and written to
-// the other buffer afterwards, so the multiply reads only LDS.  Each list entry is read by the whole
-// wave from one LDS address (a broadcast).  Lane l owns batch columns {2l, 2l+1} and {128+2l, 128+2l+1}
-// of the chunk, so each of its two ds_read_b128 per entry is one contiguous 1 KiB across the wave (no
-// bank conflicts) and feeds the fp64 FMAs directly, with no conversion per product.  A slab row is loaded
-// from memory once per 32 neurons instead of once per list entry; two workgroups share a CU.
-constexpr int kTileRows = 16;           // input neurons per LDS tile (<= 64: a tile segment fits one load)
-constexpr int kTiledCB = 256;           // batch columns per workgroup (4 per lane)
-constexpr int kTiledThreads = 256;
-constexpr int kTiledNPW = 8;            // output neurons per wave
+// A workgroup (8 wave64s) owns 32 output neurons (4 per wave) and a chunk of 256 batch columns; lane l owns
+// columns 4l..4l+3 of the chunk.  Input neurons are walked in tiles of 16 rows.  For every tile the
+// workgroup stages the 16 x 256 slab of Y^T in LDS, widened to fp64 once (32 KiB, laid out so that both the
+// staging stores and the reads are contiguous per wave); the next tile's slab is loaded into registers
+// while the current one is multiplied.  A 16-bit mask per (tile, neuron), built at set-up, says which
+// rows of the tile a fan-in list holds.  Each wave walks the 16 rows in order: it reads a row once (two
+// ds_read_b128 per lane, at immediate offsets) and, for each of its 4 neurons whose mask has that row
+// (a wave-uniform branch), takes the next list weight from the lane that loaded it (readlane) and does
+// four fp64 FMAs.  Lists are sorted by input index, so every output is still summed in ascending input
+// order.  At 50% density a row read feeds two list entries instead of one, which halves the LDS traffic
+// per FMA, and the per-entry address arithmetic of a list walk disappears.
+constexpr int kTileRows = 16;                       // input neurons per LDS tile (one mask bit each)
+constexpr int kTiledCB = 256;                       // batch columns per workgroup (4 per lane)
+constexpr int kTiledThreads = 512;
+constexpr int kTiledNPW = 4;                        // output neurons per wave
 constexpr int kTiledNJ = (kTiledThreads / 64) * kTiledNPW;
-constexpr int kRowF4 = kTiledCB / 4;                          // float4 per slab row (global side)
-constexpr int kRowD2 = kTiledCB / 2;                          // double2 per slab row (LDS side)
-constexpr int kStageF4 = kTileRows * kRowF4 / kTiledThreads;  // float4 staged per thread per tile
+constexpr int kRowF4 = kTiledCB / 4;                // float4 per slab row (global side)
+constexpr int kRowD2 = kTiledCB / 2;                // double2 per slab row (LDS side)
+constexpr int kStageF4 = kTileRows * kRowF4 / kTiledThreads;
+constexpr int kRowGroup = 2;                        // slab rows read ahead of their FMAs
 
-__global__ __launch_bounds__(kTiledThreads, 2) void spmm_tiled_kernel(
-    int64_t n, int64_t batch, int chunks, int ntiles, const int32_t *__restrict__ tile_ptr,
-    const Edge *__restrict__ fan, const float *__restrict__ bias, double ymax, const float *__restrict__ yt,
-    float *__restrict__ zt) {
-    __shared__ double2 slab[2][kTileRows * kRowD2];
-    __shared__ Edge ents[2][kTiledNJ][kTileRows];
-    __shared__ int32_t cnts[2][kTiledNJ];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: keeps list addresses scalar
-    const int64_t c = blockIdx.x % chunks;
-    const int64_t jw = (int64_t)(blockIdx.x / chunks) * kTiledNJ + wave * kTiledNPW;  // first neuron of the wave
+__global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
+    int64_t n, int64_t batch, int chunks, int ntiles, const int64_t *__restrict__ fan_ptr,
+    const uint16_t *__restrict__ tile_mask, const Edge *__restrict__ fan, const float *__restrict__ bias,
+    double ymax, const float *__restrict__ yt, float *__restrict__ zt) {
+    __shared__ double2 slab[kTileRows * kRowD2];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: masks and positions stay scalar
+    // XCD-aware order: workgroups are dealt round-robin to the 8 XCDs, and the batch chunks of one neuron
+    // group take consecutive slots of the same XCD, so they run together and read its fan-in lists from HBM
+    // once (the group count is padded to a multiple of 8)
+    const int64_t local = blockIdx.x / 8;
+    const int64_t c = local % chunks;
+    const int64_t g = (local / chunks) * 8 + blockIdx.x % 8;
+    if (g * kTiledNJ >= n) return;  // padding group: the whole workgroup leaves before any barrier
+    const int64_t jw = g * kTiledNJ + wave * kTiledNPW;  // first neuron of the wave
     const int64_t col0 = c * kTiledCB;
+    const int64_t pitch = (n + 3) & ~3ll;  // mask row pitch: keeps the 64-bit mask loads 8-byte aligned
 
-    double acc[kTiledNPW][4];  // columns 2l, 2l+1, 128+2l, 128+2l+1 of the chunk
+    double acc[kTiledNPW][4];
 #pragma unroll
     for (int q = 0; q < kTiledNPW; ++q)
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc[q][v] = 0.0;
 
     float4 st[kStageF4];
-    Edge eg[kTiledNPW];
     auto load_slab = [&](int t) {
         const int64_t i0 = (int64_t)t * kTileRows;
 #pragma unroll
@@ -191,134 +197,118 @@ __global__ __launch_bounds__(kTiledThreads, 2) void spmm_tiled_kernel(
                                            : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     };
-    // segment [b[q], e[q]) of neuron jw + q for one tile; uniform per wave, so these are scalar loads
-    auto load_bounds = [&](int t, int32_t (&b)[kTiledNPW], int32_t (&e)[kTiledNPW]) {
-        const int32_t *tp0 = tile_ptr + (int64_t)t * n + jw;
-        const int32_t *tp1 = tp0 + n;
-#pragma unroll
-        for (int q = 0; q < kTiledNPW; ++q) {
-            const bool ok = jw + q < n;
-            b[q] = ok ? tp0[q] : 0;
-            e[q] = ok ? tp1[q] : 0;
-        }
-    };
-    auto load_entries = [&](const int32_t (&b)[kTiledNPW], const int32_t (&e)[kTiledNPW]) {
-#pragma unroll
-        for (int q = 0; q < kTiledNPW; ++q) {
-            eg[q].idx = 0;
-            eg[q].w = 0.0f;
-            if (lane < e[q] - b[q]) eg[q] = fan[b[q] + lane];
-        }
-    };
-    auto stage = [&](int buf, const int32_t (&b)[kTiledNPW], const int32_t (&e)[kTiledNPW]) {
+    auto stage = [&]() {
+        // float4 q covers columns 4m..4m+3 of row q / 64 (m = q % 64): its two halves go to double2 slots m and
+        // 64 + m of the row, so each store instruction writes 1 KiB contiguous
 #pragma unroll
         for (int s = 0; s < kStageF4; ++s) {
-            const int q = s * kTiledThreads + tid;  // row q / kRowF4, columns 4 (q % kRowF4) .. +3
-            slab[buf][2 * q] = make_double2((double)st[s].x, (double)st[s].y);
-            slab[buf][2 * q + 1] = make_double2((double)st[s].z, (double)st[s].w);
+            const int q = s * kTiledThreads + tid;
+            const int row = q / kRowF4, m = q % kRowF4;
+            slab[row * kRowD2 + m] = make_double2((double)st[s].x, (double)st[s].y);
+            slab[row * kRowD2 + 64 + m] = make_double2((double)st[s].z, (double)st[s].w);
         }
-        if (lane < kTileRows) {
+    };
+    // the 4 neurons' masks of tile t as one 64-bit scalar load; neurons past n read the zeroed padding
+    auto load_mask = [&](int t) -> uint64_t {
+        return jw < n ? *reinterpret_cast<const uint64_t *>(tile_mask + (int64_t)t * pitch + jw) : 0ull;
+    };
+    int64_t pos[kTiledNPW];  // next unread entry of each list
 #pragma unroll
-            for (int q = 0; q < kTiledNPW; ++q) ents[buf][wave * kTiledNPW + q][lane] = eg[q];
-        }
-        if (lane == 0) {
+    for (int q = 0; q < kTiledNPW; ++q) pos[q] = jw + q < n ? fan_ptr[jw + q] : 0;
+    float wn[kTiledNPW], wv[kTiledNPW];  // lane u holds the weight of the u-th list entry in the tile
+    auto load_weights = [&](uint64_t mk) {
 #pragma unroll
-            for (int q = 0; q < kTiledNPW; ++q) cnts[buf][wave * kTiledNPW + q] = e[q] - b[q];
+        for (int q = 0; q < kTiledNPW; ++q) {
+            const int cnt = __builtin_popcount((uint32_t)(mk >> (16 * q)) & 0xffffu);
+            wn[q] = lane < cnt ? fan[pos[q] + lane].w : 0.0f;
+            pos[q] += cnt;
         }
     };
 
-    int32_t b_nxt[kTiledNPW], e_nxt[kTiledNPW], b_nn[kTiledNPW], e_nn[kTiledNPW];
-    load_bounds(0, b_nxt, e_nxt);
+    uint64_t mk_cur = load_mask(0), mk_nxt = ntiles > 1 ? load_mask(1) : 0ull;
     load_slab(0);
-    load_entries(b_nxt, e_nxt);
-    stage(0, b_nxt, e_nxt);
-    if (ntiles > 1) load_bounds(1, b_nxt, e_nxt);
+    load_weights(mk_cur);
+    stage();
     __syncthreads();
-
+    const double2 *sl = slab + lane;
     for (int t = 0; t < ntiles; ++t) {
-        const int cur = t & 1;
         const bool more = t + 1 < ntiles;
+#pragma unroll
+        for (int q = 0; q < kTiledNPW; ++q) wv[q] = wn[q];
+        const uint64_t mk = mk_cur;
         if (more) {
             load_slab(t + 1);
-            load_entries(b_nxt, e_nxt);
-            if (t + 2 < ntiles) load_bounds(t + 2, b_nn, e_nn);
+            load_weights(mk_nxt);
+            mk_cur = mk_nxt;
+            if (t + 2 < ntiles) mk_nxt = load_mask(t + 2);
         }
-        const int32_t i0 = t * kTileRows;
-        const double2 *sl = slab[cur] + lane;
+        uint32_t m32[kTiledNPW];
+        int kq[kTiledNPW];
 #pragma unroll
         for (int q = 0; q < kTiledNPW; ++q) {
-            // entries are read from LDS at a wave-uniform address (a broadcast), straight into VGPRs
-            const int nq = wave * kTiledNPW + q;
-            const int cnt = cnts[cur][nq];
-            const Edge *el = ents[cur][nq];
-            int u = 0;
-            for (; u + 4 <= cnt; u += 4) {
-                double2 ya[4], yb[4];
-                double w[4];
+            m32[q] = __builtin_amdgcn_readfirstlane((uint32_t)(mk >> (16 * q)) & 0xffffu);
+            kq[q] = 0;
+        }
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const Edge ed = el[u + k];
-                    const int r = (ed.idx - i0) * kRowD2;
-                    w[k] = (double)ed.w;
-                    ya[k] = sl[r];
-                    yb[k] = sl[r + 64];
-                }
+        for (int g = 0; g < kTileRows; g += kRowGroup) {
+            double2 ya[kRowGroup], yb[kRowGroup];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    acc[q][0] = __builtin_fma(ya[k].x, w[k], acc[q][0]);
-                    acc[q][1] = __builtin_fma(ya[k].y, w[k], acc[q][1]);
-                    acc[q][2] = __builtin_fma(yb[k].x, w[k], acc[q][2]);
-                    acc[q][3] = __builtin_fma(yb[k].y, w[k], acc[q][3]);
-                }
+            for (int k = 0; k < kRowGroup; ++k) {
+                ya[k] = sl[(g + k) * kRowD2];
+                yb[k] = sl[(g + k) * kRowD2 + 64];
             }
-            for (; u < cnt; ++u) {
-                const Edge ed = el[u];
-                const int r = (ed.idx - i0) * kRowD2;
-                const double w = (double)ed.w;
-                const double2 ya = sl[r], yb = sl[r + 64];
-                acc[q][0] = __builtin_fma(ya.x, w, acc[q][0]);
-                acc[q][1] = __builtin_fma(ya.y, w, acc[q][1]);
-                acc[q][2] = __builtin_fma(yb.x, w, acc[q][2]);
-                acc[q][3] = __builtin_fma(yb.y, w, acc[q][3]);
+#pragma unroll
+            for (int k = 0; k < kRowGroup; ++k) {
+#pragma unroll
+                for (int q = 0; q < kTiledNPW; ++q) {
+                    if ((m32[q] >> (g + k)) & 1u) {
+                        const double w = (double)__int_as_float(__builtin_amdgcn_readlane(__float_as_int(wv[q]), kq[q]));
+                        ++kq[q];
+                        acc[q][0] = __builtin_fma(ya[k].x, w, acc[q][0]);
+                        acc[q][1] = __builtin_fma(ya[k].y, w, acc[q][1]);
+                        acc[q][2] = __builtin_fma(yb[k].x, w, acc[q][2]);
+                        acc[q][3] = __builtin_fma(yb[k].y, w, acc[q][3]);
+                    }
+                }
             }
         }
-        if (more) {
-            stage(cur ^ 1, b_nxt, e_nxt);  // that buffer was last read in tile t-1, which ended with a barrier
-#pragma unroll
-            for (int q = 0; q < kTiledNPW; ++q) {
-                b_nxt[q] = b_nn[q];
-                e_nxt[q] = e_nn[q];
-            }
-        }
+        __syncthreads();  // every wave is done with this slab
+        if (more) stage();
         __syncthreads();
     }
-    const int64_t ca = col0 + 2 * lane, cb = ca + 128;  // batch is a multiple of 4, so pairs never straddle it
+    const int64_t ca = col0 + 4 * lane;  // batch is a multiple of 4, so ca < batch => ca + 3 < batch
 #pragma unroll
     for (int q = 0; q < kTiledNPW; ++q) {
         const int64_t j = jw + q;
         if (j >= n) break;
         const double bj = (double)bias[j];
         if (ca < batch)
-            *reinterpret_cast<float2 *>(zt + j * batch + ca) =
-                make_float2(activate(acc[q][0] + bj, ymax), activate(acc[q][1] + bj, ymax));
-        if (cb < batch)
-            *reinterpret_cast<float2 *>(zt + j * batch + cb) =
-                make_float2(activate(acc[q][2] + bj, ymax), activate(acc[q][3] + bj, ymax));
+            *reinterpret_cast<float4 *>(zt + j * batch + ca) =
+                make_float4(activate(acc[q][0] + bj, ymax), activate(acc[q][1] + bj, ymax),
+                            activate(acc[q][2] + bj, ymax), activate(acc[q][3] + bj, ymax));
     }
 }
 
-// tile_ptr[t * n + j] = first position of fan-in list j whose input index is >= t * kTileRows.
-__global__ void tile_ptr_kernel(int64_t n, int ntiles, const int64_t *__restrict__ fan_ptr,
-                                const Edge *__restrict__ fan, int32_t *__restrict__ tile_ptr) {
+// tile_mask[t * pitch + j] bit r = list j holds input neuron t * 16 + r (lists are sorted by input index);
+// pitch = n rounded up to a multiple of 4, the padding stays zero.
+__global__ void tile_mask_kernel(int64_t n, const int64_t *__restrict__ fan_ptr, const Edge *__restrict__ fan,
+                                 uint16_t *__restrict__ tile_mask) {
     const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (j >= n) return;
-    int64_t e = fan_ptr[j];
-    const int64_t end = fan_ptr[j + 1];
-    for (int t = 0; t <= ntiles; ++t) {
-        const int64_t bound = (int64_t)t * kTileRows;
-        while (e < end && fan[e].idx < bound) ++e;
-        tile_ptr[(int64_t)t * n + j] = (int32_t)e;
+    const int64_t pitch = (n + 3) & ~3ll;
+    int64_t t_cur = -1;
+    uint32_t m = 0;
+    for (int64_t e = fan_ptr[j]; e < fan_ptr[j + 1]; ++e) {
+        const int64_t i = fan[e].idx;
+        const int64_t t = i / kTileRows;
+        if (t != t_cur) {
+            if (t_cur >= 0) tile_mask[t_cur * pitch + j] = (uint16_t)m;
+            t_cur = t;
+            m = 0;
+        }
+        m |= 1u << (i % kTileRows);
     }
+    if (t_cur >= 0) tile_mask[t_cur * pitch + j] = (uint16_t)m;
 }
 
 // 64 x 64 tile transpose through LDS (padded against bank conflicts): out (cols x rows) = in^T.
@@ -350,24 +340,32 @@ hipError_t launch_transpose(const float *in, float *out, int64_t rows, int64_t c
 
 int spmm_tile_count(int64_t n) { return (int)((n + kTileRows - 1) / kTileRows); }
 
-// Measured on MI355X (n = 4096, batch = 1024): the LDS-tiled product wins at 50% density (1.34 vs 1.85 ms
-// per layer), the L2 gather wins at 10% (0.38 vs 0.78 ms); switch at an average fan-in of 1024.
+size_t spmm_tile_mask_elems(int64_t n) { return (size_t)spmm_tile_count(n) * (size_t)((n + 3) & ~3ll); }
+
+// Measured on MI355X (n = 4096, batch = 1024): the LDS-tiled product wins at 50% density (0.82 vs 1.85 ms
+// per layer) and 30% (0.67 ms), the L2 gather wins at 10% (0.38 vs 0.63 ms); switch at an average fan-in
+// of 1024.
 bool spmm_wants_tiles(int64_t n, int64_t nnz) { return n <= 65536 && nnz >= 1024 * n; }
 
-hipError_t launch_spmm_tile_ptr(int64_t n, const int64_t *fan_ptr, const Edge *fan, int32_t *tile_ptr, hipStream_t s) {
-    tile_ptr_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(n, spmm_tile_count(n), fan_ptr, fan, tile_ptr);
+hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *fan, uint16_t *tile_mask,
+                                 hipStream_t s) {
+    hipError_t e = hipMemsetAsync(tile_mask, 0, spmm_tile_mask_elems(n) * sizeof(uint16_t), s);
+    if (e != hipSuccess) return e;
+    tile_mask_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(n, fan_ptr, fan, tile_mask);
     return hipGetLastError();
 }
 
 hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
-                             const int32_t *tile_ptr, const float *bias, double ymax, const float *yt, float *zt,
+                             const uint16_t *tile_mask, const float *bias, double ymax, const float *yt, float *zt,
                              hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
-    if (tile_ptr && batch % 4 == 0 && batch >= 128) {
+    if (tile_mask && batch % 4 == 0 && batch >= 128) {
         const int64_t chunks = (batch + kTiledCB - 1) / kTiledCB;
-        const int64_t blocks = ((n + kTiledNJ - 1) / kTiledNJ) * chunks;
+        const int64_t groups = (n + kTiledNJ - 1) / kTiledNJ;
+        const int64_t blocks = (groups + 7) / 8 * 8 * chunks;
+        if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
         spmm_tiled_kernel<<<(unsigned)blocks, kTiledThreads, 0, s>>>(n, batch, (int)chunks, spmm_tile_count(n),
-                                                                     tile_ptr, fan, bias, ymax, yt, zt);
+                                                                     fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
         return hipGetLastError();
     }
     // Columns per lane: wide enough to keep 8 independent loads in flight, and a multiple that divides batch.

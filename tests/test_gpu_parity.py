@@ -73,9 +73,11 @@ def test_tiny_dense_batch(sd, arm, seed, n, L, batch):
 
 
 @pytest.mark.parametrize("seed,n,L,batch,d", [(31, 1100, 2, 128, 0.97), (32, 1100, 2, 260, 0.95),
-                                              (33, 2000, 2, 1028, 0.6), (34, 1500, 1, 516, 0.75)])
+                                              (33, 2000, 2, 1028, 0.6), (34, 1500, 1, 516, 0.75),
+                                              (35, 1030, 2, 132, 0.999), (36, 1283, 1, 388, 0.9)])
 def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
-    """Average fan-in >= 1024 selects the LDS-tiled product; ragged n and batch exercise its edges."""
+    """Average fan-in >= 1024 selects the LDS-tiled product; ragged n (not a multiple of 4, 16 or 32) and
+    batch exercise its edges."""
     p = tiny_random(seed, n, L, batch, w_density=d, y_density=0.7, dense_input=True,
                     ymax=[math.inf, 3.0][seed % 2], bias_lo=-1.0, bias_hi=1.0)
     _say("high fan-in", seed, n, L, batch, d)
