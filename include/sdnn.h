@@ -133,11 +133,15 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
  * device addresses) point into ws and stay valid until ws is reused; *out_nnz
  * (host) receives nnz(Y_{k1}).  ws is device memory of at least
  * sdnn_workspace_size(net, batch, 1) bytes.  Synchronises the net's stream
- * once, at the end, to read the nnz.  Internally, activations stay as sparse
- * rows (row-wise SpGEMM) until the first layer whose bias is positive on at
- * least a quarter of the neurons (its output is then mostly nonzero); from that
- * layer on they are kept dense and neuron-major inside ws and packed back into
- * CSR after the last layer.  The result is the same either way.
+ * at the end, to read the nnz, and at the activation-format decisions below.
+ * Internally, activations stay as sparse rows (row-wise SpGEMM) until the
+ * first layer whose input holds at least batch * n / 8 entries or whose bias
+ * is positive on at least a quarter of the neurons (its output is then mostly
+ * nonzero); from that layer on they are kept dense and neuron-major inside ws
+ * and packed back into CSR after the last layer.  The host tracks an upper
+ * bound of each layer's input size and reads the exact count (one stream
+ * synchronisation) only when the bound reaches the threshold, always for the
+ * first layer.  The result is the same either way.
  * Errors: INVALID_OBJECT, NULL_POINTER, DIMENSION_MISMATCH, INVALID_INDEX, WORKSPACE_TOO_SMALL, DEVICE.
  */
 sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const int64_t *y_row_ptr,

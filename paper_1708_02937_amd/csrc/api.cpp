@@ -3,6 +3,7 @@
 // layer's work enqueued on the net's HIP stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -42,6 +43,7 @@ struct Layer {
     const float *bias = nullptr;
     bool bias_nonpos = true;
     int64_t pos_bias = 0;      // neurons with b_j > 0
+    int32_t max_fanout = 0;    // longest fan-out row of W_k
     Edge *w_pack = nullptr;    // fan-out entries packed as (column, weight)
     int64_t *fan_ptr = nullptr;  // fan-in CSR (W_k^T)
     Edge *fan = nullptr;
@@ -87,6 +89,7 @@ struct CsrWs {
     int32_t *cnt[2];
     int32_t *col[2];
     float *val[2];
+    int32_t *lists;  // 2 * batch: the small and large sample lists of the layer being computed
     int64_t *scan_tmp;
     size_t bytes;
 };
@@ -104,6 +107,8 @@ CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
         w.val[b] = (float *)(p + off);
         off = align_up(off + slots * sizeof(float));
     }
+    w.lists = (int32_t *)(p + off);
+    off = align_up(off + 2 * (size_t)batch * sizeof(int32_t));
     w.scan_tmp = (int64_t *)(p + off);
     off = align_up(off + (size_t)sdnn::scan_tmp_elems(batch) * sizeof(int64_t));
     w.bytes = off;
@@ -123,7 +128,7 @@ struct sdnn_net_s {
     std::vector<Layer> layers;
     uint32_t *d_flags = nullptr;
     int32_t *d_int = nullptr;
-    unsigned long long *d_work = nullptr;  // one work counter per layer of a forward call
+    unsigned long long *d_stats = nullptr;  // 4 counters per layer of a forward call (see launch_spgemm_layer)
     int num_cu = 256;
 };
 
@@ -171,11 +176,11 @@ sdnn_status sdnn_net_create(sdnn_net *out, int64_t n, int32_t L, float ymax, voi
     net->layers.resize((size_t)L);
     sdnn_status st = dalloc(&net->d_flags, 4, "flags");
     if (st == SDNN_OK) st = dalloc(&net->d_int, 4, "scratch");
-    if (st == SDNN_OK) st = dalloc(&net->d_work, (size_t)(L > 0 ? L : 1), "work counters");
+    if (st == SDNN_OK) st = dalloc(&net->d_stats, (size_t)(L > 0 ? L : 1) * 4, "layer counters");
     if (st != SDNN_OK) {
         dfree(net->d_flags);
         dfree(net->d_int);
-        dfree(net->d_work);
+        dfree(net->d_stats);
         delete net;
         return st;
     }
@@ -250,11 +255,14 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     SETUP_HIP(sdnn::launch_exclusive_scan_i32_to_i64(n, counts, nl.fan_ptr, tmp, s));
     SETUP_HIP(hipMemsetAsync(counts, 0, (size_t)n * sizeof(int32_t), s));
     SETUP_HIP(sdnn::launch_fanin_scatter(n, row_ptr, col_idx, val, nl.fan_ptr, counts, nl.fan, s));
-    SETUP_HIP(hipMemsetAsync(net->d_int, 0, sizeof(int32_t), s));
+    SETUP_HIP(hipMemsetAsync(net->d_int, 0, 2 * sizeof(int32_t), s));
     SETUP_HIP(sdnn::launch_max_segment(n, nl.fan_ptr, net->d_int, s));
-    int32_t max_fanin = 0;
-    SETUP_HIP(hipMemcpyAsync(&max_fanin, net->d_int, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    SETUP_HIP(sdnn::launch_max_segment(n, row_ptr, net->d_int + 1, s));
+    int32_t maxes[2] = {0, 0};
+    SETUP_HIP(hipMemcpyAsync(maxes, net->d_int, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s));
     SETUP_HIP(hipStreamSynchronize(s));
+    const int32_t max_fanin = maxes[0];
+    nl.max_fanout = maxes[1];
     if (max_fanin > 8192) {
         char msg[128];
         std::snprintf(msg, sizeof msg, "a fan-in list has %d entries; at most 8192 are supported", max_fanin);
@@ -390,29 +398,56 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         return SDNN_OK;
     }
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
-    SDNN_HIP(hipMemsetAsync(net->d_work, 0, (size_t)(k1 - k0) * sizeof(unsigned long long), s));
+    SDNN_HIP(hipMemsetAsync(net->d_stats, 0, (size_t)(k1 - k0) * 4 * sizeof(unsigned long long), s));
 
     // Activation format per layer.  While outputs are sparse they stay as slot rows (row-wise SpGEMM).
-    // A layer whose bias is positive on at least a quarter of the neurons gives every such neuron
-    // h(b_j) > 0 in every sample that does not push it below zero, so its output is dense: from the
-    // first such layer on, activations are kept dense and neuron-major and each layer gathers over
-    // fan-in lists (the dense-Y product), and the result is packed back into rows at the end.
+    // From the first layer whose input is dense enough, activations are kept dense and neuron-major and
+    // each layer gathers over fan-in lists (the dense-Y product); the result is packed back into rows at
+    // the end.  A layer's input counts as dense when it holds at least 1/8 of batch * n entries, or when
+    // the layer's bias is positive on at least a quarter of its neurons (every such neuron is then
+    // h(b_j) > 0 in every sample that does not push it below zero, so the output is dense whatever the
+    // input).  The input size is known on the host only through a synchronisation, so the host keeps an
+    // upper bound (a layer with every b_j <= 0 writes at most (longest fan-out row) entries per input
+    // entry) and reads the exact count from the device only when the bound reaches the threshold.
+    const double dense_at = (double)batch * (double)n / 8.0;
+    double nnz_hi = (double)batch * (double)n;  // upper bound of the current layer's input entries
+    bool exact = false;
+    if (nnz_hi >= dense_at) {
+        int64_t in_nnz = 0;
+        SDNN_HIP(hipMemcpyAsync(&in_nnz, y_row_ptr + batch, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        SDNN_HIP(hipStreamSynchronize(s));
+        nnz_hi = (double)in_nnz;
+        exact = true;
+    }
     int32_t kd = k1;
-    for (int32_t k = k0; k < k1; ++k)
-        if (4 * net->layers[(size_t)k].pos_bias >= n) {
+    int cur = 0;  // slot buffer that receives the next sparse layer's output
+    for (int32_t k = k0; k < k1; ++k) {
+        const Layer &l = net->layers[(size_t)k];
+        if (4 * l.pos_bias >= n) {
             kd = k;
             break;
         }
-    int cur = 0;  // slot buffer that receives the next sparse layer's output
-    for (int32_t k = k0; k < kd; ++k) {
-        const Layer &l = net->layers[(size_t)k];
+        if (nnz_hi >= dense_at && !exact) {
+            unsigned long long got = 0;
+            SDNN_HIP(hipMemcpyAsync(&got, net->d_stats + 4 * (k - 1 - k0) + 2, sizeof(got), hipMemcpyDeviceToHost, s));
+            SDNN_HIP(hipStreamSynchronize(s));
+            nnz_hi = (double)got;
+            exact = true;
+        }
+        if (nnz_hi >= dense_at) {
+            kd = k;
+            break;
+        }
         const bool first = k == k0;
         SDNN_HIP(sdnn::launch_spgemm_layer(n, batch, first ? y_row_ptr : nullptr, first ? nullptr : w.cnt[cur ^ 1],
                                            first ? y_col : w.col[cur ^ 1], first ? y_val : w.val[cur ^ 1], l.row_ptr,
-                                           l.w_seg, l.w_pack, l.nnz, l.bias, l.bias_nonpos ? 1 : 0, net->ymax,
-                                           w.cnt[cur], w.col[cur], w.val[cur], net->d_flags, net->d_work + (k - k0),
-                                           net->num_cu, s));
+                                           l.w_seg, l.w_pack, l.nnz, l.max_fanout, l.bias, l.bias_nonpos ? 1 : 0,
+                                           net->ymax, w.cnt[cur], w.col[cur], w.val[cur], w.lists,
+                                           net->d_stats + 4 * (k - k0), net->d_flags, net->num_cu, s));
         cur ^= 1;
+        const double full = (double)batch * (double)n;
+        nnz_hi = l.bias_nonpos ? std::min(full, nnz_hi * (double)l.max_fanout) : full;
+        exact = false;
     }
     int last, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
     if (kd < k1) {
@@ -460,7 +495,7 @@ sdnn_status sdnn_net_free(sdnn_net net) {
     for (Layer &l : net->layers) release(l);
     dfree(net->d_flags);
     dfree(net->d_int);
-    dfree(net->d_work);
+    dfree(net->d_stats);
     delete net;
     return SDNN_OK;
 }

@@ -62,11 +62,15 @@ size_t spgemm_lds_bytes(int64_t n);
 int spgemm_windows(int64_t n);
 bool spgemm_wants_window_index(int64_t n);
 hipError_t launch_window_seg(int64_t n, const int64_t *w_ptr, const int32_t *col, int32_t *w_seg, hipStream_t s);
+// ylen limit of the small-sample SpGEMM kernel for a layer whose longest fan-out row has max_fanout entries.
+int64_t spgemm_small_len(int64_t n, int32_t max_fanout);
+// One sparse layer: planning pass, small-sample kernel, workgroup kernel.  lists holds 2 * batch int32;
+// stats points to the layer's 4 counters (zero on entry): small count, large count, output nnz, work.
 hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const int32_t *w_seg,
-                               const Edge *w, int64_t w_nnz, const float *bias, int bias_nonpos, double ymax,
-                               int32_t *out_cnt, int32_t *out_col, float *out_val, uint32_t *err,
-                               unsigned long long *work, int num_cu, hipStream_t s);
+                               const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
+                               double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val, int32_t *lists,
+                               unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s);
 hipError_t launch_densify(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                           const int32_t *in_col, const float *in_val, float *yt, uint32_t *err, hipStream_t s);
 hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,

@@ -7,9 +7,11 @@
 // window, reading only the window's part of each fan-out row (per-row window offsets built at set-up).
 // Products are exact in fp64 and added with LDS fp64 atomics.
 //
-// Scheduling: one persistent workgroup per CU takes chunks of samples from a device counter (every
-// workgroup leaves once the counter passes the last chunk).  A chunk is classified 64 samples at a time:
-// when every b_j <= 0 an empty sample stays empty (h(b_j) = 0) and costs one store.
+// Scheduling: a planning pass sorts the samples of a layer into three classes.  When every b_j <= 0 an
+// empty sample stays empty (h(b_j) = 0) and costs one store; a sample whose products fit a wave's share of
+// LDS (at most 1024) goes to the small-sample kernel, one wavefront per sample; every other sample goes to
+// the workgroup kernel below, where one persistent workgroup per CU takes chunks of the list from a device
+// counter (every workgroup leaves once the counter passes the last chunk).
 //
 // The epilogue visits the window in column order: z = acc + b_j, h(z), one rounding to fp32, and the
 // entries that are not zero (Sec. II.E: zeros are not stored) are compacted with a wave prefix sum of
@@ -62,19 +64,180 @@ __device__ __forceinline__ RowIn input_row(int64_t r, int64_t n, int64_t batch, 
     return ri;
 }
 
+constexpr int kSmallCap = 1024;   // products per sample in the small-sample kernel (a power of two)
+constexpr int kSmallWaves = 4;    // wavefronts per workgroup of the small-sample kernel
+
+// Per-layer counters kept by the sparse layer kernels (one row of the net's statistics array).
+enum : int { kStatSmall = 0, kStatLarge = 1, kStatNnz = 2, kStatWork = 3 };
+
+// Planning pass: one thread per sample.  Empty samples of a layer with every b_j <= 0 are finished here
+// (cnt = 0); the others are appended to the small list (lists[0 .. small)) or the large list
+// (lists[batch .. batch + large)) with one atomic per wave and list.
+__global__ __launch_bounds__(256) void spgemm_plan_kernel(int64_t n, int64_t batch, const int64_t *__restrict__ in_row_ptr,
+                                                          const int32_t *__restrict__ in_cnt,
+                                                          const int32_t *__restrict__ in_col,
+                                                          const float *__restrict__ in_val, int bias_nonpos,
+                                                          int64_t small_len, int32_t *__restrict__ out_cnt,
+                                                          int32_t *__restrict__ lists, unsigned long long *stats,
+                                                          uint32_t *err) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    const bool valid = r < batch;
+    int64_t ylen = 0;
+    if (valid) ylen = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err).ylen;
+    const bool skip = valid && bias_nonpos && ylen == 0;
+    const bool small = valid && bias_nonpos && ylen > 0 && ylen <= small_len;
+    const bool large = valid && !skip && !small;
+    if (skip) out_cnt[r] = 0;
+    const uint64_t ms = __ballot(small), ml = __ballot(large);
+    unsigned long long bs = 0, bl = 0;
+    if (lane == 0) {
+        if (ms) bs = atomicAdd(&stats[kStatSmall], (unsigned long long)__popcll(ms));
+        if (ml) bl = atomicAdd(&stats[kStatLarge], (unsigned long long)__popcll(ml));
+    }
+    bs = __shfl(bs, 0);
+    bl = __shfl(bl, 0);
+    if (small) lists[bs + lane_rank(ms)] = (int32_t)r;
+    if (large) lists[batch + bl + lane_rank(ml)] = (int32_t)r;
+}
+
+// Orders this wave's earlier LDS accesses before its later ones (the lanes of one wave exchange data
+// through LDS between the phases of the small-sample kernel).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Small samples (every b_j <= 0, at most kSmallCap products): one wavefront per sample, no accumulator
+// window.  The wave expands the sample's products (column, exact fp64 product) into its own LDS area
+// (a wave prefix sum of the fan-out row lengths gives each entry its place), sorts them by column with a
+// bitonic network, then each run of equal columns is summed, biased, activated and rounded once, and the
+// survivors are compacted in column order with a ballot.  Only touched columns can survive when
+// b_j <= 0, so nothing else is visited.
+__global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
+    int64_t n, int64_t batch, const int64_t *__restrict__ in_row_ptr, const int32_t *__restrict__ in_cnt,
+    const int32_t *__restrict__ in_col, const float *__restrict__ in_val, const int64_t *__restrict__ w_ptr,
+    const Edge *__restrict__ w, const float *__restrict__ bias, double ymax, const int32_t *__restrict__ list,
+    unsigned long long *stats, int32_t *__restrict__ out_cnt, int32_t *__restrict__ out_col,
+    float *__restrict__ out_val, uint32_t *err) {
+    __shared__ int32_t keys_all[kSmallWaves][kSmallCap];
+    __shared__ double vals_all[kSmallWaves][kSmallCap];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int32_t *keys = keys_all[wave];
+    double *vals = vals_all[wave];
+    const int64_t count = (int64_t)stats[kStatSmall];
+    const int64_t stride = (int64_t)gridDim.x * kSmallWaves;
+    for (int64_t q = (int64_t)blockIdx.x * kSmallWaves + wave; q < count; q += stride) {
+        const int64_t r = list[q];
+        const RowIn ri = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err);
+        // expand: the planner guarantees ylen * (longest fan-out row) <= kSmallCap
+        int total = 0;
+        for (int64_t base = 0; base < ri.ylen; base += 64) {
+            const int64_t t = base + lane;
+            double y = 0.0;
+            int64_t start = 0;
+            int len = 0;
+            if (t < ri.ylen) {
+                const int32_t i = in_col[ri.yb + t];
+                if (i >= 0 && i < n) {
+                    y = (double)in_val[ri.yb + t];
+                    start = w_ptr[i];
+                    len = (int)(w_ptr[i + 1] - start);
+                } else {
+                    atomicOr(err, 1u);
+                }
+            }
+            int incl = len;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int v = __shfl_up(incl, d);
+                if (lane >= d) incl += v;
+            }
+            int pos = total + incl - len;
+            total += __shfl(incl, 63);
+            for (int k0 = 0; k0 < len; k0 += 8) {
+                Edge ed[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (k0 + u < len) ed[u] = w[start + k0 + u];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (k0 + u < len) {
+                        keys[pos + k0 + u] = ed[u].idx;
+                        vals[pos + k0 + u] = y * (double)ed[u].w;
+                    }
+            }
+        }
+        int size = 64;
+        while (size < total) size <<= 1;
+        for (int e = total + lane; e < size; e += 64) keys[e] = 0x7fffffff;
+        wave_lds_sync();
+        // bitonic sort of (key, value) pairs by key over [0, size)
+        for (int k = 2; k <= size; k <<= 1) {
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                for (int p = lane; p < (size >> 1); p += 64) {
+                    const int i = ((p & ~(j - 1)) << 1) | (p & (j - 1));
+                    const int l = i + j;
+                    const int32_t ki = keys[i], kl = keys[l];
+                    const bool up = (i & k) == 0;
+                    if ((ki > kl) == up && ki != kl) {
+                        keys[i] = kl;
+                        keys[l] = ki;
+                        const double vi = vals[i];
+                        vals[i] = vals[l];
+                        vals[l] = vi;
+                    }
+                }
+                wave_lds_sync();
+            }
+        }
+        // runs of equal columns: the first element of a run sums it, then h, one rounding, compaction
+        const int64_t ob = r * n;
+        int written = 0;
+        for (int base = 0; base < total; base += 64) {
+            const int e = base + lane;
+            float f = 0.0f;
+            int32_t key = 0;
+            if (e < total) {
+                key = keys[e];
+                if (e == 0 || keys[e - 1] != key) {
+                    double z = 0.0;
+                    for (int u = e; u < total && keys[u] == key; ++u) z += vals[u];
+                    f = activate(z + (double)bias[key], ymax);
+                }
+            }
+            const bool keep = f != 0.0f;
+            const uint64_t m = __ballot(keep);
+            if (keep) {
+                const int64_t o = ob + written + lane_rank(m);
+                out_col[o] = key;
+                out_val[o] = f;
+            }
+            written += __popcll(m);
+        }
+        if (lane == 0) {
+            out_cnt[r] = written;
+            if (written) atomicAdd(&stats[kStatNnz], (unsigned long long)written);
+        }
+        wave_lds_sync();  // the next sample rewrites this wave's LDS area
+    }
+}
+
+constexpr int kRounds = kTile / (4 * kThreads);  // dense-epilogue rounds of 4 columns per thread
+
 __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
-    int64_t n, int64_t batch, int nwin, int chunk, const int64_t *__restrict__ in_row_ptr,
+    int64_t n, int64_t batch, int nwin, const int64_t *__restrict__ in_row_ptr,
     const int32_t *__restrict__ in_cnt, const int32_t *__restrict__ in_col, const float *__restrict__ in_val,
     const int64_t *__restrict__ w_ptr, const int32_t *__restrict__ w_seg, const Edge *__restrict__ w,
     const float *__restrict__ bias, int bias_nonpos, int64_t sparse_limit, int lane_segments, double ymax,
-    int32_t *__restrict__ out_cnt, int32_t *__restrict__ out_col, float *__restrict__ out_val, uint32_t *err,
-    unsigned long long *work) {
+    const int32_t *__restrict__ list, unsigned long long *stats, int32_t *__restrict__ out_cnt,
+    int32_t *__restrict__ out_col, float *__restrict__ out_val, uint32_t *err) {
     extern __shared__ double acc[];
     __shared__ RowRef refs[kThreads];
     __shared__ uint32_t bits[kBitWords];
     __shared__ int wave_tot[kWaves];
-    __shared__ int64_t rows[64];
-    __shared__ int nrows;
+    __shared__ unsigned long long wave_tot4[kWaves];
     __shared__ unsigned long long chunk_id;
     __shared__ int any;
 
@@ -84,121 +247,168 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
     for (int t = tid; t < width0; t += kThreads) acc[t] = 0.0;
     for (int t = tid; t < kBitWords; t += kThreads) bits[t] = 0u;
     if (tid == 0) any = 0;
-    const unsigned long long nchunks = (unsigned long long)((batch + chunk - 1) / chunk);
+    // the large list was filled by the planning pass of this layer; chunks of it are taken in turn
+    const int64_t count = (int64_t)stats[kStatLarge];
+    int64_t chunk = count / ((int64_t)gridDim.x * 16);
+    chunk = chunk < 1 ? 1 : (chunk > 64 ? 64 : chunk);
+    const unsigned long long nchunks = (unsigned long long)((count + chunk - 1) / chunk);
+    const int32_t *large = list + batch;
 
     for (;;) {
-        if (tid == 0) chunk_id = atomicAdd(work, 1ull);
+        if (tid == 0) chunk_id = atomicAdd(&stats[kStatWork], 1ull);
         __syncthreads();
         const unsigned long long ch = chunk_id;
         if (ch >= nchunks) break;  // uniform: every workgroup reaches this once the counter passes the end
-        if (wave == 0) {
-            const int64_t r = (int64_t)ch * chunk + lane;
-            const bool valid = lane < chunk && r < batch;
-            int64_t ylen = 0;
-            if (valid) ylen = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err).ylen;
-            const bool todo = valid && (ylen > 0 || !bias_nonpos);
-            if (valid && !todo) out_cnt[r] = 0;
-            const uint64_t m = __ballot(todo);
-            if (todo) rows[lane_rank(m)] = r;
-            if (lane == 0) nrows = __popcll(m);
-        }
-        __syncthreads();
-        const int nr = nrows;
+        const int64_t q0 = (int64_t)ch * chunk;
+        const int nr = (int)((count - q0) < chunk ? (count - q0) : chunk);
         for (int q = 0; q < nr; ++q) {
-            const int64_t r = rows[q];
+            const int64_t r = large[q0 + q];
             const RowIn ri = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err);
             const int64_t yb = ri.yb, ylen = ri.ylen;
             const bool sparse = bias_nonpos && ylen <= sparse_limit;
+            // resident mode: one stored entry per thread, kept in registers across the windows; the
+            // thread's fan-out segment for window w is [s_lo, s_hi), and the next window's segment starts
+            // where this one ends, so each window costs one more offset load, issued a window ahead
+            const bool resident = lane_segments && ylen <= kThreads;
+            double my_y = 0.0;
+            int32_t my_i = -1;
+            int64_t my_rb = 0, s_lo = 0, s_hi = 0;
+            if (resident && tid < ylen) {
+                const int32_t i = in_col[yb + tid];
+                if (i >= 0 && i < n) {
+                    my_i = i;
+                    my_y = (double)in_val[yb + tid];
+                    my_rb = w_ptr[i];
+                    s_lo = my_rb;
+                    s_hi = w_seg ? my_rb + w_seg[(int64_t)i * (nwin + 1) + 1] : w_ptr[i + 1];
+                } else {
+                    atomicOr(err, 1u);
+                }
+            }
             const int64_t ob = r * n;
             int64_t written = 0;
             for (int win = 0; win < nwin; ++win) {
                 const int64_t c0 = (int64_t)win * kTile;
                 const int64_t c1 = (c0 + kTile < n) ? c0 + kTile : n;
                 const int width = (int)(c1 - c0);
-                // scatter: each wave takes 64 stored entries of the sample at once (one per lane,
-                // coalesced), gathers the extents of their fan-out row segments and parks (y, start,
-                // length) in its own LDS area; then each half-wave reads one segment with 32 lanes (a
-                // coalesced load), four segments per half in flight, and adds the exact products
-                bool mine_any = false;
-                RowRef *my = refs + wave * 64;
-                for (int64_t base = (int64_t)wave * 64; base < ylen; base += kThreads) {
-                    const int64_t t = base + lane;
-                    RowRef ref;
-                    ref.y = 0.0;
-                    ref.start = 0;
-                    ref.len = 0;
-                    if (t < ylen) {
-                        const int32_t i = in_col[yb + t];
-                        if (i >= 0 && i < n) {
-                            ref.y = (double)in_val[yb + t];
-                            const int64_t rb = w_ptr[i];
-                            if (w_seg) {
-                                const int32_t *sg = w_seg + (int64_t)i * (nwin + 1) + win;
-                                ref.start = (int32_t)(rb + sg[0]);
-                                ref.len = sg[1] - sg[0];
-                            } else {
-                                ref.start = (int32_t)rb;
-                                ref.len = (int32_t)(w_ptr[i + 1] - rb);
-                            }
-                        } else {
-                            atomicOr(err, 1u);
+                // biases of this thread's dense-epilogue columns, loaded before the scatter so that the
+                // epilogue does not wait for them
+                float bv[kRounds][4];
+                if (!sparse) {
+#pragma unroll
+                    for (int rd = 0; rd < kRounds; ++rd)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            const int t = rd * 4 * kThreads + 4 * tid + v;
+                            bv[rd][v] = t < width ? bias[c0 + t] : 0.0f;
                         }
+                }
+                bool mine_any = false;
+                if (resident) {
+                    const int64_t lo = s_lo, hi = s_hi;
+                    if (win + 1 < nwin && my_i >= 0) {
+                        s_lo = s_hi;
+                        s_hi = my_rb + w_seg[(int64_t)my_i * (nwin + 1) + win + 2];
                     }
-                    if (lane_segments) {
-                        // short segments: every lane walks its own (it spans one or two cache lines),
-                        // eight weight loads in flight per lane
-                        int maxl = ref.len;
+                    for (int64_t e = lo; e < hi; e += 8) {
+                        Edge ed[8];
 #pragma unroll
-                        for (int off = 32; off >= 1; off >>= 1) maxl = max(maxl, __shfl_xor(maxl, off));
-                        for (int cc = 0; cc < maxl; cc += 8) {
-                            Edge ed[8];
+                        for (int u = 0; u < 8; ++u)
+                            if (e + u < hi) ed[u] = w[e + u];
 #pragma unroll
-                            for (int u = 0; u < 8; ++u) {
-                                ed[u].idx = -1;
-                                ed[u].w = 0.0f;
-                                if (cc + u < ref.len) ed[u] = w[ref.start + cc + u];
+                        for (int u = 0; u < 8; ++u)
+                            if (e + u < hi) {
+                                const int col = ed[u].idx - (int)c0;
+                                atomicAdd(&acc[col], my_y * (double)ed[u].w);
+                                if (sparse) atomicOr(&bits[col >> 5], 1u << (col & 31));
+                                mine_any = true;
                             }
+                    }
+                } else {
+                    // each wave takes 64 stored entries of the sample at once (one per lane, coalesced),
+                    // gathers the extents of their fan-out row segments and parks (y, start, length) in
+                    // its own LDS area; then each half-wave reads one segment with 32 lanes (a coalesced
+                    // load), four segments per half in flight, and adds the exact products
+                    RowRef *my = refs + wave * 64;
+                    for (int64_t base = (int64_t)wave * 64; base < ylen; base += kThreads) {
+                        const int64_t t = base + lane;
+                        RowRef ref;
+                        ref.y = 0.0;
+                        ref.start = 0;
+                        ref.len = 0;
+                        if (t < ylen) {
+                            const int32_t i = in_col[yb + t];
+                            if (i >= 0 && i < n) {
+                                ref.y = (double)in_val[yb + t];
+                                const int64_t rb = w_ptr[i];
+                                if (w_seg) {
+                                    const int32_t *sg = w_seg + (int64_t)i * (nwin + 1) + win;
+                                    ref.start = (int32_t)(rb + sg[0]);
+                                    ref.len = sg[1] - sg[0];
+                                } else {
+                                    ref.start = (int32_t)rb;
+                                    ref.len = (int32_t)(w_ptr[i + 1] - rb);
+                                }
+                            } else {
+                                atomicOr(err, 1u);
+                            }
+                        }
+                        if (lane_segments) {
+                            // short segments: every lane walks its own (it spans one or two cache
+                            // lines), eight weight loads in flight per lane
+                            int maxl = ref.len;
 #pragma unroll
-                            for (int u = 0; u < 8; ++u) {
-                                if (ed[u].idx >= c0 && ed[u].idx < c1) {
-                                    const int col = ed[u].idx - (int)c0;
-                                    atomicAdd(&acc[col], ref.y * (double)ed[u].w);
-                                    if (sparse) atomicOr(&bits[col >> 5], 1u << (col & 31));
-                                    mine_any = true;
+                            for (int off = 32; off >= 1; off >>= 1) maxl = max(maxl, __shfl_xor(maxl, off));
+                            for (int cc = 0; cc < maxl; cc += 8) {
+                                Edge ed[8];
+#pragma unroll
+                                for (int u = 0; u < 8; ++u) {
+                                    ed[u].idx = -1;
+                                    ed[u].w = 0.0f;
+                                    if (cc + u < ref.len) ed[u] = w[ref.start + cc + u];
+                                }
+#pragma unroll
+                                for (int u = 0; u < 8; ++u) {
+                                    if (ed[u].idx >= c0 && ed[u].idx < c1) {
+                                        const int col = ed[u].idx - (int)c0;
+                                        atomicAdd(&acc[col], ref.y * (double)ed[u].w);
+                                        if (sparse) atomicOr(&bits[col >> 5], 1u << (col & 31));
+                                        mine_any = true;
+                                    }
                                 }
                             }
+                            continue;
                         }
-                        continue;
-                    }
-                    my[lane] = ref;
-                    const int nref = (int)((ylen - base) < 64 ? (ylen - base) : 64);
-                    for (int rr0 = 0; rr0 < nref; rr0 += 8) {
-                        RowRef rr[4];
-#pragma unroll
-                        for (int p = 0; p < 4; ++p) {
-                            const int row = rr0 + 2 * p + half;
-                            rr[p] = my[row < nref ? row : 0];
-                            if (row >= nref) rr[p].len = 0;
-                        }
-                        int maxl = 0;
-#pragma unroll
-                        for (int p = 0; p < 4; ++p) maxl = rr[p].len > maxl ? rr[p].len : maxl;
-                        maxl = max(maxl, __shfl_xor(maxl, 32));
-                        for (int cc = 0; cc < maxl; cc += 32) {
-                            Edge ed[4];
+                        my[lane] = ref;
+                        const int nref = (int)((ylen - base) < 64 ? (ylen - base) : 64);
+                        for (int rr0 = 0; rr0 < nref; rr0 += 8) {
+                            RowRef rr[4];
 #pragma unroll
                             for (int p = 0; p < 4; ++p) {
-                                ed[p].idx = -1;
-                                ed[p].w = 0.0f;
-                                if (cc + hl < rr[p].len) ed[p] = w[rr[p].start + cc + hl];
+                                const int row = rr0 + 2 * p + half;
+                                rr[p] = my[row < nref ? row : 0];
+                                if (row >= nref) rr[p].len = 0;
                             }
+                            int maxl = 0;
 #pragma unroll
-                            for (int p = 0; p < 4; ++p) {
-                                if (ed[p].idx >= c0 && ed[p].idx < c1) {
-                                    const int col = ed[p].idx - (int)c0;
-                                    atomicAdd(&acc[col], rr[p].y * (double)ed[p].w);
-                                    if (sparse) atomicOr(&bits[col >> 5], 1u << (col & 31));
-                                    mine_any = true;
+                            for (int p = 0; p < 4; ++p) maxl = rr[p].len > maxl ? rr[p].len : maxl;
+                            maxl = max(maxl, __shfl_xor(maxl, 32));
+                            for (int cc = 0; cc < maxl; cc += 32) {
+                                Edge ed[4];
+#pragma unroll
+                                for (int p = 0; p < 4; ++p) {
+                                    ed[p].idx = -1;
+                                    ed[p].w = 0.0f;
+                                    if (cc + hl < rr[p].len) ed[p] = w[rr[p].start + cc + hl];
+                                }
+#pragma unroll
+                                for (int p = 0; p < 4; ++p) {
+                                    if (ed[p].idx >= c0 && ed[p].idx < c1) {
+                                        const int col = ed[p].idx - (int)c0;
+                                        atomicAdd(&acc[col], rr[p].y * (double)ed[p].w);
+                                        if (sparse) atomicOr(&bits[col >> 5], 1u << (col & 31));
+                                        mine_any = true;
+                                    }
                                 }
                             }
                         }
@@ -247,56 +457,69 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                         written += tot;
                     }
                 } else if (touched || !bias_nonpos) {
-                    // epilogue over the whole window in column order, 4 consecutive columns per thread
-                    // (4096 per round); reads and zeroes the accumulator
-                    for (int base = 0; base < width; base += 4 * kThreads) {
-                        const int t0 = base + 4 * tid;
-                        float f[4];
+                    // epilogue over the whole window in column order: in round rd thread t owns columns
+                    // rd * 4096 + 4t .. +3; reads and zeroes the accumulator.  One scan covers all
+                    // rounds: the survivor counts of the rounds travel in 16-bit fields of one integer.
+                    float f[kRounds][4];
+                    unsigned long long packed = 0;
+#pragma unroll
+                    for (int rd = 0; rd < kRounds; ++rd) {
                         int keep = 0;
 #pragma unroll
                         for (int v = 0; v < 4; ++v) {
-                            f[v] = 0.0f;
-                            if (t0 + v < width) {
-                                f[v] = activate(acc[t0 + v] + (double)bias[c0 + t0 + v], ymax);
-                                acc[t0 + v] = 0.0;
+                            const int t = rd * 4 * kThreads + 4 * tid + v;
+                            f[rd][v] = 0.0f;
+                            if (t < width) {
+                                f[rd][v] = activate(acc[t] + (double)bv[rd][v], ymax);
+                                acc[t] = 0.0;
                             }
-                            keep += f[v] != 0.0f;
+                            keep += f[rd][v] != 0.0f;
                         }
-                        int incl = keep;
+                        packed |= (unsigned long long)keep << (16 * rd);
+                    }
+                    unsigned long long incl = packed;
 #pragma unroll
-                        for (int d = 1; d < 64; d <<= 1) {
-                            const int v = __shfl_up(incl, d);
-                            if (lane >= d) incl += v;
-                        }
-                        if (lane == 63) wave_tot[wave] = incl;
-                        __syncthreads();
-                        int off = 0, tot = 0;
+                    for (int d = 1; d < 64; d <<= 1) {
+                        const unsigned long long v = __shfl_up(incl, d);
+                        if (lane >= d) incl += v;
+                    }
+                    if (lane == 63) wave_tot4[wave] = incl;
+                    __syncthreads();
+                    unsigned long long before = 0, all = 0;
 #pragma unroll
-                        for (int u = 0; u < kWaves; ++u) {
-                            const int v = wave_tot[u];
-                            off += (u < wave) ? v : 0;
-                            tot += v;
-                        }
-                        int64_t pos = ob + written + off + incl - keep;
+                    for (int u = 0; u < kWaves; ++u) {
+                        const unsigned long long v = wave_tot4[u];
+                        before += (u < wave) ? v : 0ull;
+                        all += v;
+                    }
+                    const unsigned long long excl = incl - packed;
+                    int64_t round_base = ob + written;
+#pragma unroll
+                    for (int rd = 0; rd < kRounds; ++rd) {
+                        const int sh = 16 * rd;
+                        int64_t pos = round_base + (int64_t)((before >> sh) & 0xffff) + (int64_t)((excl >> sh) & 0xffff);
 #pragma unroll
                         for (int v = 0; v < 4; ++v) {
-                            if (f[v] != 0.0f) {
-                                out_col[pos] = (int32_t)(c0 + t0 + v);
-                                out_val[pos] = f[v];
+                            if (f[rd][v] != 0.0f) {
+                                out_col[pos] = (int32_t)(c0 + rd * 4 * kThreads + 4 * tid + v);
+                                out_val[pos] = f[rd][v];
                                 ++pos;
                             }
                         }
-                        written += tot;
-                        __syncthreads();
+                        round_base += (int64_t)((all >> sh) & 0xffff);
                     }
+                    written = round_base - ob;
                 }
                 __syncthreads();
                 if (tid == 0) any = 0;
                 __syncthreads();
             }
-            if (tid == 0) out_cnt[r] = (int32_t)written;
+            if (tid == 0) {
+                out_cnt[r] = (int32_t)written;
+                if (written) atomicAdd(&stats[kStatNnz], (unsigned long long)written);
+            }
         }
-        __syncthreads();  // rows[] and chunk_id are rewritten for the next chunk
+        __syncthreads();  // chunk_id is rewritten for the next chunk
     }
 }
 
@@ -411,11 +634,15 @@ hipError_t launch_window_seg(int64_t n, const int64_t *w_ptr, const int32_t *col
     return hipGetLastError();
 }
 
+int64_t spgemm_small_len(int64_t n, int32_t max_fanout) {
+    return max_fanout > 0 ? kSmallCap / max_fanout : n;
+}
+
 hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const int32_t *w_seg,
-                               const Edge *w, int64_t w_nnz, const float *bias, int bias_nonpos, double ymax,
-                               int32_t *out_cnt, int32_t *out_col, float *out_val, uint32_t *err,
-                               unsigned long long *work, int num_cu, hipStream_t s) {
+                               const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
+                               double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val, int32_t *lists,
+                               unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s) {
     if (batch == 0) return hipSuccess;
     if (batch > 0x7fffffffLL) return hipErrorInvalidValue;
     static bool attr_set = false;
@@ -425,18 +652,30 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
         if (e != hipSuccess) return e;
         attr_set = true;
     }
+    const int64_t small_len = spgemm_small_len(n, max_fanout);
+    spgemm_plan_kernel<<<(unsigned)((batch + 255) / 256), 256, 0, s>>>(
+        n, batch, in_row_ptr, in_cnt, in_col, in_val, bias_nonpos, small_len, out_cnt, lists, stats, err);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (bias_nonpos) {
+        // enough waves to cover every CU several times; each wave strides through the small list
+        const int64_t waves = (batch < (int64_t)num_cu * 16 ? batch : (int64_t)num_cu * 16);
+        spgemm_small_kernel<<<(unsigned)((waves + kSmallWaves - 1) / kSmallWaves), kSmallWaves * 64, 0, s>>>(
+            n, batch, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w, bias, ymax, lists, stats, out_cnt, out_col,
+            out_val, err);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     const int nwin = spgemm_windows(n);
     const int64_t grid = batch < num_cu ? batch : num_cu;
-    int64_t chunk = batch / (grid * 16);
-    chunk = chunk < 1 ? 1 : (chunk > 64 ? 64 : chunk);
     // the bitmap epilogue pays off while a window gets at most ~2048 products
     const double per_win = (double)w_nnz / (double)n / (double)nwin;
     const int64_t sparse_limit = per_win > 0 ? (int64_t)(2048.0 / per_win) : n;
     // segments of at most ~16 entries are walked lane by lane, longer ones by half-waves
     const int lane_segments = (w_seg || nwin == 1) && per_win <= 16.0 ? 1 : 0;
     spgemm_row_kernel<<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
-        n, batch, nwin, (int)chunk, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, bias_nonpos,
-        sparse_limit, lane_segments, ymax, out_cnt, out_col, out_val, err, work);
+        n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, bias_nonpos, sparse_limit,
+        lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
     return hipGetLastError();
 }
 
