@@ -86,8 +86,9 @@ sdnn_status sdnn_net_set_stream(sdnn_net net, void *stream);
  * caller keeps alive and unchanged until the net is freed or the layer is set
  * again.  The call validates the CSR and the values on the device, builds the
  * library-owned fan-in (transposed) copy used by the dense-Y path, and
- * synchronises the net's stream once.  Fan-in lists longer than 8192 are
- * rejected with UNSUPPORTED.
+ * synchronises the net's stream once (the fan-in lists come from a stable
+ * radix sort of the entries by column, so each is sorted by input index).
+ * Layers wider than n = 2^24 are rejected with UNSUPPORTED.
  * Errors: INVALID_OBJECT, NULL_POINTER (nnz > 0 and col/val NULL), INVALID_VALUE
  * (nnz < 0 or >= 2^31, non-finite value), INVALID_INDEX, UNSUPPORTED, OUT_OF_MEMORY, DEVICE.
  */
@@ -142,7 +143,8 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
  * bound of each layer's input size and reads the exact count (one stream
  * synchronisation) only when the bound reaches the threshold, always for the
  * first layer.  The result is the same either way.
- * Errors: INVALID_OBJECT, NULL_POINTER, DIMENSION_MISMATCH, INVALID_INDEX, WORKSPACE_TOO_SMALL, DEVICE.
+ * Errors: INVALID_OBJECT, NULL_POINTER, DIMENSION_MISMATCH, INVALID_INDEX, WORKSPACE_TOO_SMALL, UNSUPPORTED
+ * (batch above 2^24), DEVICE.
  */
 sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const int64_t *y_row_ptr,
                              const int32_t *y_col, const float *y_val, void *ws, int64_t ws_bytes,

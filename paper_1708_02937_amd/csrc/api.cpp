@@ -115,6 +115,8 @@ CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
     return w;
 }
 
+constexpr int64_t kMaxScan = 16777216;  // longest array the device prefix sum handles (fan-in pointers, row pointers)
+
 size_t dense_ws_bytes(int64_t n, int64_t batch) { return 2 * align_up((size_t)n * (size_t)batch * sizeof(float)); }
 
 }  // namespace
@@ -205,6 +207,7 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     if (nnz > 0 && (!col_idx || !val)) return fail(SDNN_ERR_NULL_POINTER, "col_idx and val are required when nnz > 0");
     const int64_t n = net->n;
     hipStream_t s = net->stream;
+    if (n > kMaxScan) return fail(SDNN_ERR_UNSUPPORTED, "layers wider than 2^24 neurons are not supported");
 
     // 1. validate on the device
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, 2 * sizeof(uint32_t), s));
@@ -230,10 +233,12 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     nl.pos_bias = (int64_t)fl[1];
     int32_t *counts = nullptr;
     int64_t *tmp = nullptr;
+    char *sort_scratch = nullptr;
     sdnn_status st = SDNN_OK;
     auto cleanup = [&](sdnn_status r) {
         dfree(counts);
         dfree(tmp);
+        dfree(sort_scratch);
         if (r != SDNN_OK) release(nl);
         return r;
     };
@@ -242,6 +247,7 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     if ((st = dalloc(&nl.fan, (size_t)nnz, "fan-in lists")) != SDNN_OK) return cleanup(st);
     if ((st = dalloc(&counts, (size_t)n, "fan-in counts")) != SDNN_OK) return cleanup(st);
     if ((st = dalloc(&tmp, (size_t)sdnn::scan_tmp_elems(n), "scan scratch")) != SDNN_OK) return cleanup(st);
+    if ((st = dalloc(&sort_scratch, sdnn::fanin_sort_bytes(nnz), "sort scratch")) != SDNN_OK) return cleanup(st);
 
     hipError_t e;
 #define SETUP_HIP(call)                                            \
@@ -253,22 +259,10 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     SETUP_HIP(hipMemsetAsync(counts, 0, (size_t)n * sizeof(int32_t), s));
     SETUP_HIP(sdnn::launch_fanin_counts(nnz, col_idx, counts, s));
     SETUP_HIP(sdnn::launch_exclusive_scan_i32_to_i64(n, counts, nl.fan_ptr, tmp, s));
-    SETUP_HIP(hipMemsetAsync(counts, 0, (size_t)n * sizeof(int32_t), s));
-    SETUP_HIP(sdnn::launch_fanin_scatter(n, row_ptr, col_idx, val, nl.fan_ptr, counts, nl.fan, s));
-    SETUP_HIP(hipMemsetAsync(net->d_int, 0, 2 * sizeof(int32_t), s));
-    SETUP_HIP(sdnn::launch_max_segment(n, nl.fan_ptr, net->d_int, s));
-    SETUP_HIP(sdnn::launch_max_segment(n, row_ptr, net->d_int + 1, s));
-    int32_t maxes[2] = {0, 0};
-    SETUP_HIP(hipMemcpyAsync(maxes, net->d_int, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, s));
-    SETUP_HIP(hipStreamSynchronize(s));
-    const int32_t max_fanin = maxes[0];
-    nl.max_fanout = maxes[1];
-    if (max_fanin > 8192) {
-        char msg[128];
-        std::snprintf(msg, sizeof msg, "a fan-in list has %d entries; at most 8192 are supported", max_fanin);
-        return cleanup(fail(SDNN_ERR_UNSUPPORTED, msg));
-    }
-    SETUP_HIP(sdnn::launch_fanin_sort(n, max_fanin, nl.fan_ptr, nl.fan, s));
+    SETUP_HIP(sdnn::launch_fanin_lists(n, nnz, row_ptr, col_idx, val, nl.fan, sort_scratch, s));
+    SETUP_HIP(hipMemsetAsync(net->d_int, 0, sizeof(int32_t), s));
+    SETUP_HIP(sdnn::launch_max_segment(n, row_ptr, net->d_int, s));
+    SETUP_HIP(hipMemcpyAsync(&nl.max_fanout, net->d_int, sizeof(int32_t), hipMemcpyDeviceToHost, s));
     if (sdnn::spgemm_wants_window_index(n)) {
         if ((st = dalloc(&nl.w_seg, (size_t)n * (size_t)(sdnn::spgemm_windows(n) + 1), "window offsets")) != SDNN_OK)
             return cleanup(st);
@@ -371,6 +365,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     sdnn_status st = check_range(net, k0, k1);
     if (st != SDNN_OK) return st;
     if (batch < 0 || batch > 0x7fffffffLL) return fail(SDNN_ERR_DIMENSION_MISMATCH, "batch must be in [0, 2^31-1]");
+    if (batch > kMaxScan) return fail(SDNN_ERR_UNSUPPORTED, "CSR batches above 2^24 samples are not supported");
     if (!y_row_ptr || !out_row_ptr || !out_col || !out_val || !out_nnz)
         return fail(SDNN_ERR_NULL_POINTER, "y_row_ptr and the four outputs are required");
     if (!ws) return fail(SDNN_ERR_NULL_POINTER, "ws is required");

@@ -35,9 +35,11 @@ hipError_t launch_fanin_counts(int64_t nnz, const int32_t *col, int32_t *counts,
 hipError_t launch_exclusive_scan_i32_to_i64(int64_t count, const int32_t *in, int64_t *out, int64_t *tmp,
                                             hipStream_t s);
 int64_t scan_tmp_elems(int64_t count);
-hipError_t launch_fanin_scatter(int64_t n, const int64_t *row_ptr, const int32_t *col, const float *val,
-                                const int64_t *fan_ptr, int32_t *cursor, Edge *fan, hipStream_t s);
-hipError_t launch_fanin_sort(int64_t n, int32_t max_len, const int64_t *fan_ptr, Edge *fan, hipStream_t s);
+// Fan-in lists (W_k^T, each list sorted by input index) by a stable radix sort of the entries by column;
+// scratch holds fanin_sort_bytes(nnz) bytes.
+size_t fanin_sort_bytes(int64_t nnz);
+hipError_t launch_fanin_lists(int64_t n, int64_t nnz, const int64_t *row_ptr, const int32_t *col, const float *val,
+                              Edge *fan, void *scratch, hipStream_t s);
 hipError_t launch_max_segment(int64_t n, const int64_t *ptr, int32_t *out, hipStream_t s);
 hipError_t launch_pack_edges(int64_t nnz, const int32_t *col, const float *val, Edge *out, hipStream_t s);
 

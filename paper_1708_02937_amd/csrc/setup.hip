@@ -134,37 +134,129 @@ __global__ void scan_apply_kernel(int64_t count, const T *__restrict__ in, const
 
 // ------------------------------------------------------------------ fan-in lists
 
-// One thread per source row i: append (i, W(i, j)) to the list of every output j it reaches.
-__global__ void fanin_scatter_kernel(int64_t n, const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
-                                     const float *__restrict__ val, const int64_t *__restrict__ fan_ptr,
-                                     int32_t *cursor, Edge *__restrict__ fan) {
+// Fan-in lists by a stable LSD radix sort of the entries of W_k by output column.  The entries start in
+// CSR order (rows ascending), so a stable sort by column leaves each list sorted by input index: the fp64
+// summation order of the dense-Y kernels is then fixed, and any fan-in length is handled.
+constexpr int kSortThreads = 256;
+constexpr int kSortPer = 16;                              // entries per thread per tile
+constexpr int kSortTile = kSortThreads * kSortPer;        // 4096 entries per tile
+constexpr int kRadix = 256;                               // 8-bit digits
+
+// keys[e] = column of entry e, vals[e] = (row of e, weight): one thread per row.
+__global__ void sort_expand_kernel(int64_t n, const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+                                   const float *__restrict__ val, int32_t *__restrict__ keys, Edge *__restrict__ vals) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
     for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
-        const int32_t j = col[e];
-        const int32_t pos = atomicAdd(&cursor[j], 1);
+        keys[e] = col[e];
         Edge ed;
         ed.idx = (int32_t)i;
         ed.w = val[e];
-        fan[fan_ptr[j] + pos] = ed;
+        vals[e] = ed;
     }
 }
 
-// One wave per list: stage it in LDS, place each entry at its rank by input index (indices are distinct).
-__global__ void fanin_sort_kernel(int64_t n, const int64_t *__restrict__ fan_ptr, Edge *__restrict__ fan) {
-    extern __shared__ Edge seg[];
-    const int64_t j = blockIdx.x;
-    if (j >= n) return;
-    const int64_t b = fan_ptr[j];
-    const int len = (int)(fan_ptr[j + 1] - b);
-    if (len <= 1) return;
-    for (int t = threadIdx.x; t < len; t += blockDim.x) seg[t] = fan[b + t];
+// counts[d * ntiles + tile] = entries of the tile whose digit is d.
+__global__ __launch_bounds__(kSortThreads) void sort_hist_kernel(int64_t nnz, int shift, int64_t ntiles,
+                                                                 const int32_t *__restrict__ keys,
+                                                                 int32_t *__restrict__ counts) {
+    __shared__ int32_t h[kRadix];
+    const int64_t tile = blockIdx.x;
+    h[threadIdx.x] = 0;
     __syncthreads();
-    for (int t = threadIdx.x; t < len; t += blockDim.x) {
-        const int32_t key = seg[t].idx;
-        int rank = 0;
-        for (int u = 0; u < len; ++u) rank += seg[u].idx < key;
-        fan[b + rank] = seg[t];
+    const int64_t base = tile * kSortTile;
+    for (int k = 0; k < kSortPer; ++k) {
+        const int64_t e = base + k * kSortThreads + threadIdx.x;
+        if (e < nnz) atomicAdd(&h[(keys[e] >> shift) & (kRadix - 1)], 1);
+    }
+    __syncthreads();
+    counts[(int64_t)threadIdx.x * ntiles + tile] = h[threadIdx.x];
+}
+
+// One workgroup per digit: exclusive scan of its tile counts in place, digit total to totals[d].
+__global__ __launch_bounds__(kSortThreads) void sort_scan_kernel(int64_t ntiles, int32_t *__restrict__ counts,
+                                                                 int64_t *__restrict__ totals) {
+    __shared__ int64_t wsum[kSortThreads / 64];
+    const int d = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int32_t *row = counts + (int64_t)d * ntiles;
+    int64_t run = 0;
+    for (int64_t b0 = 0; b0 < ntiles; b0 += kSortThreads) {
+        const int64_t t = b0 + threadIdx.x;
+        const int64_t v = t < ntiles ? row[t] : 0;
+        int64_t incl = v;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int64_t u = __shfl_up(incl, o);
+            if (lane >= o) incl += u;
+        }
+        if (lane == 63) wsum[wave] = incl;
+        __syncthreads();
+        int64_t before = 0, all = 0;
+#pragma unroll
+        for (int w = 0; w < kSortThreads / 64; ++w) {
+            before += w < wave ? wsum[w] : 0;
+            all += wsum[w];
+        }
+        if (t < ntiles) row[t] = (int32_t)(run + before + incl - v);
+        run += all;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) totals[d] = run;
+}
+
+// Stable scatter of one tile: round k handles entries base + k * 256 + t in order; within a wave the rank
+// among equal digits comes from a match mask built from 8 ballots, across waves from per-wave digit counts.
+__global__ __launch_bounds__(kSortThreads) void sort_scatter_kernel(int64_t nnz, int shift, int64_t ntiles,
+                                                                    const int32_t *__restrict__ counts,
+                                                                    const int64_t *__restrict__ totals,
+                                                                    const int32_t *__restrict__ keys_in,
+                                                                    const Edge *__restrict__ vals_in,
+                                                                    int32_t *__restrict__ keys_out,
+                                                                    Edge *__restrict__ vals_out) {
+    __shared__ int64_t start[kRadix];             // where digit d of this tile goes next
+    __shared__ int32_t wcnt[kSortThreads / 64][kRadix];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t tile = blockIdx.x;
+    {
+        // digit base = entries with a smaller digit (all tiles) + entries of this digit in earlier tiles
+        int64_t base = 0;
+        for (int d = 0; d < tid; ++d) base += totals[d];
+        start[tid] = base + counts[(int64_t)tid * ntiles + tile];
+    }
+    for (int w = 0; w < kSortThreads / 64; ++w) wcnt[w][tid] = 0;
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int k = 0; k < kSortPer; ++k) {
+        const int64_t e = tile * kSortTile + (int64_t)k * kSortThreads + tid;
+        const bool valid = e < nnz;
+        const int32_t key = valid ? keys_in[e] : 0;
+        const int d = (key >> shift) & (kRadix - 1);
+        uint64_t match = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const uint64_t m = __ballot((d >> b) & 1);
+            match &= ((d >> b) & 1) ? m : ~m;
+        }
+        const int rank = __popcll(match & lt);
+        // the last lane of each digit group publishes the wave's count for that digit
+        if (valid && (match >> lane) == 1ull) wcnt[wave][d] = __popcll(match);
+        __syncthreads();
+        if (valid) {
+            int64_t pos = start[d] + rank;
+            for (int w = 0; w < wave; ++w) pos += wcnt[w][d];
+            keys_out[pos] = key;
+            vals_out[pos] = vals_in[e];
+        }
+        __syncthreads();
+        {
+            int32_t add = 0;
+            for (int w = 0; w < kSortThreads / 64; ++w) {
+                add += wcnt[w][tid];
+                wcnt[w][tid] = 0;
+            }
+            start[tid] += add;
+        }
+        __syncthreads();
     }
 }
 
@@ -213,22 +305,46 @@ hipError_t launch_exclusive_scan_i32_to_i64(int64_t count, const int32_t *in, in
     return hipGetLastError();
 }
 
-hipError_t launch_fanin_scatter(int64_t n, const int64_t *row_ptr, const int32_t *col, const float *val,
-                                const int64_t *fan_ptr, int32_t *cursor, Edge *fan, hipStream_t s) {
-    fanin_scatter_kernel<<<blocks_for(n, 256), 256, 0, s>>>(n, row_ptr, col, val, fan_ptr, cursor, fan);
-    return hipGetLastError();
-}
-
 hipError_t launch_max_segment(int64_t n, const int64_t *ptr, int32_t *out, hipStream_t s) {
     max_segment_kernel<<<blocks_for(n, 256), 256, 0, s>>>(n, ptr, out);
     return hipGetLastError();
 }
 
-// Caller guarantees every list is at most 8192 entries (64 KiB of LDS).
-hipError_t launch_fanin_sort(int64_t n, int32_t max_len, const int64_t *fan_ptr, Edge *fan, hipStream_t s) {
-    if (max_len <= 1) return hipSuccess;
-    if (max_len > 8192) return hipErrorInvalidValue;
-    fanin_sort_kernel<<<(unsigned)n, 64, (size_t)max_len * sizeof(Edge), s>>>(n, fan_ptr, fan);
+size_t fanin_sort_bytes(int64_t nnz) {
+    const int64_t ntiles = (nnz + kSortTile - 1) / kSortTile;
+    return 2 * (size_t)nnz * sizeof(int32_t) + (size_t)nnz * sizeof(Edge) +
+           (size_t)kRadix * (size_t)ntiles * sizeof(int32_t) + kRadix * sizeof(int64_t) + 1024;
+}
+
+hipError_t launch_fanin_lists(int64_t n, int64_t nnz, const int64_t *row_ptr, const int32_t *col, const float *val,
+                              Edge *fan, void *scratch, hipStream_t s) {
+    if (nnz == 0) return hipSuccess;
+    const int64_t ntiles = (nnz + kSortTile - 1) / kSortTile;
+    if (ntiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    char *p = (char *)scratch;
+    int32_t *keys[2];
+    keys[0] = (int32_t *)p;
+    p += (size_t)nnz * sizeof(int32_t);
+    keys[1] = (int32_t *)p;
+    p += (size_t)nnz * sizeof(int32_t);
+    Edge *tmp = (Edge *)p;
+    p += (size_t)nnz * sizeof(Edge);
+    int32_t *counts = (int32_t *)p;
+    p += (size_t)kRadix * (size_t)ntiles * sizeof(int32_t);
+    int64_t *totals = (int64_t *)(((uintptr_t)p + 7) & ~(uintptr_t)7);
+    int passes = 0;
+    while ((int64_t)1 << (8 * passes) < n) ++passes;
+    if (passes == 0) passes = 1;
+    // the last pass must land in fan: start in fan when the pass count is even, in tmp when it is odd
+    Edge *vals[2] = {passes % 2 ? tmp : fan, passes % 2 ? fan : tmp};
+    sort_expand_kernel<<<blocks_for(n, 256), 256, 0, s>>>(n, row_ptr, col, val, keys[0], vals[0]);
+    for (int pass = 0; pass < passes; ++pass) {
+        const int a = pass & 1, b = a ^ 1;
+        sort_hist_kernel<<<(unsigned)ntiles, kSortThreads, 0, s>>>(nnz, 8 * pass, ntiles, keys[a], counts);
+        sort_scan_kernel<<<kRadix, kSortThreads, 0, s>>>(ntiles, counts, totals);
+        sort_scatter_kernel<<<(unsigned)ntiles, kSortThreads, 0, s>>>(nnz, 8 * pass, ntiles, counts, totals, keys[a],
+                                                                     vals[a], keys[b], vals[b]);
+    }
     return hipGetLastError();
 }
 

@@ -96,6 +96,28 @@ def test_tiny_csr_batch(sd, seed, n, L, batch):
     parity.compare(p, run_csr(sd, p))
 
 
+def test_long_fanin_lists(sd):
+    """Fan-in lists longer than 8192 entries (the radix-sort transpose handles any length), n not a multiple
+    of 4, on both dense arms; sampled rows."""
+    p = tiny_random(51, 9001, 1, 132, w_density=0.97, y_density=0.6, dense_input=True, bias_lo=-1.0, bias_hi=1.0)
+    rows = np.arange(0, 132, 11)
+    for arm in (sd.SDNN_ARM_SPARSE, sd.SDNN_ARM_DENSE):
+        _say("long fan-in", arm)
+        out = run_dense(sd, p, arm)
+        parity.compare(p, dense_to_csr(out[rows]), rows=rows)
+
+
+@pytest.mark.parametrize("seed,n,L,batch,wd,yd", [(41, 5000, 3, 300, 0.0024, 0.008), (42, 3000, 2, 257, 0.003, 0.015),
+                                                  (43, 40000, 2, 64, 0.0002, 0.0012)])
+def test_small_and_large_samples_mixed(sd, seed, n, L, batch, wd, yd):
+    """Every b_j <= 0: samples with few products take the one-wave sort kernel, longer ones the workgroup
+    kernel, empty ones neither; lengths straddle the split (and one net has three accumulator windows)."""
+    p = tiny_random(seed, n, L, batch, w_density=wd, y_density=yd, bias_lo=-0.2, bias_hi=0.0,
+                    explicit_zeros=seed % 2 == 0)
+    _say("small/large mix", seed, n, L, batch)
+    parity.compare(p, run_csr(sd, p))
+
+
 @pytest.mark.parametrize("cfg,kw", [
     (1, dict(n=1024, L=4, batch=64)), (2, dict(n=512, L=3, batch=200)), (3, dict(n=2048, L=3, batch=100)),
     (4, dict(n=20000, L=3, batch=50, window=1024)), (5, dict(n=20480, L=2, batch=12, block=4096))])
