@@ -222,6 +222,90 @@ def _cpu_model():
 # ----------------------------------------------------------------------------------- other workloads
 
 
+def _crossover(points):
+    """Log-log interpolation of the x where t_sparse = t_dense, from sorted (x, t_sparse, t_dense);
+    x grows as W gets sparser, so the sparse arm is slower before the crossover and faster after it."""
+    for (x0, s0, q0), (x1, s1, q1) in zip(points, points[1:]):
+        r0, r1 = math.log(s0 / q0), math.log(s1 / q1)
+        if r0 >= 0 >= r1 and r1 != r0:
+            t = r0 / (r0 - r1)
+            return math.exp(math.log(x0) + t * (math.log(x1) - math.log(x0)))
+    return None
+
+
+def run_paper_grid(args, torch, sd):
+    """The paper's own experiment (Sec. V.B-D) on one MI355X: one layer of m x m weights with inverse
+    sparsity S (Bernoulli pattern, values U[-1,3)) applied to 64 dense samples, through the CSR arm and the
+    dense-W arm.  Per-layer time = (T(L identical layers) - T(1 layer)) / (L - 1), so the entry and exit
+    transposes cancel (the paper times one iteration of its layer loop); L = 2 for m >= 8192 and 17 below,
+    so that for small layers the GPU time, not the host's launch time, is what remains.  Also the analogues
+    of the paper's scaling parameters (Fig. 7), each normalised to m = 4096: dense time per element,
+    sparse/dense ratio at S = 1, sparse slope per nonzero between S = 1 and S = 4, and the saturation time
+    per row at S = 262144."""
+    from workloads import PAPER_GRID_INV_SPARSITY, PAPER_GRID_SIZES, paper_grid
+
+    sizes = [int(x) for x in args.grid_sizes.split(",")] if args.grid_sizes else list(PAPER_GRID_SIZES)
+    invs = [int(x) for x in args.grid_inv.split(",")] if args.grid_inv else list(PAPER_GRID_INV_SPARSITY)
+    reps = max(3, args.steps)
+    grid = {}
+    for m in sizes:
+        grid[m] = {}
+        for S in invs:
+            t0 = time.time()
+            # enough identical layers that GPU time, not host launch time, dominates the difference
+            L = 2 if m >= 8192 else 17
+            p = paper_grid(m, S, L=L)
+            l0 = p.layers[0]
+            net = sd.Net(m, L)
+            dev = [torch.from_numpy(a).cuda() for a in (l0.row_ptr, l0.col, l0.val, l0.bias)]
+            del p.layers[:]
+            for k in range(L):
+                net.set_layer(k, *dev)  # every layer references the same device arrays
+            y = torch.from_numpy(p.y0_dense).cuda()
+            o = torch.empty_like(y)
+            rec = {"nnz": int(l0.nnz)}
+            arms = [("sparse", sd.SDNN_ARM_SPARSE)]
+            if not args.no_dense:
+                net.build_dense()
+                arms.append(("dense", sd.SDNN_ARM_DENSE))
+            for name, arm in arms:
+                for k1 in (1, L):
+                    net.forward_dense(y, k1=k1, arm=arm, out=o)
+                tl = time_calls(torch, lambda: net.forward_dense(y, k1=L, arm=arm, out=o), reps)
+                t1 = time_calls(torch, lambda: net.forward_dense(y, k1=1, arm=arm, out=o), reps)
+                rec[f"{name}_ms"] = round(max(tl - t1, 0.0) / (L - 1), 5)
+            grid[m][S] = rec
+            net.free()
+            del net, dev, y, o, l0, p
+            torch.cuda.empty_cache()
+            log(f"m {m} S {S}: nnz {rec['nnz']}, sparse {rec['sparse_ms']:.4f} ms, dense {rec.get('dense_ms')}, "
+                f"{time.time() - t0:.1f}s")
+    # scaling parameters, as in the paper's Fig. 7
+    params = {}
+    for m in sizes:
+        g = grid[m]
+        q = {}
+        if 1 in g and "dense_ms" in g[1]:
+            q["dense_per_element"] = g[1]["dense_ms"] / (m * m)
+            q["sparse_over_dense_at_S1"] = g[1]["sparse_ms"] / g[1]["dense_ms"] if g[1]["dense_ms"] > 0 else None
+        if 1 in g and 4 in g:
+            q["sparse_slope_per_nnz"] = (g[1]["sparse_ms"] - g[4]["sparse_ms"]) / (0.75 * m * m)
+        if 262144 in g:
+            q["saturation_per_row"] = g[262144]["sparse_ms"] / m
+        pts = [(S, v["sparse_ms"], v["dense_ms"]) for S, v in sorted(g.items())
+               if v.get("dense_ms") and v["sparse_ms"] > 0]
+        q["crossover_inv_sparsity"] = _crossover(pts)
+        params[m] = q
+    if 4096 in params:
+        ref = params[4096]
+        for m in sizes:
+            for key in ("dense_per_element", "sparse_over_dense_at_S1", "sparse_slope_per_nnz", "saturation_per_row"):
+                if params[m].get(key) is not None and ref.get(key):
+                    params[m][key + "_rel4096"] = params[m][key] / ref[key]
+    return grid, params
+
+
+
 def run_csr_config(args, torch, sd):
     """Configs 3-5 (sparse Y through the SpGEMM path) and config 1, one forward per step."""
     from workloads import make_config
@@ -253,6 +337,10 @@ def main():
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-W arm")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--paper-grid", action="store_true",
+                    help="time the paper's own grid (m x m weights, inverse sparsity 1..262144, batch 64)")
+    ap.add_argument("--grid-sizes", default="", help="comma-separated m values for --paper-grid")
+    ap.add_argument("--grid-inv", default="", help="comma-separated inverse sparsities for --paper-grid")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes 5 times (counter calibration)")
     args = ap.parse_args()
@@ -275,6 +363,17 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": args.copy_probe}), flush=True)
+        return
+    if args.paper_grid:
+        grid, params = run_paper_grid(args, torch, sd)
+        print(json.dumps({
+            "metric": "per-layer time (ms) of the CSR arm and the dense-W arm on the paper's grid, 1 MI355X",
+            "unit": "ms", "higher_is_better": False, "n_gpus": 1, "steps": max(3, args.steps), "dtype": "f64",
+            "data": "synthetic",
+            "config": {"workload": "paper-grid: m x m W, Bernoulli(1/S) pattern, U[-1,3) values, batch 64, b = 0"},
+            "grid": {str(m): {str(S): v for S, v in g.items()} for m, g in grid.items()},
+            "scaling_params": {str(m): v for m, v in params.items()},
+        }), flush=True)
         return
     if args.config == 2:
         r = run_sweep(args, torch, sd)

@@ -117,7 +117,10 @@ CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
 
 constexpr int64_t kMaxScan = 16777216;  // longest array the device prefix sum handles (fan-in pointers, row pointers)
 
-size_t dense_ws_bytes(int64_t n, int64_t batch) { return 2 * align_up((size_t)n * (size_t)batch * sizeof(float)); }
+// two n x batch fp32 activation buffers, then the dense arm's split-K partial sums (small batches only)
+size_t dense_ws_bytes(int64_t n, int64_t batch, int num_cu) {
+    return 2 * align_up((size_t)n * (size_t)batch * sizeof(float)) + align_up(sdnn::gemm_partial_bytes(n, batch, num_cu));
+}
 
 }  // namespace
 
@@ -304,7 +307,7 @@ sdnn_status sdnn_workspace_size(sdnn_net net, int64_t batch, int32_t y_is_csr, i
     if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
     if (!bytes) return fail(SDNN_ERR_NULL_POINTER, "bytes is NULL");
     if (batch < 0) return fail(SDNN_ERR_INVALID_VALUE, "batch must be >= 0");
-    *bytes = y_is_csr ? (int64_t)carve_csr(nullptr, net->n, batch).bytes : (int64_t)dense_ws_bytes(net->n, batch);
+    *bytes = y_is_csr ? (int64_t)carve_csr(nullptr, net->n, batch).bytes : (int64_t)dense_ws_bytes(net->n, batch, net->num_cu);
     return SDNN_OK;
 }
 
@@ -333,7 +336,7 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
         return SDNN_OK;
     }
     if (!ws) return fail(SDNN_ERR_NULL_POINTER, "ws is required");
-    if (ws_bytes < (int64_t)dense_ws_bytes(n, batch))
+    if (ws_bytes < (int64_t)dense_ws_bytes(n, batch, net->num_cu))
         return fail(SDNN_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than sdnn_workspace_size(net, batch, 0)");
     if (arm == SDNN_ARM_DENSE)
         for (int32_t k = k0; k < k1; ++k)
@@ -342,6 +345,7 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
     float *buf[2];
     buf[0] = (float *)ws;
     buf[1] = (float *)((char *)ws + align_up((size_t)n * (size_t)batch * sizeof(float)));
+    double *partial = (double *)((char *)ws + 2 * align_up((size_t)n * (size_t)batch * sizeof(float)));
     SDNN_HIP(sdnn::launch_transpose(Y_in, buf[0], batch, n, s));  // batch x n -> n x batch
     int cur = 0;
     for (int32_t k = k0; k < k1; ++k) {
@@ -350,7 +354,8 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
             SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax, buf[cur],
                                              buf[cur ^ 1], s));
         else
-            SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, l.dense_wt, l.bias, net->ymax, buf[cur], buf[cur ^ 1], s));
+            SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, l.dense_wt, l.bias, net->ymax, buf[cur], buf[cur ^ 1],
+                                                   partial, net->num_cu, s));
         cur ^= 1;
     }
     SDNN_HIP(sdnn::launch_transpose(buf[cur], Y_out, n, batch, s));  // n x batch -> batch x n

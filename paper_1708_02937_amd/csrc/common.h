@@ -56,8 +56,11 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, c
 
 // gemm.hip
 hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *wt, hipStream_t s);
+int gemm_splits(int64_t n, int64_t batch, int num_cu);
+size_t gemm_partial_bytes(int64_t n, int64_t batch, int num_cu);
+// partial: gemm_partial_bytes(n, batch, num_cu) bytes of scratch (unused when that is 0).
 hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, const double *wt, const float *bias, double ymax,
-                                   const float *yt, float *zt, hipStream_t s);
+                                   const float *yt, float *zt, double *partial, int num_cu, hipStream_t s);
 
 // spgemm.hip
 size_t spgemm_lds_bytes(int64_t n);

@@ -15,6 +15,10 @@
 // at a time through double-buffered LDS (one barrier per step): the next slab is loaded into registers
 // while the current one is multiplied and stored into the other buffer afterwards.  Rows of the LDS
 // slabs are padded by 16 doubles so the four k-rows an MFMA operand reads land on different banks.
+//
+// Small batches give few tiles (n = 4096, batch 64: 32 workgroups for 256 CUs), so K is then split over
+// blockIdx.z: each split writes its fp64 partial tile, and a second kernel adds the splits in a fixed
+// order, then the bias, h and the rounding.
 #include "common.h"
 
 namespace sdnn {
@@ -30,10 +34,10 @@ constexpr int kPad = 16;
 // loads need no guards and no branch depends on the thread; otherwise every element is guarded.
 template <bool kFast>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_dense_layer_kernel(int64_t M, int64_t N, int64_t K,
-                                                               const double *__restrict__ Wk,
+                                                               int64_t kc, const double *__restrict__ Wk,
                                                                const float *__restrict__ B,
                                                                const float *__restrict__ bias, double ymax,
-                                                               float *__restrict__ C) {
+                                                               float *__restrict__ C, double *__restrict__ partial) {
     __shared__ __align__(16) double As[2][BK][BM + kPad];
     __shared__ __align__(16) double Bs[2][BK][BN + kPad];
 
@@ -44,6 +48,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // blocks of W, and the batch blocks of one of them land on one XCD and share it in its L2.
     const int64_t m0 = (int64_t)blockIdx.x * BM;
     const int64_t n0 = (int64_t)blockIdx.y * BN;
+    const int64_t kb = (int64_t)blockIdx.z * kc;             // this split's K range [kb, ke)
+    const int64_t ke = kb + kc < K ? kb + kc : K;
 
     // global -> register staging: thread -> k row tid / 16, column pairs (tid % 16) * 2 + 32 q, q = 0..3,
     // so the 16 threads of a k row store one contiguous 256-byte run per q (no LDS bank conflicts)
@@ -68,8 +74,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
                     const int64_t gm = m0 + s_c + 32 * q + h, gc = n0 + s_c + 32 * q + h;
-                    ra[2 * q + h] = (gk < K && gm < M) ? Wk[gk * M + gm] : 0.0;
-                    rb[2 * q + h] = (gk < K && gc < N) ? B[gk * N + gc] : 0.0f;
+                    ra[2 * q + h] = (gk < ke && gm < M) ? Wk[gk * M + gm] : 0.0;
+                    rb[2 * q + h] = (gk < ke && gc < N) ? B[gk * N + gc] : 0.0f;
                 }
         }
     };
@@ -105,15 +111,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         }
     };
 
-    const int64_t ktiles = (K + BK - 1) / BK;
-    load_tiles(0);
+    const int64_t ktiles = (ke - kb + BK - 1) / BK;  // >= 1: the launcher gives every split some of K
+    load_tiles(kb);
     store_tiles(0);
     __syncthreads();
     // steady state: the next slab is loaded while this one is multiplied, then stored into the other
     // buffer (last read one step earlier, before the barrier); the final step is peeled off
     for (int64_t kt = 0; kt + 1 < ktiles; ++kt) {
         const int cur = (int)(kt & 1);
-        load_tiles((kt + 1) * BK);
+        load_tiles(kb + (kt + 1) * BK);
         compute(cur);
         store_tiles(cur ^ 1);
         __syncthreads();
@@ -129,8 +135,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             for (int v = 0; v < 4; ++v) {
                 const int64_t m = m0 + wm * 64 + mi * 16 + kq + 4 * v;
                 const int64_t col = n0 + wn * 64 + ni * 16 + rc;
-                if (kFast || (m < M && col < N)) C[m * N + col] = activate(acc[mi][ni][v] + (double)bias[m], ymax);
+                if (kFast || (m < M && col < N)) {
+                    if (partial)
+                        partial[((int64_t)blockIdx.z * M + m) * N + col] = acc[mi][ni][v];
+                    else
+                        C[m * N + col] = activate(acc[mi][ni][v] + (double)bias[m], ymax);
+                }
             }
+}
+
+// Sum of the K splits in split order, then the bias, h and one rounding.
+__global__ void gemm_split_reduce_kernel(int64_t M, int64_t N, int splits, const double *__restrict__ partial,
+                                         const float *__restrict__ bias, double ymax, float *__restrict__ C) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= M * N) return;
+    double z = 0.0;
+    for (int sp = 0; sp < splits; ++sp) z += partial[(int64_t)sp * M * N + e];
+    C[e] = activate(z + (double)bias[e / N], ymax);
 }
 
 // Dense W_k (n_in x n_out, row-major, fp64) with explicit zeros: row i holds the fan-out of input i.
@@ -152,16 +173,42 @@ hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge
     return hipGetLastError();
 }
 
+// K splits for an n x n layer on `batch` samples: enough workgroups for two per CU, at least 8 K steps each.
+int gemm_splits(int64_t n, int64_t batch, int num_cu) {
+    const int64_t tiles = ((n + BM - 1) / BM) * ((batch + BN - 1) / BN);
+    if (tiles == 0 || tiles >= num_cu) return 1;
+    int64_t sp = (2 * (int64_t)num_cu + tiles - 1) / tiles;
+    const int64_t most = n / (8 * BK);
+    if (sp > most) sp = most;
+    if (sp > 64) sp = 64;
+    return sp < 1 ? 1 : (int)sp;
+}
+
+size_t gemm_partial_bytes(int64_t n, int64_t batch, int num_cu) {
+    const int sp = gemm_splits(n, batch, num_cu);
+    return sp > 1 ? (size_t)sp * (size_t)n * (size_t)batch * sizeof(double) : 0;
+}
+
 hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, const double *wt, const float *bias, double ymax,
-                                   const float *yt, float *zt, hipStream_t s) {
+                                   const float *yt, float *zt, double *partial, int num_cu, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
     const int64_t gx = (n + BM - 1) / BM, gy = (batch + BN - 1) / BN;
     if (gx > 0x7fffffffLL || gy > 65535) return hipErrorInvalidValue;
+    int sp = gemm_splits(n, batch, num_cu);
+    // split length in whole K steps; the last split may be shorter, none is empty
+    const int64_t steps = (n + BK - 1) / BK;
+    const int64_t kc = ((steps + sp - 1) / sp) * BK;
+    sp = (int)((n + kc - 1) / kc);
+    double *part = sp > 1 ? partial : nullptr;
     const bool fast = n % BM == 0 && batch % BN == 0 && n % BK == 0;
+    const dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)sp);
     if (fast)
-        gemm_dense_layer_kernel<true><<<dim3((unsigned)gx, (unsigned)gy), 256, 0, s>>>(n, batch, n, wt, yt, bias, ymax, zt);
+        gemm_dense_layer_kernel<true><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
     else
-        gemm_dense_layer_kernel<false><<<dim3((unsigned)gx, (unsigned)gy), 256, 0, s>>>(n, batch, n, wt, yt, bias, ymax, zt);
+        gemm_dense_layer_kernel<false><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || sp == 1) return e;
+    gemm_split_reduce_kernel<<<(unsigned)((n * batch + 255) / 256), 256, 0, s>>>(n, batch, sp, partial, bias, ymax, zt);
     return hipGetLastError();
 }
 

@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 from tests import parity
-from workloads import Layer, csr_rows, dense_to_csr, integer_shadow, make_config, tiny_random
+from workloads import Layer, csr_rows, dense_to_csr, integer_shadow, make_config, paper_grid, tiny_random
 
 pytestmark = pytest.mark.gpu
 
@@ -94,6 +94,15 @@ def test_tiny_csr_batch(sd, seed, n, L, batch):
                     explicit_zeros=seed % 3 == 0)
     _say("tiny csr", seed, n, L, batch)
     parity.compare(p, run_csr(sd, p))
+
+
+@pytest.mark.parametrize("arm", ARMS)
+@pytest.mark.parametrize("m,S", [(256, 1), (512, 2), (512, 16), (1024, 4), (1024, 1024), (2048, 262144)])
+def test_paper_grid_points(sd, arm, m, S):
+    """Single layers of the paper's own matrix family (Sec. V.B) on both arms, batch 64."""
+    p = paper_grid(m, S)
+    _say("paper grid", arm, m, S)
+    parity.compare(p, dense_to_csr(run_dense(sd, p, _arm(sd, arm))))
 
 
 def test_long_fanin_lists(sd):

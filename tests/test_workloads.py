@@ -5,7 +5,7 @@ import math
 import numpy as np
 import pytest
 
-from workloads import csr_rows, dense_to_csr, integer_shadow, make_config, tiny_random
+from workloads import csr_rows, dense_to_csr, integer_shadow, make_config, paper_grid, tiny_random
 
 
 def _same(p, q):
@@ -107,3 +107,26 @@ def test_csr_helpers():
     back = dense_to_csr(dense[[3, 0, 8]])
     for a, b in zip(sub, back):
         assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("m,S", [(256, 1), (512, 2), (1024, 4), (2048, 64), (512, 262144), (4096, 262144)])
+def test_paper_grid_recipe(m, S):
+    """The paper's matrices (Sec. V.B): Bernoulli(1/S) pattern over m x m, values U[-1,3), Y U[0,1),
+    64 samples; the nonzero count lies within 5 standard deviations of m^2 / S."""
+    p = paper_grid(m, S, L=2)
+    q = paper_grid(m, S, L=2)
+    _same(p, q)
+    assert p.n == m and p.batch == 64 and p.L == 2 and p.layers[0] is p.layers[1]
+    l = p.layers[0]
+    _check_csr(l.row_ptr, l.col, m)
+    mean = m * m / S
+    sd = math.sqrt(m * m * (1.0 / S) * (1.0 - 1.0 / S))
+    assert abs(l.nnz - mean) <= 5 * sd + 1
+    if S == 1:
+        assert l.nnz == m * m
+    if l.nnz:
+        assert l.val.dtype == np.float32 and l.val.min() >= -1.0 and l.val.max() < 3.0
+    assert np.all(l.bias == 0)
+    y = p.y0_dense
+    assert y.shape == (64, m) and y.min() >= 0.0 and y.max() < 1.0
+    assert paper_grid(m, S).layers[0].col.tobytes() == l.col.tobytes()  # L does not change the draw

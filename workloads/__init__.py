@@ -11,6 +11,9 @@ from .gen import (  # noqa: F401
     SEED_ROOT,
     CONFIG_NAMES,
     make_config,
+    paper_grid,
+    PAPER_GRID_SIZES,
+    PAPER_GRID_INV_SPARSITY,
     tiny_random,
     integer_shadow,
     dense_to_csr,

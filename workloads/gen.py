@@ -37,7 +37,13 @@ CONFIG_NAMES = {
     3: "sparse-activation-spgemm",
     4: "deep-sparse",
     5: "very-wide",
+    6: "paper-grid",
 }
+
+# The paper's own experiment (Sec. V.B-C): square m x m weights over a range of sizes and inverse
+# sparsities (total entries / nonzeros) from 1 to 262144, dense Y with 64 samples.
+PAPER_GRID_SIZES = (256, 512, 1024, 2048, 4096, 8192, 16384, 32768)
+PAPER_GRID_INV_SPARSITY = (1, 2, 4, 16, 64, 256, 1024, 4096, 16384, 65536, 262144)
 
 CONFIG2_DENSITIES = (0.5, 0.1, 0.01, 0.001)
 
@@ -150,10 +156,19 @@ def _bernoulli_csr(rng, rows: int, cols: int, p: float):
     cols_out, counts = [], np.zeros(rows, dtype=np.int64)
     for r0 in range(0, rows, block):
         nr = min(block, rows - r0)
-        pos = _bernoulli_positions(rng, nr * cols, p)
-        r = pos // cols
-        cols_out.append((pos - r * cols).astype(np.int32))
-        counts[r0:r0 + nr] = np.bincount(r, minlength=nr)
+        if p >= 1.0:
+            cols_out.append(np.tile(np.arange(cols, dtype=np.int32), nr))
+            counts[r0:r0 + nr] = cols
+        elif p >= 0.05:
+            # the same uniforms as _bernoulli_positions draws, read as a 2-D mask
+            mask = (rng.random(nr * cols, dtype=np.float32) < np.float32(p)).reshape(nr, cols)
+            cols_out.append(np.nonzero(mask)[1].astype(np.int32))
+            counts[r0:r0 + nr] = mask.sum(axis=1)
+        else:
+            pos = _bernoulli_positions(rng, nr * cols, p)
+            r = pos // cols
+            cols_out.append((pos - r * cols).astype(np.int32))
+            counts[r0:r0 + nr] = np.bincount(r, minlength=nr)
     row_ptr = np.zeros(rows + 1, dtype=np.int64)
     np.cumsum(counts, out=row_ptr[1:])
     return row_ptr, (np.concatenate(cols_out) if cols_out else np.zeros(0, np.int32))
@@ -286,6 +301,28 @@ def make_config(config_id: int, density: float | None = None, *, n: int | None =
                        meta={"config": 5, "block": blk})
 
     raise ValueError(f"unknown config {config_id}")
+
+
+def paper_grid(m: int, inv_sparsity: int, *, batch: int = 64, L: int = 1) -> Problem:
+    """One point of the paper's experiment (Sec. V.B): W is m x m with an independent Bernoulli pattern of
+    density 1 / inv_sparsity and values U[-1, 3); Y_0 is batch x m with values U[0, 1); batch 64.
+
+    The paper does not state the bias of its timing runs; b = 0 here.  All L layers share one W (the paper
+    times one iteration of the layer loop; identical layers let a benchmark difference out the fixed cost
+    of entering and leaving the loop).  Values grow layer by layer, as the paper notes for this matrix
+    family, so only the first layer is meaningful numerically.
+    """
+    if m < 1 or inv_sparsity < 1:
+        raise ValueError("m and inv_sparsity must be >= 1")
+    variant = m * 1000003 + inv_sparsity
+    rng = _rng(6, 0, variant)
+    row_ptr, col = _bernoulli_csr(rng, m, m, 1.0 / inv_sparsity)
+    # U[-1, 3) exactly in float32: 4 * U[0, 1) - 1 is exact and at most 3 - 2^-22
+    val = rng.random(len(col), dtype=np.float32) * np.float32(4.0) - np.float32(1.0)
+    layer = Layer(row_ptr, col, val, np.zeros(m, np.float32))
+    y = _rng(6, 1, variant).random((batch, m), dtype=np.float32)
+    return Problem(f"paper-grid-m{m}-S{inv_sparsity}", m, L, batch, math.inf, [layer] * L, y0_dense=y,
+                   meta={"config": 6, "m": m, "inv_sparsity": inv_sparsity})
 
 
 def integer_shadow(p: Problem, seed_variant: int = 7) -> Problem:
