@@ -59,7 +59,7 @@ def load(path: str | None = None):
 def _declare(lib):
     lib.oracle_forward.restype = ctypes.c_int
     lib.oracle_forward.argtypes = [
-        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_Layer), ctypes.c_double,
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_Layer), ctypes.c_double, ctypes.c_int,
         ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
     lib.oracle_preact.restype = ctypes.c_int
@@ -90,8 +90,11 @@ def default_threads() -> int:
 
 
 def forward(n: int, layers, ymax: float, y_csr, k0: int = 0, k1: int | None = None,
-            threads: int | None = None, trace: bool = False, lib=None):
+            threads: int | None = None, trace: bool = False, lib=None, bias_mode: int = 0):
     """Y_{k1} for the CSR rows `y_csr` = (row_ptr, col, val) taken as Y_{k0}.
+
+    bias_mode 0 adds the bias at every position (the dense equation); 1 only where Y_k W_k has a
+    structural entry (the pattern semantics of the Fig. 4 listing).
 
     Returns the output CSR (row_ptr int64, col int32, val float32); with
     ``trace=True`` also the per-layer nnz of Y_{k0+1} .. Y_{k1} summed over rows.
@@ -108,7 +111,7 @@ def forward(n: int, layers, ymax: float, y_csr, k0: int = 0, k1: int | None = No
     oc = np.empty(max(1, nrows * n), dtype=np.int32)
     ov = np.empty(max(1, nrows * n), dtype=np.float32)
     lnnz = np.zeros(max(1, k1 - k0), dtype=np.int64)
-    rc = lib.oracle_forward(n, k0, k1, ls, float(ymax), nrows, row_ptr.ctypes.data, _ptr(col), _ptr(val),
+    rc = lib.oracle_forward(n, k0, k1, ls, float(ymax), int(bias_mode), nrows, row_ptr.ctypes.data, _ptr(col), _ptr(val),
                             cnt.ctypes.data, oc.ctypes.data, ov.ctypes.data, lnnz.ctypes.data,
                             threads or default_threads())
     if rc != 0:

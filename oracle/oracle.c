@@ -15,8 +15,15 @@
  * Y is batch x n (one sample per row) and W_k is stored n_in x n_out in CSR,
  * so row i of W_k is the fan-out of input neuron i.  The optional clamp
  * h(y) = min(max(y, 0), ymax) generalises the ReLU (ymax = +inf is the
- * paper's h).  The bias is added at every position, as the dense equation
- * states, including positions that receive no product.
+ * paper's h).  Bias placement has two readings, chosen per call:
+ *   bias_mode 0 (default): the bias is added at every position, as the dense
+ *     equation states, including positions that receive no product;
+ *   bias_mode 1: the bias is added only where Y_k W_k has a structural entry,
+ *     the pattern semantics of Fig. 4 (Sec. IV): eWiseMult over max.+ with the
+ *     bias matrix keeps only the entries both operands store, and eWiseAdd
+ *     with the all-zero matrix leaves 0 elsewhere.  A position is structural
+ *     when some stored entry W(i, j) meets a nonzero Y(r, i): activations are
+ *     stored as their nonzeros (zeros pruned after every layer), W as its CSR.
  *
  * Arithmetic: the product of two fp32 values is exact in fp64; the products of
  * one output entry are summed in fp64 in ascending order of the sample's
@@ -54,13 +61,14 @@ typedef struct {
     int32_t *out_col;
     float *out_val;
     int64_t *layer_nnz; /* optional: nnz of Y_{k+1} summed over rows, per layer */
+    int bias_mode;      /* 0: bias everywhere; 1: bias on the structural pattern only */
     int64_t next_row;   /* shared work counter */
     int status;
 } forward_job;
 
 /* One sample through layers [k0, k1).  cur/nxt hold sorted (index, value) lists. */
-static void forward_one_row(forward_job *job, int64_t r, double *acc, int32_t *cur_col, float *cur_val,
-                            int32_t *nxt_col, float *nxt_val, int64_t *layer_cnt)
+static void forward_one_row(forward_job *job, int64_t r, double *acc, char *touched, int32_t *cur_col,
+                            float *cur_val, int32_t *nxt_col, float *nxt_val, int64_t *layer_cnt)
 {
     const int64_t n = job->n;
     int64_t cur_len = 0;
@@ -73,15 +81,19 @@ static void forward_one_row(forward_job *job, int64_t r, double *acc, int32_t *c
         const oracle_layer *W = &job->layers[k];
         /* Y_k W_k for this row: acc(j) = sum_i y(i) * W(i, j) */
         for (int64_t j = 0; j < n; ++j) acc[j] = 0.0;
+        if (job->bias_mode) memset(touched, 0, (size_t)n);
         for (int64_t t = 0; t < cur_len; ++t) {
             const int32_t i = cur_col[t];
             const double y = (double)cur_val[t];
-            for (int64_t e = W->row_ptr[i]; e < W->row_ptr[i + 1]; ++e)
+            for (int64_t e = W->row_ptr[i]; e < W->row_ptr[i + 1]; ++e) {
                 acc[W->col[e]] += y * (double)W->val[e];
+                if (y != 0.0) touched[W->col[e]] = 1;
+            }
         }
         /* + b, then h, then round once to fp32; keep only nonzeros */
         int64_t nxt_len = 0;
         for (int64_t j = 0; j < n; ++j) {
+            if (job->bias_mode && !touched[j]) continue; /* no structural entry: stays 0 */
             double z = acc[j] + (double)W->bias[j];
             if (z < 0.0) z = 0.0;
             if (z > job->ymax) z = job->ymax;
@@ -108,23 +120,24 @@ static void *forward_worker(void *arg)
     const int64_t n = job->n;
     const int32_t nl = job->k1 - job->k0;
     double *acc = (double *)malloc((size_t)n * sizeof(double));
+    char *touched = (char *)calloc((size_t)n, 1);
     int32_t *c0 = (int32_t *)malloc((size_t)n * sizeof(int32_t));
     int32_t *c1 = (int32_t *)malloc((size_t)n * sizeof(int32_t));
     float *v0 = (float *)malloc((size_t)n * sizeof(float));
     float *v1 = (float *)malloc((size_t)n * sizeof(float));
     int64_t *cnt = job->layer_nnz ? (int64_t *)calloc((size_t)(nl > 0 ? nl : 1), sizeof(int64_t)) : NULL;
-    if (!acc || !c0 || !c1 || !v0 || !v1 || (job->layer_nnz && !cnt)) {
+    if (!acc || !touched || !c0 || !c1 || !v0 || !v1 || (job->layer_nnz && !cnt)) {
         __atomic_store_n(&job->status, -2, __ATOMIC_SEQ_CST);
     } else {
         for (;;) {
             const int64_t r = __atomic_fetch_add(&job->next_row, 1, __ATOMIC_SEQ_CST);
             if (r >= job->nrows) break;
-            forward_one_row(job, r, acc, c0, v0, c1, v1, cnt);
+            forward_one_row(job, r, acc, touched, c0, v0, c1, v1, cnt);
         }
         if (cnt)
             for (int32_t k = 0; k < nl; ++k) __atomic_fetch_add(&job->layer_nnz[k], cnt[k], __ATOMIC_SEQ_CST);
     }
-    free(acc); free(c0); free(c1); free(v0); free(v1); free(cnt);
+    free(acc); free(touched); free(c0); free(c1); free(v0); free(v1); free(cnt);
     return NULL;
 }
 
@@ -157,14 +170,15 @@ static int run_threads(void *(*fn)(void *), void *job, int nthreads)
 /*
  * Y_{k1} from Y_{k0} for `nrows` samples given as CSR rows (columns ascending).
  * Output row r goes to out_col/out_val[r*n .. r*n + out_count[r]) with ascending
- * columns and no stored zeros.  Returns 0, -1 on invalid input, -2 on
- * allocation failure.
+ * columns and no stored zeros.  bias_mode selects the bias reading (see the
+ * top of this file).  Returns 0, -1 on invalid input, -2 on allocation failure.
  */
-int oracle_forward(int64_t n, int32_t k0, int32_t k1, const oracle_layer *layers, double ymax, int64_t nrows,
-                   const int64_t *y_row_ptr, const int32_t *y_col, const float *y_val, int64_t *out_count,
-                   int32_t *out_col, float *out_val, int64_t *layer_nnz, int nthreads)
+int oracle_forward(int64_t n, int32_t k0, int32_t k1, const oracle_layer *layers, double ymax, int bias_mode,
+                   int64_t nrows, const int64_t *y_row_ptr, const int32_t *y_col, const float *y_val,
+                   int64_t *out_count, int32_t *out_col, float *out_val, int64_t *layer_nnz, int nthreads)
 {
     if (n <= 0 || k0 < 0 || k1 < k0 || nrows < 0 || !y_row_ptr || !out_count || !out_col || !out_val) return -1;
+    if (bias_mode != 0 && bias_mode != 1) return -1;
     for (int32_t k = k0; k < k1; ++k)
         if (check_layer(n, &layers[k])) return -1;
     for (int64_t r = 0; r < nrows; ++r) {
@@ -175,7 +189,7 @@ int oracle_forward(int64_t n, int32_t k0, int32_t k1, const oracle_layer *layers
     if (layer_nnz)
         for (int32_t k = k0; k < k1; ++k) layer_nnz[k - k0] = 0;
     forward_job job = {n, k0, k1, layers, ymax, nrows, y_row_ptr, y_col, y_val,
-                       out_count, out_col, out_val, layer_nnz, 0, 0};
+                       out_count, out_col, out_val, layer_nnz, bias_mode, 0, 0};
     if (run_threads(forward_worker, &job, nthreads)) return -2;
     return job.status;
 }

@@ -11,8 +11,15 @@
   product W_k Y_k) on generic semiring objects, so it checks both the
   two-semiring rewrite (Sec. III) and our transposed orientation.
 
-Both run in fp64 and round to fp32 once per layer, like the oracle, so on the
-same inputs all three must agree bit for bit.
+* `fig4_forward_pattern` is the same listing with GraphBLAS pattern semantics:
+  matrices are dictionaries of stored entries, mxm stores an entry only where
+  some stored W entry meets a stored Y entry, eWiseMult with the (full) bias
+  matrix is an intersection and eWiseAdd with the (full) zero matrix a union;
+  activations are stored as their nonzeros.  It pins the oracle's
+  bias-on-the-pattern mode.
+
+All run in fp64 and round to fp32 once per layer, like the oracle, so on the
+same inputs they must agree with it bit for bit.
 """
 
 from __future__ import annotations
@@ -89,3 +96,35 @@ def fig4_forward(Y0, Ws, bs):
         Z = ewise(Z, zero, S2.add)  # max(..., 0) (S2's add is max)
         Yp = [[_to_f32(v) for v in row] for row in Z]
     return np.array([list(col) for col in zip(*Yp)], dtype=np.float32)
+
+
+def fig4_forward_pattern(Y0, W_entries, bs, ymax=math.inf):
+    """Y_L via the listing with pattern semantics, in the paper's orientation (neurons x batch).
+
+    Y0: batch x n dense (its nonzeros are the stored entries); W_entries[k]: list of stored (i, j, w)
+    of W_k (input i -> output j, explicit zeros allowed); bs[k]: bias vector.
+    """
+    nb, n = len(Y0), len(Y0[0])
+    Y = {(i, r): float(Y0[r][i]) for r in range(nb) for i in range(n) if Y0[r][i] != 0}
+    for Wl, b in zip(W_entries, bs):
+        # paper's W_k is our W transposed: Wp(j, i) = W(i, j); mxm over S1 stores (j, r) when some
+        # stored Wp(j, i) meets a stored Y(i, r)
+        by_input = {}
+        for i, j, w in Wl:
+            by_input.setdefault(i, []).append((j, float(w)))
+        Z = {}
+        for (i, r), y in sorted(Y.items()):
+            for j, w in by_input.get(i, ()):
+                Z[(j, r)] = S1.add(Z.get((j, r), S1.zero), S1.mul(w, y))
+        # eWiseMult over S2 with the full bias matrix: intersection keeps Z's pattern, value z + b_j
+        Z = {(j, r): S2.mul(z, float(b[j])) for (j, r), z in Z.items()}
+        # eWiseAdd over S2 with the full zero matrix: union; on Z's pattern max(z, 0), elsewhere 0
+        Y = {}
+        for (j, r), z in Z.items():
+            v = _to_f32(min(S2.add(z, 0.0), ymax))
+            if v != 0.0:
+                Y[(j, r)] = v  # stored as nonzeros
+    out = np.zeros((nb, n), dtype=np.float32)
+    for (j, r), v in Y.items():
+        out[r, j] = v
+    return out

@@ -24,8 +24,10 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 _ACC_BLOCK = """        for (int64_t t = 0; t < cur_len; ++t) {
             const int32_t i = cur_col[t];
             const double y = (double)cur_val[t];
-            for (int64_t e = W->row_ptr[i]; e < W->row_ptr[i + 1]; ++e)
+            for (int64_t e = W->row_ptr[i]; e < W->row_ptr[i + 1]; ++e) {
                 acc[W->col[e]] += y * (double)W->val[e];
+                if (y != 0.0) touched[W->col[e]] = 1;
+            }
         }"""
 
 _TRANSPOSED = """        for (int64_t t = 0; t < cur_len; ++t) {
@@ -33,7 +35,10 @@ _TRANSPOSED = """        for (int64_t t = 0; t < cur_len; ++t) {
             const double y = (double)cur_val[t];
             for (int64_t j2 = 0; j2 < n; ++j2)
                 for (int64_t e = W->row_ptr[j2]; e < W->row_ptr[j2 + 1]; ++e)
-                    if (W->col[e] == i) acc[j2] += y * (double)W->val[e];
+                    if (W->col[e] == i) {
+                        acc[j2] += y * (double)W->val[e];
+                        if (y != 0.0) touched[j2] = 1;
+                    }
         }"""
 
 MUTANTS = {
@@ -42,14 +47,17 @@ MUTANTS = {
     "transposed_W": (_ACC_BLOCK, _TRANSPOSED),
     "no_relu": ("if (z < 0.0) z = 0.0;", ""),
     "no_clamp": ("if (z > job->ymax) z = job->ymax;", ""),
-    "skip_last_weight": ("e < W->row_ptr[i + 1]; ++e)\n                acc",
-                         "e + 1 < W->row_ptr[i + 1]; ++e)\n                acc"),
+    "skip_last_weight": ("e < W->row_ptr[i + 1]; ++e) {\n                acc",
+                         "e + 1 < W->row_ptr[i + 1]; ++e) {\n                acc"),
     "skip_first_input": ("for (int64_t t = 0; t < cur_len; ++t) {\n            const int32_t i",
                          "for (int64_t t = 1; t < cur_len; ++t) {\n            const int32_t i"),
     "fp32_accumulate": ("acc[W->col[e]] += y * (double)W->val[e];",
                         "acc[W->col[e]] = (float)(acc[W->col[e]] + (float)(y * (double)W->val[e]));"),
     "bias_index": ("(double)W->bias[j];\n            if (z < 0.0)", "(double)W->bias[0];\n            if (z < 0.0)"),
     "keep_zero": ("if (f != 0.0f) {", "if (f != 0.0f || j == 0) {"),
+    "pattern_bias_everywhere": ("if (job->bias_mode && !touched[j]) continue;", ""),
+    "pattern_touch_zero_inputs": ("if (y != 0.0) touched[W->col[e]] = 1;", "touched[W->col[e]] = 1;"),
+    "pattern_never_touch": ("if (y != 0.0) touched[W->col[e]] = 1;", ""),
 }
 
 
@@ -87,6 +95,19 @@ def battery(lib):
         want = dense_to_csr(Yi.astype(np.float32))  # canonical CSR of the exact answer
         if not (np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])):
             failed.append("integer_shadow_pattern")
+        # bias on the structural pattern (reading B): the hand example, and the pattern-semantics listing
+        # on random inputs with positive biases and explicit zeros in Y_0
+        out = oracle.forward(3, lay, math.inf, y0, lib=lib, bias_mode=1)
+        if not np.array_equal(oracle.csr_to_dense(out, 3), np.array(g["pattern_bias"]["Y2"], np.float32)):
+            failed.append("hand_pattern")
+        for seed in (3, 4):
+            p = tiny_random(seed, 19, 3, 5, w_density=0.15, y_density=0.3, bias_lo=-0.2, bias_hi=0.6,
+                            explicit_zeros=True)
+            y0d = oracle.csr_to_dense(p.y0_csr, 19)
+            got = oracle.forward(19, p.layers, math.inf, p.y0_csr, lib=lib, bias_mode=1)
+            want = brute.fig4_forward_pattern(y0d, [l.entries() for l in p.layers], [l.bias for l in p.layers])
+            if oracle.csr_to_dense(got, 19).tobytes() != want.tobytes():
+                failed.append(f"pattern{seed}")
     except ValueError:
         failed.append("error")
     return failed

@@ -274,3 +274,49 @@ def test_rejects_bad_input():
         c2[0], c2[1] = c2[1], c2[0]
         with pytest.raises(ValueError):
             oracle.forward(10, [l], math.inf, (rp, c2, v))
+
+
+# --------------------------------------------------------------------------- bias on the structural pattern
+
+
+def test_pattern_bias_hand_example():
+    """Reading (B) of the bias (Fig. 4 pattern semantics) on the worked example, two layers."""
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    layers = _layers_from_dense([g["W"]] * 2, [g["b"]] * 2)
+    pb = g["pattern_bias"]
+    assert np.array_equal(_run(3, layers[:1], math.inf, g["Y0"], bias_mode=1), np.array(pb["Y1"], np.float32))
+    assert np.array_equal(_run(3, layers, math.inf, g["Y0"], bias_mode=1), np.array(pb["Y2"], np.float32))
+
+
+@pytest.mark.parametrize("seed", [5, 6, 7, 8])
+def test_pattern_bias_equals_pattern_listing(seed):
+    """The oracle's pattern mode equals the listing run on dictionaries of stored entries, bit for bit,
+    with positive biases, explicit zeros in W and Y_0, and a clamp."""
+    n = 23
+    ymax = [math.inf, 1.25][seed % 2]
+    p = tiny_random(seed, n, 3, 6, w_density=0.12, y_density=0.3, bias_lo=-0.3, bias_hi=0.8,
+                    explicit_zeros=True, ymax=ymax)
+    y0d = oracle.csr_to_dense(p.y0_csr, n)
+    got = oracle.csr_to_dense(oracle.forward(n, p.layers, ymax, p.y0_csr, bias_mode=1), n)
+    want = brute.fig4_forward_pattern(y0d, [l.entries() for l in p.layers], [l.bias for l in p.layers], ymax)
+    assert got.tobytes() == want.tobytes()
+
+
+@pytest.mark.parametrize("seed", [9, 10])
+def test_pattern_bias_invariants(seed):
+    """With every b <= 0 the two readings agree; otherwise the pattern reading stores a subset of the
+    structural product pattern, and a row with nothing stored stays empty."""
+    n = 40
+    p = tiny_random(seed, n, 3, 8, w_density=0.06, y_density=0.1, bias_lo=-0.5, bias_hi=0.0)
+    a = oracle.forward(n, p.layers, math.inf, p.y0_csr)
+    b = oracle.forward(n, p.layers, math.inf, p.y0_csr, bias_mode=1)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    q = tiny_random(seed, n, 1, 8, w_density=0.06, y_density=0.1, bias_lo=0.1, bias_hi=0.5)
+    y0d = oracle.csr_to_dense(q.y0_csr, n)
+    y0d[0] = 0.0  # an empty sample
+    out = oracle.csr_to_dense(oracle.forward(n, q.layers, math.inf, dense_to_csr(y0d), bias_mode=1), n)
+    struct = ((y0d != 0).astype(np.int64) @ (q.layers[0].to_dense(n) != 0).astype(np.int64)) > 0
+    assert np.all(out[~struct] == 0)
+    assert np.all(out[0] == 0)
+    dense_a = oracle.csr_to_dense(oracle.forward(n, q.layers, math.inf, dense_to_csr(y0d)), n)
+    assert np.array_equal(out[struct], dense_a[struct])  # on the pattern both readings agree

@@ -71,6 +71,11 @@ class Layer:
         w[rows, self.col] = self.val
         return w
 
+    def entries(self):
+        """Stored entries as (i, j, w) triples (explicit zeros included)."""
+        rows = np.repeat(np.arange(len(self.row_ptr) - 1), np.diff(self.row_ptr))
+        return [(int(i), int(j), float(w)) for i, j, w in zip(rows, self.col, self.val)]
+
 
 @dataclass
 class Problem:
