@@ -64,6 +64,16 @@ enum {
     SDNN_ARM_DENSE = 1   /* dense W_k with explicit zeros on the matrix cores (Sec. V dense baseline) */
 };
 
+/* Where the bias b_k is added (sdnn_net_set_bias_mode). */
+enum {
+    SDNN_BIAS_EVERYWHERE = 0, /* every position, as the dense equation states (Sec. III); the default */
+    SDNN_BIAS_PATTERN = 1     /* only where Y_k W_k has a structural entry: some stored W_k(i, j) meets a
+                                 nonzero Y_k(r, i).  This is the Fig. 4 listing read with GraphBLAS
+                                 pattern semantics (Sec. IV: eWiseMult with the bias matrix keeps the
+                                 pattern of Y_k W_k, eWiseAdd with the zero matrix leaves 0 elsewhere),
+                                 with activations stored as their nonzeros. */
+};
+
 typedef struct sdnn_net_s *sdnn_net;
 
 /*
@@ -78,6 +88,16 @@ sdnn_status sdnn_net_create(sdnn_net *net, int64_t n, int32_t L, float ymax, voi
 
 /* Replace the stream later work is enqueued on. */
 sdnn_status sdnn_net_set_stream(sdnn_net net, void *stream);
+
+/*
+ * Select where the bias is added (SDNN_BIAS_EVERYWHERE or SDNN_BIAS_PATTERN)
+ * for later forward calls.  The two readings differ only at positions with no
+ * structural product and b_j > 0.  The dense arm (SDNN_ARM_DENSE) stores every
+ * zero of W_k, so it computes SDNN_BIAS_EVERYWHERE only; a dense-arm forward
+ * in pattern mode fails with UNSUPPORTED.
+ * Errors: INVALID_OBJECT, INVALID_VALUE (unknown mode).
+ */
+sdnn_status sdnn_net_set_bias_mode(sdnn_net net, int32_t mode);
 
 /*
  * Set layer k (0 <= k < L) from a CSR W_k (n_in x n_out, row i = fan-out of
@@ -117,7 +137,7 @@ sdnn_status sdnn_workspace_size(sdnn_net net, int64_t batch, int32_t y_is_csr, i
  * bytes that the call may overwrite.  Asynchronous on the net's stream; no
  * host synchronisation.  k0 == k1 copies Y_in to Y_out.
  * Errors: INVALID_OBJECT, NULL_POINTER, DIMENSION_MISMATCH, INVALID_VALUE (arm),
- * WORKSPACE_TOO_SMALL, DEVICE.
+ * WORKSPACE_TOO_SMALL, UNSUPPORTED (dense arm with SDNN_BIAS_PATTERN), DEVICE.
  */
 sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const float *Y_in,
                                float *Y_out, void *ws, int64_t ws_bytes, int32_t arm);

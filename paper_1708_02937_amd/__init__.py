@@ -22,6 +22,8 @@ LIB_PATH = os.path.join(_HERE, "libsdnn.so")
 SDNN_OK = 0
 SDNN_ARM_SPARSE = 0
 SDNN_ARM_DENSE = 1
+SDNN_BIAS_EVERYWHERE = 0
+SDNN_BIAS_PATTERN = 1
 
 STATUS_NAMES = {
     0: "SDNN_OK", 1: "SDNN_ERR_NULL_POINTER", 2: "SDNN_ERR_INVALID_VALUE", 3: "SDNN_ERR_INVALID_INDEX",
@@ -48,6 +50,7 @@ _I32 = _c.c_int32
 _sig = {
     "sdnn_net_create": [_c.POINTER(_P), _I64, _I32, _c.c_float, _P],
     "sdnn_net_set_stream": [_P, _P],
+    "sdnn_net_set_bias_mode": [_P, _I32],
     "sdnn_net_set_layer": [_P, _I32, _I64, _P, _P, _P, _P],
     "sdnn_net_build_dense": [_P],
     "sdnn_workspace_size": [_P, _I64, _I32, _c.POINTER(_I64)],
@@ -96,6 +99,10 @@ def sdnn_net_create(n: int, L: int, ymax: float = math.inf, stream=None):
 
 def sdnn_net_set_stream(net, stream):
     _check(lib.sdnn_net_set_stream(net, _ptr(stream)))
+
+
+def sdnn_net_set_bias_mode(net, mode: int):
+    _check(lib.sdnn_net_set_bias_mode(net, mode))
 
 
 def sdnn_net_set_layer(net, k: int, nnz: int, row_ptr, col_idx, val, bias):
@@ -161,6 +168,9 @@ class Net:
     def build_dense(self):
         sdnn_net_build_dense(self.handle)
 
+    def set_bias_mode(self, mode: int):
+        sdnn_net_set_bias_mode(self.handle, mode)
+
     def workspace(self, batch: int, y_is_csr: int):
         key = (batch, y_is_csr)
         need = sdnn_workspace_size(self.handle, batch, y_is_csr)
@@ -212,9 +222,11 @@ class Net:
             pass
 
 
-def net_from_problem(problem, device: str = "cuda:0", dense: bool = False) -> Net:
+def net_from_problem(problem, device: str = "cuda:0", dense: bool = False, bias_mode: int = SDNN_BIAS_EVERYWHERE) -> Net:
     """Upload every layer of a workloads.Problem."""
     net = Net(problem.n, problem.L, problem.ymax, device)
+    if bias_mode != SDNN_BIAS_EVERYWHERE:
+        net.set_bias_mode(bias_mode)
     for k, l in enumerate(problem.layers):
         net.set_layer(k, l.row_ptr, l.col, l.val, l.bias)
     if dense:

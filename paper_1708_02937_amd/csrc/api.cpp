@@ -128,6 +128,7 @@ struct sdnn_net_s {
     int64_t n = 0;
     int32_t L = 0;
     double ymax = INFINITY;
+    int bias_pattern = 0;  // SDNN_BIAS_PATTERN: bias only on the structural pattern of Y_k W_k
     hipStream_t stream = nullptr;
     int device = 0;
     std::vector<Layer> layers;
@@ -197,6 +198,14 @@ sdnn_status sdnn_net_set_stream(sdnn_net net, void *stream) {
     g_last_error.clear();
     if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
     net->stream = (hipStream_t)stream;
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_net_set_bias_mode(sdnn_net net, int32_t mode) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    if (mode != SDNN_BIAS_EVERYWHERE && mode != SDNN_BIAS_PATTERN) return fail(SDNN_ERR_INVALID_VALUE, "unknown bias mode");
+    net->bias_pattern = mode == SDNN_BIAS_PATTERN ? 1 : 0;
     return SDNN_OK;
 }
 
@@ -326,6 +335,8 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
     if (st != SDNN_OK) return st;
     if (batch < 0) return fail(SDNN_ERR_DIMENSION_MISMATCH, "batch must be >= 0");
     if (arm != SDNN_ARM_SPARSE && arm != SDNN_ARM_DENSE) return fail(SDNN_ERR_INVALID_VALUE, "unknown arm");
+    if (arm == SDNN_ARM_DENSE && net->bias_pattern)
+        return fail(SDNN_ERR_UNSUPPORTED, "the dense arm stores every zero of W_k, so it has no bias pattern");
     if (batch == 0) return SDNN_OK;
     if (!Y_in || !Y_out) return fail(SDNN_ERR_NULL_POINTER, "Y_in and Y_out are required");
     const int64_t n = net->n;
@@ -351,7 +362,8 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
     for (int32_t k = k0; k < k1; ++k) {
         const Layer &l = net->layers[(size_t)k];
         if (arm == SDNN_ARM_SPARSE)
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax, buf[cur],
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax,
+                                             net->bias_pattern, buf[cur],
                                              buf[cur ^ 1], s));
         else
             SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, l.dense_wt, l.bias, net->ymax, buf[cur], buf[cur ^ 1],
@@ -404,11 +416,12 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     // From the first layer whose input is dense enough, activations are kept dense and neuron-major and
     // each layer gathers over fan-in lists (the dense-Y product); the result is packed back into rows at
     // the end.  A layer's input counts as dense when it holds at least 1/8 of batch * n entries, or when
-    // the layer's bias is positive on at least a quarter of its neurons (every such neuron is then
-    // h(b_j) > 0 in every sample that does not push it below zero, so the output is dense whatever the
-    // input).  The input size is known on the host only through a synchronisation, so the host keeps an
-    // upper bound (a layer with every b_j <= 0 writes at most (longest fan-out row) entries per input
-    // entry) and reads the exact count from the device only when the bound reaches the threshold.
+    // the layer's bias is positive on at least a quarter of its neurons and applies everywhere (every such
+    // neuron is then h(b_j) > 0 in every sample that does not push it below zero, so the output is dense
+    // whatever the input).  The input size is known on the host only through a synchronisation, so the
+    // host keeps an upper bound (a layer whose untouched columns stay zero, every b_j <= 0 or bias on the
+    // pattern only, writes at most (longest fan-out row) entries per input entry) and reads the exact
+    // count from the device only when the bound reaches the threshold.
     const double dense_at = (double)batch * (double)n / 8.0;
     double nnz_hi = (double)batch * (double)n;  // upper bound of the current layer's input entries
     bool exact = false;
@@ -423,7 +436,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     int cur = 0;  // slot buffer that receives the next sparse layer's output
     for (int32_t k = k0; k < k1; ++k) {
         const Layer &l = net->layers[(size_t)k];
-        if (4 * l.pos_bias >= n) {
+        if (!net->bias_pattern && 4 * l.pos_bias >= n) {
             kd = k;
             break;
         }
@@ -442,11 +455,11 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         SDNN_HIP(sdnn::launch_spgemm_layer(n, batch, first ? y_row_ptr : nullptr, first ? nullptr : w.cnt[cur ^ 1],
                                            first ? y_col : w.col[cur ^ 1], first ? y_val : w.val[cur ^ 1], l.row_ptr,
                                            l.w_seg, l.w_pack, l.nnz, l.max_fanout, l.bias, l.bias_nonpos ? 1 : 0,
-                                           net->ymax, w.cnt[cur], w.col[cur], w.val[cur], w.lists,
+                                           net->bias_pattern, net->ymax, w.cnt[cur], w.col[cur], w.val[cur], w.lists,
                                            net->d_stats + 4 * (k - k0), net->d_flags, net->num_cu, s));
         cur ^= 1;
         const double full = (double)batch * (double)n;
-        nnz_hi = l.bias_nonpos ? std::min(full, nnz_hi * (double)l.max_fanout) : full;
+        nnz_hi = (l.bias_nonpos || net->bias_pattern) ? std::min(full, nnz_hi * (double)l.max_fanout) : full;
         exact = false;
     }
     int last, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
@@ -460,7 +473,8 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         int dc = 0;
         for (int32_t k = kd; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax, dense[dc],
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax,
+                                             net->bias_pattern, dense[dc],
                                              dense[dc ^ 1], s));
             dc ^= 1;
         }

@@ -50,9 +50,10 @@ size_t spmm_tile_mask_elems(int64_t n);
 bool spmm_wants_tiles(int64_t n, int64_t nnz);
 hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *fan, uint16_t *tile_mask,
                                  hipStream_t s);
+// pattern != 0: the bias and h apply only where some fan-in entry meets a nonzero input (else 0).
 hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
-                             const uint16_t *tile_mask, const float *bias, double ymax, const float *yt, float *zt,
-                             hipStream_t s);
+                             const uint16_t *tile_mask, const float *bias, double ymax, int pattern, const float *yt,
+                             float *zt, hipStream_t s);
 
 // gemm.hip
 hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *wt, hipStream_t s);
@@ -71,11 +72,12 @@ hipError_t launch_window_seg(int64_t n, const int64_t *w_ptr, const int32_t *col
 int64_t spgemm_small_len(int64_t n, int32_t max_fanout);
 // One sparse layer: planning pass, small-sample kernel, workgroup kernel.  lists holds 2 * batch int32;
 // stats points to the layer's 4 counters (zero on entry): small count, large count, output nnz, work.
+// pattern != 0: the bias and h apply only on the structural pattern of Y_k W_k.
 hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const int32_t *w_seg,
                                const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
-                               double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val, int32_t *lists,
-                               unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s);
+                               int pattern, double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val,
+                               int32_t *lists, unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s);
 hipError_t launch_densify(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                           const int32_t *in_col, const float *in_val, float *yt, uint32_t *err, hipStream_t s);
 hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,

@@ -70,13 +70,14 @@ constexpr int kSmallWaves = 4;    // wavefronts per workgroup of the small-sampl
 // Per-layer counters kept by the sparse layer kernels (one row of the net's statistics array).
 enum : int { kStatSmall = 0, kStatLarge = 1, kStatNnz = 2, kStatWork = 3 };
 
-// Planning pass: one thread per sample.  Empty samples of a layer with every b_j <= 0 are finished here
+// Planning pass: one thread per sample.  When only touched columns can be nonzero (every b_j <= 0, or the
+// bias applies only on the structural pattern), empty samples are finished here
 // (cnt = 0); the others are appended to the small list (lists[0 .. small)) or the large list
 // (lists[batch .. batch + large)) with one atomic per wave and list.
 __global__ __launch_bounds__(256) void spgemm_plan_kernel(int64_t n, int64_t batch, const int64_t *__restrict__ in_row_ptr,
                                                           const int32_t *__restrict__ in_cnt,
                                                           const int32_t *__restrict__ in_col,
-                                                          const float *__restrict__ in_val, int bias_nonpos,
+                                                          const float *__restrict__ in_val, int only_touched,
                                                           int64_t small_len, int32_t *__restrict__ out_cnt,
                                                           int32_t *__restrict__ lists, unsigned long long *stats,
                                                           uint32_t *err) {
@@ -85,8 +86,8 @@ __global__ __launch_bounds__(256) void spgemm_plan_kernel(int64_t n, int64_t bat
     const bool valid = r < batch;
     int64_t ylen = 0;
     if (valid) ylen = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err).ylen;
-    const bool skip = valid && bias_nonpos && ylen == 0;
-    const bool small = valid && bias_nonpos && ylen > 0 && ylen <= small_len;
+    const bool skip = valid && only_touched && ylen == 0;
+    const bool small = valid && only_touched && ylen > 0 && ylen <= small_len;
     const bool large = valid && !skip && !small;
     if (skip) out_cnt[r] = 0;
     const uint64_t ms = __ballot(small), ml = __ballot(large);
@@ -114,7 +115,7 @@ __device__ __forceinline__ void wave_lds_sync() {
 // (a wave prefix sum of the fan-out row lengths gives each entry its place), sorts them by column with a
 // bitonic network, then each run of equal columns is summed, biased, activated and rounded once, and the
 // survivors are compacted in column order with a ballot.  Only touched columns can survive when
-// b_j <= 0, so nothing else is visited.
+// b_j <= 0 or when the bias applies only on the structural pattern, so nothing else is visited.
 __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
     int64_t n, int64_t batch, const int64_t *__restrict__ in_row_ptr, const int32_t *__restrict__ in_cnt,
     const int32_t *__restrict__ in_col, const float *__restrict__ in_val, const int64_t *__restrict__ w_ptr,
@@ -143,7 +144,8 @@ __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
                 if (i >= 0 && i < n) {
                     y = (double)in_val[ri.yb + t];
                     start = w_ptr[i];
-                    len = (int)(w_ptr[i + 1] - start);
+                    // a zero input adds nothing and is no structural entry: its products are not expanded
+                    len = y != 0.0 ? (int)(w_ptr[i + 1] - start) : 0;
                 } else {
                     atomicOr(err, 1u);
                 }
@@ -230,9 +232,11 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
     int64_t n, int64_t batch, int nwin, const int64_t *__restrict__ in_row_ptr,
     const int32_t *__restrict__ in_cnt, const int32_t *__restrict__ in_col, const float *__restrict__ in_val,
     const int64_t *__restrict__ w_ptr, const int32_t *__restrict__ w_seg, const Edge *__restrict__ w,
-    const float *__restrict__ bias, int bias_nonpos, int64_t sparse_limit, int lane_segments, double ymax,
-    const int32_t *__restrict__ list, unsigned long long *stats, int32_t *__restrict__ out_cnt,
+    const float *__restrict__ bias, int bias_nonpos, int pattern, int64_t sparse_limit, int lane_segments,
+    double ymax, const int32_t *__restrict__ list, unsigned long long *stats, int32_t *__restrict__ out_cnt,
     int32_t *__restrict__ out_col, float *__restrict__ out_val, uint32_t *err) {
+    // bias_nonpos: only touched columns can be nonzero (every b_j <= 0, or pattern mode); pattern: the
+    // bias applies only on the structural pattern, so the touched-column bitmap is always kept
     extern __shared__ double acc[];
     __shared__ RowRef refs[kThreads];
     __shared__ uint32_t bits[kBitWords];
@@ -265,7 +269,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
             const int64_t r = large[q0 + q];
             const RowIn ri = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err);
             const int64_t yb = ri.yb, ylen = ri.ylen;
-            const bool sparse = bias_nonpos && ylen <= sparse_limit;
+            const bool sparse = pattern || (bias_nonpos && ylen <= sparse_limit);
             // resident mode: one stored entry per thread, kept in registers across the windows; the
             // thread's fan-out segment for window w is [s_lo, s_hi), and the next window's segment starts
             // where this one ends, so each window costs one more offset load, issued a window ahead
@@ -320,7 +324,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                             if (e + u < hi) {
                                 const int col = ed[u].idx - (int)c0;
                                 atomicAdd(&acc[col], my_y * (double)ed[u].w);
-                                if (sparse) atomicOr(&bits[col >> 5], 1u << (col & 31));
+                                if (sparse && my_y != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
                                 mine_any = true;
                             }
                     }
@@ -372,7 +376,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                                     if (ed[u].idx >= c0 && ed[u].idx < c1) {
                                         const int col = ed[u].idx - (int)c0;
                                         atomicAdd(&acc[col], ref.y * (double)ed[u].w);
-                                        if (sparse) atomicOr(&bits[col >> 5], 1u << (col & 31));
+                                        if (sparse && ref.y != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
                                         mine_any = true;
                                     }
                                 }
@@ -406,7 +410,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                                     if (ed[p].idx >= c0 && ed[p].idx < c1) {
                                         const int col = ed[p].idx - (int)c0;
                                         atomicAdd(&acc[col], rr[p].y * (double)ed[p].w);
-                                        if (sparse) atomicOr(&bits[col >> 5], 1u << (col & 31));
+                                        if (sparse && rr[p].y != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
                                         mine_any = true;
                                     }
                                 }
@@ -641,9 +645,10 @@ int64_t spgemm_small_len(int64_t n, int32_t max_fanout) {
 hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const int32_t *w_seg,
                                const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
-                               double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val, int32_t *lists,
-                               unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s) {
+                               int pattern, double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val,
+                               int32_t *lists, unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s) {
     if (batch == 0) return hipSuccess;
+    const int only_touched = bias_nonpos || pattern;
     if (batch > 0x7fffffffLL) return hipErrorInvalidValue;
     static bool attr_set = false;
     if (!attr_set) {
@@ -654,10 +659,10 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     }
     const int64_t small_len = spgemm_small_len(n, max_fanout);
     spgemm_plan_kernel<<<(unsigned)((batch + 255) / 256), 256, 0, s>>>(
-        n, batch, in_row_ptr, in_cnt, in_col, in_val, bias_nonpos, small_len, out_cnt, lists, stats, err);
+        n, batch, in_row_ptr, in_cnt, in_col, in_val, only_touched, small_len, out_cnt, lists, stats, err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (bias_nonpos) {
+    if (only_touched) {
         // enough waves to cover every CU several times; each wave strides through the small list
         const int64_t waves = (batch < (int64_t)num_cu * 16 ? batch : (int64_t)num_cu * 16);
         spgemm_small_kernel<<<(unsigned)((waves + kSmallWaves - 1) / kSmallWaves), kSmallWaves * 64, 0, s>>>(
@@ -674,8 +679,8 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     // segments of at most ~16 entries are walked lane by lane, longer ones by half-waves
     const int lane_segments = (w_seg || nwin == 1) && per_win <= 16.0 ? 1 : 0;
     spgemm_row_kernel<<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
-        n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, bias_nonpos, sparse_limit,
-        lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
+        n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, only_touched, pattern,
+        sparse_limit, lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
     return hipGetLastError();
 }
 

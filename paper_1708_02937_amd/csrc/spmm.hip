@@ -67,7 +67,7 @@ __device__ __forceinline__ float bcast_f(float v, int lane) {
 
 constexpr int kUnroll = 8;
 
-template <int V>
+template <int V, bool kPattern>
 __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batch, int chunks,
                                                          const int64_t *__restrict__ fan_ptr,
                                                          const Edge *__restrict__ fan, const float *__restrict__ bias,
@@ -94,8 +94,12 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
     const int64_t colc = active ? col : 0; // inactive lanes read a valid address and discard it
 
     double acc[V];
+    uint32_t hit[V];  // pattern mode: OR of the input bits; nonzero magnitude bits = a structural product
 #pragma unroll
-    for (int v = 0; v < V; ++v) acc[v] = 0.0;
+    for (int v = 0; v < V; ++v) {
+        acc[v] = 0.0;
+        hit[v] = 0u;
+    }
 
     const int64_t e_beg = fan_ptr[j], e_end = fan_ptr[j + 1];
     for (int64_t e0 = e_beg; e0 < e_end; e0 += 64) {
@@ -118,7 +122,10 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
             for (int u = 0; u < kUnroll; ++u) {
                 const double wd = (double)w[u];
 #pragma unroll
-                for (int v = 0; v < V; ++v) acc[v] = __builtin_fma((double)y[u][v], wd, acc[v]);
+                for (int v = 0; v < V; ++v) {
+                    acc[v] = __builtin_fma((double)y[u][v], wd, acc[v]);
+                    if constexpr (kPattern) hit[v] |= __float_as_uint(y[u][v]);
+                }
             }
         }
         for (; t < cnt; ++t) {
@@ -127,14 +134,18 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
             const double wd = (double)bcast_f(mine.w, t);
             load_v<V>(yt + (int64_t)i * batch + colc, y);
 #pragma unroll
-            for (int v = 0; v < V; ++v) acc[v] = __builtin_fma((double)y[v], wd, acc[v]);
+            for (int v = 0; v < V; ++v) {
+                acc[v] = __builtin_fma((double)y[v], wd, acc[v]);
+                if constexpr (kPattern) hit[v] |= __float_as_uint(y[v]);
+            }
         }
     }
     if (!active) return;
     const double bj = (double)bias[j];
     float out[V];
 #pragma unroll
-    for (int v = 0; v < V; ++v) out[v] = activate(acc[v] + bj, ymax);
+    for (int v = 0; v < V; ++v)
+        out[v] = (kPattern && (hit[v] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[v] + bj, ymax);
     store_v<V>(zt + j * batch + col, out);
 }
 
@@ -162,6 +173,7 @@ constexpr int kRowD2 = kTiledCB / 2;                // double2 per slab row (LDS
 constexpr int kStageF4 = kTileRows * kRowF4 / kTiledThreads;
 constexpr int kRowGroup = 2;                        // slab rows read ahead of their FMAs
 
+template <bool kPattern>
 __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
     int64_t n, int64_t batch, int chunks, int ntiles, const int64_t *__restrict__ fan_ptr,
     const uint16_t *__restrict__ tile_mask, const Edge *__restrict__ fan, const float *__restrict__ bias,
@@ -181,10 +193,14 @@ __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
     const int64_t pitch = (n + 3) & ~3ll;  // mask row pitch: keeps the 64-bit mask loads 8-byte aligned
 
     double acc[kTiledNPW][4];
+    uint32_t hit[kTiledNPW][4];  // pattern mode: OR of the inputs' high words (magnitude bits = nonzero)
 #pragma unroll
     for (int q = 0; q < kTiledNPW; ++q)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) acc[q][v] = 0.0;
+        for (int v = 0; v < 4; ++v) {
+            acc[q][v] = 0.0;
+            hit[q][v] = 0u;
+        }
 
     float4 st[kStageF4];
     auto load_slab = [&](int t) {
@@ -268,6 +284,12 @@ __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
                         acc[q][1] = __builtin_fma(ya[k].y, w, acc[q][1]);
                         acc[q][2] = __builtin_fma(yb[k].x, w, acc[q][2]);
                         acc[q][3] = __builtin_fma(yb[k].y, w, acc[q][3]);
+                        if constexpr (kPattern) {
+                            hit[q][0] |= (uint32_t)__double2hiint(ya[k].x);
+                            hit[q][1] |= (uint32_t)__double2hiint(ya[k].y);
+                            hit[q][2] |= (uint32_t)__double2hiint(yb[k].x);
+                            hit[q][3] |= (uint32_t)__double2hiint(yb[k].y);
+                        }
                     }
                 }
             }
@@ -282,10 +304,11 @@ __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
         const int64_t j = jw + q;
         if (j >= n) break;
         const double bj = (double)bias[j];
-        if (ca < batch)
-            *reinterpret_cast<float4 *>(zt + j * batch + ca) =
-                make_float4(activate(acc[q][0] + bj, ymax), activate(acc[q][1] + bj, ymax),
-                            activate(acc[q][2] + bj, ymax), activate(acc[q][3] + bj, ymax));
+        float f[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            f[v] = (kPattern && (hit[q][v] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[q][v] + bj, ymax);
+        if (ca < batch) *reinterpret_cast<float4 *>(zt + j * batch + ca) = make_float4(f[0], f[1], f[2], f[3]);
     }
 }
 
@@ -356,16 +379,20 @@ hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *
 }
 
 hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
-                             const uint16_t *tile_mask, const float *bias, double ymax, const float *yt, float *zt,
-                             hipStream_t s) {
+                             const uint16_t *tile_mask, const float *bias, double ymax, int pattern, const float *yt,
+                             float *zt, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
     if (tile_mask && batch % 4 == 0 && batch >= 128) {
         const int64_t chunks = (batch + kTiledCB - 1) / kTiledCB;
         const int64_t groups = (n + kTiledNJ - 1) / kTiledNJ;
         const int64_t blocks = (groups + 7) / 8 * 8 * chunks;
         if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-        spmm_tiled_kernel<<<(unsigned)blocks, kTiledThreads, 0, s>>>(n, batch, (int)chunks, spmm_tile_count(n),
-                                                                     fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
+        if (pattern)
+            spmm_tiled_kernel<true><<<(unsigned)blocks, kTiledThreads, 0, s>>>(
+                n, batch, (int)chunks, spmm_tile_count(n), fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
+        else
+            spmm_tiled_kernel<false><<<(unsigned)blocks, kTiledThreads, 0, s>>>(
+                n, batch, (int)chunks, spmm_tile_count(n), fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
         return hipGetLastError();
     }
     // Columns per lane: wide enough to keep 8 independent loads in flight, and a multiple that divides batch.
@@ -376,16 +403,17 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, c
     const int64_t groups = (n + 3) / 4;
     const int64_t blocks = groups * chunks;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    switch (V) {
-        case 4:
-            spmm_fanin_kernel<4><<<(unsigned)blocks, 256, 0, s>>>(n, batch, (int)chunks, fan_ptr, fan, bias, ymax, yt, zt);
-            break;
-        case 2:
-            spmm_fanin_kernel<2><<<(unsigned)blocks, 256, 0, s>>>(n, batch, (int)chunks, fan_ptr, fan, bias, ymax, yt, zt);
-            break;
-        default:
-            spmm_fanin_kernel<1><<<(unsigned)blocks, 256, 0, s>>>(n, batch, (int)chunks, fan_ptr, fan, bias, ymax, yt, zt);
+#define SDNN_GATHER(VV, PP) \
+    spmm_fanin_kernel<VV, PP><<<(unsigned)blocks, 256, 0, s>>>(n, batch, (int)chunks, fan_ptr, fan, bias, ymax, yt, zt)
+    switch (V * 2 + (pattern ? 1 : 0)) {
+        case 8: SDNN_GATHER(4, false); break;
+        case 9: SDNN_GATHER(4, true); break;
+        case 4: SDNN_GATHER(2, false); break;
+        case 5: SDNN_GATHER(2, true); break;
+        case 3: SDNN_GATHER(1, true); break;
+        default: SDNN_GATHER(1, false);
     }
+#undef SDNN_GATHER
     return hipGetLastError();
 }
 

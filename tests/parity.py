@@ -30,18 +30,20 @@ def dense_to_csr_keep_all(d):
     return dense_to_csr(d)
 
 
-def oracle_rows(problem, rows=None, k0=0, k1=None, threads=None):
+def oracle_rows(problem, rows=None, k0=0, k1=None, threads=None, bias_mode=0):
     y = problem.y0_as_csr()
     if rows is not None:
         y = csr_rows(y, rows)
-    return oracle.forward(problem.n, problem.layers, problem.ymax, y, k0=k0, k1=k1, threads=threads)
+    return oracle.forward(problem.n, problem.layers, problem.ymax, y, k0=k0, k1=k1, threads=threads,
+                          bias_mode=bias_mode)
 
 
-def compare(problem, got_csr, rows=None, exact=False, k1=None):
-    """Compare GPU output rows (CSR, in the order of `rows`) with the oracle; returns a stats dict."""
+def compare(problem, got_csr, rows=None, exact=False, k1=None, bias_mode=0):
+    """Compare GPU output rows (CSR, in the order of `rows`) with the oracle; returns a stats dict.
+    bias_mode 1 compares against the oracle's bias-on-the-structural-pattern reading."""
     n = problem.n
     k1 = problem.L if k1 is None else k1
-    want_csr = oracle_rows(problem, rows, k1=k1)
+    want_csr = oracle_rows(problem, rows, k1=k1, bias_mode=bias_mode)
     got = to_dense(got_csr, n)
     want = to_dense(want_csr, n)
     assert got.shape == want.shape
@@ -62,7 +64,7 @@ def compare(problem, got_csr, rows=None, exact=False, k1=None):
     if odd.any():
         r_idx = np.unique(np.nonzero(odd)[0])
         sub_rows = r_idx if rows is None else np.asarray(rows)[r_idx]
-        prev = oracle_rows(problem, sub_rows, k1=k1 - 1)
+        prev = oracle_rows(problem, sub_rows, k1=k1 - 1, bias_mode=bias_mode)
         z, s = oracle.preact(n, problem.layers[k1 - 1], prev)
         for t, r in enumerate(r_idx):
             cols = np.nonzero(odd[r])[0]

@@ -30,18 +30,18 @@ def _say(*a):
     print("[case]", *a, flush=True)
 
 
-def run_dense(sd, p, arm, y0=None):
+def run_dense(sd, p, arm, y0=None, bias_mode=0):
     import torch
 
-    net = sd.net_from_problem(p, dense=(arm == sd.SDNN_ARM_DENSE))
+    net = sd.net_from_problem(p, dense=(arm == sd.SDNN_ARM_DENSE), bias_mode=bias_mode)
     y = torch.from_numpy(p.y0_dense if y0 is None else y0).cuda()
     out = net.forward_dense(y, arm=arm).cpu().numpy()
     net.free()
     return out
 
 
-def run_csr(sd, p, y0=None, k0=0, k1=None):
-    net = sd.net_from_problem(p)
+def run_csr(sd, p, y0=None, k0=0, k1=None, bias_mode=0):
+    net = sd.net_from_problem(p, bias_mode=bias_mode)
     rp, c, v = net.forward_csr(*(p.y0_as_csr() if y0 is None else y0), k0=k0, k1=k1)
     res = (rp.cpu().numpy(), c.cpu().numpy(), v.cpu().numpy())
     net.free()
@@ -103,6 +103,43 @@ def test_paper_grid_points(sd, arm, m, S):
     p = paper_grid(m, S)
     _say("paper grid", arm, m, S)
     parity.compare(p, dense_to_csr(run_dense(sd, p, _arm(sd, arm))))
+
+
+# ------------------------------------------------------------------ bias on the structural pattern only
+
+
+@pytest.mark.parametrize("seed,n,L,batch,wd,yd", [(61, 300, 3, 40, 0.02, 0.05), (62, 3000, 2, 257, 0.003, 0.015),
+                                                  (63, 40000, 2, 24, 0.0002, 0.0012), (64, 500, 3, 64, 0.05, 0.3),
+                                                  (65, 2000, 2, 100, 0.016, 0.1)])
+def test_pattern_bias_csr_path(sd, seed, n, L, batch, wd, yd):
+    """SDNN_BIAS_PATTERN with positive biases through the CSR path: small-sample and workgroup SpGEMM
+    (one and three windows), and the density-driven switch to dense activations (denser cases)."""
+    p = tiny_random(seed, n, L, batch, w_density=wd, y_density=yd, bias_lo=-0.2, bias_hi=0.6,
+                    explicit_zeros=seed % 2 == 1, ymax=[math.inf, 2.0][seed % 2])
+    _say("pattern csr", seed, n, L, batch)
+    parity.compare(p, run_csr(sd, p, bias_mode=1), bias_mode=1)
+
+
+@pytest.mark.parametrize("seed,n,L,batch,d,yd", [(66, 200, 2, 130, 0.05, 0.3), (67, 1100, 2, 260, 0.95, 0.001),
+                                                 (68, 333, 3, 3, 0.1, 0.5), (69, 4100, 1, 2048, 0.002, 0.01)])
+def test_pattern_bias_dense_batch(sd, seed, n, L, batch, d, yd):
+    """SDNN_BIAS_PATTERN on the sparse arm with dense batches: the gather SpMM (one, two and four columns
+    per lane) and the LDS-tiled SpMM (fan-in >= 1024); sparse inputs leave many positions untouched."""
+    p = tiny_random(seed, n, L, batch, w_density=d, y_density=yd, dense_input=True, bias_lo=-0.2, bias_hi=0.6)
+    _say("pattern dense", seed, n, L, batch)
+    parity.compare(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE, bias_mode=1)), bias_mode=1)
+
+
+def test_pattern_bias_integer_shadow_and_dense_arm(sd):
+    """Integer shadow of the very wide workload (positive biases, scaled) matches bit for bit in pattern
+    mode; the dense arm has no pattern and refuses it."""
+    q = integer_shadow(make_config(5, n=20480, L=2, batch=12, block=4096))
+    _say("pattern integer shadow")
+    parity.compare(q, run_csr(sd, q, bias_mode=1), exact=True, bias_mode=1)
+    p = tiny_random(70, 64, 1, 4, dense_input=True)
+    with pytest.raises(sd.SdnnError) as ei:
+        run_dense(sd, p, sd.SDNN_ARM_DENSE, bias_mode=1)
+    assert ei.value.status == 9
 
 
 def test_long_fanin_lists(sd):
