@@ -62,6 +62,9 @@ def _declare(lib):
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(_Layer), ctypes.c_double, ctypes.c_int,
         ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+    lib.oracle_mxm.restype = ctypes.c_int
+    lib.oracle_mxm.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.POINTER(_Layer), ctypes.c_int64,
+                               ctypes.c_void_p, ctypes.c_void_p]
     lib.oracle_preact.restype = ctypes.c_int
     lib.oracle_preact.argtypes = [
         ctypes.c_int64, ctypes.POINTER(_Layer), ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
@@ -154,3 +157,20 @@ def csr_to_dense(csr, n: int) -> np.ndarray:
 
 
 INF = math.inf
+
+
+SEMIRINGS = {"plus_times": 0, "max_plus": 1, "max_min": 2, "min_max": 3, "xor_and": 4}
+
+
+def mxm(semiring, n: int, layer, y_dense, lib=None):
+    """Z = Y (+).(x) W over one of SEMIRINGS (name or id) for dense rows y_dense (rows x n float32)."""
+    lib = lib or load()
+    sr = SEMIRINGS[semiring] if isinstance(semiring, str) else int(semiring)
+    y = np.ascontiguousarray(y_dense, dtype=np.float32).reshape(-1, n)
+    keep = []
+    ls = _layer_structs([layer], keep)
+    z = np.empty((max(1, y.shape[0]), n), dtype=np.float32)
+    rc = lib.oracle_mxm(sr, n, ls, y.shape[0], _ptr(y), z.ctypes.data)
+    if rc != 0:
+        raise ValueError(f"oracle_mxm failed with status {rc}")
+    return z[: y.shape[0]]

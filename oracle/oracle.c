@@ -250,3 +250,65 @@ int oracle_preact(int64_t n, const oracle_layer *W, int64_t nrows, const int64_t
     if (run_threads(preact_worker, &job, nthreads)) return -2;
     return 0;
 }
+
+/*
+ * Matrix multiply over a semiring (Sec. II.D: C(i,j) = (+)_k A(i,k) (x) B(k,j)),
+ * Z = Y (+).(x) W for `nrows` dense rows of Y (row-major nrows x n) and a CSR
+ * W: Z(r, j) = (+) over the stored entries W(i, j) of Y(r, i) (x) W(i, j),
+ * starting from the semiring's 0-element, in ascending i, in fp64, rounded
+ * once to fp32.  The semirings are those Sec. II names:
+ *   0  +.x     on R                   0-element 0
+ *   1  max.+   on {-inf} u R          0-element -inf
+ *   2  max.min on {-inf} u R          0-element -inf
+ *   3  min.max on R u {+inf}          0-element +inf
+ *   4  xor.and on {0, 1} (GF(2))      0-element 0; a value counts as 1 when nonzero
+ * The bias of W's layer is not used.  Returns 0, or -1 on invalid input.
+ */
+static double sr_zero(int sr)
+{
+    switch (sr) {
+    case 1: case 2: return -INFINITY;
+    case 3: return INFINITY;
+    default: return 0.0;
+    }
+}
+
+static double sr_add(int sr, double a, double b)
+{
+    switch (sr) {
+    case 1: case 2: return a > b ? a : b;
+    case 3: return a < b ? a : b;
+    case 4: return (double)((a != 0.0) != (b != 0.0));
+    default: return a + b;
+    }
+}
+
+static double sr_mul(int sr, double a, double b)
+{
+    switch (sr) {
+    case 1: return a + b;
+    case 2: return a < b ? a : b;
+    case 3: return a > b ? a : b;
+    case 4: return (double)(a != 0.0 && b != 0.0);
+    default: return a * b;
+    }
+}
+
+int oracle_mxm(int semiring, int64_t n, const oracle_layer *W, int64_t nrows, const float *y, float *z)
+{
+    if (semiring < 0 || semiring > 4 || n <= 0 || nrows < 0 || !W || (nrows > 0 && (!y || !z))) return -1;
+    if (check_layer(n, W)) return -1;
+    double *acc = (double *)malloc((size_t)n * sizeof(double));
+    if (!acc) return -2;
+    for (int64_t r = 0; r < nrows; ++r) {
+        for (int64_t j = 0; j < n; ++j) acc[j] = sr_zero(semiring);
+        for (int64_t i = 0; i < n; ++i) {
+            const double yv = (double)y[r * n + i];
+            for (int64_t e = W->row_ptr[i]; e < W->row_ptr[i + 1]; ++e)
+                acc[W->col[e]] = sr_add(semiring, acc[W->col[e]], sr_mul(semiring, yv, (double)W->val[e]));
+        }
+        for (int64_t j = 0; j < n; ++j) z[r * n + j] = (float)acc[j];
+    }
+    free(acc);
+    return 0;
+}

@@ -320,3 +320,86 @@ def test_pattern_bias_invariants(seed):
     assert np.all(out[0] == 0)
     dense_a = oracle.csr_to_dense(oracle.forward(n, q.layers, math.inf, dense_to_csr(y0d)), n)
     assert np.array_equal(out[struct], dense_a[struct])  # on the pattern both readings agree
+
+
+# --------------------------------------------------------------------------- semiring mxm (Sec. II)
+
+_SR = {
+    "plus_times": brute.S1,
+    "max_plus": brute.S2,
+    "max_min": brute.Semiring("max.min", max, min, -math.inf, math.inf),
+    "min_max": brute.Semiring("min.max", min, max, math.inf, -math.inf),
+    "xor_and": brute.Semiring("xor.and", lambda a, b: float((a != 0) != (b != 0)),
+                              lambda a, b: float(a != 0 and b != 0), 0.0, 1.0),
+}
+
+
+def _stored_dense(layer, n, fill):
+    """W with its unstored entries set to `fill` (the semiring's 0-element)."""
+    w = np.full((n, n), fill, dtype=np.float64)
+    rows = np.repeat(np.arange(n), np.diff(layer.row_ptr))
+    w[rows, layer.col] = layer.val
+    return w
+
+
+def test_semiring_mxm_maxplus_hand_example():
+    """The worked max.+ product (Sec. II.D over S2): null entries of B are unstored (the 0-element)."""
+    g = json.load(open(os.path.join(GOLDEN, "maxplus_example.json")))
+    A = np.array([[(-math.inf if v is None else v) for v in row] for row in g["A"]], np.float32)
+    B = np.array([[(0.0 if v is None else v) for v in row] for row in g["B"]], np.float32)
+    mask = np.array([[v is not None for v in row] for row in g["B"]])
+    rows, cols = np.nonzero(mask)
+    rp = np.zeros(4, np.int64)
+    np.cumsum(np.bincount(rows, minlength=3), out=rp[1:])
+    lay = Layer(rp, cols.astype(np.int32), B[mask].astype(np.float32), np.zeros(3, np.float32))
+    assert np.array_equal(oracle.mxm("max_plus", 3, lay, A), np.array(g["C"], np.float32))
+
+
+@pytest.mark.parametrize("name", sorted(_SR))
+@pytest.mark.parametrize("seed", [1, 2])
+def test_semiring_mxm_equals_generic_listing(name, seed):
+    """The oracle's mxm equals the semiring-generic dense mxm (unstored W entries are the 0-element), bit
+    for bit, with explicit zeros stored in W."""
+    n = 13
+    p = tiny_random(70 + seed, n, 1, 5, w_density=0.3, dense_input=True, y_density=0.7, explicit_zeros=True)
+    l = p.layers[0]
+    y = p.y0_dense
+    if name == "xor_and":
+        y = (y != 0).astype(np.float32)
+        l = Layer(l.row_ptr, l.col, (l.val > 0).astype(np.float32), l.bias)
+    sr = _SR[name]
+    Wd = _stored_dense(l, n, sr.zero).tolist()
+    want = np.array(brute.mxm(y.astype(np.float64).tolist(), Wd, sr), dtype=np.float64).astype(np.float32)
+    assert oracle.mxm(name, n, l, y).tobytes() == want.tobytes()
+
+
+def test_semiring_mxm_against_numpy():
+    """Special cases that reduce to library routines: +.x to a matmul (integer values, exact), GF(2) to a
+    matmul mod 2, max.+ / max.min / min.max to broadcast reductions."""
+    n = 40
+    p = tiny_random(77, n, 1, 7, w_density=0.2, dense_input=True, y_density=0.6, integer=True)
+    l = p.layers[0]
+    y = p.y0_dense
+    w0 = _stored_dense(l, n, 0.0)
+    assert np.array_equal(oracle.mxm("plus_times", n, l, y), (y.astype(np.float64) @ w0).astype(np.float32))
+    yb = (y != 0).astype(np.int64)
+    wb = (w0 != 0).astype(np.int64)
+    assert np.array_equal(oracle.mxm("xor_and", n, l, y), ((yb @ wb) % 2).astype(np.float32))
+    wm = _stored_dense(l, n, -math.inf)
+    assert np.array_equal(oracle.mxm("max_plus", n, l, y), np.max(y[:, :, None] + wm[None], axis=1).astype(np.float32))
+    assert np.array_equal(oracle.mxm("max_min", n, l, y),
+                          np.max(np.minimum(y[:, :, None], wm[None]), axis=1).astype(np.float32))
+    wp = _stored_dense(l, n, math.inf)
+    assert np.array_equal(oracle.mxm("min_max", n, l, y),
+                          np.min(np.maximum(y[:, :, None], wp[None]), axis=1).astype(np.float32))
+
+
+def test_semiring_zero_rows_give_zero_element():
+    """A row of Y holding only the 0-element yields the 0-element everywhere (additive identity and
+    multiplicative annihilator, Sec. II.E)."""
+    n = 9
+    l = tiny_random(78, n, 1, 1, w_density=0.5).layers[0]
+    for name, zero in (("max_plus", -math.inf), ("max_min", -math.inf), ("min_max", math.inf),
+                       ("plus_times", 0.0), ("xor_and", 0.0)):
+        z = oracle.mxm(name, n, l, np.full((1, n), zero, np.float32))
+        assert np.all(z == zero), name
