@@ -306,6 +306,31 @@ def run_paper_grid(args, torch, sd):
 
 
 
+def run_semiring(args, torch, sd):
+    """Matrix multiply over each semiring of Sec. II (sdnn_mxm_dense) on the density-sweep shape
+    (n = 4096, batch = 1024): time per call (two transposes included) and edges/s."""
+    from workloads import make_config
+
+    names = ["plus_times", "max_plus", "max_min", "min_max", "xor_and"]
+    densities = [float(x) for x in args.densities.split(",")]
+    reps = max(3, args.steps)
+    out = {}
+    for d in densities:
+        p = make_config(2, d, L=1)
+        net = sd.net_from_problem(p)
+        y = torch.from_numpy(p.y0_dense).cuda()
+        z = torch.empty_like(y)
+        out[f"{d:g}"] = {}
+        for sr, name in enumerate(names):
+            net.mxm(0, sr, y, out=z)
+            ms = time_calls(torch, lambda: net.mxm(0, sr, y, out=z), reps)
+            out[f"{d:g}"][name] = {"ms": round(ms, 5), "edges_per_s": p.edges() / (ms / 1e3)}
+            log(f"semiring {name} d {d}: {ms:.4f} ms")
+        net.free()
+    return out
+
+
+
 def run_csr_config(args, torch, sd):
     """Configs 3-5 (sparse Y through the SpGEMM path) and config 1, one forward per step."""
     from workloads import make_config
@@ -340,6 +365,8 @@ def main():
     ap.add_argument("--paper-grid", action="store_true",
                     help="time the paper's own grid (m x m weights, inverse sparsity 1..262144, batch 64)")
     ap.add_argument("--grid-sizes", default="", help="comma-separated m values for --paper-grid")
+    ap.add_argument("--semiring", action="store_true",
+                    help="time matrix multiply over each semiring of Sec. II on the density-sweep shape")
     ap.add_argument("--grid-inv", default="", help="comma-separated inverse sparsities for --paper-grid")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes 5 times (counter calibration)")
@@ -374,6 +401,14 @@ def main():
             "grid": {str(m): {str(S): v for S, v in g.items()} for m, g in grid.items()},
             "scaling_params": {str(m): v for m, v in params.items()},
         }), flush=True)
+        return
+    if args.semiring:
+        res = run_semiring(args, torch, sd)
+        print(json.dumps({
+            "metric": "time per sdnn_mxm_dense call (ms) and edges/s, one MI355X", "unit": "ms",
+            "higher_is_better": False, "n_gpus": 1, "dtype": "f64", "data": "synthetic",
+            "config": {"workload": "density-sweep shape n=4096 batch=1024, one layer, each semiring"},
+            "semiring": res}), flush=True)
         return
     if args.config == 2:
         r = run_sweep(args, torch, sd)

@@ -123,6 +123,42 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
  */
 sdnn_status sdnn_net_build_dense(sdnn_net net);
 
+/* Semirings of Sec. II for sdnn_mxm_dense / sdnn_mxm_csr: (+) . (x), 0-element. */
+enum {
+    SDNN_SEMIRING_PLUS_TIMES = 0, /* + . x        on R,            0 */
+    SDNN_SEMIRING_MAX_PLUS = 1,   /* max . +      on {-inf} u R,   -inf */
+    SDNN_SEMIRING_MAX_MIN = 2,    /* max . min    on {-inf} u R,   -inf */
+    SDNN_SEMIRING_MIN_MAX = 3,    /* min . max    on R u {+inf},   +inf */
+    SDNN_SEMIRING_XOR_AND = 4     /* xor . and    GF(2): a value is 1 when nonzero; results are 0 or 1 */
+};
+
+/*
+ * Matrix multiply over a semiring (Sec. II.D) with layer k's weights:
+ * Z = Y (+).(x) W_k, Z(r, j) = (+) over the stored entries W_k(i, j) of
+ * Y(r, i) (x) W_k(i, j), starting from the semiring's 0-element (so a column
+ * with no stored entry holds the 0-element).  No bias, no activation.
+ * Y and Z are device fp32 arrays of batch x n, row-major; Z may alias Y.
+ * Values are carried in fp64 and rounded once; every semiring but + . x is
+ * exact.  ws: at least sdnn_workspace_size(net, batch, 0) bytes.  Asynchronous
+ * on the net's stream.
+ * Errors: INVALID_OBJECT (net NULL or layer k not set), NULL_POINTER,
+ * DIMENSION_MISMATCH (k or batch), INVALID_VALUE (semiring), WORKSPACE_TOO_SMALL, DEVICE.
+ */
+sdnn_status sdnn_mxm_dense(sdnn_net net, int32_t k, int32_t semiring, int64_t batch, const float *Y, float *Z,
+                           void *ws, int64_t ws_bytes);
+
+/*
+ * The same product for a CSR batch Y (y_row_ptr[batch+1], y_col, y_val; device
+ * arrays, columns in [0, n)): entries Y does not store are the semiring's
+ * 0-element (the additive identity and multiplicative annihilator, Sec. II.E,
+ * so they contribute nothing).  Z (device, batch x n fp32, row-major) receives
+ * every entry.  Synchronises the stream once to report invalid CSR extents or
+ * columns (INVALID_INDEX; the offending rows are skipped).
+ * Errors: as sdnn_mxm_dense, plus INVALID_INDEX.
+ */
+sdnn_status sdnn_mxm_csr(sdnn_net net, int32_t k, int32_t semiring, int64_t batch, const int64_t *y_row_ptr,
+                         const int32_t *y_col, const float *y_val, float *Z, void *ws, int64_t ws_bytes);
+
 /*
  * Bytes of device workspace a forward call over `batch` samples needs:
  * y_is_csr = 0 for sdnn_forward_dense, 1 for sdnn_forward_csr.

@@ -24,6 +24,11 @@ SDNN_ARM_SPARSE = 0
 SDNN_ARM_DENSE = 1
 SDNN_BIAS_EVERYWHERE = 0
 SDNN_BIAS_PATTERN = 1
+SDNN_SEMIRING_PLUS_TIMES = 0
+SDNN_SEMIRING_MAX_PLUS = 1
+SDNN_SEMIRING_MAX_MIN = 2
+SDNN_SEMIRING_MIN_MAX = 3
+SDNN_SEMIRING_XOR_AND = 4
 
 STATUS_NAMES = {
     0: "SDNN_OK", 1: "SDNN_ERR_NULL_POINTER", 2: "SDNN_ERR_INVALID_VALUE", 3: "SDNN_ERR_INVALID_INDEX",
@@ -57,6 +62,8 @@ _sig = {
     "sdnn_forward_dense": [_P, _I32, _I32, _I64, _P, _P, _P, _I64, _I32],
     "sdnn_forward_csr": [_P, _I32, _I32, _I64, _P, _P, _P, _P, _I64, _P, _c.POINTER(_P), _c.POINTER(_P),
                          _c.POINTER(_I64)],
+    "sdnn_mxm_dense": [_P, _I32, _I32, _I64, _P, _P, _P, _I64],
+    "sdnn_mxm_csr": [_P, _I32, _I32, _I64, _P, _P, _P, _P, _P, _I64],
     "sdnn_net_free": [_P],
 }
 for _name, _args in _sig.items():
@@ -131,6 +138,15 @@ def sdnn_forward_csr(net, k0: int, k1: int, batch: int, y_row_ptr, y_col, y_val,
     return oc.value or 0, ov.value or 0, nnz.value
 
 
+def sdnn_mxm_dense(net, k: int, semiring: int, batch: int, y, z, ws, ws_bytes: int):
+    _check(lib.sdnn_mxm_dense(net, k, semiring, batch, _ptr(y), _ptr(z), _ptr(ws), ws_bytes))
+
+
+def sdnn_mxm_csr(net, k: int, semiring: int, batch: int, y_row_ptr, y_col, y_val, z, ws, ws_bytes: int):
+    _check(lib.sdnn_mxm_csr(net, k, semiring, batch, _ptr(y_row_ptr), _ptr(y_col), _ptr(y_val), _ptr(z),
+                            _ptr(ws), ws_bytes))
+
+
 def sdnn_net_free(net):
     _check(lib.sdnn_net_free(net))
 
@@ -189,6 +205,29 @@ class Net:
         out = t.empty_like(y) if out is None else out
         ws = self.workspace(batch, 0)
         sdnn_forward_dense(self.handle, k0, k1, batch, y, out, ws, ws.numel(), arm)
+        return out
+
+    def mxm(self, k: int, semiring: int, y, out=None):
+        """Z = Y (+).(x) W_k over a semiring (dense batch x n in and out)."""
+        t = self.torch
+        y = self._dev(y, t.float32)
+        batch = y.shape[0]
+        out = t.empty_like(y) if out is None else out
+        ws = self.workspace(batch, 0)
+        sdnn_mxm_dense(self.handle, k, semiring, batch, y, out, ws, ws.numel())
+        return out
+
+    def mxm_csr(self, k: int, semiring: int, row_ptr, col, val):
+        """Z = Y (+).(x) W_k for a CSR batch (unstored entries are the 0-element); Z dense batch x n."""
+        t = self.torch
+        rp = self._dev(row_ptr, t.int64)
+        c = self._dev(col, t.int32)
+        v = self._dev(val, t.float32)
+        batch = rp.numel() - 1
+        out = t.empty((batch, self.n), dtype=t.float32, device=self.device)
+        ws = self.workspace(batch, 0)
+        sdnn_mxm_csr(self.handle, k, semiring, batch, rp, c if c.numel() else None, v if v.numel() else None,
+                     out, ws, ws.numel())
         return out
 
     def forward_csr(self, row_ptr, col, val, k0: int = 0, k1: int | None = None):

@@ -86,4 +86,14 @@ hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, con
                                const int32_t *in_col, const float *in_val, int32_t *out_col, float *out_val,
                                hipStream_t s);
 
+// semiring.hip
+enum : int { kSemiringPlusTimes = 0, kSemiringMaxPlus = 1, kSemiringMaxMin = 2, kSemiringMinMax = 3, kSemiringXorAnd = 4 };
+float semiring_zero(int semiring);
+// Z^T = (Y (+).(x) W)^T from Y^T (n x batch) over the fan-in lists; no bias, no activation.
+hipError_t launch_semiring_mxm(int semiring, int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
+                               const float *yt, float *zt, hipStream_t s);
+// Y^T (n x batch) = `fill` everywhere, then the stored entries of the CSR rows (extents checked, flagged in err).
+hipError_t launch_semiring_densify(int64_t n, int64_t batch, float fill, const int64_t *row_ptr, const int32_t *col,
+                                   const float *val, float *yt, uint32_t *err, hipStream_t s);
+
 }  // namespace sdnn

@@ -142,6 +142,49 @@ def test_pattern_bias_integer_shadow_and_dense_arm(sd):
     assert ei.value.status == 9
 
 
+# ------------------------------------------------------------------ semiring mxm (Sec. II)
+
+SEMIRINGS = ["plus_times", "max_plus", "max_min", "min_max", "xor_and"]
+
+
+@pytest.mark.parametrize("name", SEMIRINGS)
+@pytest.mark.parametrize("seed,n,batch,d", [(81, 37, 3, 0.3), (82, 300, 130, 0.05), (83, 1000, 2048, 0.01),
+                                            (84, 700, 64, 0.6)])
+def test_semiring_mxm_dense(sd, name, seed, n, batch, d):
+    """Z = Y (+).(x) W_k on the gather skeleton equals the oracle bit for bit (one order of reduction,
+    exact products), for 1, 2 and 4 columns per lane and with explicit zeros stored in W."""
+    import oracle
+    import torch
+
+    p = tiny_random(seed, n, 1, batch, w_density=d, dense_input=True, y_density=0.7, explicit_zeros=True)
+    want = oracle.mxm(name, n, p.layers[0], p.y0_dense)
+    net = sd.net_from_problem(p)
+    _say("semiring dense", name, seed, n, batch)
+    got = net.mxm(0, oracle.SEMIRINGS[name], torch.from_numpy(p.y0_dense).cuda()).cpu().numpy()
+    net.free()
+    assert got.tobytes() == want.tobytes()
+
+
+@pytest.mark.parametrize("name", SEMIRINGS)
+def test_semiring_mxm_csr(sd, name):
+    """The CSR form: entries Y does not store are the 0-element (they contribute nothing)."""
+    import oracle
+
+    n, batch = 500, 97
+    p = tiny_random(85, n, 1, batch, w_density=0.02, y_density=0.05)
+    zero = {"max_plus": -math.inf, "max_min": -math.inf, "min_max": math.inf}.get(name, 0.0)
+    yd = np.full((batch, n), zero, np.float32)
+    rp, c, v = p.y0_csr
+    rows = np.repeat(np.arange(batch), np.diff(rp))
+    yd[rows, c] = v
+    want = oracle.mxm(name, n, p.layers[0], yd)
+    net = sd.net_from_problem(p)
+    _say("semiring csr", name)
+    got = net.mxm_csr(0, oracle.SEMIRINGS[name], rp, c, v).cpu().numpy()
+    net.free()
+    assert got.tobytes() == want.tobytes()
+
+
 def test_long_fanin_lists(sd):
     """Fan-in lists longer than 8192 entries (the radix-sort transpose handles any length), n not a multiple
     of 4, on both dense arms; sampled rows."""
