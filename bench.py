@@ -172,7 +172,7 @@ def run_sweep(args, torch, sd):
     else:
         roof = {"bound": "hbm", "achieved": round(byt / t_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    kernel = "spmm_tiled_kernel" if nnz_avg >= 1024 * p.n else "spmm_fanin_kernel"  # the library's selection rule
+    kernel = "spmm_tiled_kernel" if nnz_avg >= 1280 * p.n else "spmm_fanin_kernel"  # the library's selection rule
     roof["traffic"] = _pmc_traffic(f"{kernel}_d{dom:g}", ["spmm.hip", "common.h"])
     roof["kernel"] = kernel
     roof["per_launch_ms"] = round(per_launch[dom], 5)

@@ -87,7 +87,7 @@ static void forward_one_row(forward_job *job, int64_t r, double *acc, char *touc
             const double y = (double)cur_val[t];
             for (int64_t e = W->row_ptr[i]; e < W->row_ptr[i + 1]; ++e) {
                 acc[W->col[e]] += y * (double)W->val[e];
-                if (y != 0.0) touched[W->col[e]] = 1;
+                if (job->bias_mode && y != 0.0) touched[W->col[e]] = 1;
             }
         }
         /* + b, then h, then round once to fp32; keep only nonzeros */

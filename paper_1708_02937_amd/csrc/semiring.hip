@@ -122,7 +122,7 @@ template <class SR>
 hipError_t launch_sr(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan, const float *yt, float *zt,
                      hipStream_t s) {
     int V = 1;
-    if (batch % 4 == 0 && batch >= 2048) V = 4;
+    if (batch % 4 == 0 && batch >= 256) V = 4;
     else if (batch % 2 == 0 && batch >= 128) V = 2;
     const int64_t chunks = (batch + 64 * V - 1) / (64 * V);
     const int64_t blocks = ((n + 3) / 4) * chunks;

@@ -365,10 +365,10 @@ int spmm_tile_count(int64_t n) { return (int)((n + kTileRows - 1) / kTileRows); 
 
 size_t spmm_tile_mask_elems(int64_t n) { return (size_t)spmm_tile_count(n) * (size_t)((n + 3) & ~3ll); }
 
-// Measured on MI355X (n = 4096, batch = 1024): the LDS-tiled product wins at 50% density (0.82 vs 1.85 ms
-// per layer) and 30% (0.67 ms), the L2 gather wins at 10% (0.38 vs 0.63 ms); switch at an average fan-in
-// of 1024.
-bool spmm_wants_tiles(int64_t n, int64_t nnz) { return n <= 65536 && nnz >= 1024 * n; }
+// Measured on MI355X (n = 4096, batch = 1024): the LDS-tiled product wins at 50% density (0.83 vs 1.11 ms
+// per layer for the L2 gather), they tie at 30% (0.69 vs 0.68 ms), the gather wins below; switch at an
+// average fan-in of 1280.
+bool spmm_wants_tiles(int64_t n, int64_t nnz) { return n <= 65536 && nnz >= 1280 * n; }
 
 hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *fan, uint16_t *tile_mask,
                                  hipStream_t s) {
@@ -396,8 +396,10 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, c
         return hipGetLastError();
     }
     // Columns per lane: wide enough to keep 8 independent loads in flight, and a multiple that divides batch.
+    // Columns per lane: four (one 16-byte load per lane, a 1 KiB row segment per wave) whenever the batch
+    // allows; measured on MI355X at n = 4096, batch = 1024, four beat two by 1.4-1.6x at 0.1-10% density.
     int V = 1;
-    if (batch % 4 == 0 && batch >= 2048) V = 4;
+    if (batch % 4 == 0 && batch >= 256) V = 4;
     else if (batch % 2 == 0 && batch >= 128) V = 2;
     const int64_t chunks = (batch + 64 * V - 1) / (64 * V);
     const int64_t groups = (n + 3) / 4;

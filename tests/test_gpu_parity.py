@@ -72,11 +72,11 @@ def test_tiny_dense_batch(sd, arm, seed, n, L, batch):
     parity.compare(p, dense_to_csr(out))
 
 
-@pytest.mark.parametrize("seed,n,L,batch,d", [(31, 1100, 2, 128, 0.97), (32, 1100, 2, 260, 0.95),
-                                              (33, 2000, 2, 1028, 0.6), (34, 1500, 1, 516, 0.75),
-                                              (35, 1030, 2, 132, 0.999), (36, 1283, 1, 388, 0.9)])
+@pytest.mark.parametrize("seed,n,L,batch,d", [(31, 1400, 2, 128, 0.97), (32, 1400, 2, 260, 0.95),
+                                              (33, 2000, 2, 1028, 0.7), (34, 1500, 1, 516, 0.9),
+                                              (35, 1290, 2, 132, 0.999), (36, 1503, 1, 388, 0.9)])
 def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
-    """Average fan-in >= 1024 selects the LDS-tiled product; ragged n (not a multiple of 4, 16 or 32) and
+    """Average fan-in >= 1280 selects the LDS-tiled product; ragged n (not a multiple of 4, 16 or 32) and
     batch exercise its edges."""
     p = tiny_random(seed, n, L, batch, w_density=d, y_density=0.7, dense_input=True,
                     ymax=[math.inf, 3.0][seed % 2], bias_lo=-1.0, bias_hi=1.0)
@@ -120,11 +120,11 @@ def test_pattern_bias_csr_path(sd, seed, n, L, batch, wd, yd):
     parity.compare(p, run_csr(sd, p, bias_mode=1), bias_mode=1)
 
 
-@pytest.mark.parametrize("seed,n,L,batch,d,yd", [(66, 200, 2, 130, 0.05, 0.3), (67, 1100, 2, 260, 0.95, 0.001),
+@pytest.mark.parametrize("seed,n,L,batch,d,yd", [(66, 200, 2, 130, 0.05, 0.3), (67, 1400, 2, 260, 0.95, 0.001),
                                                  (68, 333, 3, 3, 0.1, 0.5), (69, 4100, 1, 2048, 0.002, 0.01)])
 def test_pattern_bias_dense_batch(sd, seed, n, L, batch, d, yd):
     """SDNN_BIAS_PATTERN on the sparse arm with dense batches: the gather SpMM (one, two and four columns
-    per lane) and the LDS-tiled SpMM (fan-in >= 1024); sparse inputs leave many positions untouched."""
+    per lane) and the LDS-tiled SpMM (fan-in >= 1280); sparse inputs leave many positions untouched."""
     p = tiny_random(seed, n, L, batch, w_density=d, y_density=yd, dense_input=True, bias_lo=-0.2, bias_hi=0.6)
     _say("pattern dense", seed, n, L, batch)
     parity.compare(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE, bias_mode=1)), bias_mode=1)

@@ -26,7 +26,7 @@ _ACC_BLOCK = """        for (int64_t t = 0; t < cur_len; ++t) {
             const double y = (double)cur_val[t];
             for (int64_t e = W->row_ptr[i]; e < W->row_ptr[i + 1]; ++e) {
                 acc[W->col[e]] += y * (double)W->val[e];
-                if (y != 0.0) touched[W->col[e]] = 1;
+                if (job->bias_mode && y != 0.0) touched[W->col[e]] = 1;
             }
         }"""
 
@@ -37,7 +37,7 @@ _TRANSPOSED = """        for (int64_t t = 0; t < cur_len; ++t) {
                 for (int64_t e = W->row_ptr[j2]; e < W->row_ptr[j2 + 1]; ++e)
                     if (W->col[e] == i) {
                         acc[j2] += y * (double)W->val[e];
-                        if (y != 0.0) touched[j2] = 1;
+                        if (job->bias_mode && y != 0.0) touched[j2] = 1;
                     }
         }"""
 
@@ -56,8 +56,9 @@ MUTANTS = {
     "bias_index": ("(double)W->bias[j];\n            if (z < 0.0)", "(double)W->bias[0];\n            if (z < 0.0)"),
     "keep_zero": ("if (f != 0.0f) {", "if (f != 0.0f || j == 0) {"),
     "pattern_bias_everywhere": ("if (job->bias_mode && !touched[j]) continue;", ""),
-    "pattern_touch_zero_inputs": ("if (y != 0.0) touched[W->col[e]] = 1;", "touched[W->col[e]] = 1;"),
-    "pattern_never_touch": ("if (y != 0.0) touched[W->col[e]] = 1;", ""),
+    "pattern_touch_zero_inputs": ("if (job->bias_mode && y != 0.0) touched[W->col[e]] = 1;",
+                                  "if (job->bias_mode) touched[W->col[e]] = 1;"),
+    "pattern_never_touch": ("if (job->bias_mode && y != 0.0) touched[W->col[e]] = 1;", ""),
 }
 
 
