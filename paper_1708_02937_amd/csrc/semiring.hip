@@ -43,13 +43,15 @@ constexpr int kSrUnroll = 8;
 
 template <int V, class SR>
 __global__ __launch_bounds__(256) void semiring_gather_kernel(int64_t n, int64_t batch, int chunks,
+                                                              int64_t block_base,
                                                               const int64_t *__restrict__ fan_ptr,
                                                               const Edge *__restrict__ fan,
                                                               const float *__restrict__ yt, float *__restrict__ zt) {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
-    const int64_t c = blockIdx.x % chunks;
-    const int64_t j = (int64_t)(blockIdx.x / chunks) * 4 + wave;
+    const int64_t b = block_base + blockIdx.x;  // large grids are launched in segments
+    const int64_t c = b % chunks;
+    const int64_t j = (b / chunks) * 4 + wave;
     if (j >= n) return;
     const int64_t col = c * (64 * V) + (int64_t)lane * V;
     const bool active = col < batch;        // batch is a multiple of V
@@ -126,13 +128,18 @@ hipError_t launch_sr(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edg
     else if (batch % 2 == 0 && batch >= 128) V = 2;
     const int64_t chunks = (batch + 64 * V - 1) / (64 * V);
     const int64_t blocks = ((n + 3) / 4) * chunks;
-    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    if (V == 4)
-        semiring_gather_kernel<4, SR><<<(unsigned)blocks, 256, 0, s>>>(n, batch, (int)chunks, fan_ptr, fan, yt, zt);
-    else if (V == 2)
-        semiring_gather_kernel<2, SR><<<(unsigned)blocks, 256, 0, s>>>(n, batch, (int)chunks, fan_ptr, fan, yt, zt);
-    else
-        semiring_gather_kernel<1, SR><<<(unsigned)blocks, 256, 0, s>>>(n, batch, (int)chunks, fan_ptr, fan, yt, zt);
+    constexpr int64_t kSeg = 1ll << 23;  // at most 2^32 - 1 work-items per launch
+    for (int64_t base = 0; base < blocks; base += kSeg) {
+        const unsigned nb = (unsigned)(blocks - base < kSeg ? blocks - base : kSeg);
+        if (V == 4)
+            semiring_gather_kernel<4, SR><<<nb, 256, 0, s>>>(n, batch, (int)chunks, base, fan_ptr, fan, yt, zt);
+        else if (V == 2)
+            semiring_gather_kernel<2, SR><<<nb, 256, 0, s>>>(n, batch, (int)chunks, base, fan_ptr, fan, yt, zt);
+        else
+            semiring_gather_kernel<1, SR><<<nb, 256, 0, s>>>(n, batch, (int)chunks, base, fan_ptr, fan, yt, zt);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     return hipGetLastError();
 }
 

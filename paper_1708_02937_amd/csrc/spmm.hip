@@ -68,24 +68,25 @@ __device__ __forceinline__ float bcast_f(float v, int lane) {
 constexpr int kUnroll = 8;
 
 template <int V, bool kPattern>
-__global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batch, int chunks,
+__global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batch, int chunks, int64_t block_base,
                                                          const int64_t *__restrict__ fan_ptr,
                                                          const Edge *__restrict__ fan, const float *__restrict__ bias,
                                                          double ymax, const float *__restrict__ yt,
                                                          float *__restrict__ zt) {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
+    const int64_t b = block_base + blockIdx.x;  // large grids are launched in segments (see the launcher)
     int64_t c, g;
     if (chunks % 8 == 0) {
         // chunk-major per XCD: XCD x works through chunks x, x+8, ... one at a time, every neuron group
         // of a chunk before the next, so the input rows its current neurons gather stay in its L2
         const int64_t groups = (n + 3) / 4;
-        const int64_t local = blockIdx.x / 8;
-        c = (blockIdx.x % 8) + 8 * (local / groups);
+        const int64_t local = b / 8;
+        c = (b % 8) + 8 * (local / groups);
         g = local % groups;
     } else {
-        c = blockIdx.x % chunks;
-        g = blockIdx.x / chunks;
+        c = b % chunks;
+        g = b / chunks;
     }
     const int64_t j = g * 4 + wave;
     if (j >= n) return;
@@ -404,18 +405,26 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, c
     const int64_t chunks = (batch + 64 * V - 1) / (64 * V);
     const int64_t groups = (n + 3) / 4;
     const int64_t blocks = groups * chunks;
-    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    if (chunks > 0x7fffffffLL) return hipErrorInvalidValue;
+    // a launch holds at most 2^32 - 1 work-items: segments of 2^23 workgroups (a multiple of 8, so the
+    // XCD of a workgroup, its linear index mod 8, is unchanged)
+    constexpr int64_t kSeg = 1ll << 23;
+    for (int64_t base = 0; base < blocks; base += kSeg) {
+        const unsigned nb = (unsigned)(blocks - base < kSeg ? blocks - base : kSeg);
 #define SDNN_GATHER(VV, PP) \
-    spmm_fanin_kernel<VV, PP><<<(unsigned)blocks, 256, 0, s>>>(n, batch, (int)chunks, fan_ptr, fan, bias, ymax, yt, zt)
-    switch (V * 2 + (pattern ? 1 : 0)) {
-        case 8: SDNN_GATHER(4, false); break;
-        case 9: SDNN_GATHER(4, true); break;
-        case 4: SDNN_GATHER(2, false); break;
-        case 5: SDNN_GATHER(2, true); break;
-        case 3: SDNN_GATHER(1, true); break;
-        default: SDNN_GATHER(1, false);
-    }
+    spmm_fanin_kernel<VV, PP><<<nb, 256, 0, s>>>(n, batch, (int)chunks, base, fan_ptr, fan, bias, ymax, yt, zt)
+        switch (V * 2 + (pattern ? 1 : 0)) {
+            case 8: SDNN_GATHER(4, false); break;
+            case 9: SDNN_GATHER(4, true); break;
+            case 4: SDNN_GATHER(2, false); break;
+            case 5: SDNN_GATHER(2, true); break;
+            case 3: SDNN_GATHER(1, true); break;
+            default: SDNN_GATHER(1, false);
+        }
 #undef SDNN_GATHER
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     return hipGetLastError();
 }
 

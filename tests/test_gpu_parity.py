@@ -185,6 +185,37 @@ def test_semiring_mxm_csr(sd, name):
     assert got.tobytes() == want.tobytes()
 
 
+def test_gather_grid_larger_than_one_launch(sd):
+    """n = 2^20 and batch 4098 (two columns per lane, 33 chunks) need 8.65M workgroups: more than one
+    launch holds, so the gather runs in segments.  Y is drawn on the device from a seeded generator and
+    the sampled rows are handed to the oracle; 68 GB of device memory."""
+    import torch
+
+    n, batch = 1 << 20, 4098
+    rng = np.random.default_rng(20170802)
+    col = np.sort(rng.integers(0, n, size=(n, 2)), axis=1).astype(np.int32)
+    col[:, 1] = np.where(col[:, 1] == col[:, 0], (col[:, 0] + 1) % n, col[:, 1])
+    col.sort(axis=1)
+    row_ptr = np.arange(0, 2 * n + 1, 2, dtype=np.int64)
+    layer = Layer(row_ptr, col.reshape(-1), rng.uniform(-1, 1, size=2 * n).astype(np.float32),
+                  rng.uniform(-0.1, 0.1, size=n).astype(np.float32))
+    gen = torch.Generator(device="cuda").manual_seed(20170802)
+    y = torch.rand((batch, n), generator=gen, device="cuda", dtype=torch.float32)
+    net = sd.Net(n, 1)
+    net.set_layer(0, layer.row_ptr, layer.col, layer.val, layer.bias)
+    _say("segmented gather grid", n, batch)
+    out = net.forward_dense(y, arm=sd.SDNN_ARM_SPARSE)
+    rows = [0, 1, 2047, 4096, 4097]
+    got = out[rows].cpu().numpy()
+    y_rows = y[rows].cpu().numpy()
+    del out, y
+    net.free()
+    torch.cuda.empty_cache()
+    from workloads import Problem
+    p = Problem("segmented", n, 1, len(rows), math.inf, [layer], y0_dense=y_rows)
+    parity.compare(p, dense_to_csr(got))
+
+
 def test_long_fanin_lists(sd):
     """Fan-in lists longer than 8192 entries (the radix-sort transpose handles any length), n not a multiple
     of 4, on both dense arms; sampled rows."""
