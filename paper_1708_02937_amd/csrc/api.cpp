@@ -89,7 +89,7 @@ struct CsrWs {
     int32_t *cnt[2];
     int32_t *col[2];
     float *val[2];
-    int32_t *lists;  // 2 * batch: the small and large sample lists of the layer being computed
+    int32_t *lists;  // 3 * batch: the sample lists of the layer being computed
     int64_t *scan_tmp;
     size_t bytes;
 };
@@ -108,7 +108,7 @@ CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
         off = align_up(off + slots * sizeof(float));
     }
     w.lists = (int32_t *)(p + off);
-    off = align_up(off + 2 * (size_t)batch * sizeof(int32_t));
+    off = align_up(off + 3 * (size_t)batch * sizeof(int32_t));
     w.scan_tmp = (int64_t *)(p + off);
     off = align_up(off + (size_t)sdnn::scan_tmp_elems(batch) * sizeof(int64_t));
     w.bytes = off;
@@ -134,7 +134,7 @@ struct sdnn_net_s {
     std::vector<Layer> layers;
     uint32_t *d_flags = nullptr;
     int32_t *d_int = nullptr;
-    unsigned long long *d_stats = nullptr;  // 4 counters per layer of a forward call (see launch_spgemm_layer)
+    unsigned long long *d_stats = nullptr;  // kSpgemmStats counters per layer of a forward call
     int num_cu = 256;
 };
 
@@ -182,7 +182,7 @@ sdnn_status sdnn_net_create(sdnn_net *out, int64_t n, int32_t L, float ymax, voi
     net->layers.resize((size_t)L);
     sdnn_status st = dalloc(&net->d_flags, 4, "flags");
     if (st == SDNN_OK) st = dalloc(&net->d_int, 4, "scratch");
-    if (st == SDNN_OK) st = dalloc(&net->d_stats, (size_t)(L > 0 ? L : 1) * 4, "layer counters");
+    if (st == SDNN_OK) st = dalloc(&net->d_stats, (size_t)(L > 0 ? L : 1) * sdnn::kSpgemmStats, "layer counters");
     if (st != SDNN_OK) {
         dfree(net->d_flags);
         dfree(net->d_int);
@@ -410,7 +410,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         return SDNN_OK;
     }
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
-    SDNN_HIP(hipMemsetAsync(net->d_stats, 0, (size_t)(k1 - k0) * 4 * sizeof(unsigned long long), s));
+    SDNN_HIP(hipMemsetAsync(net->d_stats, 0, (size_t)(k1 - k0) * sdnn::kSpgemmStats * sizeof(unsigned long long), s));
 
     // Activation format per layer.  While outputs are sparse they stay as slot rows (row-wise SpGEMM).
     // From the first layer whose input is dense enough, activations are kept dense and neuron-major and
@@ -442,7 +442,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         }
         if (nnz_hi >= dense_at && !exact) {
             unsigned long long got = 0;
-            SDNN_HIP(hipMemcpyAsync(&got, net->d_stats + 4 * (k - 1 - k0) + 2, sizeof(got), hipMemcpyDeviceToHost, s));
+            SDNN_HIP(hipMemcpyAsync(&got, net->d_stats + sdnn::kSpgemmStats * (k - 1 - k0) + sdnn::kSpgemmStatNnz, sizeof(got), hipMemcpyDeviceToHost, s));
             SDNN_HIP(hipStreamSynchronize(s));
             nnz_hi = (double)got;
             exact = true;
@@ -456,7 +456,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
                                            first ? y_col : w.col[cur ^ 1], first ? y_val : w.val[cur ^ 1], l.row_ptr,
                                            l.w_seg, l.w_pack, l.nnz, l.max_fanout, l.bias, l.bias_nonpos ? 1 : 0,
                                            net->bias_pattern, net->ymax, w.cnt[cur], w.col[cur], w.val[cur], w.lists,
-                                           net->d_stats + 4 * (k - k0), net->d_flags, net->num_cu, s));
+                                           net->d_stats + sdnn::kSpgemmStats * (k - k0), net->d_flags, net->num_cu, s));
         cur ^= 1;
         const double full = (double)batch * (double)n;
         nnz_hi = (l.bias_nonpos || net->bias_pattern) ? std::min(full, nnz_hi * (double)l.max_fanout) : full;

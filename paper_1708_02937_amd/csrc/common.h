@@ -70,8 +70,11 @@ bool spgemm_wants_window_index(int64_t n);
 hipError_t launch_window_seg(int64_t n, const int64_t *w_ptr, const int32_t *col, int32_t *w_seg, hipStream_t s);
 // ylen limit of the small-sample SpGEMM kernel for a layer whose longest fan-out row has max_fanout entries.
 int64_t spgemm_small_len(int64_t n, int32_t max_fanout);
-// One sparse layer: planning pass, small-sample kernel, workgroup kernel.  lists holds 2 * batch int32;
-// stats points to the layer's 4 counters (zero on entry): small count, large count, output nnz, work.
+// One sparse layer: planning pass, small-sample kernel, the two workgroup kernels (entries kept in
+// registers, general).  lists holds 3 * batch int32; stats points to the layer's kSpgemmStats counters
+// (zero on entry); counter kSpgemmStatNnz receives the output nnz.
+constexpr int kSpgemmStats = 8;
+constexpr int kSpgemmStatNnz = 2;
 // pattern != 0: the bias and h apply only on the structural pattern of Y_k W_k.
 hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const int32_t *w_seg,

@@ -68,19 +68,19 @@ constexpr int kSmallCap = 1024;   // products per sample in the small-sample ker
 constexpr int kSmallWaves = 4;    // wavefronts per workgroup of the small-sample kernel
 
 // Per-layer counters kept by the sparse layer kernels (one row of the net's statistics array).
-enum : int { kStatSmall = 0, kStatLarge = 1, kStatNnz = 2, kStatWork = 3 };
+enum : int { kStatSmall = 0, kStatLarge = 1, kStatNnz = 2, kStatWork = 3, kStatResident = 4, kStatResidentWork = 5 };
 
 // Planning pass: one thread per sample.  When only touched columns can be nonzero (every b_j <= 0, or the
-// bias applies only on the structural pattern), empty samples are finished here
-// (cnt = 0); the others are appended to the small list (lists[0 .. small)) or the large list
-// (lists[batch .. batch + large)) with one atomic per wave and list.
+// bias applies only on the structural pattern), empty samples are finished here (cnt = 0); the others are
+// appended, with one atomic per wave and list, to the small list (lists[0 ..)), the list of samples the
+// workgroup kernel can keep in registers (lists[2 batch ..)) or the general list (lists[batch ..)).
 __global__ __launch_bounds__(256) void spgemm_plan_kernel(int64_t n, int64_t batch, const int64_t *__restrict__ in_row_ptr,
                                                           const int32_t *__restrict__ in_cnt,
                                                           const int32_t *__restrict__ in_col,
                                                           const float *__restrict__ in_val, int only_touched,
-                                                          int64_t small_len, int32_t *__restrict__ out_cnt,
-                                                          int32_t *__restrict__ lists, unsigned long long *stats,
-                                                          uint32_t *err) {
+                                                          int64_t small_len, int64_t resident_len,
+                                                          int32_t *__restrict__ out_cnt, int32_t *__restrict__ lists,
+                                                          unsigned long long *stats, uint32_t *err) {
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int lane = threadIdx.x & 63;
     const bool valid = r < batch;
@@ -88,18 +88,22 @@ __global__ __launch_bounds__(256) void spgemm_plan_kernel(int64_t n, int64_t bat
     if (valid) ylen = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err).ylen;
     const bool skip = valid && only_touched && ylen == 0;
     const bool small = valid && only_touched && ylen > 0 && ylen <= small_len;
-    const bool large = valid && !skip && !small;
+    const bool resident = valid && !skip && !small && ylen <= resident_len;
+    const bool large = valid && !skip && !small && !resident;
     if (skip) out_cnt[r] = 0;
-    const uint64_t ms = __ballot(small), ml = __ballot(large);
-    unsigned long long bs = 0, bl = 0;
+    const uint64_t ms = __ballot(small), ml = __ballot(large), mr = __ballot(resident);
+    unsigned long long bs = 0, bl = 0, br = 0;
     if (lane == 0) {
         if (ms) bs = atomicAdd(&stats[kStatSmall], (unsigned long long)__popcll(ms));
         if (ml) bl = atomicAdd(&stats[kStatLarge], (unsigned long long)__popcll(ml));
+        if (mr) br = atomicAdd(&stats[kStatResident], (unsigned long long)__popcll(mr));
     }
     bs = __shfl(bs, 0);
     bl = __shfl(bl, 0);
+    br = __shfl(br, 0);
     if (small) lists[bs + lane_rank(ms)] = (int32_t)r;
     if (large) lists[batch + bl + lane_rank(ml)] = (int32_t)r;
+    if (resident) lists[2 * batch + br + lane_rank(mr)] = (int32_t)r;
 }
 
 // Orders this wave's earlier LDS accesses before its later ones (the lanes of one wave exchange data
@@ -227,7 +231,10 @@ __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
 }
 
 constexpr int kRounds = kTile / (4 * kThreads);  // dense-epilogue rounds of 4 columns per thread
+constexpr int kRes = 1;                           // stored entries a thread keeps in registers (resident mode)
+constexpr int kResLoads = 4;                      // weight loads in flight per resident entry
 
+template <bool kResident>
 __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
     int64_t n, int64_t batch, int nwin, const int64_t *__restrict__ in_row_ptr,
     const int32_t *__restrict__ in_cnt, const int32_t *__restrict__ in_col, const float *__restrict__ in_val,
@@ -251,15 +258,15 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
     for (int t = tid; t < width0; t += kThreads) acc[t] = 0.0;
     for (int t = tid; t < kBitWords; t += kThreads) bits[t] = 0u;
     if (tid == 0) any = 0;
-    // the large list was filled by the planning pass of this layer; chunks of it are taken in turn
-    const int64_t count = (int64_t)stats[kStatLarge];
+    // this instance's list was filled by the planning pass of the layer; chunks of it are taken in turn
+    const int64_t count = (int64_t)stats[kResident ? kStatResident : kStatLarge];
     int64_t chunk = count / ((int64_t)gridDim.x * 16);
     chunk = chunk < 1 ? 1 : (chunk > 64 ? 64 : chunk);
     const unsigned long long nchunks = (unsigned long long)((count + chunk - 1) / chunk);
-    const int32_t *large = list + batch;
+    const int32_t *large = list + (kResident ? 2 : 1) * batch;
 
     for (;;) {
-        if (tid == 0) chunk_id = atomicAdd(&stats[kStatWork], 1ull);
+        if (tid == 0) chunk_id = atomicAdd(&stats[kResident ? kStatResidentWork : kStatWork], 1ull);
         __syncthreads();
         const unsigned long long ch = chunk_id;
         if (ch >= nchunks) break;  // uniform: every workgroup reaches this once the counter passes the end
@@ -270,23 +277,31 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
             const RowIn ri = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err);
             const int64_t yb = ri.yb, ylen = ri.ylen;
             const bool sparse = pattern || (bias_nonpos && ylen <= sparse_limit);
-            // resident mode: one stored entry per thread, kept in registers across the windows; the
-            // thread's fan-out segment for window w is [s_lo, s_hi), and the next window's segment starts
-            // where this one ends, so each window costs one more offset load, issued a window ahead
-            const bool resident = lane_segments && ylen <= kThreads;
-            double my_y = 0.0;
-            int32_t my_i = -1;
-            int64_t my_rb = 0, s_lo = 0, s_hi = 0;
-            if (resident && tid < ylen) {
-                const int32_t i = in_col[yb + tid];
-                if (i >= 0 && i < n) {
-                    my_i = i;
-                    my_y = (double)in_val[yb + tid];
-                    my_rb = w_ptr[i];
-                    s_lo = my_rb;
-                    s_hi = w_seg ? my_rb + w_seg[(int64_t)i * (nwin + 1) + 1] : w_ptr[i + 1];
-                } else {
-                    atomicOr(err, 1u);
+            // resident instance: up to kRes stored entries per thread, kept in registers across the
+            // windows; the thread's fan-out segment for window w is [s_lo, s_hi), and the next window's
+            // segment starts where this one ends, so each window costs one more offset load, issued a
+            // window ahead.  The planner sends only samples that fit here (and short fan-out segments).
+            constexpr bool resident = kResident;
+            double my_y[kRes];
+            int32_t my_i[kRes];
+            int64_t my_rb[kRes], s_lo[kRes], s_hi[kRes];
+#pragma unroll
+            for (int k = 0; k < kRes; ++k) {
+                my_y[k] = 0.0;
+                my_i[k] = -1;
+                my_rb[k] = s_lo[k] = s_hi[k] = 0;
+                const int64_t t = tid + (int64_t)k * kThreads;
+                if (resident && t < ylen) {
+                    const int32_t i = in_col[yb + t];
+                    if (i >= 0 && i < n) {
+                        my_i[k] = i;
+                        my_y[k] = (double)in_val[yb + t];
+                        my_rb[k] = w_ptr[i];
+                        s_lo[k] = my_rb[k];
+                        s_hi[k] = w_seg ? my_rb[k] + w_seg[(int64_t)i * (nwin + 1) + 1] : w_ptr[i + 1];
+                    } else {
+                        atomicOr(err, 1u);
+                    }
                 }
             }
             const int64_t ob = r * n;
@@ -295,38 +310,29 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                 const int64_t c0 = (int64_t)win * kTile;
                 const int64_t c1 = (c0 + kTile < n) ? c0 + kTile : n;
                 const int width = (int)(c1 - c0);
-                // biases of this thread's dense-epilogue columns, loaded before the scatter so that the
-                // epilogue does not wait for them
-                float bv[kRounds][4];
-                if (!sparse) {
-#pragma unroll
-                    for (int rd = 0; rd < kRounds; ++rd)
-#pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            const int t = rd * 4 * kThreads + 4 * tid + v;
-                            bv[rd][v] = t < width ? bias[c0 + t] : 0.0f;
-                        }
-                }
                 bool mine_any = false;
-                if (resident) {
-                    const int64_t lo = s_lo, hi = s_hi;
-                    if (win + 1 < nwin && my_i >= 0) {
-                        s_lo = s_hi;
-                        s_hi = my_rb + w_seg[(int64_t)my_i * (nwin + 1) + win + 2];
-                    }
-                    for (int64_t e = lo; e < hi; e += 8) {
-                        Edge ed[8];
+                if constexpr (kResident) {
 #pragma unroll
-                        for (int u = 0; u < 8; ++u)
-                            if (e + u < hi) ed[u] = w[e + u];
+                    for (int k = 0; k < kRes; ++k) {
+                        const int64_t lo = s_lo[k], hi = s_hi[k];
+                        if (win + 1 < nwin && my_i[k] >= 0) {
+                            s_lo[k] = s_hi[k];
+                            s_hi[k] = my_rb[k] + w_seg[(int64_t)my_i[k] * (nwin + 1) + win + 2];
+                        }
+                        for (int64_t e = lo; e < hi; e += kResLoads) {
+                            Edge ed[kResLoads];
 #pragma unroll
-                        for (int u = 0; u < 8; ++u)
-                            if (e + u < hi) {
-                                const int col = ed[u].idx - (int)c0;
-                                atomicAdd(&acc[col], my_y * (double)ed[u].w);
-                                if (sparse && my_y != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
-                                mine_any = true;
-                            }
+                            for (int u = 0; u < kResLoads; ++u)
+                                if (e + u < hi) ed[u] = w[e + u];
+#pragma unroll
+                            for (int u = 0; u < kResLoads; ++u)
+                                if (e + u < hi) {
+                                    const int col = ed[u].idx - (int)c0;
+                                    atomicAdd(&acc[col], my_y[k] * (double)ed[u].w);
+                                    if (sparse && my_y[k] != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
+                                    mine_any = true;
+                                }
+                        }
                     }
                 } else {
                     // each wave takes 64 stored entries of the sample at once (one per lane, coalesced),
@@ -474,7 +480,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                             const int t = rd * 4 * kThreads + 4 * tid + v;
                             f[rd][v] = 0.0f;
                             if (t < width) {
-                                f[rd][v] = activate(acc[t] + (double)bv[rd][v], ymax);
+                                f[rd][v] = activate(acc[t] + (double)bias[c0 + t], ymax);
                                 acc[t] = 0.0;
                             }
                             keep += f[rd][v] != 0.0f;
@@ -590,17 +596,20 @@ __global__ __launch_bounds__(256) void densify_kernel(int64_t n, int64_t batch, 
 
 // Slot rows from dense batch-major activations (already h(.)-applied): keep the nonzeros of row r in
 // column order at [r*n, r*n + cnt[r]), compacted with a wave ballot and a scan of the wave totals.
-__global__ __launch_bounds__(kThreads) void dense_to_slots_kernel(int64_t n, const float *__restrict__ y,
+constexpr int kSlotThreads = 1024;
+constexpr int kSlotWaves = kSlotThreads / 64;
+
+__global__ __launch_bounds__(kSlotThreads) void dense_to_slots_kernel(int64_t n, const float *__restrict__ y,
                                                                   int32_t *__restrict__ out_cnt,
                                                                   int32_t *__restrict__ out_col,
                                                                   float *__restrict__ out_val) {
-    __shared__ int wave_tot[kWaves];
+    __shared__ int wave_tot[kSlotWaves];
     const int64_t r = blockIdx.x;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const float *row = y + r * n;
     const int64_t ob = r * n;
     int64_t written = 0;
-    for (int64_t base = 0; base < n; base += kThreads) {
+    for (int64_t base = 0; base < n; base += kSlotThreads) {
         const int64_t j = base + threadIdx.x;
         const float f = j < n ? row[j] : 0.0f;
         const bool keep = f != 0.0f;
@@ -610,7 +619,7 @@ __global__ __launch_bounds__(kThreads) void dense_to_slots_kernel(int64_t n, con
         __syncthreads();
         int off = 0, tot = 0;
 #pragma unroll
-        for (int u = 0; u < kWaves; ++u) {
+        for (int u = 0; u < kSlotWaves; ++u) {
             const int v = wave_tot[u];
             off += (u < wave) ? v : 0;
             tot += v;
@@ -652,14 +661,24 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     if (batch > 0x7fffffffLL) return hipErrorInvalidValue;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)spgemm_row_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)((size_t)kTile * sizeof(double)));
-        if (e != hipSuccess) return e;
+        for (const void *f : {(const void *)spgemm_row_kernel<true>, (const void *)spgemm_row_kernel<false>}) {
+            hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               (int)((size_t)kTile * sizeof(double)));
+            if (e != hipSuccess) return e;
+        }
         attr_set = true;
     }
+    const int nwin = spgemm_windows(n);
+    // the bitmap epilogue pays off while a window gets at most ~2048 products
+    const double per_win = (double)w_nnz / (double)n / (double)nwin;
+    const int64_t sparse_limit = per_win > 0 ? (int64_t)(2048.0 / per_win) : n;
+    // segments of at most ~16 entries are walked lane by lane, longer ones by half-waves
+    const int lane_segments = (w_seg || nwin == 1) && per_win <= 16.0 ? 1 : 0;
     const int64_t small_len = spgemm_small_len(n, max_fanout);
+    const int64_t resident_len = lane_segments ? (int64_t)kRes * kThreads : 0;
     spgemm_plan_kernel<<<(unsigned)((batch + 255) / 256), 256, 0, s>>>(
-        n, batch, in_row_ptr, in_cnt, in_col, in_val, only_touched, small_len, out_cnt, lists, stats, err);
+        n, batch, in_row_ptr, in_cnt, in_col, in_val, only_touched, small_len, resident_len, out_cnt, lists, stats,
+        err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (only_touched) {
@@ -671,14 +690,15 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const int nwin = spgemm_windows(n);
     const int64_t grid = batch < num_cu ? batch : num_cu;
-    // the bitmap epilogue pays off while a window gets at most ~2048 products
-    const double per_win = (double)w_nnz / (double)n / (double)nwin;
-    const int64_t sparse_limit = per_win > 0 ? (int64_t)(2048.0 / per_win) : n;
-    // segments of at most ~16 entries are walked lane by lane, longer ones by half-waves
-    const int lane_segments = (w_seg || nwin == 1) && per_win <= 16.0 ? 1 : 0;
-    spgemm_row_kernel<<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
+    if (resident_len > 0) {
+        spgemm_row_kernel<true><<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
+            n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, only_touched, pattern,
+            sparse_limit, lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    spgemm_row_kernel<false><<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
         n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, only_touched, pattern,
         sparse_limit, lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
     return hipGetLastError();
@@ -704,7 +724,7 @@ hipError_t launch_densify(int64_t n, int64_t batch, const int64_t *in_row_ptr, c
 hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,
                                  float *out_val, hipStream_t s) {
     if (batch == 0) return hipSuccess;
-    dense_to_slots_kernel<<<(unsigned)batch, kThreads, 0, s>>>(n, y, out_cnt, out_col, out_val);
+    dense_to_slots_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, out_cnt, out_col, out_val);
     return hipGetLastError();
 }
 
