@@ -92,6 +92,14 @@ def spmm_algorithmic(n, batch, nnz):
     return 8 * n * batch + 8 * nnz + 8 * (n + 1) + 4 * n, 2.0 * batch * nnz
 
 
+def spmm_kernel_name(n, nnz):
+    """The dense-Y layer kernel the library selects (mirrors spmm_wants_tiles / spmm_wants_slots)."""
+    if n <= 65536 and nnz >= 1280 * n:
+        slot_bytes = -(-n // 16) * 16 * (-(-n // 64) * 64) * 8
+        return "spmm_slots_kernel" if slot_bytes <= 2 ** 31 else "spmm_tiled_kernel"
+    return "spmm_fanin_kernel"
+
+
 def run_sweep(args, torch, sd):
     from workloads import make_config
 
@@ -172,7 +180,7 @@ def run_sweep(args, torch, sd):
     else:
         roof = {"bound": "hbm", "achieved": round(byt / t_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    kernel = "spmm_tiled_kernel" if nnz_avg >= 1280 * p.n else "spmm_fanin_kernel"  # the library's selection rule
+    kernel = spmm_kernel_name(p.n, nnz_avg)
     roof["traffic"] = _pmc_traffic(f"{kernel}_d{dom:g}", ["spmm.hip", "common.h"])
     roof["kernel"] = kernel
     roof["per_launch_ms"] = round(per_launch[dom], 5)

@@ -48,6 +48,7 @@ struct Layer {
     int64_t *fan_ptr = nullptr;  // fan-in CSR (W_k^T)
     Edge *fan = nullptr;
     uint16_t *tile_mask = nullptr;  // which rows of each 16-row input tile each fan-in list holds (high fan-in only)
+    double *slots = nullptr;        // fp64 weight of every (input, output) pair, tile-major (high fan-in, n^2 fits)
     int32_t *w_seg = nullptr;     // where each fan-out row crosses each accumulator window (wide layers only)
     double *dense_wt = nullptr;  // n x n, W_k row-major in fp64 (zeros explicit), for the dense arm
 };
@@ -63,6 +64,7 @@ void release(Layer &l) {
     dfree(l.fan_ptr);
     dfree(l.fan);
     dfree(l.tile_mask);
+    dfree(l.slots);
     dfree(l.w_seg);
     dfree(l.dense_wt);
     l = Layer();
@@ -285,6 +287,10 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
             return cleanup(st);
         SETUP_HIP(sdnn::launch_spmm_tile_mask(n, nl.fan_ptr, nl.fan, nl.tile_mask, s));
     }
+    if (sdnn::spmm_wants_slots(n, nnz)) {
+        if ((st = dalloc(&nl.slots, sdnn::spmm_slot_elems(n), "weight slots")) != SDNN_OK) return cleanup(st);
+        SETUP_HIP(sdnn::launch_spmm_slots(n, nl.fan_ptr, nl.fan, nl.slots, s));
+    }
     SETUP_HIP(hipStreamSynchronize(s));
 #undef SETUP_HIP
     cleanup(SDNN_OK);
@@ -362,7 +368,7 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
     for (int32_t k = k0; k < k1; ++k) {
         const Layer &l = net->layers[(size_t)k];
         if (arm == SDNN_ARM_SPARSE)
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax,
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias, net->ymax,
                                              net->bias_pattern, buf[cur],
                                              buf[cur ^ 1], s));
         else
@@ -473,7 +479,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         int dc = 0;
         for (int32_t k = kd; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.bias, net->ymax,
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias, net->ymax,
                                              net->bias_pattern, dense[dc],
                                              dense[dc ^ 1], s));
             dc ^= 1;

@@ -50,10 +50,15 @@ size_t spmm_tile_mask_elems(int64_t n);
 bool spmm_wants_tiles(int64_t n, int64_t nnz);
 hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *fan, uint16_t *tile_mask,
                                  hipStream_t s);
+// fp64 weight slots of every (input, output) pair for the scalar-register SpMM (zero where W has no entry).
+size_t spmm_slot_elems(int64_t n);
+bool spmm_wants_slots(int64_t n, int64_t nnz);
+hipError_t launch_spmm_slots(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *slots, hipStream_t s);
 // pattern != 0: the bias and h apply only where some fan-in entry meets a nonzero input (else 0).
+// tile_mask / slots: the high fan-in structures when the layer has them (else null).
 hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
-                             const uint16_t *tile_mask, const float *bias, double ymax, int pattern, const float *yt,
-                             float *zt, hipStream_t s);
+                             const uint16_t *tile_mask, const double *slots, const float *bias, double ymax, int pattern,
+                             const float *yt, float *zt, hipStream_t s);
 
 // gemm.hip
 hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *wt, hipStream_t s);

@@ -174,6 +174,11 @@ constexpr int kRowD2 = kTiledCB / 2;                // double2 per slab row (LDS
 constexpr int kStageF4 = kTileRows * kRowF4 / kTiledThreads;
 constexpr int kRowGroup = 2;                        // slab rows read ahead of their FMAs
 
+// Row pitch of the per-(tile, neuron) arrays (masks, slot weights): n rounded up to a whole 64-neuron workgroup
+// of the slot kernel, so every wave reads in bounds and the 64-bit mask loads stay 8-byte aligned; the padding
+// stays zero.
+__host__ __device__ inline int64_t mask_pitch(int64_t n) { return (n + 63) / 64 * 64; }
+
 template <bool kPattern>
 __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
     int64_t n, int64_t batch, int chunks, int ntiles, const int64_t *__restrict__ fan_ptr,
@@ -191,7 +196,7 @@ __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
     if (g * kTiledNJ >= n) return;  // padding group: the whole workgroup leaves before any barrier
     const int64_t jw = g * kTiledNJ + wave * kTiledNPW;  // first neuron of the wave
     const int64_t col0 = c * kTiledCB;
-    const int64_t pitch = (n + 3) & ~3ll;  // mask row pitch: keeps the 64-bit mask loads 8-byte aligned
+    const int64_t pitch = mask_pitch(n);
 
     double acc[kTiledNPW][4];
     uint32_t hit[kTiledNPW][4];  // pattern mode: OR of the inputs' high words (magnitude bits = nonzero)
@@ -313,13 +318,205 @@ __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
     }
 }
 
-// tile_mask[t * pitch + j] bit r = list j holds input neuron t * 16 + r (lists are sorted by input index);
-// pitch = n rounded up to a multiple of 4, the padding stays zero.
+// High fan-in variant with the weights in scalar registers (used when the n x n slot array below fits).
+//
+// The same product as the tiled kernel above, restructured after measuring gfx950: an fp64 FMA whose weight
+// operand is a scalar register pair issues at about 1.25x the rate of one with three vector operands, and a
+// readlane per list entry (the tiled kernel's way of broadcasting the weight) costs more than the FMAs it feeds.
+// So the weights come from a "slot" array built at set-up: for input tile t (16 rows), quarter u (4 rows) and
+// output neuron j, the four fp64 weights W(16t + 4u + r, j), r = 0..3, zero where the list has no entry.  A
+// wave's 4 neurons read 2 rows' weights (16 scalar registers) with scalar loads.
+//
+// A workgroup is 16 wave64s owning 64 output neurons (4 per wave) and 256 batch columns (4 per lane); the
+// 16 x 256 slab of Y^T is staged in LDS widened to fp64, double-buffered (one barrier per tile).  A tile is
+// walked in phases of 2 rows; at the start of phase h a wave waits for phase h's data (the scalar weights and
+// the two slab rows in registers), issues the loads of phase h + 1, then does the FMAs of phase h for every
+// (row, neuron) whose mask bit is set.  Scalar loads may complete out of order, so the only safe wait on them
+// is "all outstanding", which is why the loads of the next phase are issued only after that wait.  Every output
+// is still summed in ascending input order (each FMA adds one product to one accumulator, rows in order).
+constexpr int kSlotThreads = 1024;
+constexpr int kSlotNPW = 4;                                  // output neurons per wave
+constexpr int kSlotNJ = (kSlotThreads / 64) * kSlotNPW;      // 64 per workgroup
+constexpr int kSlotPR = 2;                                   // slab rows per phase
+constexpr int kSlotPrefetch = 1;                 // tiles ahead whose weight lines are pulled into L2
+static_assert(kSlotNJ == 64, "mask_pitch() rounds n to whole workgroups");
+
+template <bool kPattern>
+__global__ __launch_bounds__(kSlotThreads, 1) void spmm_slots_kernel(
+    int64_t n, int64_t batch, int chunks, int ntiles, const uint16_t *__restrict__ tile_mask,
+    const double *__restrict__ slots, const float *__restrict__ bias, double ymax, const float *__restrict__ yt,
+    float *__restrict__ zt) {
+    __shared__ double2 slab[2][kTileRows * kRowD2];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t pitch = mask_pitch(n);
+    // XCD-aware order as in the tiled kernel: the batch chunks of one neuron group run together on one XCD
+    const int64_t local = blockIdx.x / 8;
+    const int64_t c = local % chunks;
+    const int64_t g = (local / chunks) * 8 + blockIdx.x % 8;
+    if (g * kSlotNJ >= pitch) return;  // padding group: the whole workgroup leaves before any barrier
+    const int64_t jw = g * kSlotNJ + wave * kSlotNPW;  // < pitch: masks and slots of padded neurons are zero
+    const int64_t col0 = c * kTiledCB;
+
+    double acc[kSlotNPW][4];
+    uint32_t hit[kSlotNPW][4];  // pattern mode: OR of the inputs' high words (magnitude bits = nonzero)
+#pragma unroll
+    for (int q = 0; q < kSlotNPW; ++q)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            acc[q][v] = 0.0;
+            hit[q][v] = 0u;
+        }
+
+    // staging: one float4 of the 16 x 256 slab per thread (row tid / 64, columns 4 (tid % 64) ..)
+    const int srow = tid / kRowF4, sm = tid % kRowF4;
+    const int64_t sgc = col0 + 4 * (int64_t)sm;
+    float4 st;
+    auto load_slab = [&](int t) {
+        const int64_t gi = (int64_t)t * kTileRows + srow;
+        st = (gi < n && sgc < batch) ? *reinterpret_cast<const float4 *>(yt + gi * batch + sgc)
+                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+    auto stage = [&](int buf) {
+        slab[buf][srow * kRowD2 + sm] = make_double2((double)st.x, (double)st.y);
+        slab[buf][srow * kRowD2 + 64 + sm] = make_double2((double)st.z, (double)st.w);
+    };
+    // weights of rows 2h, 2h + 1 of tile t for the wave's 4 neurons (scalar loads: the address is wave-uniform)
+    auto load_w = [&](int t, int h, double (&w)[kSlotNPW][kSlotPR]) {
+        const int r0 = kSlotPR * h;
+        const double *wp = slots + (((int64_t)t * 4 + r0 / 4) * pitch + jw) * 4 + (r0 % 4);
+#pragma unroll
+        for (int q = 0; q < kSlotNPW; ++q)
+#pragma unroll
+            for (int r = 0; r < kSlotPR; ++r) w[q][r] = wp[q * 4 + r];
+    };
+    auto load_y = [&](int buf, int h, double2 (&y)[kSlotPR][2]) {
+        const double2 *sl = slab[buf] + lane;
+#pragma unroll
+        for (int r = 0; r < kSlotPR; ++r) {
+            y[r][0] = sl[(kSlotPR * h + r) * kRowD2];
+            y[r][1] = sl[(kSlotPR * h + r) * kRowD2 + 64];
+        }
+    };
+    // an empty asm that reads the phase's registers: the compiler must complete their loads before it
+    auto ready = [&](const double (&w)[kSlotNPW][kSlotPR], const double2 (&y)[kSlotPR][2]) {
+#pragma unroll
+        for (int q = 0; q < kSlotNPW; ++q)
+#pragma unroll
+            for (int r = 0; r < kSlotPR; ++r) asm volatile("" ::"s"(w[q][r]));
+#pragma unroll
+        for (int r = 0; r < kSlotPR; ++r)
+            asm volatile("" ::"v"(y[r][0].x), "v"(y[r][0].y), "v"(y[r][1].x), "v"(y[r][1].y));
+    };
+    auto load_mask = [&](int t) -> uint64_t {
+        return *reinterpret_cast<const uint64_t *>(tile_mask + (int64_t)t * pitch + jw);
+    };
+
+    double wc[kSlotNPW][kSlotPR], wn[kSlotNPW][kSlotPR];
+    double2 yc[kSlotPR][2], yn[kSlotPR][2];
+    uint64_t mk = load_mask(0), mkn = 0;
+    load_slab(0);
+    stage(0);
+    load_w(0, 0, wc);
+    __syncthreads();
+    load_y(0, 0, yc);
+    for (int t = 0; t < ntiles; ++t) {
+        const bool more = t + 1 < ntiles;
+        const int buf = t & 1;
+        if (more) {
+            load_slab(t + 1);
+            mkn = load_mask(t + 1);
+        }
+        // Pull the weight lines of tile t + kSlotPrefetch into L2 with a vector load (lanes 0..7: the wave's 8 lines
+        // of 64 bytes, lane 8: its masks): a scalar load that misses L2 stalls the whole phase, a vector load is
+        // waited for only here, at the staging below.
+        uint32_t pf = 0;
+        if (t + kSlotPrefetch < ntiles && lane < 9) {
+            pf = lane < 8 ? *reinterpret_cast<const uint32_t *>(
+                                slots + (((int64_t)(t + kSlotPrefetch) * 4 + lane / 2) * pitch + jw) * 4 + (lane % 2) * 8)
+                          : *reinterpret_cast<const uint32_t *>(tile_mask + (int64_t)(t + kSlotPrefetch) * pitch + jw);
+        }
+#pragma unroll
+        for (int h = 0; h < kTileRows / kSlotPR; ++h) {
+            ready(wc, yc);
+            __builtin_amdgcn_sched_barrier(0);
+            if (h + 1 < kTileRows / kSlotPR) {
+                load_w(t, h + 1, wn);
+                load_y(buf, h + 1, yn);
+            } else if (more) {
+                load_w(t + 1, 0, wn);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int r = 0; r < kSlotPR; ++r) {
+#pragma unroll
+                for (int q = 0; q < kSlotNPW; ++q) {
+                    if (__builtin_expect((uint32_t)(mk >> (16 * q + kSlotPR * h + r)) & 1u, 1u)) {
+                        const double w = wc[q][r];
+                        acc[q][0] = __builtin_fma(yc[r][0].x, w, acc[q][0]);
+                        acc[q][1] = __builtin_fma(yc[r][0].y, w, acc[q][1]);
+                        acc[q][2] = __builtin_fma(yc[r][1].x, w, acc[q][2]);
+                        acc[q][3] = __builtin_fma(yc[r][1].y, w, acc[q][3]);
+                        if constexpr (kPattern) {
+                            hit[q][0] |= (uint32_t)__double2hiint(yc[r][0].x);
+                            hit[q][1] |= (uint32_t)__double2hiint(yc[r][0].y);
+                            hit[q][2] |= (uint32_t)__double2hiint(yc[r][1].x);
+                            hit[q][3] |= (uint32_t)__double2hiint(yc[r][1].y);
+                        }
+                    }
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = 0; q < kSlotNPW; ++q)
+#pragma unroll
+                for (int r = 0; r < kSlotPR; ++r) wc[q][r] = wn[q][r];
+            if (h + 1 < kTileRows / kSlotPR) {
+#pragma unroll
+                for (int r = 0; r < kSlotPR; ++r) {
+                    yc[r][0] = yn[r][0];
+                    yc[r][1] = yn[r][1];
+                }
+            }
+        }
+        if (more) stage((t + 1) & 1);  // that buffer was last read in tile t - 1, before the previous barrier
+        asm volatile("" ::"v"(pf));     // keeps the prefetch load (its value is not needed)
+        mk = mkn;
+        __syncthreads();
+        if (more) load_y((t + 1) & 1, 0, yc);
+    }
+    const int64_t ca = col0 + 4 * lane;  // batch is a multiple of 4, so ca < batch => ca + 3 < batch
+#pragma unroll
+    for (int q = 0; q < kSlotNPW; ++q) {
+        const int64_t j = jw + q;
+        if (j >= n) break;
+        const double bj = (double)bias[j];
+        float f[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            f[v] = (kPattern && (hit[q][v] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[q][v] + bj, ymax);
+        if (ca < batch) *reinterpret_cast<float4 *>(zt + j * batch + ca) = make_float4(f[0], f[1], f[2], f[3]);
+    }
+}
+
+// slots[((t * 4 + u) * pitch + j) * 4 + r] = W(16t + 4u + r, j): one wave per fan-in list, lanes over its entries.
+__global__ void slots_kernel(int64_t n, const int64_t *__restrict__ fan_ptr, const Edge *__restrict__ fan,
+                             double *__restrict__ slots) {
+    const int64_t j = (int64_t)blockIdx.x * (blockDim.x / 64) + threadIdx.x / 64;
+    if (j >= n) return;
+    const int64_t pitch = mask_pitch(n);
+    for (int64_t e = fan_ptr[j] + (threadIdx.x & 63); e < fan_ptr[j + 1]; e += 64) {
+        const int64_t i = fan[e].idx;
+        slots[((i / 4) * pitch + j) * 4 + (i % 4)] = (double)fan[e].w;
+    }
+}
+
+// tile_mask[t * pitch + j] bit r = list j holds input neuron t * 16 + r (lists are sorted by input index).
 __global__ void tile_mask_kernel(int64_t n, const int64_t *__restrict__ fan_ptr, const Edge *__restrict__ fan,
                                  uint16_t *__restrict__ tile_mask) {
     const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (j >= n) return;
-    const int64_t pitch = (n + 3) & ~3ll;
+    const int64_t pitch = mask_pitch(n);
     int64_t t_cur = -1;
     uint32_t m = 0;
     for (int64_t e = fan_ptr[j]; e < fan_ptr[j + 1]; ++e) {
@@ -364,12 +561,26 @@ hipError_t launch_transpose(const float *in, float *out, int64_t rows, int64_t c
 
 int spmm_tile_count(int64_t n) { return (int)((n + kTileRows - 1) / kTileRows); }
 
-size_t spmm_tile_mask_elems(int64_t n) { return (size_t)spmm_tile_count(n) * (size_t)((n + 3) & ~3ll); }
+size_t spmm_tile_mask_elems(int64_t n) { return (size_t)spmm_tile_count(n) * (size_t)mask_pitch(n); }
 
 // Measured on MI355X (n = 4096, batch = 1024): the LDS-tiled product wins at 50% density (0.83 vs 1.11 ms
 // per layer for the L2 gather), they tie at 30% (0.69 vs 0.68 ms), the gather wins below; switch at an
 // average fan-in of 1280.
 bool spmm_wants_tiles(int64_t n, int64_t nnz) { return n <= 65536 && nnz >= 1280 * n; }
+
+size_t spmm_slot_elems(int64_t n) { return (size_t)spmm_tile_count(n) * kTileRows * (size_t)mask_pitch(n); }
+
+// The slot array holds every (input, output) pair in fp64: used while it stays at or below 2 GiB per layer.
+bool spmm_wants_slots(int64_t n, int64_t nnz) {
+    return spmm_wants_tiles(n, nnz) && spmm_slot_elems(n) * sizeof(double) <= (size_t(1) << 31);
+}
+
+hipError_t launch_spmm_slots(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *slots, hipStream_t s) {
+    hipError_t e = hipMemsetAsync(slots, 0, spmm_slot_elems(n) * sizeof(double), s);
+    if (e != hipSuccess) return e;
+    slots_kernel<<<(unsigned)((n + 3) / 4), 256, 0, s>>>(n, fan_ptr, fan, slots);
+    return hipGetLastError();
+}
 
 hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *fan, uint16_t *tile_mask,
                                  hipStream_t s) {
@@ -380,9 +591,22 @@ hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *
 }
 
 hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
-                             const uint16_t *tile_mask, const float *bias, double ymax, int pattern, const float *yt,
-                             float *zt, hipStream_t s) {
+                             const uint16_t *tile_mask, const double *slots, const float *bias, double ymax, int pattern,
+                             const float *yt, float *zt, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
+    if (slots && tile_mask && batch % 4 == 0 && batch >= 128) {
+        const int64_t chunks = (batch + kTiledCB - 1) / kTiledCB;
+        const int64_t groups = mask_pitch(n) / kSlotNJ;
+        const int64_t blocks = (groups + 7) / 8 * 8 * chunks;
+        if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+        if (pattern)
+            spmm_slots_kernel<true><<<(unsigned)blocks, kSlotThreads, 0, s>>>(
+                n, batch, (int)chunks, spmm_tile_count(n), tile_mask, slots, bias, ymax, yt, zt);
+        else
+            spmm_slots_kernel<false><<<(unsigned)blocks, kSlotThreads, 0, s>>>(
+                n, batch, (int)chunks, spmm_tile_count(n), tile_mask, slots, bias, ymax, yt, zt);
+        return hipGetLastError();
+    }
     if (tile_mask && batch % 4 == 0 && batch >= 128) {
         const int64_t chunks = (batch + kTiledCB - 1) / kTiledCB;
         const int64_t groups = (n + kTiledNJ - 1) / kTiledNJ;

@@ -76,8 +76,8 @@ def test_tiny_dense_batch(sd, arm, seed, n, L, batch):
                                               (33, 2000, 2, 1028, 0.7), (34, 1500, 1, 516, 0.9),
                                               (35, 1290, 2, 132, 0.999), (36, 1503, 1, 388, 0.9)])
 def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
-    """Average fan-in >= 1280 selects the LDS-tiled product; ragged n (not a multiple of 4, 16 or 32) and
-    batch exercise its edges."""
+    """Average fan-in >= 1280 selects the LDS-tiled product with scalar-register weights; ragged n (not a
+    multiple of 4, 16 or 64) and batch exercise its edges."""
     p = tiny_random(seed, n, L, batch, w_density=d, y_density=0.7, dense_input=True,
                     ymax=[math.inf, 3.0][seed % 2], bias_lo=-1.0, bias_hi=1.0)
     _say("high fan-in", seed, n, L, batch, d)
@@ -85,6 +85,17 @@ def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
     q = integer_shadow(p)
     q.y0_dense = np.where(p.y0_dense != 0, q.y0_dense if q.y0_dense is not None else 1, 0).astype(np.float32)
     parity.compare(q, dense_to_csr(run_dense(sd, q, sd.SDNN_ARM_SPARSE)), exact=True)
+
+
+def test_high_fanin_beyond_slot_limit(sd):
+    """n = 16448: the fp64 weight slots of every (input, output) pair would exceed 2 GiB, so the high fan-in
+    layer takes the readlane-fed LDS-tiled kernel instead of the scalar-register one; sampled rows, ragged batch."""
+    p = tiny_random(37, 16448, 1, 132, w_density=0.08, y_density=0.7, dense_input=True, bias_lo=-1.0, bias_hi=1.0)
+    assert p.layers[0].nnz >= 1280 * p.n
+    rows = np.arange(0, 132, 12)
+    _say("high fan-in beyond the slot limit")
+    out = run_dense(sd, p, sd.SDNN_ARM_SPARSE)
+    parity.compare(p, dense_to_csr(out[rows]), rows=rows)
 
 
 @pytest.mark.parametrize("seed,n,L,batch", TINY + [(9, 5000, 2, 17), (10, 17000, 2, 9), (11, 40000, 1, 5)])
