@@ -159,14 +159,39 @@ def run_sweep(args, torch, sd):
                 net.set_layer(k, l.row_ptr, l.col, l.val, l.bias)
             torch.cuda.synchronize()
 
-    crossover = None
-    pts = sorted((d, v["sparse_ms"], v.get("dense_ms")) for d, v in
-                 ((float(k), v) for k, v in sweep.items()) if v.get("dense_ms"))
-    for (d0, s0, q0), (d1, s1, q1) in zip(pts, pts[1:]):
-        r0, r1 = math.log(s0 / q0), math.log(s1 / q1)
-        if r0 <= 0 <= r1 and r1 != r0:  # sparse faster at d0, slower at d1
-            t = -r0 / (r1 - r0)
-            crossover = math.exp(math.log(d0) + t * (math.log(d1) - math.log(d0)))
+    def find_crossover():
+        pts = sorted((d, v["sparse_ms"], v.get("dense_ms")) for d, v in
+                     ((float(k), v) for k, v in sweep.items()) if v.get("dense_ms"))
+        for (d0, s0, q0), (d1, s1, q1) in zip(pts, pts[1:]):
+            r0, r1 = math.log(s0 / q0), math.log(s1 / q1)
+            if r0 <= 0 <= r1 and r1 != r0:  # sparse faster at d0, slower at d1
+                t = -r0 / (r1 - r0)
+                return math.exp(math.log(d0) + t * (math.log(d1) - math.log(d0)))
+        return None
+
+    crossover = find_crossover()
+    if crossover is None and not args.no_dense and max(densities) < 1.0:
+        # the sparse arm wins at every sweep density: bracket the crossover with denser weights (same recipe,
+        # same L); these points inform the crossover only and are not part of the step
+        for d in (0.75, 1.0):
+            if d <= max(densities):
+                continue
+            q = make_config(2, d)
+            net = sd.net_from_problem(q)
+            y = torch.from_numpy(q.y0_dense).cuda()
+            o = torch.empty_like(y)
+            net.workspace(q.batch, 0)
+            t_sp = time_calls(torch, lambda: net.forward_dense(y, out=o), max(2, reps // 2))
+            net.build_dense()
+            t_dn = time_calls(torch, lambda: net.forward_dense(y, out=o, arm=sd.SDNN_ARM_DENSE), max(2, reps // 2))
+            net.free()
+            sweep[f"{d:g}"] = {"sparse_ms": round(t_sp, 4), "dense_ms": round(t_dn, 4),
+                               "nnz_per_layer": int(q.layers[0].nnz), "bracket": True}
+            log(f"bracket density {d}: sparse {t_sp:.3f} ms, dense {t_dn:.3f} ms")
+            del q
+            crossover = find_crossover()
+            if crossover is not None:
+                break
     # dominant kernel: the layer launch with the largest share of the step
     dom = max(densities, key=lambda d: per_launch[d])
     p = probs[densities.index(dom)]
@@ -360,6 +385,64 @@ def run_csr_config(args, torch, sd):
     return dict(value=p.edges() / (ms / 1e3), ms_step=ms, config=cfg, roofline=None, sweep=None, crossover=None)
 
 
+# ----------------------------------------------------------------------------- profile summaries (no GPU)
+
+
+def _short_name(kname):
+    base = kname.replace("sdnn::(anonymous namespace)::", "").replace("sdnn::", "").replace("void ", "")
+    return base.split("(")[0].strip()
+
+
+def summarize_stats(csv_dir, title, command, out):
+    """Markdown table of a rocprofv3 --kernel-trace --stats run (the *kernel_stats.csv it wrote)."""
+    import csv
+    import glob
+
+    path = sorted(glob.glob(os.path.join(csv_dir, "**", "*kernel_stats.csv"), recursive=True))[0]
+    rows = list(csv.DictReader(open(path)))
+    lines = ["# rocprofv3 kernel statistics", "", "command (from the repository root on the MI355X box):", "",
+             f"    {command}", "", title, "", "| kernel | calls | avg us | min us | max us | share % |",
+             "|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {_short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def _pmc_avg(csv_dir, counter, kernel):
+    import csv
+    import glob
+
+    path = sorted(glob.glob(os.path.join(csv_dir, "**", "*counter_collection.csv"), recursive=True))[0]
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
+            if r["Counter_Name"] == counter and _short_name(r["Kernel_Name"]).startswith(kernel)]
+    assert vals, f"no {counter} records for {kernel} in {path}"
+    return sum(vals) / len(vals), len(vals)
+
+
+def summarize_pmc(kernel, tag, dirs, copy_bytes, commands, out, src_names):
+    """HBM traffic per launch of `kernel` from FETCH_SIZE / WRITE_SIZE runs, each scaled by what the same
+    counter reads for a plain device copy of copy_bytes bytes (dirs: fetch, write, copy-fetch, copy-write)."""
+    fetch, nf = _pmc_avg(dirs[0], "FETCH_SIZE", kernel)
+    write, nw = _pmc_avg(dirs[1], "WRITE_SIZE", kernel)
+    cfetch, _ = _pmc_avg(dirs[2], "FETCH_SIZE", "__amd_rocclr_copyBuffer")
+    cwrite, _ = _pmc_avg(dirs[3], "WRITE_SIZE", "__amd_rocclr_copyBuffer")
+    fs, ws = copy_bytes / 1024 / cfetch, copy_bytes / 1024 / cwrite
+    hbm = int(round((fetch * fs + write * ws) * 1024))
+    lines = [f"# rocprofv3 HBM traffic counters: {kernel}", "",
+             f"FETCH_SIZE and WRITE_SIZE (KiB per dispatch), averaged over {nf} / {nw} dispatches of the kernel,",
+             f"each scaled by what the same counter reads for a plain device copy of {copy_bytes} bytes",
+             f"(rocclr copyBuffer: FETCH_SIZE {cfetch:.1f} KiB -> scale {fs:.3f}; WRITE_SIZE {cwrite:.1f} KiB -> "
+             f"scale {ws:.3f}).", "", "commands (from the repository root on the MI355X box):", ""]
+    lines += [f"    {c}" for c in commands]
+    lines += ["", f"workload: {tag}", f"fetch_kib_per_dispatch: {fetch:.1f}", f"write_kib_per_dispatch: {write:.1f}",
+              f"fetch_scale: {fs:.4f}", f"write_scale: {ws:.4f}", f"hbm_bytes_per_launch: {hbm}",
+              f"source_hash: {_src_hash(*src_names)}"]
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -378,7 +461,20 @@ def main():
     ap.add_argument("--grid-inv", default="", help="comma-separated inverse sparsities for --paper-grid")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes 5 times (counter calibration)")
+    ap.add_argument("--summarize-stats", nargs=4, metavar=("CSV_DIR", "TITLE", "COMMAND", "OUT"),
+                    help="write a profiles/ table from a rocprofv3 --stats run (no GPU needed)")
+    ap.add_argument("--summarize-pmc", nargs=9,
+                    metavar=("KERNEL", "WORKLOAD", "FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR",
+                             "COPY_BYTES", "COMMANDS", "OUT"),
+                    help="write a profiles/ HBM-traffic summary from rocprofv3 --pmc runs ('|'-separated commands)")
     args = ap.parse_args()
+    if args.summarize_stats:
+        summarize_stats(*args.summarize_stats)
+        return
+    if args.summarize_pmc:
+        a = args.summarize_pmc
+        summarize_pmc(a[0], a[1], a[2:6], int(a[6]), a[7].split("|"), a[8], ["spmm.hip", "common.h"])
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (batch rows would shard "
               "across GPUs with no per-layer exchange; see the design notes). Use --gpus 1.", file=sys.stderr)
