@@ -323,9 +323,9 @@ __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
 // The same product as the tiled kernel above, restructured after measuring gfx950: an fp64 FMA whose weight
 // operand is a scalar register pair issues at about 1.25x the rate of one with three vector operands, and a
 // readlane per list entry (the tiled kernel's way of broadcasting the weight) costs more than the FMAs it feeds.
-// So the weights come from a "slot" array built at set-up: for input tile t (16 rows), quarter u (4 rows) and
-// output neuron j, the four fp64 weights W(16t + 4u + r, j), r = 0..3, zero where the list has no entry.  A
-// wave's 4 neurons read 2 rows' weights (16 scalar registers) with scalar loads.
+// So the weights come from a "slot" array built at set-up: for input tile t (16 rows), phase h (2 rows) and
+// output neuron j, the two fp64 weights W(16t + 2h + r, j), r = 0, 1, zero where the list has no entry, so a
+// wave's 4 neurons find a phase's weights (16 scalar registers) in one 64-byte line, read with one scalar load.
 //
 // A workgroup is 16 wave64s owning 64 output neurons (4 per wave) and 256 batch columns (4 per lane); the
 // 16 x 256 slab of Y^T is staged in LDS widened to fp64, double-buffered (one barrier per tile).  A tile is
@@ -338,6 +338,7 @@ constexpr int kSlotThreads = 1024;
 constexpr int kSlotNPW = 4;                                  // output neurons per wave
 constexpr int kSlotNJ = (kSlotThreads / 64) * kSlotNPW;      // 64 per workgroup
 constexpr int kSlotPR = 2;                                   // slab rows per phase
+constexpr int kSlotPhases = kTileRows / kSlotPR;             // phases per tile
 constexpr int kSlotPrefetch = 1;                 // tiles ahead whose weight lines are pulled into L2
 static_assert(kSlotNJ == 64, "mask_pitch() rounds n to whole workgroups");
 
@@ -381,14 +382,13 @@ __global__ __launch_bounds__(kSlotThreads, 1) void spmm_slots_kernel(
         slab[buf][srow * kRowD2 + sm] = make_double2((double)st.x, (double)st.y);
         slab[buf][srow * kRowD2 + 64 + sm] = make_double2((double)st.z, (double)st.w);
     };
-    // weights of rows 2h, 2h + 1 of tile t for the wave's 4 neurons (scalar loads: the address is wave-uniform)
+    // weights of rows 2h, 2h + 1 of tile t for the wave's 4 neurons: one 64-byte line, one scalar load
     auto load_w = [&](int t, int h, double (&w)[kSlotNPW][kSlotPR]) {
-        const int r0 = kSlotPR * h;
-        const double *wp = slots + (((int64_t)t * 4 + r0 / 4) * pitch + jw) * 4 + (r0 % 4);
+        const double *wp = slots + (((int64_t)t * kSlotPhases + h) * pitch + jw) * kSlotPR;
 #pragma unroll
         for (int q = 0; q < kSlotNPW; ++q)
 #pragma unroll
-            for (int r = 0; r < kSlotPR; ++r) w[q][r] = wp[q * 4 + r];
+            for (int r = 0; r < kSlotPR; ++r) w[q][r] = wp[q * kSlotPR + r];
     };
     auto load_y = [&](int buf, int h, double2 (&y)[kSlotPR][2]) {
         const double2 *sl = slab[buf] + lane;
@@ -408,82 +408,85 @@ __global__ __launch_bounds__(kSlotThreads, 1) void spmm_slots_kernel(
         for (int r = 0; r < kSlotPR; ++r)
             asm volatile("" ::"v"(y[r][0].x), "v"(y[r][0].y), "v"(y[r][1].x), "v"(y[r][1].y));
     };
-    auto load_mask = [&](int t) -> uint64_t {
-        return *reinterpret_cast<const uint64_t *>(tile_mask + (int64_t)t * pitch + jw);
-    };
 
-    double wc[kSlotNPW][kSlotPR], wn[kSlotNPW][kSlotPR];
-    double2 yc[kSlotPR][2], yn[kSlotPR][2];
-    uint64_t mk = load_mask(0), mkn = 0;
-    load_slab(0);
-    stage(0);
-    load_w(0, 0, wc);
-    __syncthreads();
-    load_y(0, 0, yc);
-    for (int t = 0; t < ntiles; ++t) {
-        const bool more = t + 1 < ntiles;
-        const int buf = t & 1;
-        if (more) {
-            load_slab(t + 1);
-            mkn = load_mask(t + 1);
+    // two register sets, used alternately by even and odd phases, so no copies between phases
+    double wa[kSlotNPW][kSlotPR], wb[kSlotNPW][kSlotPR];
+    double2 ya[kSlotPR][2], yb[kSlotPR][2];
+    uint32_t mk[kSlotNPW], mkn[kSlotNPW];  // each neuron's 16 mask bits of the current / next tile
+    auto load_mask = [&](int t, uint32_t (&m)[kSlotNPW]) {
+        const uint64_t v = *reinterpret_cast<const uint64_t *>(tile_mask + (int64_t)t * pitch + jw);
+#pragma unroll
+        for (int q = 0; q < kSlotNPW; ++q) m[q] = (uint32_t)(v >> (16 * q)) & 0xffffu;
+    };
+    // phase h of tile t: wait for (wc, yc), issue the loads of the next phase into (wn, yn), then the FMAs
+    // (tn: the next tile, or the last tile again at the end, so that every load is unconditional and the
+    // weights never pass through a branch merge, which would move them to vector registers)
+    auto phase = [&](int t, int h, int tn, int buf, double (&wc)[kSlotNPW][kSlotPR], double2 (&yc)[kSlotPR][2],
+                     double (&wn)[kSlotNPW][kSlotPR], double2 (&yn)[kSlotPR][2]) {
+        ready(wc, yc);
+        __builtin_amdgcn_sched_barrier(0);
+        if (h + 1 < kSlotPhases) {
+            load_w(t, h + 1, wn);
+            load_y(buf, h + 1, yn);
+        } else {
+            load_w(tn, 0, wn);  // the next tile's rows are read after the barrier
         }
-        // Pull the weight lines of tile t + kSlotPrefetch into L2 with a vector load (lanes 0..7: the wave's 8 lines
-        // of 64 bytes, lane 8: its masks): a scalar load that misses L2 stalls the whole phase, a vector load is
-        // waited for only here, at the staging below.
-        uint32_t pf = 0;
-        if (t + kSlotPrefetch < ntiles && lane < 9) {
-            pf = lane < 8 ? *reinterpret_cast<const uint32_t *>(
-                                slots + (((int64_t)(t + kSlotPrefetch) * 4 + lane / 2) * pitch + jw) * 4 + (lane % 2) * 8)
-                          : *reinterpret_cast<const uint32_t *>(tile_mask + (int64_t)(t + kSlotPrefetch) * pitch + jw);
-        }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int h = 0; h < kTileRows / kSlotPR; ++h) {
-            ready(wc, yc);
-            __builtin_amdgcn_sched_barrier(0);
-            if (h + 1 < kTileRows / kSlotPR) {
-                load_w(t, h + 1, wn);
-                load_y(buf, h + 1, yn);
-            } else if (more) {
-                load_w(t + 1, 0, wn);
-            }
-            __builtin_amdgcn_sched_barrier(0);
+        for (int r = 0; r < kSlotPR; ++r) {
 #pragma unroll
-            for (int r = 0; r < kSlotPR; ++r) {
-#pragma unroll
-                for (int q = 0; q < kSlotNPW; ++q) {
-                    if (__builtin_expect((uint32_t)(mk >> (16 * q + kSlotPR * h + r)) & 1u, 1u)) {
-                        const double w = wc[q][r];
-                        acc[q][0] = __builtin_fma(yc[r][0].x, w, acc[q][0]);
-                        acc[q][1] = __builtin_fma(yc[r][0].y, w, acc[q][1]);
-                        acc[q][2] = __builtin_fma(yc[r][1].x, w, acc[q][2]);
-                        acc[q][3] = __builtin_fma(yc[r][1].y, w, acc[q][3]);
-                        if constexpr (kPattern) {
-                            hit[q][0] |= (uint32_t)__double2hiint(yc[r][0].x);
-                            hit[q][1] |= (uint32_t)__double2hiint(yc[r][0].y);
-                            hit[q][2] |= (uint32_t)__double2hiint(yc[r][1].x);
-                            hit[q][3] |= (uint32_t)__double2hiint(yc[r][1].y);
-                        }
+            for (int q = 0; q < kSlotNPW; ++q) {
+                if (__builtin_expect((mk[q] >> (kSlotPR * h + r)) & 1u, 1u)) {
+                    const double w = wc[q][r];
+                    acc[q][0] = __builtin_fma(yc[r][0].x, w, acc[q][0]);
+                    acc[q][1] = __builtin_fma(yc[r][0].y, w, acc[q][1]);
+                    acc[q][2] = __builtin_fma(yc[r][1].x, w, acc[q][2]);
+                    acc[q][3] = __builtin_fma(yc[r][1].y, w, acc[q][3]);
+                    if constexpr (kPattern) {
+                        hit[q][0] |= (uint32_t)__double2hiint(yc[r][0].x);
+                        hit[q][1] |= (uint32_t)__double2hiint(yc[r][0].y);
+                        hit[q][2] |= (uint32_t)__double2hiint(yc[r][1].x);
+                        hit[q][3] |= (uint32_t)__double2hiint(yc[r][1].y);
                     }
                 }
             }
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int q = 0; q < kSlotNPW; ++q)
-#pragma unroll
-                for (int r = 0; r < kSlotPR; ++r) wc[q][r] = wn[q][r];
-            if (h + 1 < kTileRows / kSlotPR) {
-#pragma unroll
-                for (int r = 0; r < kSlotPR; ++r) {
-                    yc[r][0] = yn[r][0];
-                    yc[r][1] = yn[r][1];
-                }
-            }
         }
-        if (more) stage((t + 1) & 1);  // that buffer was last read in tile t - 1, before the previous barrier
-        asm volatile("" ::"v"(pf));     // keeps the prefetch load (its value is not needed)
-        mk = mkn;
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    static_assert(kSlotPhases % 2 == 0, "a tile ends on an odd phase, so the next starts on set a");
+
+    load_mask(0, mk);
+    load_slab(0);
+    stage(0);
+    load_w(0, 0, wa);
+    __syncthreads();
+    load_y(0, 0, ya);
+    for (int t = 0; t < ntiles; ++t) {
+        const int tn = t + 1 < ntiles ? t + 1 : t;
+        const int buf = t & 1;
+        load_slab(tn);
+        load_mask(tn, mkn);
+        // Pull the weight lines of tile t + kSlotPrefetch into L2 with a vector load (lane h < 8: the wave's line of
+        // phase h, lane 8: its masks): a scalar load that misses L2 stalls the whole phase, a vector load is waited
+        // for only here, at the staging below.
+        uint32_t pf = 0;
+        if (t + kSlotPrefetch < ntiles && lane < kSlotPhases + 1) {
+            pf = lane < kSlotPhases
+                     ? *reinterpret_cast<const uint32_t *>(
+                           slots + (((int64_t)(t + kSlotPrefetch) * kSlotPhases + lane) * pitch + jw) * kSlotPR)
+                     : *reinterpret_cast<const uint32_t *>(tile_mask + (int64_t)(t + kSlotPrefetch) * pitch + jw);
+        }
+#pragma unroll
+        for (int h = 0; h < kSlotPhases; h += 2) {
+            phase(t, h, tn, buf, wa, ya, wb, yb);
+            phase(t, h + 1, tn, buf, wb, yb, wa, ya);
+        }
+        stage((t + 1) & 1);          // that buffer was last read in tile t - 1, before the previous barrier
+        asm volatile("" ::"v"(pf));  // keeps the prefetch load (its value is not needed)
+#pragma unroll
+        for (int q = 0; q < kSlotNPW; ++q) mk[q] = mkn[q];
         __syncthreads();
-        if (more) load_y((t + 1) & 1, 0, yc);
+        load_y((t + 1) & 1, 0, ya);  // after the last tile: read and not used
     }
     const int64_t ca = col0 + 4 * lane;  // batch is a multiple of 4, so ca < batch => ca + 3 < batch
 #pragma unroll
@@ -499,7 +502,7 @@ __global__ __launch_bounds__(kSlotThreads, 1) void spmm_slots_kernel(
     }
 }
 
-// slots[((t * 4 + u) * pitch + j) * 4 + r] = W(16t + 4u + r, j): one wave per fan-in list, lanes over its entries.
+// slots[((t * 8 + h) * pitch + j) * 2 + r] = W(16t + 2h + r, j): one wave per fan-in list, lanes over its entries.
 __global__ void slots_kernel(int64_t n, const int64_t *__restrict__ fan_ptr, const Edge *__restrict__ fan,
                              double *__restrict__ slots) {
     const int64_t j = (int64_t)blockIdx.x * (blockDim.x / 64) + threadIdx.x / 64;
@@ -507,7 +510,7 @@ __global__ void slots_kernel(int64_t n, const int64_t *__restrict__ fan_ptr, con
     const int64_t pitch = mask_pitch(n);
     for (int64_t e = fan_ptr[j] + (threadIdx.x & 63); e < fan_ptr[j + 1]; e += 64) {
         const int64_t i = fan[e].idx;
-        slots[((i / 4) * pitch + j) * 4 + (i % 4)] = (double)fan[e].w;
+        slots[((i / kSlotPR) * pitch + j) * kSlotPR + (i % kSlotPR)] = (double)fan[e].w;
     }
 }
 
