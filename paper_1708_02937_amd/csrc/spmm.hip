@@ -84,6 +84,12 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
         const int64_t local = b / 8;
         c = (b % 8) + 8 * (local / groups);
         g = local % groups;
+    } else if (8 % chunks == 0) {
+        // 1, 2 or 4 chunks: XCD x keeps to chunk x % chunks and takes every (8 / chunks)-th neuron group of
+        // it, so its L2 holds one chunk's slice of Y^T rather than all of Y^T
+        const int64_t xcd = b % 8;
+        c = xcd % chunks;
+        g = (b / 8) * (8 / chunks) + xcd / chunks;
     } else {
         c = b % chunks;
         g = b / chunks;
@@ -631,7 +637,9 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, c
     else if (batch % 2 == 0 && batch >= 128) V = 2;
     const int64_t chunks = (batch + 64 * V - 1) / (64 * V);
     const int64_t groups = (n + 3) / 4;
-    const int64_t blocks = groups * chunks;
+    // with 1, 2 or 4 chunks each row of 8 consecutive workgroups covers 8 / chunks groups of every chunk
+    const int64_t blocks = (chunks < 8 && 8 % chunks == 0) ? (groups + 8 / chunks - 1) / (8 / chunks) * 8
+                                                            : groups * chunks;
     if (chunks > 0x7fffffffLL) return hipErrorInvalidValue;
     // a launch holds at most 2^32 - 1 work-items: segments of 2^23 workgroups (a multiple of 8, so the
     // XCD of a workgroup, its linear index mod 8, is unchanged)
