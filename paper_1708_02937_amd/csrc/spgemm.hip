@@ -231,6 +231,16 @@ __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
 }
 
 constexpr int kRounds = kTile / (4 * kThreads);  // dense-epilogue rounds of 4 columns per thread
+constexpr int kRoundCols = 4 * kThreads;          // columns per dense-epilogue round
+static_assert(kTile % kRoundCols == 0, "whole rounds per window");
+
+// LDS position of accumulator column `col` of a window: within each round of 4096 columns, column 4t + v sits
+// at v * 1024 + t, so when thread t reads its 4 consecutive columns in the dense epilogue the 64 lanes of a
+// wave touch 64 consecutive doubles (column-major per thread would put the lanes 32 bytes apart: an 8-way
+// bank conflict on every read and write).  The scatter uses the same map.
+__device__ __forceinline__ int acc_pos(int col) {
+    return (col & ~(kRoundCols - 1)) | ((col & 3) * kThreads) | ((col & (kRoundCols - 1)) >> 2);
+}
 constexpr int kRes = 1;                           // stored entries a thread keeps in registers (resident mode)
 constexpr int kResLoads = 4;                      // weight loads in flight per resident entry
 
@@ -254,7 +264,8 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, hl = lane & 31;
-    const int width0 = (int)(n < kTile ? n : kTile);
+    // the accumulator covers whole rounds (the positions of a partial round's columns spread over the round)
+    const int width0 = (int)(n < kTile ? (n + kRoundCols - 1) / kRoundCols * kRoundCols : kTile);
     for (int t = tid; t < width0; t += kThreads) acc[t] = 0.0;
     for (int t = tid; t < kBitWords; t += kThreads) bits[t] = 0u;
     if (tid == 0) any = 0;
@@ -328,7 +339,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                             for (int u = 0; u < kResLoads; ++u)
                                 if (e + u < hi) {
                                     const int col = ed[u].idx - (int)c0;
-                                    atomicAdd(&acc[col], my_y[k] * (double)ed[u].w);
+                                    atomicAdd(&acc[acc_pos(col)], my_y[k] * (double)ed[u].w);
                                     if (sparse && my_y[k] != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
                                     mine_any = true;
                                 }
@@ -381,7 +392,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                                 for (int u = 0; u < 8; ++u) {
                                     if (ed[u].idx >= c0 && ed[u].idx < c1) {
                                         const int col = ed[u].idx - (int)c0;
-                                        atomicAdd(&acc[col], ref.y * (double)ed[u].w);
+                                        atomicAdd(&acc[acc_pos(col)], ref.y * (double)ed[u].w);
                                         if (sparse && ref.y != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
                                         mine_any = true;
                                     }
@@ -415,7 +426,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                                 for (int p = 0; p < 4; ++p) {
                                     if (ed[p].idx >= c0 && ed[p].idx < c1) {
                                         const int col = ed[p].idx - (int)c0;
-                                        atomicAdd(&acc[col], rr[p].y * (double)ed[p].w);
+                                        atomicAdd(&acc[acc_pos(col)], rr[p].y * (double)ed[p].w);
                                         if (sparse && rr[p].y != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
                                         mine_any = true;
                                     }
@@ -435,7 +446,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                         int keep = 0;
                         for (uint32_t m = word; m; m &= m - 1) {
                             const int col = tid * 32 + __builtin_ctz(m);
-                            keep += activate(acc[col] + (double)bias[c0 + col], ymax) != 0.0f;
+                            keep += activate(acc[acc_pos(col)] + (double)bias[c0 + col], ymax) != 0.0f;
                         }
                         int incl = keep;
 #pragma unroll
@@ -455,8 +466,8 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                         int64_t pos = ob + written + off + incl - keep;
                         for (uint32_t m = word; m; m &= m - 1) {
                             const int col = tid * 32 + __builtin_ctz(m);
-                            const float f = activate(acc[col] + (double)bias[c0 + col], ymax);
-                            acc[col] = 0.0;
+                            const float f = activate(acc[acc_pos(col)] + (double)bias[c0 + col], ymax);
+                            acc[acc_pos(col)] = 0.0;
                             if (f != 0.0f) {
                                 out_col[pos] = (int32_t)(c0 + col);
                                 out_val[pos] = f;
@@ -478,10 +489,11 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
 #pragma unroll
                         for (int v = 0; v < 4; ++v) {
                             const int t = rd * 4 * kThreads + 4 * tid + v;
+                            const int at = rd * kRoundCols + v * kThreads + tid;  // acc_pos(t)
                             f[rd][v] = 0.0f;
                             if (t < width) {
-                                f[rd][v] = activate(acc[t] + (double)bias[c0 + t], ymax);
-                                acc[t] = 0.0;
+                                f[rd][v] = activate(acc[at] + (double)bias[c0 + t], ymax);
+                                acc[at] = 0.0;
                             }
                             keep += f[rd][v] != 0.0f;
                         }
@@ -636,7 +648,9 @@ __global__ __launch_bounds__(kSlotThreads) void dense_to_slots_kernel(int64_t n,
 
 }  // namespace
 
-size_t spgemm_lds_bytes(int64_t n) { return (size_t)(n < kTile ? n : kTile) * sizeof(double); }
+size_t spgemm_lds_bytes(int64_t n) {
+    return (size_t)(n < kTile ? (n + kRoundCols - 1) / kRoundCols * kRoundCols : kTile) * sizeof(double);
+}
 
 int spgemm_windows(int64_t n) { return (int)((n + kTile - 1) / kTile); }
 
