@@ -207,6 +207,32 @@ class Net:
         sdnn_forward_dense(self.handle, k0, k1, batch, y, out, ws, ws.numel(), arm)
         return out
 
+    def capture_forward_dense(self, y, out, k0: int = 0, k1: int | None = None, arm: int = SDNN_ARM_SPARSE):
+        """Record forward_dense(y -> out) as a HIP graph (a torch.cuda.CUDAGraph); g.replay() launches the same
+        kernels from the graph instead of one call at a time, on the current stream.  y and out (device,
+        float32, contiguous, batch x n) and the workspace stay bound to the graph: write new inputs into y
+        before a replay and read out after it."""
+        t = self.torch
+        k1 = self.L if k1 is None else k1
+        if not (isinstance(y, t.Tensor) and isinstance(out, t.Tensor) and y.is_contiguous() and out.is_contiguous()
+                and y.dtype == t.float32 and out.dtype == t.float32 and y.device == self.device
+                and out.shape == y.shape and y.dim() == 2 and y.shape[1] == self.n):
+            raise ValueError("y and out must be contiguous float32 batch x n tensors on the net's device")
+        batch = y.shape[0]
+        ws = self.workspace(batch, 0)
+        self.forward_dense(y, k0, k1, arm, out)  # any one-time device set-up happens outside the capture
+        t.cuda.synchronize(self.device)
+        prev = t.cuda.current_stream(self.device).cuda_stream
+        g = t.cuda.CUDAGraph()
+        try:
+            with t.cuda.graph(g, stream=t.cuda.Stream(device=self.device)):
+                sdnn_net_set_stream(self.handle, t.cuda.current_stream(self.device).cuda_stream)
+                sdnn_forward_dense(self.handle, k0, k1, batch, y, out, ws, ws.numel(), arm)
+        finally:
+            sdnn_net_set_stream(self.handle, prev)
+        g.sdnn_buffers = (y, out, ws)  # the graph reads and writes these addresses
+        return g
+
     def mxm(self, k: int, semiring: int, y, out=None):
         """Z = Y (+).(x) W_k over a semiring (dense batch x n in and out)."""
         t = self.torch

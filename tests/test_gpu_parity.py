@@ -367,6 +367,33 @@ def test_identity_input_reads_back_weights(sd):
     assert got.tobytes() == want.tobytes()
 
 
+def test_graph_replay_matches_eager(sd):
+    """A HIP graph of forward_dense replays the eager result bit for bit, replay after replay, with new inputs
+    written into the bound input and unrelated eager work between the replays (both arms)."""
+    import torch
+
+    p = make_config(1, n=1000, L=3, batch=132)
+    for arm in ARMS:
+        net = sd.net_from_problem(p, dense=(arm == "dense"))
+        rng = np.random.default_rng(5)
+        inputs = [p.y0_dense] + [rng.random((p.batch, p.n), dtype=np.float32) for _ in range(3)]
+        want = [net.forward_dense(torch.from_numpy(x).cuda(), arm=_arm(sd, arm)).cpu().numpy() for x in inputs]
+        y = torch.from_numpy(inputs[0]).cuda()
+        o = torch.empty_like(y)
+        g = net.capture_forward_dense(y, o, arm=_arm(sd, arm))
+        for rep, which in enumerate([0, 1, 2, 3, 3, 2, 1, 0]):
+            _say("graph replay", arm, rep)
+            y.copy_(torch.from_numpy(inputs[which]))
+            g.replay()
+            torch.cuda.synchronize()
+            assert o.cpu().numpy().tobytes() == want[which].tobytes()
+            # unrelated eager work on the same net and stream between replays
+            net.forward_dense(torch.from_numpy(inputs[(rep + 1) % 4]).cuda(), arm=_arm(sd, arm))
+            torch.cuda.synchronize()
+        parity.compare(p, dense_to_csr(want[0]))
+        net.free()
+
+
 def test_run_twice_identical(sd):
     p = make_config(3, n=4096, L=4, batch=128)
     a, b = run_csr(sd, p), run_csr(sd, p)
