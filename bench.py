@@ -68,6 +68,23 @@ def _events(torch):
     return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
 
+def time_steps(torch, fn, steps: int):
+    """Time exactly `steps` calls of fn() back to back on the current stream, with one HIP event between
+    consecutive calls; returns (mean, median, min) milliseconds per call.  The mean is the span from the
+    first event to the last over `steps`."""
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(steps):
+        fn()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
+    mid = steps // 2
+    median = per[mid] if steps % 2 else 0.5 * (per[mid - 1] + per[mid])
+    return ev[0].elapsed_time(ev[-1]) / steps, median, per[0]
+
+
 def time_calls(torch, fn, reps: int) -> float:
     """Average milliseconds per call of fn(), timed with HIP events on the current stream."""
     a, b = _events(torch)
@@ -122,16 +139,9 @@ def run_sweep(args, torch, sd):
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    a, b = _events(torch)
     t_wall = time.perf_counter()
-    a.record()
-    for _ in range(args.steps):
-        step()
-    b.record()
-    torch.cuda.synchronize()
+    ms_step, ms_med, ms_min = time_steps(torch, step, args.steps)
     t_wall = time.perf_counter() - t_wall
-    ms_step = a.elapsed_time(b) / args.steps
     edges = sum(p.edges() for p in probs)
     value = edges / (ms_step / 1e3)
     log(f"step {ms_step:.3f} ms (wall {1e3 * t_wall / args.steps:.3f} ms), {value:.4g} edges/s")
@@ -217,33 +227,55 @@ def run_sweep(args, torch, sd):
     cfg = {"workload": "density-sweep n=4096 L=16 batch=1024 d=" + "/".join(f"{d:g}" for d in densities)
                        + " (CSR sparse-W path; fp32 storage, fp64 accumulate)",
            "n": 4096, "L": 16, "batch": 1024, "densities": densities}
-    return dict(value=value, ms_step=ms_step, edges=edges, sweep=sweep, crossover=crossover, roofline=roof,
-                config=cfg, probs=probs, densities=densities)
+    return dict(value=value, ms_step=ms_step, ms_median=ms_med, ms_min=ms_min, edges=edges, sweep=sweep,
+                crossover=crossover, roofline=roof, config=cfg, probs=probs, densities=densities)
 
 
-def cpu_baseline(args, probs, densities):
-    """Oracle on the host cores: the first R samples of every density, all L layers."""
+# oracle sample per workload (rows of the batch): all-core rate, and single-thread rate where the density-sweep
+# and tiny-MLP workloads set one beside the paper's single-thread measurements
+CPU_ROWS = {1: 64, 2: 1024, 3: 256, 4: 1024, 5: 16}
+CPU_ROWS_SINGLE = {1: 64, 2: 8}
+
+
+def _oracle_rate(probs, rows, threads, min_seconds):
+    """Whole passes of the oracle over the first `rows` samples of every problem, all layers, until at least
+    min_seconds of CPU work; returns (edges/s, seconds, passes)."""
     import oracle
     from workloads import csr_rows
 
-    rows = min(args.cpu_rows, probs[0].batch)
-    threads = oracle.default_threads()
     ys = [csr_rows(p.y0_as_csr(), np.arange(rows)) for p in probs]
     edges = 0
     t_total = 0.0
     passes = 0
-    # whole passes over the sample until at least 10 s of CPU work have been timed
-    while passes == 0 or t_total < 10.0:
+    while passes == 0 or t_total < min_seconds:
         for y, p in zip(ys, probs):
             t0 = time.perf_counter()
             oracle.forward(p.n, p.layers, p.ymax, y, threads=threads)
             t_total += time.perf_counter() - t0
             edges += rows * sum(l.nnz for l in p.layers)
         passes += 1
-    return {"value": edges / t_total, "unit": "edges/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {rows} of {probs[0].batch} samples at each density, all {probs[0].L} layers, "
-                      f"{passes} passes ({t_total:.1f} s of CPU work)", "seconds": round(t_total, 2),
-            "cpu": _cpu_model()}
+    return edges / t_total, t_total, passes
+
+
+def cpu_baseline(args, probs, config):
+    """Oracle on the host cores: the first R samples of the workload (of every density for the sweep), all
+    L layers; whole passes repeated until at least 10 s of CPU work."""
+    import oracle
+
+    rows = min(args.cpu_rows or CPU_ROWS[config], probs[0].batch)
+    threads = oracle.default_threads()
+    where = " at each density" if len(probs) > 1 else ""
+    rate, secs, passes = _oracle_rate(probs, rows, threads, 10.0)
+    rec = {"value": rate, "unit": "edges/s", "cores": threads, "kind": "oracle",
+           "sample": f"first {rows} of {probs[0].batch} samples{where}, all {probs[0].L} layers, "
+                     f"{passes} passes ({secs:.1f} s of CPU work)", "seconds": round(secs, 2), "cpu": _cpu_model()}
+    if config in CPU_ROWS_SINGLE:
+        r1 = min(CPU_ROWS_SINGLE[config], probs[0].batch)
+        rate1, secs1, passes1 = _oracle_rate(probs, r1, 1, 3.0)
+        rec["single_thread"] = {"value": rate1, "unit": "edges/s", "cores": 1,
+                                "sample": f"first {r1} samples{where}, all {probs[0].L} layers, {passes1} passes",
+                                "seconds": round(secs1, 2)}
+    return rec
 
 
 def _cpu_model():
@@ -368,6 +400,20 @@ def run_semiring(args, torch, sd):
 
 
 
+def layer_trace(torch, net, p, y):
+    """nnz of Y_0 .. Y_L and the products of each layer (sum over the stored entries (r, i) of Y_k of the
+    fan-out of neuron i in W_k), from the same forward run one layer at a time (not timed)."""
+    rp, c, v = y
+    nnz = [int(c.numel())]
+    products = []
+    for k, l in enumerate(p.layers):
+        fanout = torch.from_numpy(np.diff(l.row_ptr)).cuda()
+        products.append(int(fanout[c.long()].sum().item()) if c.numel() else 0)
+        rp, c, v = (t.clone() for t in net.forward_csr(rp, c, v, k0=k, k1=k + 1))
+        nnz.append(int(c.numel()))
+    return nnz, products
+
+
 def run_csr_config(args, torch, sd):
     """Configs 3-5 (sparse Y through the SpGEMM path) and config 1, one forward per step."""
     from workloads import make_config
@@ -383,20 +429,27 @@ def run_csr_config(args, torch, sd):
         fn = lambda: net.forward_dense(y, out=o)
     for _ in range(args.warmup):
         fn()
-    ms = time_calls(torch, fn, args.steps)
+    ms, ms_med, ms_min = time_steps(torch, fn, args.steps)
     extra = {}
     if p.y0_csr is None:
         # a dense batch: the same forward replayed from a HIP graph (launch-bound at small sizes)
         g = net.capture_forward_dense(y, o)
         for _ in range(args.warmup):
             g.replay()
-        ms_graph = time_calls(torch, g.replay, args.steps)
-        extra = {"eager_ms_per_step": round(ms, 4), "graph_ms_per_step": round(ms_graph, 4)}
-        log(f"eager {ms:.4f} ms, graph replay {ms_graph:.4f} ms per forward")
-        ms = min(ms, ms_graph)
+        timed = time_steps(torch, g.replay, args.steps)
+        extra = {"eager_ms_per_step": round(ms, 4), "graph_ms_per_step": round(timed[0], 4)}
+        log(f"eager {ms:.4f} ms, graph replay {timed[0]:.4f} ms per forward")
+        if timed[0] < ms:
+            ms, ms_med, ms_min = timed
+    elif args.config in (3, 4):
+        nnz, products = layer_trace(torch, net, p, y)
+        extra = {"nnz_trace": nnz, "products_per_layer": products,
+                 "products_per_s": sum(products) / (ms / 1e3)}
+        log(f"nnz trace {nnz[:4]} ..., {sum(products):.4g} products per forward")
     net.free()
     cfg = {"workload": f"{p.name} n={p.n} L={p.L} batch={p.batch}", "n": p.n, "L": p.L, "batch": p.batch, **extra}
-    return dict(value=p.edges() / (ms / 1e3), ms_step=ms, config=cfg, roofline=None, sweep=None, crossover=None)
+    return dict(value=p.edges() / (ms / 1e3), ms_step=ms, ms_median=ms_med, ms_min=ms_min, config=cfg,
+                roofline=None, sweep=None, crossover=None, probs=[p])
 
 
 # ----------------------------------------------------------------------------- profile summaries (no GPU)
@@ -466,7 +519,7 @@ def main():
     ap.add_argument("--densities", default="0.5,0.1,0.01,0.001")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-W arm")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0: per-workload default)")
     ap.add_argument("--paper-grid", action="store_true",
                     help="time the paper's own grid (m x m weights, inverse sparsity 1..262144, batch 64)")
     ap.add_argument("--grid-sizes", default="", help="comma-separated m values for --paper-grid")
@@ -536,13 +589,14 @@ def main():
         "metric": METRIC, "value": r["value"], "unit": "edges/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(r["ms_step"], 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic", "config": r["config"],
-        "roofline": r["roofline"],
+        "roofline": r["roofline"], "ms_per_step_median": round(r["ms_median"], 4),
+        "ms_per_step_min": round(r["ms_min"], 4),
     }
     if r.get("sweep"):
         out["sweep"] = r["sweep"]
         out["crossover_density"] = r["crossover"]
-    if args.config == 2 and not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args, r["probs"], r["densities"])
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args, r["probs"], args.config)
     print(json.dumps(out), flush=True)
 
 

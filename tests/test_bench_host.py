@@ -1,0 +1,114 @@
+"""Host logic of bench.py (no GPU): the one-GPU guard, crossover interpolation, per-step statistics and the
+rocprofv3 counter summary."""
+import math
+import os
+import subprocess
+import sys
+
+import pytest
+
+REPO = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, REPO)
+
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(REPO, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def test_crossover_log_log_interpolation():
+    # t_sparse / t_dense = (x / 8)^-1: sparse slower below x = 8, faster above, equal at x = 8 exactly
+    pts = [(x, 1.0 / (x / 8.0), 1.0) for x in (1, 4, 16, 64)]
+    assert bench._crossover(pts) == pytest.approx(8.0, rel=1e-12)
+    # sparse always faster: no crossover
+    assert bench._crossover([(x, 0.5, 1.0) for x in (1, 4, 16)]) is None
+
+
+def test_spmm_algorithmic_counts():
+    byt, flops = bench.spmm_algorithmic(4096, 1024, 8 * 10 ** 6)
+    assert byt == 8 * 4096 * 1024 + 8 * 8 * 10 ** 6 + 8 * 4097 + 4 * 4096
+    assert flops == 2.0 * 1024 * 8 * 10 ** 6
+
+
+class _FakeEvent:
+    """Stand-in for torch.cuda.Event on a clock that advances by a scripted duration per call."""
+
+    clock = [0.0]
+
+    def __init__(self, enable_timing=True):
+        self.t = None
+
+    def record(self):
+        self.t = self.clock[0]
+
+    def elapsed_time(self, other):
+        return other.t - self.t
+
+
+class _FakeTorch:
+    class cuda:
+        Event = _FakeEvent
+
+        @staticmethod
+        def synchronize():
+            pass
+
+
+@pytest.mark.parametrize("durations", [[3.0, 1.0, 2.0, 10.0, 4.0], [5.0, 1.0, 2.0, 8.0]])
+def test_time_steps_mean_median_min(durations):
+    _FakeEvent.clock = [0.0]
+    it = iter(durations)
+
+    def step():
+        _FakeEvent.clock[0] += next(it)
+
+    mean, median, lo = bench.time_steps(_FakeTorch, step, len(durations))
+    s = sorted(durations)
+    m = len(s) // 2
+    want_median = s[m] if len(s) % 2 else 0.5 * (s[m - 1] + s[m])
+    assert mean == pytest.approx(sum(durations) / len(durations))
+    assert median == pytest.approx(want_median)
+    assert lo == min(durations)
+
+
+def _write_pmc(path, counter, kernel, values):
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "p_counter_collection.csv"), "w") as f:
+        f.write("Kernel_Name,Counter_Name,Counter_Value\n")
+        for v in values:
+            f.write(f'"{kernel}",{counter},{v}\n')
+        f.write(f'"other_kernel",{counter},999999\n')
+
+
+def test_summarize_pmc_scales_by_the_copy_probe(tmp_path):
+    copy_bytes = 1 << 20
+    k = "void sdnn::(anonymous namespace)::spmm_slots_kernel<false>(long, long)"
+    cp = "__amd_rocclr_copyBuffer"
+    _write_pmc(tmp_path / "f", "FETCH_SIZE", k, [100.0, 300.0])
+    _write_pmc(tmp_path / "w", "WRITE_SIZE", k, [50.0])
+    _write_pmc(tmp_path / "cf", "FETCH_SIZE", cp, [512.0])  # half of the 1024 KiB copied
+    _write_pmc(tmp_path / "cw", "WRITE_SIZE", cp, [1024.0])
+    out = tmp_path / "summary.txt"
+    bench.summarize_pmc("spmm_slots_kernel", "test", [str(tmp_path / d) for d in ("f", "w", "cf", "cw")],
+                        copy_bytes, ["cmd one", "cmd two"], str(out), ["spmm.hip", "common.h"])
+    rec = dict(line.split(": ", 1) for line in out.read_text().splitlines() if ": " in line and " " not in
+               line.split(": ", 1)[0])
+    assert float(rec["fetch_scale"]) == pytest.approx(2.0)
+    assert float(rec["write_scale"]) == pytest.approx(1.0)
+    # (avg fetch 200 KiB x 2 + write 50 KiB x 1) x 1024 bytes
+    assert int(rec["hbm_bytes_per_launch"]) == (200 * 2 + 50) * 1024
+    assert rec["source_hash"] == bench._src_hash("spmm.hip", "common.h")
+    assert "    cmd one" in out.read_text()
+
+
+def test_kernel_name_matches_the_selection_rule():
+    assert bench.spmm_kernel_name(4096, 1280 * 4096) == "spmm_slots_kernel"
+    assert bench.spmm_kernel_name(4096, 1280 * 4096 - 1) == "spmm_fanin_kernel"
+    # the slot array (16-row tiles x 64-padded columns, fp64) beyond 2 GiB: tiled kernel
+    n = 16448
+    assert math.ceil(n / 16) * 16 * math.ceil(n / 64) * 64 * 8 > 2 ** 31
+    assert bench.spmm_kernel_name(n, 1280 * n) == "spmm_tiled_kernel"
