@@ -132,7 +132,8 @@ def test_pattern_bias_csr_path(sd, seed, n, L, batch, wd, yd):
 
 
 @pytest.mark.parametrize("seed,n,L,batch,d,yd", [(66, 200, 2, 130, 0.05, 0.3), (67, 1400, 2, 260, 0.95, 0.001),
-                                                 (68, 333, 3, 3, 0.1, 0.5), (69, 4100, 1, 2048, 0.002, 0.01)])
+                                                 (68, 333, 3, 3, 0.1, 0.5), (69, 4100, 1, 2048, 0.002, 0.01),
+                                                 (71, 2000, 2, 516, 0.7, 0.002)])
 def test_pattern_bias_dense_batch(sd, seed, n, L, batch, d, yd):
     """SDNN_BIAS_PATTERN on the sparse arm with dense batches: the gather SpMM (one, two and four columns
     per lane) and the LDS-tiled SpMM (fan-in >= 1280); sparse inputs leave many positions untouched."""
