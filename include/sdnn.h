@@ -24,8 +24,10 @@
  *
  * Conventions for every call:
  *   - Pointers named in comments as "device" must point to memory on the
- *     current HIP device; "host" pointers to host memory.  The library never
- *     frees memory it did not allocate.
+ *     net's device (the HIP device current when the net was created); "host"
+ *     pointers to host memory.  A call that does device work makes the net's
+ *     device current while it runs and restores the caller's device before it
+ *     returns.  The library never frees memory it did not allocate.
  *   - CSR matrices use int64 row_ptr (rows + 1 entries, row_ptr[0] = 0),
  *     int32 column indices strictly increasing within a row, fp32 values.
  *   - Work is enqueued on the net's HIP stream and is asynchronous unless the

@@ -28,6 +28,29 @@ sdnn_status fail_hip(hipError_t e, const char *what) {
     return fail(SDNN_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// Makes the net's device current for one call and gives the caller's device back on return.
+struct DeviceScope {
+    int prev = -1;  // the caller's device when it has to be restored
+    hipError_t err = hipSuccess;
+    explicit DeviceScope(int dev) {
+        int cur = 0;
+        err = hipGetDevice(&cur);
+        if (err == hipSuccess && cur != dev) {
+            err = hipSetDevice(dev);
+            if (err == hipSuccess) prev = cur;
+        }
+    }
+    ~DeviceScope() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+    DeviceScope(const DeviceScope &) = delete;
+    DeviceScope &operator=(const DeviceScope &) = delete;
+};
+
+#define SDNN_ON_DEVICE(net)                                                     \
+    DeviceScope device_scope_((net)->device);                                   \
+    if (device_scope_.err != hipSuccess) return fail_hip(device_scope_.err, "hipSetDevice")
+
 #define SDNN_HIP(call)                                      \
     do {                                                    \
         hipError_t e_ = (call);                             \
@@ -222,6 +245,7 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     if (n > kMaxScan) return fail(SDNN_ERR_UNSUPPORTED, "layers wider than 2^24 neurons are not supported");
+    SDNN_ON_DEVICE(net);
 
     // 1. validate on the device
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, 2 * sizeof(uint32_t), s));
@@ -303,6 +327,7 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
 sdnn_status sdnn_net_build_dense(sdnn_net net) {
     g_last_error.clear();
     if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    SDNN_ON_DEVICE(net);
     const int64_t n = net->n;
     for (int32_t k = 0; k < net->L; ++k) {
         Layer &l = net->layers[(size_t)k];
@@ -345,6 +370,7 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
         return fail(SDNN_ERR_UNSUPPORTED, "the dense arm stores every zero of W_k, so it has no bias pattern");
     if (batch == 0) return SDNN_OK;
     if (!Y_in || !Y_out) return fail(SDNN_ERR_NULL_POINTER, "Y_in and Y_out are required");
+    SDNN_ON_DEVICE(net);
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     if (k0 == k1) {
@@ -392,6 +418,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     if (!y_row_ptr || !out_row_ptr || !out_col || !out_val || !out_nnz)
         return fail(SDNN_ERR_NULL_POINTER, "y_row_ptr and the four outputs are required");
     if (!ws) return fail(SDNN_ERR_NULL_POINTER, "ws is required");
+    SDNN_ON_DEVICE(net);
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     CsrWs w = carve_csr(ws, n, batch);
@@ -527,6 +554,7 @@ sdnn_status sdnn_mxm_dense(sdnn_net net, int32_t k, int32_t semiring, int64_t ba
     sdnn_status st = mxm_common(net, k, semiring, batch, ws, ws_bytes);
     if (st != SDNN_OK || batch == 0) return st;
     if (!Y || !Z) return fail(SDNN_ERR_NULL_POINTER, "Y and Z are required");
+    SDNN_ON_DEVICE(net);
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     const Layer &l = net->layers[(size_t)k];
@@ -544,6 +572,7 @@ sdnn_status sdnn_mxm_csr(sdnn_net net, int32_t k, int32_t semiring, int64_t batc
     sdnn_status st = mxm_common(net, k, semiring, batch, ws, ws_bytes);
     if (st != SDNN_OK || batch == 0) return st;
     if (!y_row_ptr || !Z) return fail(SDNN_ERR_NULL_POINTER, "y_row_ptr and Z are required");
+    SDNN_ON_DEVICE(net);
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     const Layer &l = net->layers[(size_t)k];
@@ -564,6 +593,7 @@ sdnn_status sdnn_mxm_csr(sdnn_net net, int32_t k, int32_t semiring, int64_t batc
 sdnn_status sdnn_net_free(sdnn_net net) {
     g_last_error.clear();
     if (!net) return SDNN_OK;
+    DeviceScope device_scope(net->device);  // frees on the net's device even if it cannot be made current
     (void)hipStreamSynchronize(net->stream);
     for (Layer &l : net->layers) release(l);
     dfree(net->d_flags);

@@ -21,6 +21,8 @@
 // windows that received no product are skipped.  Rows go to fixed slots of the output buffer (row r
 // starts at r * n, its length goes to cnt[r]), so the next layer reads them without a global scan; only
 // the final layer is packed into contiguous CSR.
+#include <atomic>
+
 #include "common.h"
 
 namespace sdnn {
@@ -673,14 +675,20 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     if (batch == 0) return hipSuccess;
     const int only_touched = bias_nonpos || pattern;
     if (batch > 0x7fffffffLL) return hipErrorInvalidValue;
-    static bool attr_set = false;
-    if (!attr_set) {
+    // the accumulator window exceeds the default dynamic LDS limit: raise it once per device (bit d of
+    // attr_devices; devices beyond 63 set it on every call)
+    static std::atomic<unsigned long long> attr_devices{0};
+    int dev = 0;
+    hipError_t ed = hipGetDevice(&dev);
+    if (ed != hipSuccess) return ed;
+    const unsigned long long bit = dev >= 0 && dev < 64 ? 1ull << dev : 0ull;
+    if (!bit || !(attr_devices.load(std::memory_order_acquire) & bit)) {
         for (const void *f : {(const void *)spgemm_row_kernel<true>, (const void *)spgemm_row_kernel<false>}) {
             hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
                                                (int)((size_t)kTile * sizeof(double)));
             if (e != hipSuccess) return e;
         }
-        attr_set = true;
+        attr_devices.fetch_or(bit, std::memory_order_release);
     }
     const int nwin = spgemm_windows(n);
     // the bitmap epilogue pays off while a window gets at most ~2048 products
