@@ -87,6 +87,21 @@ def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
     parity.compare(q, dense_to_csr(run_dense(sd, q, sd.SDNN_ARM_SPARSE)), exact=True)
 
 
+@pytest.mark.parametrize("seed,n,L,batch,d", [(38, 1400, 2, 130, 0.95), (39, 1333, 1, 63, 0.99)])
+def test_high_fanin_gather_fallback(sd, seed, n, L, batch, d):
+    """Average fan-in >= 1280 but a batch the LDS-tiled kernels do not take (not a multiple of 4, or below
+    128): the layer falls back to the gather SpMM with two or one columns per lane over lists far longer
+    than one 64-entry load; integer shadow bit for bit."""
+    p = tiny_random(seed, n, L, batch, w_density=d, y_density=0.7, dense_input=True,
+                    ymax=[math.inf, 3.0][seed % 2], bias_lo=-1.0, bias_hi=1.0)
+    assert p.layers[0].nnz >= 1280 * p.n
+    _say("high fan-in gather fallback", seed, n, L, batch, d)
+    parity.compare(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE)))
+    q = integer_shadow(p)
+    q.y0_dense = np.where(p.y0_dense != 0, q.y0_dense if q.y0_dense is not None else 1, 0).astype(np.float32)
+    parity.compare(q, dense_to_csr(run_dense(sd, q, sd.SDNN_ARM_SPARSE)), exact=True)
+
+
 def test_high_fanin_beyond_slot_limit(sd):
     """n = 16448: the fp64 weight slots of every (input, output) pair would exceed 2 GiB, so the high fan-in
     layer takes the readlane-fed LDS-tiled kernel instead of the scalar-register one; sampled rows, ragged batch."""
