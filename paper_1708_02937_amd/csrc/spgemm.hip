@@ -319,6 +319,10 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
             }
             const int64_t ob = r * n;
             int64_t written = 0;
+            // resident instance: the first kResLoads entries of the next window's segment, loaded before this
+            // window's epilogue so that their latency is covered by it
+            Edge pre[kRes][kResLoads];
+            bool have_pre = false;
             for (int win = 0; win < nwin; ++win) {
                 const int64_t c0 = (int64_t)win * kTile;
                 const int64_t c1 = (c0 + kTile < n) ? c0 + kTile : n;
@@ -332,7 +336,19 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                             s_lo[k] = s_hi[k];
                             s_hi[k] = my_rb[k] + w_seg[(int64_t)my_i[k] * (nwin + 1) + win + 2];
                         }
-                        for (int64_t e = lo; e < hi; e += kResLoads) {
+                        int64_t e = lo;
+                        if (have_pre) {
+#pragma unroll
+                            for (int u = 0; u < kResLoads; ++u)
+                                if (e + u < hi) {
+                                    const int col = pre[k][u].idx - (int)c0;
+                                    atomicAdd(&acc[acc_pos(col)], my_y[k] * (double)pre[k][u].w);
+                                    if (sparse && my_y[k] != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
+                                    mine_any = true;
+                                }
+                            e += kResLoads;
+                        }
+                        for (; e < hi; e += kResLoads) {
                             Edge ed[kResLoads];
 #pragma unroll
                             for (int u = 0; u < kResLoads; ++u)
@@ -345,6 +361,13 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                                     if (sparse && my_y[k] != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
                                     mine_any = true;
                                 }
+                        }
+                        // the next window's segment is [s_lo, s_hi) now: start its loads
+                        have_pre = win + 1 < nwin;
+                        if (have_pre) {
+#pragma unroll
+                            for (int u = 0; u < kResLoads; ++u)
+                                if (s_lo[k] + u < s_hi[k]) pre[k][u] = w[s_lo[k] + u];
                         }
                     }
                 } else {
