@@ -441,7 +441,7 @@ def run_csr_config(args, torch, sd):
         log(f"eager {ms:.4f} ms, graph replay {timed[0]:.4f} ms per forward")
         if timed[0] < ms:
             ms, ms_med, ms_min = timed
-    elif args.config in (3, 4):
+    elif args.config in (3, 4) and not args.no_layer_trace:
         nnz, products = layer_trace(torch, net, p, y)
         extra = {"nnz_trace": nnz, "products_per_layer": products,
                  "products_per_s": sum(products) / (ms / 1e3)}
@@ -519,6 +519,8 @@ def main():
     ap.add_argument("--densities", default="0.5,0.1,0.01,0.001")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-W arm")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-layer-trace", action="store_true",
+                    help="skip the untimed layer-by-layer run that gives the nnz trace (for profiling runs)")
     ap.add_argument("--cpu-rows", type=int, default=0, help="oracle sample rows (0: per-workload default)")
     ap.add_argument("--paper-grid", action="store_true",
                     help="time the paper's own grid (m x m weights, inverse sparsity 1..262144, batch 64)")
