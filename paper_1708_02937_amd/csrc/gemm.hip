@@ -10,8 +10,9 @@
 // (v_mfma_f64_16x16x4_f64), so every product is exact and partial sums carry fp64 rounding only, the
 // same arithmetic as the sparse paths; the epilogue adds b_j in fp64, applies h and rounds once to fp32.
 //
-// Tiling for CDNA4: a 256-thread workgroup computes a 128 x 128 tile of C; each of its four wave64s owns
-// a 64 x 64 quadrant as 4 x 4 blocks of 16 x 16 MFMAs (64 fp64 accumulators per lane).  K advances 16
+// Tiling for CDNA4: a 256-thread workgroup computes a 128 x BN tile of C (BN = 128, or 64 when the batch has
+// at most 64 samples, so a small batch does not pay for a half-empty tile); each of its four wave64s owns a
+// 64 x BN/2 quadrant as 4 x BN/32 blocks of 16 x 16 MFMAs (up to 64 fp64 accumulators per lane).  K advances 16
 // at a time through double-buffered LDS (one barrier per step): the next slab is loaded into registers
 // while the current one is multiplied and stored into the other buffer afterwards.  Rows of the LDS
 // slabs are padded by 16 doubles so the four k-rows an MFMA operand reads land on different banks.
@@ -27,12 +28,15 @@ namespace {
 
 typedef double doublex4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = 128, BN = 128, BK = 16;
+constexpr int BM = 128, BK = 16;
 constexpr int kPad = 16;
+
+// batch columns per workgroup tile
+int tile_bn(int64_t batch) { return batch <= 64 ? 64 : 128; }
 
 // kFast: every tile is interior and aligned (M % 128 == 0, N % 128 == 0, K % 16 == 0, 16-byte rows), so
 // loads need no guards and no branch depends on the thread; otherwise every element is guarded.
-template <bool kFast>
+template <bool kFast, int BN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_dense_layer_kernel(int64_t M, int64_t N, int64_t K,
                                                                int64_t kc, const double *__restrict__ Wk,
                                                                const float *__restrict__ B,
@@ -40,6 +44,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
                                                                float *__restrict__ C, double *__restrict__ partial) {
     __shared__ __align__(16) double As[2][BK][BM + kPad];
     __shared__ __align__(16) double Bs[2][BK][BN + kPad];
+    static_assert(BN == 64 || BN == 128, "tile widths");
+    constexpr int kNB = BN / 32;  // 16-column MFMA blocks per wave, and 32-column staging groups of B
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -51,11 +57,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int64_t kb = (int64_t)blockIdx.z * kc;             // this split's K range [kb, ke)
     const int64_t ke = kb + kc < K ? kb + kc : K;
 
-    // global -> register staging: thread -> k row tid / 16, column pairs (tid % 16) * 2 + 32 q, q = 0..3,
-    // so the 16 threads of a k row store one contiguous 256-byte run per q (no LDS bank conflicts)
+    // global -> register staging: thread -> k row tid / 16, column pairs (tid % 16) * 2 + 32 q (q = 0..3 for
+    // A, q < BN / 32 for B), so the 16 threads of a k row store one contiguous 256-byte run per q (no LDS bank
+    // conflicts)
     const int s_k = tid >> 4, s_c = (tid & 15) * 2;
     double ra[8];
-    float rb[8];
+    float rb[2 * kNB];
     auto load_tiles = [&](int64_t k0) {
         const int64_t gk = k0 + s_k;
         if constexpr (kFast) {
@@ -64,6 +71,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
                 const double2 v = *reinterpret_cast<const double2 *>(Wk + gk * M + m0 + s_c + 32 * q);
                 ra[2 * q] = v.x;
                 ra[2 * q + 1] = v.y;
+            }
+#pragma unroll
+            for (int q = 0; q < kNB; ++q) {
                 const float2 u = *reinterpret_cast<const float2 *>(B + gk * N + n0 + s_c + 32 * q);
                 rb[2 * q] = u.x;
                 rb[2 * q + 1] = u.y;
@@ -73,40 +83,47 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             for (int q = 0; q < 4; ++q)
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
-                    const int64_t gm = m0 + s_c + 32 * q + h, gc = n0 + s_c + 32 * q + h;
+                    const int64_t gm = m0 + s_c + 32 * q + h;
                     ra[2 * q + h] = (gk < ke && gm < M) ? Wk[gk * M + gm] : 0.0;
+                }
+#pragma unroll
+            for (int q = 0; q < kNB; ++q)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int64_t gc = n0 + s_c + 32 * q + h;
                     rb[2 * q + h] = (gk < ke && gc < N) ? B[gk * N + gc] : 0.0f;
                 }
         }
     };
     auto store_tiles = [&](int buf) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < 4; ++q)
             *reinterpret_cast<double2 *>(&As[buf][s_k][s_c + 32 * q]) = make_double2(ra[2 * q], ra[2 * q + 1]);
+#pragma unroll
+        for (int q = 0; q < kNB; ++q)
             *reinterpret_cast<double2 *>(&Bs[buf][s_k][s_c + 32 * q]) =
                 make_double2((double)rb[2 * q], (double)rb[2 * q + 1]);
-        }
     };
 
-    doublex4 acc[4][4];
+    doublex4 acc[4][kNB];
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = doublex4{0.0, 0.0, 0.0, 0.0};
+        for (int ni = 0; ni < kNB; ++ni) acc[mi][ni] = doublex4{0.0, 0.0, 0.0, 0.0};
 
     const int rc = lane & 15, kq = lane >> 4;  // operand row/column within a 16-block, k within a step of 4
     auto compute = [&](int cur) {
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 4) {
-            double a[4], b[4];
+            double a[4], b[kNB];
 #pragma unroll
             for (int mi = 0; mi < 4; ++mi) a[mi] = As[cur][kk + kq][wm * 64 + mi * 16 + rc];
 #pragma unroll
-            for (int ni = 0; ni < 4; ++ni) b[ni] = Bs[cur][kk + kq][wn * 64 + ni * 16 + rc];
+            for (int ni = 0; ni < kNB; ++ni) b[ni] = Bs[cur][kk + kq][wn * (BN / 2) + ni * 16 + rc];
 #pragma unroll
             for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-                for (int ni = 0; ni < 4; ++ni)
+                for (int ni = 0; ni < kNB; ++ni)
                     acc[mi][ni] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
         }
     };
@@ -130,11 +147,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
+        for (int ni = 0; ni < kNB; ++ni)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int64_t m = m0 + wm * 64 + mi * 16 + kq + 4 * v;
-                const int64_t col = n0 + wn * 64 + ni * 16 + rc;
+                const int64_t col = n0 + wn * (BN / 2) + ni * 16 + rc;
                 if (kFast || (m < M && col < N)) {
                     if (partial)
                         partial[((int64_t)blockIdx.z * M + m) * N + col] = acc[mi][ni][v];
@@ -175,7 +192,8 @@ hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge
 
 // K splits for an n x n layer on `batch` samples: enough workgroups for two per CU, at least 8 K steps each.
 int gemm_splits(int64_t n, int64_t batch, int num_cu) {
-    const int64_t tiles = ((n + BM - 1) / BM) * ((batch + BN - 1) / BN);
+    const int bn = tile_bn(batch);
+    const int64_t tiles = ((n + BM - 1) / BM) * ((batch + bn - 1) / bn);
     if (tiles == 0 || tiles >= num_cu) return 1;
     int64_t sp = (2 * (int64_t)num_cu + tiles - 1) / tiles;
     const int64_t most = n / (8 * BK);
@@ -192,7 +210,8 @@ size_t gemm_partial_bytes(int64_t n, int64_t batch, int num_cu) {
 hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, const double *wt, const float *bias, double ymax,
                                    const float *yt, float *zt, double *partial, int num_cu, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
-    const int64_t gx = (n + BM - 1) / BM, gy = (batch + BN - 1) / BN;
+    const int bn = tile_bn(batch);
+    const int64_t gx = (n + BM - 1) / BM, gy = (batch + bn - 1) / bn;
     if (gx > 0x7fffffffLL || gy > 65535) return hipErrorInvalidValue;
     int sp = gemm_splits(n, batch, num_cu);
     // split length in whole K steps; the last split may be shorter, none is empty
@@ -200,12 +219,19 @@ hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, const double *wt, c
     const int64_t kc = ((steps + sp - 1) / sp) * BK;
     sp = (int)((n + kc - 1) / kc);
     double *part = sp > 1 ? partial : nullptr;
-    const bool fast = n % BM == 0 && batch % BN == 0 && n % BK == 0;
+    const bool fast = n % BM == 0 && batch % bn == 0 && n % BK == 0;
     const dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)sp);
-    if (fast)
-        gemm_dense_layer_kernel<true><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
-    else
-        gemm_dense_layer_kernel<false><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
+    if (bn == 64) {
+        if (fast)
+            gemm_dense_layer_kernel<true, 64><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
+        else
+            gemm_dense_layer_kernel<false, 64><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
+    } else {
+        if (fast)
+            gemm_dense_layer_kernel<true, 128><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
+        else
+            gemm_dense_layer_kernel<false, 128><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || sp == 1) return e;
     gemm_split_reduce_kernel<<<(unsigned)((n * batch + 255) / 256), 256, 0, s>>>(n, batch, sp, partial, bias, ymax, zt);
