@@ -111,9 +111,12 @@ def spmm_algorithmic(n, batch, nnz):
 
 def spmm_kernel_name(n, nnz):
     """The dense-Y layer kernel the library selects (mirrors spmm_wants_tiles / spmm_wants_slots)."""
-    if n <= 65536 and nnz >= 1280 * n:
-        slot_bytes = -(-n // 16) * 16 * (-(-n // 64) * 64) * 8
-        return "spmm_slots_kernel" if slot_bytes <= 2 ** 31 else "spmm_tiled_kernel"
+    if n <= 65536:
+        if -(-n // 16) * 16 * (-(-n // 64) * 64) * 8 <= 2 ** 31:
+            if 9 * nnz >= 2 * n * n:
+                return "spmm_slots_kernel"
+        elif 10 * nnz >= 3 * n * n:
+            return "spmm_tiled_kernel"
     return "spmm_fanin_kernel"
 
 

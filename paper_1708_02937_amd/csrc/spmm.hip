@@ -572,17 +572,23 @@ int spmm_tile_count(int64_t n) { return (int)((n + kTileRows - 1) / kTileRows); 
 
 size_t spmm_tile_mask_elems(int64_t n) { return (size_t)spmm_tile_count(n) * (size_t)mask_pitch(n); }
 
-// Measured on MI355X (n = 4096, batch = 1024): the LDS-tiled product wins at 50% density (0.83 vs 1.11 ms
-// per layer for the L2 gather), they tie at 30% (0.69 vs 0.68 ms), the gather wins below; switch at an
-// average fan-in of 1280.
-bool spmm_wants_tiles(int64_t n, int64_t nnz) { return n <= 65536 && nnz >= 1280 * n; }
+// Kernel choice for a dense-Y layer.  Both LDS-tiled kernels visit every (input, output) slot, so their cost
+// grows with n^2 and hardly with the density; the gather's grows with nnz.  Measured on MI355X (n = 4096,
+// batch = 1024, per layer): the scalar-register kernel takes 0.51-0.54 ms from d = 0.15 to 0.5, the gather
+// 0.47 ms at d = 0.2, 0.59 at 0.25, 0.70 at 0.3, so the former is used from d = 2/9; the readlane-fed kernel
+// (for layers whose slot array would not fit) tied with the gather at d = 0.3 (0.69 ms) and took 0.83 ms at
+// d = 0.5, so it is used from d = 0.3.  Thresholds on nnz / n^2 in exact integer arithmetic (n <= 65536).
+static bool slots_fit(int64_t n);
+bool spmm_wants_tiles(int64_t n, int64_t nnz) {
+    if (n > 65536) return false;
+    return slots_fit(n) ? 9 * nnz >= 2 * n * n : 10 * nnz >= 3 * n * n;
+}
 
 size_t spmm_slot_elems(int64_t n) { return (size_t)spmm_tile_count(n) * kTileRows * (size_t)mask_pitch(n); }
 
 // The slot array holds every (input, output) pair in fp64: used while it stays at or below 2 GiB per layer.
-bool spmm_wants_slots(int64_t n, int64_t nnz) {
-    return spmm_wants_tiles(n, nnz) && spmm_slot_elems(n) * sizeof(double) <= (size_t(1) << 31);
-}
+static bool slots_fit(int64_t n) { return spmm_slot_elems(n) * sizeof(double) <= (size_t(1) << 31); }
+bool spmm_wants_slots(int64_t n, int64_t nnz) { return spmm_wants_tiles(n, nnz) && slots_fit(n); }
 
 hipError_t launch_spmm_slots(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *slots, hipStream_t s) {
     hipError_t e = hipMemsetAsync(slots, 0, spmm_slot_elems(n) * sizeof(double), s);

@@ -106,9 +106,13 @@ def test_summarize_pmc_scales_by_the_copy_probe(tmp_path):
 
 
 def test_kernel_name_matches_the_selection_rule():
-    assert bench.spmm_kernel_name(4096, 1280 * 4096) == "spmm_slots_kernel"
-    assert bench.spmm_kernel_name(4096, 1280 * 4096 - 1) == "spmm_fanin_kernel"
-    # the slot array (16-row tiles x 64-padded columns, fp64) beyond 2 GiB: tiled kernel
+    # scalar-register kernel from density 2/9 (9 nnz >= 2 n^2)
+    assert bench.spmm_kernel_name(4096, 3728271) == "spmm_slots_kernel"
+    assert bench.spmm_kernel_name(4096, 3728270) == "spmm_fanin_kernel"
+    # the slot array (16-row tiles x 64-padded columns, fp64) beyond 2 GiB: readlane-fed tiled kernel from
+    # density 0.3 (10 nnz >= 3 n^2)
     n = 16448
     assert math.ceil(n / 16) * 16 * math.ceil(n / 64) * 64 * 8 > 2 ** 31
-    assert bench.spmm_kernel_name(n, 1280 * n) == "spmm_tiled_kernel"
+    assert bench.spmm_kernel_name(n, 81161012) == "spmm_tiled_kernel"
+    assert bench.spmm_kernel_name(n, 81161011) == "spmm_fanin_kernel"
+    assert bench.spmm_kernel_name(65537, 65537 ** 2) == "spmm_fanin_kernel"

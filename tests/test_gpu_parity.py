@@ -76,7 +76,7 @@ def test_tiny_dense_batch(sd, arm, seed, n, L, batch):
                                               (33, 2000, 2, 1028, 0.7), (34, 1500, 1, 516, 0.9),
                                               (35, 1290, 2, 132, 0.999), (36, 1503, 1, 388, 0.9)])
 def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
-    """Average fan-in >= 1280 selects the LDS-tiled product with scalar-register weights; ragged n (not a
+    """Density >= 2/9 selects the LDS-tiled product with scalar-register weights; ragged n (not a
     multiple of 4, 16 or 64) and batch exercise its edges."""
     p = tiny_random(seed, n, L, batch, w_density=d, y_density=0.7, dense_input=True,
                     ymax=[math.inf, 3.0][seed % 2], bias_lo=-1.0, bias_hi=1.0)
@@ -89,12 +89,12 @@ def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
 
 @pytest.mark.parametrize("seed,n,L,batch,d", [(38, 1400, 2, 130, 0.95), (39, 1333, 1, 63, 0.99)])
 def test_high_fanin_gather_fallback(sd, seed, n, L, batch, d):
-    """Average fan-in >= 1280 but a batch the LDS-tiled kernels do not take (not a multiple of 4, or below
+    """Density >= 2/9 but a batch the LDS-tiled kernels do not take (not a multiple of 4, or below
     128): the layer falls back to the gather SpMM with two or one columns per lane over lists far longer
     than one 64-entry load; integer shadow bit for bit."""
     p = tiny_random(seed, n, L, batch, w_density=d, y_density=0.7, dense_input=True,
                     ymax=[math.inf, 3.0][seed % 2], bias_lo=-1.0, bias_hi=1.0)
-    assert p.layers[0].nnz >= 1280 * p.n
+    assert 9 * p.layers[0].nnz >= 2 * p.n * p.n
     _say("high fan-in gather fallback", seed, n, L, batch, d)
     parity.compare(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE)))
     q = integer_shadow(p)
@@ -103,10 +103,11 @@ def test_high_fanin_gather_fallback(sd, seed, n, L, batch, d):
 
 
 def test_high_fanin_beyond_slot_limit(sd):
-    """n = 16448: the fp64 weight slots of every (input, output) pair would exceed 2 GiB, so the high fan-in
-    layer takes the readlane-fed LDS-tiled kernel instead of the scalar-register one; sampled rows, ragged batch."""
-    p = tiny_random(37, 16448, 1, 132, w_density=0.08, y_density=0.7, dense_input=True, bias_lo=-1.0, bias_hi=1.0)
-    assert p.layers[0].nnz >= 1280 * p.n
+    """n = 16448: the fp64 weight slots of every (input, output) pair would exceed 2 GiB, so a layer of
+    density >= 0.3 takes the readlane-fed LDS-tiled kernel instead of the scalar-register one; sampled rows,
+    ragged batch."""
+    p = tiny_random(37, 16448, 1, 132, w_density=0.31, y_density=0.7, dense_input=True, bias_lo=-1.0, bias_hi=1.0)
+    assert 10 * p.layers[0].nnz >= 3 * p.n * p.n
     rows = np.arange(0, 132, 12)
     _say("high fan-in beyond the slot limit")
     out = run_dense(sd, p, sd.SDNN_ARM_SPARSE)
@@ -151,7 +152,7 @@ def test_pattern_bias_csr_path(sd, seed, n, L, batch, wd, yd):
                                                  (71, 2000, 2, 516, 0.7, 0.002)])
 def test_pattern_bias_dense_batch(sd, seed, n, L, batch, d, yd):
     """SDNN_BIAS_PATTERN on the sparse arm with dense batches: the gather SpMM (one, two and four columns
-    per lane) and the LDS-tiled SpMM (fan-in >= 1280); sparse inputs leave many positions untouched."""
+    per lane) and the LDS-tiled SpMM (density >= 2/9); sparse inputs leave many positions untouched."""
     p = tiny_random(seed, n, L, batch, w_density=d, y_density=yd, dense_input=True, bias_lo=-0.2, bias_hi=0.6)
     _say("pattern dense", seed, n, L, batch)
     parity.compare(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE, bias_mode=1)), bias_mode=1)
