@@ -74,10 +74,12 @@ def test_tiny_dense_batch(sd, arm, seed, n, L, batch):
 
 @pytest.mark.parametrize("seed,n,L,batch,d", [(31, 1400, 2, 128, 0.97), (32, 1400, 2, 260, 0.95),
                                               (33, 2000, 2, 1028, 0.7), (34, 1500, 1, 516, 0.9),
-                                              (35, 1290, 2, 132, 0.999), (36, 1503, 1, 388, 0.9)])
+                                              (35, 1290, 2, 132, 0.999), (36, 1503, 1, 388, 0.9),
+                                              (40, 1500, 2, 256, 0.25)])
 def test_high_fanin_lds_tiles(sd, seed, n, L, batch, d):
     """Density >= 2/9 selects the LDS-tiled product with scalar-register weights; ragged n (not a
-    multiple of 4, 16 or 64) and batch exercise its edges."""
+    multiple of 4, 16 or 64) and batch exercise its edges; d = 0.25, just above the switch, leaves most slots
+    empty."""
     p = tiny_random(seed, n, L, batch, w_density=d, y_density=0.7, dense_input=True,
                     ymax=[math.inf, 3.0][seed % 2], bias_lo=-1.0, bias_hi=1.0)
     _say("high fan-in", seed, n, L, batch, d)
