@@ -386,12 +386,19 @@ def test_identity_input_reads_back_weights(sd):
     assert got.tobytes() == want.tobytes()
 
 
-def test_graph_replay_matches_eager(sd):
+@pytest.mark.parametrize("layers", ["gather", "slots"])
+def test_graph_replay_matches_eager(sd, layers):
     """A HIP graph of forward_dense replays the eager result bit for bit, replay after replay, with new inputs
-    written into the bound input and unrelated eager work between the replays (both arms)."""
+    written into the bound input and unrelated eager work between the replays (both arms); the layers take the
+    gather SpMM (tiny MLP recipe) or the scalar-register LDS-tiled SpMM (d = 0.5)."""
     import torch
 
-    p = make_config(1, n=1000, L=3, batch=132)
+    if layers == "gather":
+        p = make_config(1, n=1000, L=3, batch=132)
+    else:
+        p = tiny_random(45, 1300, 2, 128, w_density=0.5, y_density=0.7, dense_input=True, bias_lo=-1.0,
+                        bias_hi=1.0)
+        assert 9 * p.layers[0].nnz >= 2 * p.n * p.n
     for arm in ARMS:
         net = sd.net_from_problem(p, dense=(arm == "dense"))
         rng = np.random.default_rng(5)
