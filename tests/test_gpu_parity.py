@@ -297,8 +297,10 @@ def test_config1_csr_path(sd):
     parity.compare(p, run_csr(sd, p))
 
 
-@pytest.mark.parametrize("d", [0.5, 0.1, 0.01, 0.001])
+@pytest.mark.parametrize("d", [0.5, 0.25, 0.1, 0.01, 0.001])
 def test_config2_sparse_arm_sampled(sd, d):
+    """The density-sweep workload at full size through the CSR path, sampled rows; d = 0.25 sits just above the
+    switch to the scalar-register LDS-tiled SpMM."""
     p = make_config(2, d)
     _say("config 2 sparse arm", d)
     out = run_dense(sd, p, sd.SDNN_ARM_SPARSE)
