@@ -109,14 +109,17 @@ def spmm_algorithmic(n, batch, nnz):
     return 8 * n * batch + 8 * nnz + 8 * (n + 1) + 4 * n, 2.0 * batch * nnz
 
 
-def spmm_kernel_name(n, nnz):
-    """The dense-Y layer kernel the library selects (mirrors spmm_wants_tiles / spmm_wants_slots)."""
-    if n <= 65536:
+def spmm_kernel_name(n, nnz, batch=1024):
+    """The dense-Y layer kernel the library selects (mirrors spmm_wants_tiles / spmm_wants_slots and the
+    gather's narrow-chunk range in launch_spmm_fanin)."""
+    if n <= 65536 and batch % 4 == 0 and batch >= 128:
         if -(-n // 16) * 16 * (-(-n // 64) * 64) * 8 <= 2 ** 31:
             if 9 * nnz >= 2 * n * n:
                 return "spmm_slots_kernel"
         elif 10 * nnz >= 3 * n * n:
             return "spmm_tiled_kernel"
+    if 4096 < n <= 16384 and batch % 4 == 0:
+        return "spmm_narrow_kernel"
     return "spmm_fanin_kernel"
 
 
@@ -218,7 +221,7 @@ def run_sweep(args, torch, sd):
     else:
         roof = {"bound": "hbm", "achieved": round(byt / t_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    kernel = spmm_kernel_name(p.n, nnz_avg)
+    kernel = spmm_kernel_name(p.n, nnz_avg, p.batch)
     roof["traffic"] = _pmc_traffic(f"{kernel}_d{dom:g}", ["spmm.hip", "common.h"])
     roof["kernel"] = kernel
     roof["per_launch_ms"] = round(per_launch[dom], 5)

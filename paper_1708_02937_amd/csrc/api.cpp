@@ -109,7 +109,8 @@ sdnn_status dalloc(T **p, size_t count, const char *what) {
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Workspace of a CSR forward: two slot buffers (count[batch], col[batch*n], val[batch*n]) and a scan area.
+// Workspace of a CSR forward: two slot buffers (count[batch], col[n*ld], val[n*ld] with ld = act_ld(n, batch)
+// >= batch, so that a pair of them also holds two n x batch activation buffers at row pitch ld) and a scan area.
 struct CsrWs {
     int32_t *cnt[2];
     int32_t *col[2];
@@ -123,7 +124,7 @@ CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
     CsrWs w{};
     char *p = (char *)base;
     size_t off = 0;
-    const size_t slots = (size_t)batch * (size_t)n;
+    const size_t slots = (size_t)sdnn::act_ld(n, batch) * (size_t)n;
     for (int b = 0; b < 2; ++b) {
         w.cnt[b] = (int32_t *)(p + off);
         off = align_up(off + (size_t)batch * sizeof(int32_t));
@@ -142,9 +143,14 @@ CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
 
 constexpr int64_t kMaxScan = 16777216;  // longest array the device prefix sum handles (fan-in pointers, row pointers)
 
-// two n x batch fp32 activation buffers, then the dense arm's split-K partial sums (small batches only)
+// bytes of one n x batch fp32 activation buffer at row pitch act_ld(n, batch)
+size_t act_bytes(int64_t n, int64_t batch) {
+    return align_up((size_t)n * (size_t)sdnn::act_ld(n, batch) * sizeof(float));
+}
+
+// two activation buffers, then the dense arm's split-K partial sums (small batches only)
 size_t dense_ws_bytes(int64_t n, int64_t batch, int num_cu) {
-    return 2 * align_up((size_t)n * (size_t)batch * sizeof(float)) + align_up(sdnn::gemm_partial_bytes(n, batch, num_cu));
+    return 2 * act_bytes(n, batch) + align_up(sdnn::gemm_partial_bytes(n, batch, num_cu));
 }
 
 }  // namespace
@@ -385,24 +391,24 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
         for (int32_t k = k0; k < k1; ++k)
             if (!net->layers[(size_t)k].dense_wt)
                 return fail(SDNN_ERR_INVALID_OBJECT, "dense arm requested before sdnn_net_build_dense");
+    const int64_t ld = sdnn::act_ld(n, batch);
     float *buf[2];
     buf[0] = (float *)ws;
-    buf[1] = (float *)((char *)ws + align_up((size_t)n * (size_t)batch * sizeof(float)));
-    double *partial = (double *)((char *)ws + 2 * align_up((size_t)n * (size_t)batch * sizeof(float)));
-    SDNN_HIP(sdnn::launch_transpose(Y_in, buf[0], batch, n, s));  // batch x n -> n x batch
+    buf[1] = (float *)((char *)ws + act_bytes(n, batch));
+    double *partial = (double *)((char *)ws + 2 * act_bytes(n, batch));
+    SDNN_HIP(sdnn::launch_transpose(Y_in, n, buf[0], ld, batch, n, s));  // batch x n -> n x batch
     int cur = 0;
     for (int32_t k = k0; k < k1; ++k) {
         const Layer &l = net->layers[(size_t)k];
         if (arm == SDNN_ARM_SPARSE)
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias, net->ymax,
-                                             net->bias_pattern, buf[cur],
-                                             buf[cur ^ 1], s));
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, ld, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias,
+                                             net->ymax, net->bias_pattern, buf[cur], buf[cur ^ 1], s));
         else
-            SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, l.dense_wt, l.bias, net->ymax, buf[cur], buf[cur ^ 1],
-                                                   partial, net->num_cu, s));
+            SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, ld, l.dense_wt, l.bias, net->ymax, buf[cur],
+                                                   buf[cur ^ 1], partial, net->num_cu, s));
         cur ^= 1;
     }
-    SDNN_HIP(sdnn::launch_transpose(buf[cur], Y_out, n, batch, s));  // n x batch -> batch x n
+    SDNN_HIP(sdnn::launch_transpose(buf[cur], ld, Y_out, n, n, batch, s));  // n x batch -> batch x n
     return SDNN_OK;
 }
 
@@ -499,19 +505,20 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     if (kd < k1) {
         const bool from_user = kd == k0;
         const int db = from_user ? 0 : cur;  // the input rows (if any) sit in buffer cur ^ 1
-        float *dense[2] = {reinterpret_cast<float *>(w.col[db]), w.val[db]};  // two n x batch fp32 buffers
-        SDNN_HIP(sdnn::launch_densify(n, batch, from_user ? y_row_ptr : nullptr, from_user ? nullptr : w.cnt[cur ^ 1],
+        // two n x batch fp32 buffers at row pitch ld
+        float *dense[2] = {reinterpret_cast<float *>(w.col[db]), w.val[db]};
+        const int64_t ld = sdnn::act_ld(n, batch);
+        SDNN_HIP(sdnn::launch_densify(n, batch, ld, from_user ? y_row_ptr : nullptr, from_user ? nullptr : w.cnt[cur ^ 1],
                                       from_user ? y_col : w.col[cur ^ 1], from_user ? y_val : w.val[cur ^ 1],
                                       dense[0], net->d_flags, s));
         int dc = 0;
         for (int32_t k = kd; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
-            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias, net->ymax,
-                                             net->bias_pattern, dense[dc],
-                                             dense[dc ^ 1], s));
+            SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, ld, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias,
+                                             net->ymax, net->bias_pattern, dense[dc], dense[dc ^ 1], s));
             dc ^= 1;
         }
-        SDNN_HIP(sdnn::launch_transpose(dense[dc], dense[dc ^ 1], n, batch, s));  // -> batch x n
+        SDNN_HIP(sdnn::launch_transpose(dense[dc], ld, dense[dc ^ 1], n, n, batch, s));  // -> batch x n
         SDNN_HIP(sdnn::launch_dense_to_slots(n, batch, dense[dc ^ 1], w.cnt[db ^ 1], w.col[db ^ 1], w.val[db ^ 1], s));
         last = db ^ 1;
         outb = db;
@@ -558,11 +565,12 @@ sdnn_status sdnn_mxm_dense(sdnn_net net, int32_t k, int32_t semiring, int64_t ba
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     const Layer &l = net->layers[(size_t)k];
+    const int64_t ld = sdnn::act_ld(n, batch);
     float *yt = (float *)ws;
-    float *zt = (float *)((char *)ws + align_up((size_t)n * (size_t)batch * sizeof(float)));
-    SDNN_HIP(sdnn::launch_transpose(Y, yt, batch, n, s));  // batch x n -> n x batch
-    SDNN_HIP(sdnn::launch_semiring_mxm(semiring, n, batch, l.fan_ptr, l.fan, yt, zt, s));
-    SDNN_HIP(sdnn::launch_transpose(zt, Z, n, batch, s));  // n x batch -> batch x n
+    float *zt = (float *)((char *)ws + act_bytes(n, batch));
+    SDNN_HIP(sdnn::launch_transpose(Y, n, yt, ld, batch, n, s));  // batch x n -> n x batch
+    SDNN_HIP(sdnn::launch_semiring_mxm(semiring, n, batch, ld, l.fan_ptr, l.fan, yt, zt, s));
+    SDNN_HIP(sdnn::launch_transpose(zt, ld, Z, n, n, batch, s));  // n x batch -> batch x n
     return SDNN_OK;
 }
 
@@ -576,13 +584,14 @@ sdnn_status sdnn_mxm_csr(sdnn_net net, int32_t k, int32_t semiring, int64_t batc
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     const Layer &l = net->layers[(size_t)k];
+    const int64_t ld = sdnn::act_ld(n, batch);
     float *yt = (float *)ws;
-    float *zt = (float *)((char *)ws + align_up((size_t)n * (size_t)batch * sizeof(float)));
+    float *zt = (float *)((char *)ws + act_bytes(n, batch));
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
-    SDNN_HIP(sdnn::launch_semiring_densify(n, batch, sdnn::semiring_zero(semiring), y_row_ptr, y_col, y_val, yt,
+    SDNN_HIP(sdnn::launch_semiring_densify(n, batch, ld, sdnn::semiring_zero(semiring), y_row_ptr, y_col, y_val, yt,
                                            net->d_flags, s));
-    SDNN_HIP(sdnn::launch_semiring_mxm(semiring, n, batch, l.fan_ptr, l.fan, yt, zt, s));
-    SDNN_HIP(sdnn::launch_transpose(zt, Z, n, batch, s));
+    SDNN_HIP(sdnn::launch_semiring_mxm(semiring, n, batch, ld, l.fan_ptr, l.fan, yt, zt, s));
+    SDNN_HIP(sdnn::launch_transpose(zt, ld, Z, n, n, batch, s));
     uint32_t flags = 0;
     SDNN_HIP(hipMemcpyAsync(&flags, net->d_flags, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
     SDNN_HIP(hipStreamSynchronize(s));

@@ -43,8 +43,20 @@ hipError_t launch_fanin_lists(int64_t n, int64_t nnz, const int64_t *row_ptr, co
 hipError_t launch_max_segment(int64_t n, const int64_t *ptr, int32_t *out, hipStream_t s);
 hipError_t launch_pack_edges(int64_t nnz, const int32_t *col, const float *val, Edge *out, hipStream_t s);
 
+// Row pitch (floats) of the neuron-major activation buffers Y^T (n rows of `batch` samples).  Lines taken one
+// per row at a power-of-two byte pitch fall into a fraction of an XCD's L2 sets (measured on MI355X: at a
+// 16 KiB pitch a 1 MiB working set already misses about half the time, at 16 KiB + 256 B a 3 MiB one stays
+// resident), so for wide layers (n > 4096) of 256 samples or more the pitch is an odd multiple of 64 floats
+// (256 bytes).  At n = 4096, batch 1024 the padding measured 1-3% slower per layer, so narrower layers keep
+// the dense pitch.
+inline int64_t act_ld(int64_t n, int64_t batch) {
+    return (n <= 4096 || batch < 256) ? batch : (((batch + 63) / 64) | 1) * 64;
+}
+
 // spmm.hip
-hipError_t launch_transpose(const float *in, float *out, int64_t rows, int64_t cols, hipStream_t s);
+// rows x cols (row pitch in_ld >= cols) -> cols x rows (row pitch out_ld >= rows)
+hipError_t launch_transpose(const float *in, int64_t in_ld, float *out, int64_t out_ld, int64_t rows, int64_t cols,
+                            hipStream_t s);
 int spmm_tile_count(int64_t n);
 size_t spmm_tile_mask_elems(int64_t n);
 bool spmm_wants_tiles(int64_t n, int64_t nnz);
@@ -56,7 +68,8 @@ bool spmm_wants_slots(int64_t n, int64_t nnz);
 hipError_t launch_spmm_slots(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *slots, hipStream_t s);
 // pattern != 0: the bias and h apply only where some fan-in entry meets a nonzero input (else 0).
 // tile_mask / slots: the high fan-in structures when the layer has them (else null).
-hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
+// yt, zt: n x batch at row pitch ld (act_ld(n, batch)).
+hipError_t launch_spmm_fanin(int64_t n, int64_t batch, int64_t ld, const int64_t *fan_ptr, const Edge *fan,
                              const uint16_t *tile_mask, const double *slots, const float *bias, double ymax, int pattern,
                              const float *yt, float *zt, hipStream_t s);
 
@@ -65,7 +78,7 @@ hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge
 int gemm_splits(int64_t n, int64_t batch, int num_cu);
 size_t gemm_partial_bytes(int64_t n, int64_t batch, int num_cu);
 // partial: gemm_partial_bytes(n, batch, num_cu) bytes of scratch (unused when that is 0).
-hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, const double *wt, const float *bias, double ymax,
+hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, int64_t ld, const double *wt, const float *bias, double ymax,
                                    const float *yt, float *zt, double *partial, int num_cu, hipStream_t s);
 
 // spgemm.hip
@@ -86,7 +99,7 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
                                const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
                                int pattern, double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val,
                                int32_t *lists, unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s);
-hipError_t launch_densify(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
+hipError_t launch_densify(int64_t n, int64_t batch, int64_t ld, const int64_t *in_row_ptr, const int32_t *in_cnt,
                           const int32_t *in_col, const float *in_val, float *yt, uint32_t *err, hipStream_t s);
 hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,
                                  float *out_val, hipStream_t s);
@@ -97,11 +110,12 @@ hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, con
 // semiring.hip
 enum : int { kSemiringPlusTimes = 0, kSemiringMaxPlus = 1, kSemiringMaxMin = 2, kSemiringMinMax = 3, kSemiringXorAnd = 4 };
 float semiring_zero(int semiring);
-// Z^T = (Y (+).(x) W)^T from Y^T (n x batch) over the fan-in lists; no bias, no activation.
-hipError_t launch_semiring_mxm(int semiring, int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
+// Z^T = (Y (+).(x) W)^T from Y^T (n x batch, row pitch ld) over the fan-in lists; no bias, no activation.
+hipError_t launch_semiring_mxm(int semiring, int64_t n, int64_t batch, int64_t ld, const int64_t *fan_ptr, const Edge *fan,
                                const float *yt, float *zt, hipStream_t s);
-// Y^T (n x batch) = `fill` everywhere, then the stored entries of the CSR rows (extents checked, flagged in err).
-hipError_t launch_semiring_densify(int64_t n, int64_t batch, float fill, const int64_t *row_ptr, const int32_t *col,
+// Y^T (n x batch, row pitch ld) = `fill` everywhere, then the stored entries of the CSR rows (extents checked,
+// flagged in err).
+hipError_t launch_semiring_densify(int64_t n, int64_t batch, int64_t ld, float fill, const int64_t *row_ptr, const int32_t *col,
                                    const float *val, float *yt, uint32_t *err, hipStream_t s);
 
 }  // namespace sdnn

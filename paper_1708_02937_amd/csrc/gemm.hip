@@ -37,7 +37,7 @@ constexpr int kPad = 16;
 // loads need no guards and no branch depends on the thread; otherwise every element is guarded.
 template <bool kFast>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_dense_layer_kernel(int64_t M, int64_t N, int64_t K,
-                                                               int64_t kc, const double *__restrict__ Wk,
+                                                               int64_t ld, int64_t kc, const double *__restrict__ Wk,
                                                                const float *__restrict__ B,
                                                                const float *__restrict__ bias, double ymax,
                                                                float *__restrict__ C, double *__restrict__ partial) {
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             }
 #pragma unroll
             for (int q = 0; q < kNB; ++q) {
-                const float2 u = *reinterpret_cast<const float2 *>(B + gk * N + n0 + s_c + 32 * q);
+                const float2 u = *reinterpret_cast<const float2 *>(B + gk * ld + n0 + s_c + 32 * q);
                 rb[2 * q] = u.x;
                 rb[2 * q + 1] = u.y;
             }
@@ -89,7 +89,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
                     const int64_t gc = n0 + s_c + 32 * q + h;
-                    rb[2 * q + h] = (gk < ke && gc < N) ? B[gk * N + gc] : 0.0f;
+                    rb[2 * q + h] = (gk < ke && gc < N) ? B[gk * ld + gc] : 0.0f;
                 }
         }
     };
@@ -154,19 +154,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                     if (partial)
                         partial[((int64_t)blockIdx.z * M + m) * N + col] = acc[mi][ni][v];
                     else
-                        C[m * N + col] = activate(acc[mi][ni][v] + (double)bias[m], ymax);
+                        C[m * ld + col] = activate(acc[mi][ni][v] + (double)bias[m], ymax);
                 }
             }
 }
 
 // Sum of the K splits in split order, then the bias, h and one rounding.
-__global__ void gemm_split_reduce_kernel(int64_t M, int64_t N, int splits, const double *__restrict__ partial,
+__global__ void gemm_split_reduce_kernel(int64_t M, int64_t N, int64_t ld, int splits, const double *__restrict__ partial,
                                          const float *__restrict__ bias, double ymax, float *__restrict__ C) {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= M * N) return;
     double z = 0.0;
     for (int sp = 0; sp < splits; ++sp) z += partial[(int64_t)sp * M * N + e];
-    C[e] = activate(z + (double)bias[e / N], ymax);
+    C[(e / N) * ld + e % N] = activate(z + (double)bias[e / N], ymax);
 }
 
 // Dense W_k (n_in x n_out, row-major, fp64) with explicit zeros: row i holds the fan-out of input i.
@@ -204,7 +204,7 @@ size_t gemm_partial_bytes(int64_t n, int64_t batch, int num_cu) {
     return sp > 1 ? (size_t)sp * (size_t)n * (size_t)batch * sizeof(double) : 0;
 }
 
-hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, const double *wt, const float *bias, double ymax,
+hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, int64_t ld, const double *wt, const float *bias, double ymax,
                                    const float *yt, float *zt, double *partial, int num_cu, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
     const int64_t gx = (n + BM - 1) / BM, gy = (batch + BN - 1) / BN;
@@ -215,15 +215,16 @@ hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, const double *wt, c
     const int64_t kc = ((steps + sp - 1) / sp) * BK;
     sp = (int)((n + kc - 1) / kc);
     double *part = sp > 1 ? partial : nullptr;
-    const bool fast = n % BM == 0 && batch % BN == 0 && n % BK == 0;
+    const bool fast = n % BM == 0 && batch % BN == 0 && n % BK == 0 && ld % 4 == 0;
     const dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)sp);
     if (fast)
-        gemm_dense_layer_kernel<true><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
+        gemm_dense_layer_kernel<true><<<grid, 256, 0, s>>>(n, batch, n, ld, kc, wt, yt, bias, ymax, zt, part);
     else
-        gemm_dense_layer_kernel<false><<<grid, 256, 0, s>>>(n, batch, n, kc, wt, yt, bias, ymax, zt, part);
+        gemm_dense_layer_kernel<false><<<grid, 256, 0, s>>>(n, batch, n, ld, kc, wt, yt, bias, ymax, zt, part);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || sp == 1) return e;
-    gemm_split_reduce_kernel<<<(unsigned)((n * batch + 255) / 256), 256, 0, s>>>(n, batch, sp, partial, bias, ymax, zt);
+    gemm_split_reduce_kernel<<<(unsigned)((n * batch + 255) / 256), 256, 0, s>>>(n, batch, ld, sp, partial, bias, ymax,
+                                                                                zt);
     return hipGetLastError();
 }
 

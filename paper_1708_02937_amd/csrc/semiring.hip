@@ -42,7 +42,7 @@ struct XorAnd {  // GF(2): a value counts as 1 when it is nonzero
 constexpr int kSrUnroll = 8;
 
 template <int V, class SR>
-__global__ __launch_bounds__(256) void semiring_gather_kernel(int64_t n, int64_t batch, int chunks,
+__global__ __launch_bounds__(256) void semiring_gather_kernel(int64_t n, int64_t batch, int64_t ld, int chunks,
                                                               int64_t block_base,
                                                               const int64_t *__restrict__ fan_ptr,
                                                               const Edge *__restrict__ fan,
@@ -74,7 +74,7 @@ __global__ __launch_bounds__(256) void semiring_gather_kernel(int64_t n, int64_t
                 const int src = t + u < cnt ? t + u : t;  // past the list end: repeat a valid entry, unused
                 const int32_t i = __builtin_amdgcn_readlane(mine.idx, src);
                 w[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine.w), src));
-                const float *p = yt + (int64_t)i * batch + colc;
+                const float *p = yt + (int64_t)i * ld + colc;
 #pragma unroll
                 for (int v = 0; v < V; ++v) y[u][v] = p[v];
             }
@@ -89,16 +89,16 @@ __global__ __launch_bounds__(256) void semiring_gather_kernel(int64_t n, int64_t
     }
     if (!active) return;
 #pragma unroll
-    for (int v = 0; v < V; ++v) zt[j * batch + col + v] = (float)acc[v];
+    for (int v = 0; v < V; ++v) zt[j * ld + col + v] = (float)acc[v];
 }
 
-// Y^T (n x batch) filled with `fill`, then the stored entries of CSR rows scattered into it.
+// Y^T (n x batch, row pitch ld) filled with `fill`, then the stored entries of CSR rows scattered into it.
 __global__ void semiring_fill_kernel(int64_t count, float fill, float *__restrict__ yt) {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e < count) yt[e] = fill;
 }
 
-__global__ __launch_bounds__(256) void semiring_scatter_kernel(int64_t n, int64_t batch,
+__global__ __launch_bounds__(256) void semiring_scatter_kernel(int64_t n, int64_t batch, int64_t ld,
                                                                const int64_t *__restrict__ row_ptr,
                                                                const int32_t *__restrict__ col,
                                                                const float *__restrict__ val, float *__restrict__ yt,
@@ -116,12 +116,12 @@ __global__ __launch_bounds__(256) void semiring_scatter_kernel(int64_t n, int64_
             atomicOr(err, 1u);
             continue;
         }
-        yt[(int64_t)i * batch + r] = val[b + t];
+        yt[(int64_t)i * ld + r] = val[b + t];
     }
 }
 
 template <class SR>
-hipError_t launch_sr(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan, const float *yt, float *zt,
+hipError_t launch_sr(int64_t n, int64_t batch, int64_t ld, const int64_t *fan_ptr, const Edge *fan, const float *yt, float *zt,
                      hipStream_t s) {
     int V = 1;
     if (batch % 4 == 0 && batch >= 256) V = 4;
@@ -132,11 +132,11 @@ hipError_t launch_sr(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edg
     for (int64_t base = 0; base < blocks; base += kSeg) {
         const unsigned nb = (unsigned)(blocks - base < kSeg ? blocks - base : kSeg);
         if (V == 4)
-            semiring_gather_kernel<4, SR><<<nb, 256, 0, s>>>(n, batch, (int)chunks, base, fan_ptr, fan, yt, zt);
+            semiring_gather_kernel<4, SR><<<nb, 256, 0, s>>>(n, batch, ld, (int)chunks, base, fan_ptr, fan, yt, zt);
         else if (V == 2)
-            semiring_gather_kernel<2, SR><<<nb, 256, 0, s>>>(n, batch, (int)chunks, base, fan_ptr, fan, yt, zt);
+            semiring_gather_kernel<2, SR><<<nb, 256, 0, s>>>(n, batch, ld, (int)chunks, base, fan_ptr, fan, yt, zt);
         else
-            semiring_gather_kernel<1, SR><<<nb, 256, 0, s>>>(n, batch, (int)chunks, base, fan_ptr, fan, yt, zt);
+            semiring_gather_kernel<1, SR><<<nb, 256, 0, s>>>(n, batch, ld, (int)chunks, base, fan_ptr, fan, yt, zt);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -154,25 +154,25 @@ float semiring_zero(int semiring) {
     }
 }
 
-hipError_t launch_semiring_mxm(int semiring, int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
+hipError_t launch_semiring_mxm(int semiring, int64_t n, int64_t batch, int64_t ld, const int64_t *fan_ptr, const Edge *fan,
                                const float *yt, float *zt, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
     switch (semiring) {
-        case kSemiringPlusTimes: return launch_sr<PlusTimes>(n, batch, fan_ptr, fan, yt, zt, s);
-        case kSemiringMaxPlus: return launch_sr<MaxPlus>(n, batch, fan_ptr, fan, yt, zt, s);
-        case kSemiringMaxMin: return launch_sr<MaxMin>(n, batch, fan_ptr, fan, yt, zt, s);
-        case kSemiringMinMax: return launch_sr<MinMax>(n, batch, fan_ptr, fan, yt, zt, s);
-        case kSemiringXorAnd: return launch_sr<XorAnd>(n, batch, fan_ptr, fan, yt, zt, s);
+        case kSemiringPlusTimes: return launch_sr<PlusTimes>(n, batch, ld, fan_ptr, fan, yt, zt, s);
+        case kSemiringMaxPlus: return launch_sr<MaxPlus>(n, batch, ld, fan_ptr, fan, yt, zt, s);
+        case kSemiringMaxMin: return launch_sr<MaxMin>(n, batch, ld, fan_ptr, fan, yt, zt, s);
+        case kSemiringMinMax: return launch_sr<MinMax>(n, batch, ld, fan_ptr, fan, yt, zt, s);
+        case kSemiringXorAnd: return launch_sr<XorAnd>(n, batch, ld, fan_ptr, fan, yt, zt, s);
         default: return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_semiring_densify(int64_t n, int64_t batch, float fill, const int64_t *row_ptr, const int32_t *col,
+hipError_t launch_semiring_densify(int64_t n, int64_t batch, int64_t ld, float fill, const int64_t *row_ptr, const int32_t *col,
                                    const float *val, float *yt, uint32_t *err, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
-    const int64_t count = n * batch;
+    const int64_t count = n * ld;
     semiring_fill_kernel<<<(unsigned)((count + 255) / 256), 256, 0, s>>>(count, fill, yt);
-    semiring_scatter_kernel<<<(unsigned)batch, 256, 0, s>>>(n, batch, row_ptr, col, val, yt, err);
+    semiring_scatter_kernel<<<(unsigned)batch, 256, 0, s>>>(n, batch, ld, row_ptr, col, val, yt, err);
     return hipGetLastError();
 }
 

@@ -599,10 +599,12 @@ __global__ __launch_bounds__(256) void compact_rows_kernel(int64_t n, const int3
     }
 }
 
-// Dense activations from a batch of sparse rows: yt (n x batch, neuron-major, zero-filled by the caller)
+// Dense activations from a batch of sparse rows: yt (n x batch at row pitch ld, neuron-major, zero-filled by the
+// caller)
 // receives every stored entry.  Input is either caller CSR (row extents checked as in the SpGEMM) or
 // slot rows written by a previous layer.
-__global__ __launch_bounds__(256) void densify_kernel(int64_t n, int64_t batch, const int64_t *__restrict__ in_row_ptr,
+__global__ __launch_bounds__(256) void densify_kernel(int64_t n, int64_t batch, int64_t ld,
+                                                      const int64_t *__restrict__ in_row_ptr,
                                                       const int32_t *__restrict__ in_cnt,
                                                       const int32_t *__restrict__ in_col,
                                                       const float *__restrict__ in_val, float *__restrict__ yt,
@@ -627,7 +629,7 @@ __global__ __launch_bounds__(256) void densify_kernel(int64_t n, int64_t batch, 
             atomicOr(err, 1u);
             continue;
         }
-        yt[(int64_t)i * batch + r] = in_val[yb + t];
+        yt[(int64_t)i * ld + r] = in_val[yb + t];
     }
 }
 
@@ -757,12 +759,12 @@ hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, con
     return hipGetLastError();
 }
 
-hipError_t launch_densify(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
+hipError_t launch_densify(int64_t n, int64_t batch, int64_t ld, const int64_t *in_row_ptr, const int32_t *in_cnt,
                           const int32_t *in_col, const float *in_val, float *yt, uint32_t *err, hipStream_t s) {
     if (batch == 0) return hipSuccess;
-    hipError_t e = hipMemsetAsync(yt, 0, (size_t)n * (size_t)batch * sizeof(float), s);
+    hipError_t e = hipMemsetAsync(yt, 0, (size_t)n * (size_t)ld * sizeof(float), s);
     if (e != hipSuccess) return e;
-    densify_kernel<<<(unsigned)batch, 256, 0, s>>>(n, batch, in_row_ptr, in_cnt, in_col, in_val, yt, err);
+    densify_kernel<<<(unsigned)batch, 256, 0, s>>>(n, batch, ld, in_row_ptr, in_cnt, in_col, in_val, yt, err);
     return hipGetLastError();
 }
 

@@ -68,7 +68,8 @@ __device__ __forceinline__ float bcast_f(float v, int lane) {
 constexpr int kUnroll = 8;
 
 template <int V, bool kPattern>
-__global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batch, int chunks, int64_t block_base,
+__global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batch, int64_t ld, int chunks,
+                                                         int64_t block_base,
                                                          const int64_t *__restrict__ fan_ptr,
                                                          const Edge *__restrict__ fan, const float *__restrict__ bias,
                                                          double ymax, const float *__restrict__ yt,
@@ -123,7 +124,7 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
             for (int u = 0; u < kUnroll; ++u) {
                 const int32_t i = bcast_i(mine.idx, t + u);
                 w[u] = bcast_f(mine.w, t + u);
-                load_v<V>(yt + (int64_t)i * batch + colc, y[u]);
+                load_v<V>(yt + (int64_t)i * ld + colc, y[u]);
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
@@ -139,7 +140,7 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
             float y[V];
             const int32_t i = bcast_i(mine.idx, t);
             const double wd = (double)bcast_f(mine.w, t);
-            load_v<V>(yt + (int64_t)i * batch + colc, y);
+            load_v<V>(yt + (int64_t)i * ld + colc, y);
 #pragma unroll
             for (int v = 0; v < V; ++v) {
                 acc[v] = __builtin_fma((double)y[v], wd, acc[v]);
@@ -153,7 +154,150 @@ __global__ __launch_bounds__(256) void spmm_fanin_kernel(int64_t n, int64_t batc
 #pragma unroll
     for (int v = 0; v < V; ++v)
         out[v] = (kPattern && (hit[v] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[v] + bj, ymax);
-    store_v<V>(zt + j * batch + col, out);
+    store_v<V>(zt + j * ld + col, out);
+}
+
+// Narrow-chunk variant for wide layers.  A chunk of the kernel above is 256 batch columns, so its slice of
+// Y^T is n KiB: beyond n = 4096 it no longer fits an XCD's 4 MiB L2, and every one of a row segment's ~32
+// consumers fetches it from memory again.  Here each 16-lane row of a wave owns one output neuron and 64
+// columns (4 per lane), so a chunk's slice is n x 256 bytes (4 MiB at n = 16384), which the L2 keeps when
+// the rows sit at a padded pitch (act_ld).  All XCDs work on the same chunk at a time, XCD x on its own
+// contiguous eighth of the neurons (a layer whose lists stay near the diagonal keeps its rows local; a ragged
+// last chunk still spreads over every XCD).  A row loads 16 list entries at once (lane k holds entry k) and
+// broadcasts entry t to its 16 lanes with a DPP row broadcast; the four rows of a wave walk their lists in
+// step, the shortest list's length unpredicated and the rest with a per-row guard.  Each output is still
+// summed in list (ascending input) order, as in the kernel above.
+constexpr int kNarrowP = 16;  // lanes per output neuron: one DPP row
+
+template <int T>
+__device__ __forceinline__ int32_t bcast_row(int32_t v) {
+    return __builtin_amdgcn_mov_dpp(v, 0x150 + T, 0xf, 0xf, false);  // row_newbcast: lane T of each 16-lane row
+}
+
+constexpr int kNarrowUnroll = 8;
+
+// f(integral_constant<int, U>) for U = B .. E - 1 (a DPP lane select must be a compile-time constant)
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+// row i of Y^T at this lane's columns: i < 2^24 and the row pitch in bytes < 2^24 (the launcher checks)
+__device__ __forceinline__ const float *narrow_row(const char *yl, int32_t i, uint32_t pitch) {
+    return reinterpret_cast<const float *>(yl + (uint64_t)((uint32_t)i & 0xffffffu) * (uint64_t)(pitch & 0xffffffu));
+}
+
+// list slots T0 .. T0 + kNarrowUnroll - 1 of the 16 a row holds: unpredicated while every row of the wave has
+// them (full), else with each row's loads guarded by its own length
+template <int V, bool kPattern, int T0>
+__device__ __forceinline__ void narrow_batch(const Edge &mine, int full, int base, int cnt, const char *yl,
+                                             uint32_t pitch, double (&acc)[V], uint32_t (&hit)[V]) {
+    float y[kNarrowUnroll][V];
+    float w[kNarrowUnroll];
+    int32_t idx[kNarrowUnroll];
+    static_for<0, kNarrowUnroll>([&](auto u) {
+        idx[u] = bcast_row<T0 + u>(mine.idx);
+        w[u] = __int_as_float(bcast_row<T0 + u>(__float_as_int(mine.w)));
+    });
+#pragma unroll
+    for (int u = 0; u < kNarrowUnroll; ++u) load_v<V>(narrow_row(yl, idx[u], pitch), y[u]);
+    if (T0 + kNarrowUnroll <= full) {
+#pragma unroll
+        for (int u = 0; u < kNarrowUnroll; ++u) {
+            const double wd = (double)w[u];
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                acc[v] = __builtin_fma((double)y[u][v], wd, acc[v]);
+                if constexpr (kPattern) hit[v] |= __float_as_uint(y[u][v]);
+            }
+        }
+    } else {
+        // a row whose list has ended read row 0 of Y^T (the zero index its lanes hold past the end: a line the
+        // chunk keeps hot) and adds the product of a zeroed input and the zero weight held there: +0 leaves an
+        // accumulator unchanged (one that starts at +0 never becomes -0)
+#pragma unroll
+        for (int u = 0; u < kNarrowUnroll; ++u) {
+            const bool ok = base + T0 + u < cnt;
+            const double wd = (double)w[u];
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+                asm volatile("" : "+v"(y[u][v]));  // keeps the load whole and unconditional
+                const float yv = ok ? y[u][v] : 0.0f;
+                acc[v] = __builtin_fma((double)yv, wd, acc[v]);
+                if constexpr (kPattern) hit[v] |= __float_as_uint(yv);
+            }
+        }
+    }
+}
+
+template <int V, bool kPattern>
+__global__ __launch_bounds__(256) void spmm_narrow_kernel(int64_t n, int64_t batch, int64_t ld, int64_t gpx,
+                                                          int64_t block_base,
+                                                          const int64_t *__restrict__ fan_ptr,
+                                                          const Edge *__restrict__ fan,
+                                                          const float *__restrict__ bias, double ymax,
+                                                          const float *__restrict__ yt, float *__restrict__ zt) {
+    constexpr int P = kNarrowP, G = 64 / P;  // G neurons per wave
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int grp = lane / P, k = lane % P;
+    // block b: XCD b % 8; chunk c for every XCD at once, neuron groups [x gpx, (x + 1) gpx) on XCD x
+    const int64_t b = block_base + blockIdx.x;
+    const int64_t local = b >> 3;
+    const int64_t c = local / gpx;
+    const int64_t g = (b & 7) * gpx + local % gpx;
+    const int64_t j = (g * 4 + wave) * G + grp;
+    const bool jv = j < n;
+    const int64_t col = c * (P * V) + (int64_t)k * V;
+    const bool active = jv && col < batch;  // batch is a multiple of V, so col < batch => col + V <= batch
+    const int64_t colc = col < batch ? col : 0;  // lanes past the batch read a valid address and discard it
+    const char *yl = reinterpret_cast<const char *>(yt + colc);
+    const uint32_t pitch = (uint32_t)(ld * (int64_t)sizeof(float));
+    int64_t eb = 0;
+    int cnt = 0;
+    if (jv) {
+        eb = fan_ptr[j];
+        cnt = (int)(fan_ptr[j + 1] - eb);
+    }
+    // the wave's shortest and longest list (every lane keeps running: the broadcasts read lanes of all groups)
+    int lo = cnt, hi = cnt;
+    static_for<0, G>([&](auto q) {
+        const int cq = __builtin_amdgcn_readlane(cnt, q * P);
+        lo = q == 0 ? cq : min(lo, cq);
+        hi = q == 0 ? cq : max(hi, cq);
+    });
+
+    double acc[V];
+    uint32_t hit[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        acc[v] = 0.0;
+        hit[v] = 0u;
+    }
+    Edge mine;
+    mine.idx = 0;
+    mine.w = 0.0f;
+    if (k < cnt) mine = fan[eb + k];
+    for (int base = 0; base < hi; base += P) {
+        Edge next;  // the group's next P entries, loaded while these are used
+        next.idx = 0;
+        next.w = 0.0f;
+        if (base + P + k < cnt) next = fan[eb + base + P + k];
+        const int full = lo - base;
+        narrow_batch<V, kPattern, 0>(mine, full, base, cnt, yl, pitch, acc, hit);
+        if (hi - base > kNarrowUnroll)
+            narrow_batch<V, kPattern, kNarrowUnroll>(mine, full, base, cnt, yl, pitch, acc, hit);
+        mine = next;
+    }
+    if (!active) return;
+    const double bj = (double)bias[j];
+    float out[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+        out[v] = (kPattern && (hit[v] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[v] + bj, ymax);
+    store_v<V>(zt + j * ld + col, out);
 }
 
 // High fan-in variant: the same product with the gathered rows of Y^T served from LDS and each row read once
@@ -187,7 +331,7 @@ __host__ __device__ inline int64_t mask_pitch(int64_t n) { return (n + 63) / 64 
 
 template <bool kPattern>
 __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
-    int64_t n, int64_t batch, int chunks, int ntiles, const int64_t *__restrict__ fan_ptr,
+    int64_t n, int64_t batch, int64_t ld, int chunks, int ntiles, const int64_t *__restrict__ fan_ptr,
     const uint16_t *__restrict__ tile_mask, const Edge *__restrict__ fan, const float *__restrict__ bias,
     double ymax, const float *__restrict__ yt, float *__restrict__ zt) {
     __shared__ double2 slab[kTileRows * kRowD2];
@@ -221,7 +365,7 @@ __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
         for (int s = 0; s < kStageF4; ++s) {
             const int q = s * kTiledThreads + tid;
             const int64_t gi = i0 + q / kRowF4, gc = col0 + (int64_t)(q % kRowF4) * 4;
-            st[s] = (gi < n && gc < batch) ? *reinterpret_cast<const float4 *>(yt + gi * batch + gc)
+            st[s] = (gi < n && gc < batch) ? *reinterpret_cast<const float4 *>(yt + gi * ld + gc)
                                            : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     };
@@ -320,7 +464,7 @@ __global__ __launch_bounds__(kTiledThreads, 3) void spmm_tiled_kernel(
 #pragma unroll
         for (int v = 0; v < 4; ++v)
             f[v] = (kPattern && (hit[q][v] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[q][v] + bj, ymax);
-        if (ca < batch) *reinterpret_cast<float4 *>(zt + j * batch + ca) = make_float4(f[0], f[1], f[2], f[3]);
+        if (ca < batch) *reinterpret_cast<float4 *>(zt + j * ld + ca) = make_float4(f[0], f[1], f[2], f[3]);
     }
 }
 
@@ -350,7 +494,7 @@ static_assert(kSlotNJ == 64, "mask_pitch() rounds n to whole workgroups");
 
 template <bool kPattern>
 __global__ __launch_bounds__(kSlotThreads, 1) void spmm_slots_kernel(
-    int64_t n, int64_t batch, int chunks, int ntiles, const uint16_t *__restrict__ tile_mask,
+    int64_t n, int64_t batch, int64_t ld, int chunks, int ntiles, const uint16_t *__restrict__ tile_mask,
     const double *__restrict__ slots, const float *__restrict__ bias, double ymax, const float *__restrict__ yt,
     float *__restrict__ zt) {
     __shared__ double2 slab[2][kTileRows * kRowD2];
@@ -381,7 +525,7 @@ __global__ __launch_bounds__(kSlotThreads, 1) void spmm_slots_kernel(
     float4 st;
     auto load_slab = [&](int t) {
         const int64_t gi = (int64_t)t * kTileRows + srow;
-        st = (gi < n && sgc < batch) ? *reinterpret_cast<const float4 *>(yt + gi * batch + sgc)
+        st = (gi < n && sgc < batch) ? *reinterpret_cast<const float4 *>(yt + gi * ld + sgc)
                                      : make_float4(0.f, 0.f, 0.f, 0.f);
     };
     auto stage = [&](int buf) {
@@ -504,7 +648,7 @@ __global__ __launch_bounds__(kSlotThreads, 1) void spmm_slots_kernel(
 #pragma unroll
         for (int v = 0; v < 4; ++v)
             f[v] = (kPattern && (hit[q][v] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[q][v] + bj, ymax);
-        if (ca < batch) *reinterpret_cast<float4 *>(zt + j * batch + ca) = make_float4(f[0], f[1], f[2], f[3]);
+        if (ca < batch) *reinterpret_cast<float4 *>(zt + j * ld + ca) = make_float4(f[0], f[1], f[2], f[3]);
     }
 }
 
@@ -547,8 +691,9 @@ __global__ void tile_mask_kernel(int64_t n, const int64_t *__restrict__ fan_ptr,
 // against 16 tiles and 6.8 us at 64 x 64), while 64 x 64 tiles read whole 256-byte row segments and move a
 // 34 GB matrix in 16.2 ms instead of 18.1.
 template <int T>
-__global__ __launch_bounds__(256) void transpose_kernel(const float *__restrict__ in, float *__restrict__ out,
-                                                        int64_t rows, int64_t cols, int64_t col_tiles) {
+__global__ __launch_bounds__(256) void transpose_kernel(const float *__restrict__ in, int64_t in_ld,
+                                                        float *__restrict__ out, int64_t out_ld, int64_t rows,
+                                                        int64_t cols, int64_t col_tiles) {
     __shared__ float tile[T][T + 1];
     constexpr int kStep = 256 / T;
     const int64_t r0 = (int64_t)(blockIdx.x / col_tiles) * T, c0 = (int64_t)(blockIdx.x % col_tiles) * T;
@@ -556,27 +701,29 @@ __global__ __launch_bounds__(256) void transpose_kernel(const float *__restrict_
 #pragma unroll
     for (int rr = ty; rr < T; rr += kStep) {
         const int64_t r = r0 + rr, c = c0 + tx;
-        if (r < rows && c < cols) tile[rr][tx] = in[r * cols + c];
+        if (r < rows && c < cols) tile[rr][tx] = in[r * in_ld + c];
     }
     __syncthreads();
 #pragma unroll
     for (int cc = ty; cc < T; cc += kStep) {
         const int64_t c = c0 + cc, r = r0 + tx;
-        if (r < rows && c < cols) out[c * rows + r] = tile[tx][cc];
+        if (r < rows && c < cols) out[c * out_ld + r] = tile[tx][cc];
     }
 }
 
 }  // namespace
 
-hipError_t launch_transpose(const float *in, float *out, int64_t rows, int64_t cols, hipStream_t s) {
+hipError_t launch_transpose(const float *in, int64_t in_ld, float *out, int64_t out_ld, int64_t rows, int64_t cols,
+                            hipStream_t s) {
     if (rows == 0 || cols == 0) return hipSuccess;
+    if (in_ld < cols || out_ld < rows) return hipErrorInvalidValue;
     const int T = rows * cols <= (int64_t(1) << 24) ? 32 : 64;
     const int64_t ct = (cols + T - 1) / T, rt = (rows + T - 1) / T;
     if (rt * ct > 0x7fffffffLL) return hipErrorInvalidValue;
     if (T == 32)
-        transpose_kernel<32><<<(unsigned)(rt * ct), 256, 0, s>>>(in, out, rows, cols, ct);
+        transpose_kernel<32><<<(unsigned)(rt * ct), 256, 0, s>>>(in, in_ld, out, out_ld, rows, cols, ct);
     else
-        transpose_kernel<64><<<(unsigned)(rt * ct), 256, 0, s>>>(in, out, rows, cols, ct);
+        transpose_kernel<64><<<(unsigned)(rt * ct), 256, 0, s>>>(in, in_ld, out, out_ld, rows, cols, ct);
     return hipGetLastError();
 }
 
@@ -617,7 +764,7 @@ hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *
     return hipGetLastError();
 }
 
-hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, const Edge *fan,
+hipError_t launch_spmm_fanin(int64_t n, int64_t batch, int64_t ld, const int64_t *fan_ptr, const Edge *fan,
                              const uint16_t *tile_mask, const double *slots, const float *bias, double ymax, int pattern,
                              const float *yt, float *zt, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
@@ -628,10 +775,10 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, c
         if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
         if (pattern)
             spmm_slots_kernel<true><<<(unsigned)blocks, kSlotThreads, 0, s>>>(
-                n, batch, (int)chunks, spmm_tile_count(n), tile_mask, slots, bias, ymax, yt, zt);
+                n, batch, ld, (int)chunks, spmm_tile_count(n), tile_mask, slots, bias, ymax, yt, zt);
         else
             spmm_slots_kernel<false><<<(unsigned)blocks, kSlotThreads, 0, s>>>(
-                n, batch, (int)chunks, spmm_tile_count(n), tile_mask, slots, bias, ymax, yt, zt);
+                n, batch, ld, (int)chunks, spmm_tile_count(n), tile_mask, slots, bias, ymax, yt, zt);
         return hipGetLastError();
     }
     if (tile_mask && batch % 4 == 0 && batch >= 128) {
@@ -641,11 +788,35 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, c
         if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
         if (pattern)
             spmm_tiled_kernel<true><<<(unsigned)blocks, kTiledThreads, 0, s>>>(
-                n, batch, (int)chunks, spmm_tile_count(n), fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
+                n, batch, ld, (int)chunks, spmm_tile_count(n), fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
         else
             spmm_tiled_kernel<false><<<(unsigned)blocks, kTiledThreads, 0, s>>>(
-                n, batch, (int)chunks, spmm_tile_count(n), fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
+                n, batch, ld, (int)chunks, spmm_tile_count(n), fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
         return hipGetLastError();
+    }
+    // wide layers whose 64-column slice of Y^T (n x 256 bytes) fits an XCD's 4 MiB L2, with a batch of whole
+    // 16-byte lane loads: the narrow-chunk gather (measured on MI355X at n = 16384, batch 4096: 0.58 ms per
+    // layer against 0.93 for the kernel below; at n = 2^20, where neither slice fits, the kernel below is
+    // slightly faster: 957 against 990 ms per very wide forward)
+    if (n > 4096 && n <= 16384 && batch % 4 == 0 && ld * 4 < (1 << 24)) {
+        constexpr int V = 4;
+        const int64_t chunks = (batch + kNarrowP * V - 1) / (kNarrowP * V);
+        const int64_t groups = (n + 4 * (64 / kNarrowP) - 1) / (4 * (64 / kNarrowP));  // 16 neurons per workgroup
+        const int64_t gpx = (groups + 7) / 8;  // per XCD
+        const int64_t blocks = 8 * gpx * chunks;
+        constexpr int64_t kSeg = 1ll << 23;  // a multiple of 8: a segment keeps every block's XCD
+        for (int64_t base = 0; base < blocks; base += kSeg) {
+            const unsigned nb = (unsigned)(blocks - base < kSeg ? blocks - base : kSeg);
+            if (pattern)
+                spmm_narrow_kernel<V, true><<<nb, 256, 0, s>>>(n, batch, ld, gpx, base, fan_ptr, fan, bias, ymax,
+                                                                  yt, zt);
+            else
+                spmm_narrow_kernel<V, false><<<nb, 256, 0, s>>>(n, batch, ld, gpx, base, fan_ptr, fan, bias, ymax,
+                                                                   yt, zt);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
     }
     // Columns per lane: wide enough to keep 8 independent loads in flight, and a multiple that divides batch.
     // Columns per lane: four (one 16-byte load per lane, a 1 KiB row segment per wave) whenever the batch
@@ -665,7 +836,8 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, const int64_t *fan_ptr, c
     for (int64_t base = 0; base < blocks; base += kSeg) {
         const unsigned nb = (unsigned)(blocks - base < kSeg ? blocks - base : kSeg);
 #define SDNN_GATHER(VV, PP) \
-    spmm_fanin_kernel<VV, PP><<<nb, 256, 0, s>>>(n, batch, (int)chunks, base, fan_ptr, fan, bias, ymax, yt, zt)
+    spmm_fanin_kernel<VV, PP><<<nb, 256, 0, s>>>(n, batch, ld, (int)chunks, base, fan_ptr, fan, bias, ymax, yt, \
+                                                 zt)
         switch (V * 2 + (pattern ? 1 : 0)) {
             case 8: SDNN_GATHER(4, false); break;
             case 9: SDNN_GATHER(4, true); break;

@@ -116,3 +116,8 @@ def test_kernel_name_matches_the_selection_rule():
     assert bench.spmm_kernel_name(n, 81161012) == "spmm_tiled_kernel"
     assert bench.spmm_kernel_name(n, 81161011) == "spmm_fanin_kernel"
     assert bench.spmm_kernel_name(65537, 65537 ** 2) == "spmm_fanin_kernel"
+    # wide layers up to n = 16384 with whole 16-byte lane loads: the narrow-chunk gather
+    assert bench.spmm_kernel_name(16384, 524288, 4096) == "spmm_narrow_kernel"
+    assert bench.spmm_kernel_name(4097, 10 ** 5, 302) == "spmm_fanin_kernel"
+    assert bench.spmm_kernel_name(16385, 524288, 4096) == "spmm_fanin_kernel"
+    assert bench.spmm_kernel_name(4096, 3728271, 130) == "spmm_fanin_kernel"  # the tiled kernels need 4 | batch

@@ -216,8 +216,8 @@ def test_semiring_mxm_csr(sd, name):
 
 
 def test_gather_grid_larger_than_one_launch(sd):
-    """n = 2^20 and batch 4098 (two columns per lane, 33 chunks) need 8.65M workgroups: more than one
-    launch holds, so the gather runs in segments.  Y is drawn on the device from a seeded generator and
+    """n = 2^20 and batch 4098 (the narrow-chunk gather: 129 chunks of 32 columns, 8.45M workgroups) need
+    more than one launch holds, so the gather runs in segments.  Y is drawn on the device from a seeded generator and
     the sampled rows are handed to the oracle; 68 GB of device memory."""
     import torch
 
@@ -244,6 +244,43 @@ def test_gather_grid_larger_than_one_launch(sd):
     from workloads import Problem
     p = Problem("segmented", n, 1, len(rows), math.inf, [layer], y0_dense=y_rows)
     parity.compare(p, dense_to_csr(got))
+
+
+def _mixed_length_layer(rng, n, lengths):
+    """W whose output neuron j gathers lengths[j % len(lengths)] distinct inputs (so the four neurons of a
+    wave have very different list lengths); returns the Layer in its input-major CSR form."""
+    ii, jj = [], []
+    for j in range(n):
+        k = min(lengths[j % len(lengths)], n)
+        ii.append(rng.choice(n, size=k, replace=False))
+        jj.append(np.full(k, j))
+    i = np.concatenate(ii).astype(np.int64)
+    j = np.concatenate(jj).astype(np.int64)
+    order = np.lexsort((j, i))
+    i, j = i[order], j[order]
+    row_ptr = np.zeros(n + 1, np.int64)
+    np.add.at(row_ptr, i + 1, 1)
+    return Layer(np.cumsum(row_ptr), j.astype(np.int32), rng.uniform(-1, 1, size=len(i)).astype(np.float32),
+                 rng.uniform(-0.3, 0.3, size=n).astype(np.float32))
+
+
+@pytest.mark.parametrize("seed,n,batch,lengths,bias_mode", [
+    (81, 4097, 34, [0, 1, 15, 16, 17, 40, 100], 0), (82, 5003, 96, [3, 0, 0, 33, 8, 9, 64, 1], 0),
+    (83, 6144, 130, [16, 16, 16, 16, 32, 31, 48, 7], 1), (84, 4099, 2, [120, 0, 5, 17], 1),
+    (85, 4500, 300, [2, 30, 31, 33, 0, 64], 0), (86, 16384, 512, [32, 25, 40, 32], 1)])
+def test_narrow_chunk_gather(sd, seed, n, batch, lengths, bias_mode):
+    """Wide layers (n > 4096) with an even batch take the narrow-chunk gather (16 lanes and 32 columns per
+    neuron): ragged n and batch, and list lengths from 0 to 120 side by side in one wave, which exercises
+    the unpredicated prefix, the guarded tail and lists spanning several loads of 16 entries."""
+    rng = np.random.default_rng(seed)
+    layers = [_mixed_length_layer(rng, n, lengths), _mixed_length_layer(rng, n, lengths[::-1])]
+    y = rng.random((batch, n), dtype=np.float32)
+    y[rng.random((batch, n)) < 0.3] = 0.0
+    from workloads import Problem
+    p = Problem(f"narrow-{seed}", n, 2, batch, math.inf, layers, y0_dense=y)
+    _say("narrow gather", seed, n, batch, bias_mode)
+    parity.compare(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE, bias_mode=bias_mode)),
+                   bias_mode=bias_mode)
 
 
 def test_long_fanin_lists(sd):
@@ -278,6 +315,54 @@ def test_integer_shadows_bit_exact(sd, cfg, kw):
         for arm in ARMS:
             parity.compare(p, dense_to_csr(run_dense(sd, p, _arm(sd, arm))), exact=True)
     parity.compare(p, run_csr(sd, p), exact=True)
+
+
+# --------------------------------------------------------------- padded row pitch of the activations
+
+# n > 4096 and batch >= 256: the neuron-major activations sit at a padded row pitch (batch 256 -> 320 floats,
+# 300 -> 320), so every kernel that reads or writes them indexes rows by the pitch, not by the batch.
+@pytest.mark.parametrize("case", ["gather", "slots", "dense_arm", "csr_switch"])
+@pytest.mark.parametrize("batch", [256, 300])
+def test_padded_pitch_every_kernel(sd, case, batch):
+    """The narrow-chunk gather, the scalar-register SpMM (density >= 2/9), the dense-W arm (K split, then the
+    split sum) and the CSR path's switch to dense activations (densify, gather, transpose and compaction) at a
+    padded pitch, ragged in n and batch."""
+    n = 4500
+    d = {"gather": 0.01, "slots": 0.3, "dense_arm": 0.05, "csr_switch": 0.02}[case]
+    if case == "csr_switch":
+        p = tiny_random(90, n, 3, batch, w_density=d, y_density=0.3, bias_lo=0.0, bias_hi=0.2)
+        _say("padded pitch", case, batch)
+        parity.compare(p, run_csr(sd, p))
+        return
+    p = tiny_random(91, n, 2, batch, w_density=d, y_density=0.6, dense_input=True, bias_lo=-0.3, bias_hi=0.3)
+    if case == "slots":
+        assert 9 * p.layers[0].nnz >= 2 * n * n
+    arm = sd.SDNN_ARM_DENSE if case == "dense_arm" else sd.SDNN_ARM_SPARSE
+    rows = np.arange(0, batch, 7)
+    _say("padded pitch", case, batch)
+    out = run_dense(sd, p, arm)
+    parity.compare(p, dense_to_csr(out[rows]), rows=rows)
+
+
+@pytest.mark.parametrize("name", ["plus_times", "max_min"])
+def test_semiring_mxm_padded_pitch(sd, name):
+    """Semiring products at a padded activation pitch (n 4500, batch 260 -> 320), dense and CSR input."""
+    import oracle
+    import torch
+
+    n, batch = 4500, 260
+    p = tiny_random(92, n, 1, batch, w_density=0.004, dense_input=True, y_density=0.5)
+    net = sd.net_from_problem(p)
+    _say("semiring padded", name)
+    got = net.mxm(0, oracle.SEMIRINGS[name], torch.from_numpy(p.y0_dense).cuda()).cpu().numpy()
+    assert got.tobytes() == oracle.mxm(name, n, p.layers[0], p.y0_dense).tobytes()
+    zero = {"max_min": -math.inf}.get(name, 0.0)
+    rp, c, v = dense_to_csr(p.y0_dense)
+    yd = np.full((batch, n), zero, np.float32)
+    yd[np.repeat(np.arange(batch), np.diff(rp)), c] = v
+    got = net.mxm_csr(0, oracle.SEMIRINGS[name], rp, c, v).cpu().numpy()
+    net.free()
+    assert got.tobytes() == oracle.mxm(name, n, p.layers[0], yd).tobytes()
 
 
 # ------------------------------------------------------------------------------------------ the workloads
