@@ -508,9 +508,13 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         // two n x batch fp32 buffers at row pitch ld
         float *dense[2] = {reinterpret_cast<float *>(w.col[db]), w.val[db]};
         const int64_t ld = sdnn::act_ld(n, batch);
+        // dense[1] is free until the first layer: it stages the rows batch-major when they hold at least a
+        // quarter of batch * n entries (measured on MI355X: 0.34 instead of 0.69 ms for 32M entries into
+        // 16384 x 4096; at 2% density the extra transpose costs more than the scattered stores it saves)
+        float *stage = nnz_hi >= (double)batch * (double)n / 4.0 ? dense[1] : nullptr;
         SDNN_HIP(sdnn::launch_densify(n, batch, ld, from_user ? y_row_ptr : nullptr, from_user ? nullptr : w.cnt[cur ^ 1],
                                       from_user ? y_col : w.col[cur ^ 1], from_user ? y_val : w.val[cur ^ 1],
-                                      dense[0], net->d_flags, s));
+                                      dense[0], stage, net->d_flags, s));
         int dc = 0;
         for (int32_t k = kd; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];

@@ -99,8 +99,10 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
                                const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
                                int pattern, double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val,
                                int32_t *lists, unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s);
+// Y^T (n x batch at row pitch ld) from sparse rows; tmp (batch x n floats, may be null) stages them batch-major.
 hipError_t launch_densify(int64_t n, int64_t batch, int64_t ld, const int64_t *in_row_ptr, const int32_t *in_cnt,
-                          const int32_t *in_col, const float *in_val, float *yt, uint32_t *err, hipStream_t s);
+                          const int32_t *in_col, const float *in_val, float *yt, float *tmp, uint32_t *err,
+                          hipStream_t s);
 hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,
                                  float *out_val, hipStream_t s);
 hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, const int64_t *row_ptr,

@@ -599,11 +599,10 @@ __global__ __launch_bounds__(256) void compact_rows_kernel(int64_t n, const int3
     }
 }
 
-// Dense activations from a batch of sparse rows: yt (n x batch at row pitch ld, neuron-major, zero-filled by the
-// caller)
-// receives every stored entry.  Input is either caller CSR (row extents checked as in the SpGEMM) or
-// slot rows written by a previous layer.
-__global__ __launch_bounds__(256) void densify_kernel(int64_t n, int64_t batch, int64_t ld,
+// Dense activations from a batch of sparse rows: element (r, i) of y (zero-filled by the caller) is at
+// r * rs + i * cs and receives every stored entry.  Input is either caller CSR (row extents checked as in the
+// SpGEMM) or slot rows written by a previous layer.
+__global__ __launch_bounds__(256) void densify_kernel(int64_t n, int64_t batch, int64_t rs, int64_t cs,
                                                       const int64_t *__restrict__ in_row_ptr,
                                                       const int32_t *__restrict__ in_cnt,
                                                       const int32_t *__restrict__ in_col,
@@ -629,7 +628,7 @@ __global__ __launch_bounds__(256) void densify_kernel(int64_t n, int64_t batch, 
             atomicOr(err, 1u);
             continue;
         }
-        yt[(int64_t)i * ld + r] = in_val[yb + t];
+        yt[r * rs + (int64_t)i * cs] = in_val[yb + t];
     }
 }
 
@@ -667,6 +666,51 @@ __global__ __launch_bounds__(kSlotThreads) void dense_to_slots_kernel(int64_t n,
             out_col[ob + written + off + pre] = (int32_t)j;
             out_val[ob + written + off + pre] = f;
         }
+        written += tot;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out_cnt[r] = (int32_t)written;
+}
+
+// The same with four consecutive columns per thread (one 16-byte load; rows 16-byte aligned, n % 4 == 0): a
+// lane's survivor count (0-4) is scanned across the wave by three bit-sliced ballots, so an iteration covers
+// 4096 columns with the same two barriers.
+__global__ __launch_bounds__(kSlotThreads) void dense_to_slots4_kernel(int64_t n, const float *__restrict__ y,
+                                                                   int32_t *__restrict__ out_cnt,
+                                                                   int32_t *__restrict__ out_col,
+                                                                   float *__restrict__ out_val) {
+    __shared__ int wave_tot[kSlotWaves];
+    const int64_t r = blockIdx.x;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float4 *row = reinterpret_cast<const float4 *>(y + r * n);
+    const int64_t ob = r * n, n4 = n / 4;
+    int64_t written = 0;
+    for (int64_t base = 0; base < n4; base += kSlotThreads) {
+        const int64_t q = base + threadIdx.x;
+        const float4 f = q < n4 ? row[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float v[4] = {f.x, f.y, f.z, f.w};
+        int c = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) c += v[e] != 0.0f ? 1 : 0;
+        const uint64_t b0 = __ballot(c & 1), b1 = __ballot(c & 2), b2 = __ballot(c & 4);
+        const int pre = lane_rank(b0) + 2 * lane_rank(b1) + 4 * lane_rank(b2);
+        if (lane == 0) wave_tot[wave] = __popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2);
+        __syncthreads();
+        int off = 0, tot = 0;
+#pragma unroll
+        for (int u = 0; u < kSlotWaves; ++u) {
+            const int t = wave_tot[u];
+            off += (u < wave) ? t : 0;
+            tot += t;
+        }
+        int64_t o = ob + written + off + pre;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (v[e] != 0.0f) {
+                out_col[o] = (int32_t)(4 * q + e);
+                out_val[o] = v[e];
+                ++o;
+            }
         written += tot;
         __syncthreads();
     }
@@ -760,18 +804,32 @@ hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, con
 }
 
 hipError_t launch_densify(int64_t n, int64_t batch, int64_t ld, const int64_t *in_row_ptr, const int32_t *in_cnt,
-                          const int32_t *in_col, const float *in_val, float *yt, uint32_t *err, hipStream_t s) {
+                          const int32_t *in_col, const float *in_val, float *yt, float *tmp, uint32_t *err,
+                          hipStream_t s) {
     if (batch == 0) return hipSuccess;
-    hipError_t e = hipMemsetAsync(yt, 0, (size_t)n * (size_t)ld * sizeof(float), s);
+    if (!tmp) {
+        hipError_t e = hipMemsetAsync(yt, 0, (size_t)n * (size_t)ld * sizeof(float), s);
+        if (e != hipSuccess) return e;
+        densify_kernel<<<(unsigned)batch, 256, 0, s>>>(n, batch, 1, ld, in_row_ptr, in_cnt, in_col, in_val, yt, err);
+        return hipGetLastError();
+    }
+    // batch-major first (a sample's entries land in one contiguous row, so its stores coalesce; scattered
+    // straight into Y^T every 4-byte store hits another row), then one tiled transpose
+    hipError_t e = hipMemsetAsync(tmp, 0, (size_t)n * (size_t)batch * sizeof(float), s);
     if (e != hipSuccess) return e;
-    densify_kernel<<<(unsigned)batch, 256, 0, s>>>(n, batch, ld, in_row_ptr, in_cnt, in_col, in_val, yt, err);
-    return hipGetLastError();
+    densify_kernel<<<(unsigned)batch, 256, 0, s>>>(n, batch, n, 1, in_row_ptr, in_cnt, in_col, in_val, tmp, err);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_transpose(tmp, n, yt, ld, batch, n, s);
 }
 
 hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,
                                  float *out_val, hipStream_t s) {
     if (batch == 0) return hipSuccess;
-    dense_to_slots_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, out_cnt, out_col, out_val);
+    if (n % 4 == 0)
+        dense_to_slots4_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, out_cnt, out_col, out_val);
+    else
+        dense_to_slots_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, out_cnt, out_col, out_val);
     return hipGetLastError();
 }
 

@@ -402,10 +402,12 @@ def test_config2_dense_arm_sampled(sd, d):
     parity.compare(p, dense_to_csr(out[rows]), rows=rows)
 
 
+@pytest.mark.parametrize("n", [700, 701])
 @pytest.mark.parametrize("sparse_layers", [0, 1, 2, 3])
-def test_csr_path_switches_to_dense_activations(sd, sparse_layers):
-    """Layers with mostly positive bias move the CSR path to dense activations; switch after 0..3 layers."""
-    p = tiny_random(40 + sparse_layers, 700, 4, 37, w_density=0.02, y_density=0.05, bias_lo=-0.2, bias_hi=0.0)
+def test_csr_path_switches_to_dense_activations(sd, sparse_layers, n):
+    """Layers with mostly positive bias move the CSR path to dense activations; switch after 0..3 layers
+    (the exit compaction with four columns per thread when 4 | n, one otherwise)."""
+    p = tiny_random(40 + sparse_layers, n, 4, 37, w_density=0.02, y_density=0.05, bias_lo=-0.2, bias_hi=0.0)
     for k in range(sparse_layers, p.L):
         p.layers[k].bias = np.full(p.n, 0.02, np.float32)
     _say("format switch", sparse_layers)
