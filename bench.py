@@ -551,7 +551,7 @@ def main():
         summarize_pmc(a[0], a[1], a[2:6], int(a[6]), a[7].split("|"), a[8], ["spmm.hip", "common.h"])
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (batch rows would shard "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path (batch rows would shard "
               "across GPUs with no per-layer exchange; see the design notes). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 

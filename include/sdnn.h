@@ -57,7 +57,7 @@ typedef enum {
     SDNN_ERR_WORKSPACE_TOO_SMALL = 6,/* ws_bytes below sdnn_workspace_size() */
     SDNN_ERR_OUT_OF_MEMORY = 7,      /* device allocation by the library failed */
     SDNN_ERR_DEVICE = 8,             /* a HIP call failed; detail in sdnn_last_error() */
-    SDNN_ERR_UNSUPPORTED = 9         /* a size this build does not handle (see the message) */
+    SDNN_ERR_UNSUPPORTED = 9         /* a size the library does not handle (see the message) */
 } sdnn_status;
 
 /* Which product a dense-Y forward uses for Y_k W_k. */
