@@ -501,7 +501,8 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         nnz_hi = (l.bias_nonpos || net->bias_pattern) ? std::min(full, nnz_hi * (double)l.max_fanout) : full;
         exact = false;
     }
-    int last, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
+    int last = 0, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
+    bool packed = false;  // the CSR is already in buffer outb
     if (kd < k1) {
         const bool from_user = kd == k0;
         const int db = from_user ? 0 : cur;  // the input rows (if any) sit in buffer cur ^ 1
@@ -523,16 +524,27 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
             dc ^= 1;
         }
         SDNN_HIP(sdnn::launch_transpose(dense[dc], ld, dense[dc ^ 1], n, n, batch, s));  // -> batch x n
-        SDNN_HIP(sdnn::launch_dense_to_slots(n, batch, dense[dc ^ 1], w.cnt[db ^ 1], w.col[db ^ 1], w.val[db ^ 1], s));
-        last = db ^ 1;
-        outb = db;
+        if (n % 4 == 0) {
+            // counted first, then packed straight into the other buffer pair (no slot rows in between)
+            SDNN_HIP(sdnn::launch_dense_to_csr(n, batch, dense[dc ^ 1], w.cnt[db ^ 1], out_row_ptr, w.scan_tmp,
+                                               w.col[db ^ 1], w.val[db ^ 1], s));
+            packed = true;
+            outb = db ^ 1;
+        } else {
+            SDNN_HIP(sdnn::launch_dense_to_slots(n, batch, dense[dc ^ 1], w.cnt[db ^ 1], w.col[db ^ 1],
+                                                 w.val[db ^ 1], s));
+            last = db ^ 1;
+            outb = db;
+        }
     } else {
         last = cur ^ 1;
         outb = cur;
     }
-    SDNN_HIP(sdnn::launch_exclusive_scan_i32_to_i64(batch, w.cnt[last], out_row_ptr, w.scan_tmp, s));
-    SDNN_HIP(sdnn::launch_compact_rows(n, batch, w.cnt[last], out_row_ptr, w.col[last], w.val[last], w.col[outb],
-                                       w.val[outb], s));
+    if (!packed) {
+        SDNN_HIP(sdnn::launch_exclusive_scan_i32_to_i64(batch, w.cnt[last], out_row_ptr, w.scan_tmp, s));
+        SDNN_HIP(sdnn::launch_compact_rows(n, batch, w.cnt[last], out_row_ptr, w.col[last], w.val[last],
+                                           w.col[outb], w.val[outb], s));
+    }
     int64_t nnz = 0;
     uint32_t flags = 0;
     SDNN_HIP(hipMemcpyAsync(&nnz, out_row_ptr + batch, sizeof(int64_t), hipMemcpyDeviceToHost, s));

@@ -105,6 +105,10 @@ hipError_t launch_densify(int64_t n, int64_t batch, int64_t ld, const int64_t *i
                           hipStream_t s);
 hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,
                                  float *out_val, hipStream_t s);
+// Dense batch-major rows (n % 4 == 0) straight to CSR: counts, their exclusive scan into row_ptr[batch + 1],
+// then the survivors of each row at row_ptr[r] in column order.
+hipError_t launch_dense_to_csr(int64_t n, int64_t batch, const float *y, int32_t *cnt, int64_t *row_ptr,
+                               int64_t *scan_tmp, int32_t *out_col, float *out_val, hipStream_t s);
 hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, const int64_t *row_ptr,
                                const int32_t *in_col, const float *in_val, int32_t *out_col, float *out_val,
                                hipStream_t s);

@@ -674,8 +674,10 @@ __global__ __launch_bounds__(kSlotThreads) void dense_to_slots_kernel(int64_t n,
 
 // The same with four consecutive columns per thread (one 16-byte load; rows 16-byte aligned, n % 4 == 0): a
 // lane's survivor count (0-4) is scanned across the wave by three bit-sliced ballots, so an iteration covers
-// 4096 columns with the same two barriers.
+// 4096 columns with the same two barriers.  Row r's survivors go to [row_off[r], ...) when row_off is given
+// (rows packed back to back: the final CSR), else to [r*n, ...).
 __global__ __launch_bounds__(kSlotThreads) void dense_to_slots4_kernel(int64_t n, const float *__restrict__ y,
+                                                                   const int64_t *__restrict__ row_off,
                                                                    int32_t *__restrict__ out_cnt,
                                                                    int32_t *__restrict__ out_col,
                                                                    float *__restrict__ out_val) {
@@ -683,7 +685,7 @@ __global__ __launch_bounds__(kSlotThreads) void dense_to_slots4_kernel(int64_t n
     const int64_t r = blockIdx.x;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const float4 *row = reinterpret_cast<const float4 *>(y + r * n);
-    const int64_t ob = r * n, n4 = n / 4;
+    const int64_t ob = row_off ? row_off[r] : r * n, n4 = n / 4;
     int64_t written = 0;
     for (int64_t base = 0; base < n4; base += kSlotThreads) {
         const int64_t q = base + threadIdx.x;
@@ -715,6 +717,30 @@ __global__ __launch_bounds__(kSlotThreads) void dense_to_slots4_kernel(int64_t n
         __syncthreads();
     }
     if (threadIdx.x == 0) out_cnt[r] = (int32_t)written;
+}
+
+// Nonzeros of each dense batch-major row (n % 4 == 0), for packing the rows straight into CSR.
+__global__ __launch_bounds__(kSlotThreads) void dense_count4_kernel(int64_t n, const float *__restrict__ y,
+                                                                int32_t *__restrict__ cnt) {
+    __shared__ int wave_tot[kSlotWaves];
+    const int64_t r = blockIdx.x;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float4 *row = reinterpret_cast<const float4 *>(y + r * n);
+    int c = 0;
+    for (int64_t q = threadIdx.x; q < n / 4; q += kSlotThreads) {
+        const float4 f = row[q];
+        c += (f.x != 0.0f ? 1 : 0) + (f.y != 0.0f ? 1 : 0) + (f.z != 0.0f ? 1 : 0) + (f.w != 0.0f ? 1 : 0);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+    if (lane == 0) wave_tot[wave] = c;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int t = 0;
+#pragma unroll
+        for (int u = 0; u < kSlotWaves; ++u) t += wave_tot[u];
+        cnt[r] = t;
+    }
 }
 
 }  // namespace
@@ -823,11 +849,23 @@ hipError_t launch_densify(int64_t n, int64_t batch, int64_t ld, const int64_t *i
     return launch_transpose(tmp, n, yt, ld, batch, n, s);
 }
 
+hipError_t launch_dense_to_csr(int64_t n, int64_t batch, const float *y, int32_t *cnt, int64_t *row_ptr,
+                               int64_t *scan_tmp, int32_t *out_col, float *out_val, hipStream_t s) {
+    if (batch == 0 || n % 4 != 0) return hipErrorInvalidValue;
+    dense_count4_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, cnt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_exclusive_scan_i32_to_i64(batch, cnt, row_ptr, scan_tmp, s);
+    if (e != hipSuccess) return e;
+    dense_to_slots4_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, row_ptr, cnt, out_col, out_val);
+    return hipGetLastError();
+}
+
 hipError_t launch_dense_to_slots(int64_t n, int64_t batch, const float *y, int32_t *out_cnt, int32_t *out_col,
                                  float *out_val, hipStream_t s) {
     if (batch == 0) return hipSuccess;
     if (n % 4 == 0)
-        dense_to_slots4_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, out_cnt, out_col, out_val);
+        dense_to_slots4_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, nullptr, out_cnt, out_col, out_val);
     else
         dense_to_slots_kernel<<<(unsigned)batch, kSlotThreads, 0, s>>>(n, y, out_cnt, out_col, out_val);
     return hipGetLastError();
