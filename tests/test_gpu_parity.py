@@ -475,15 +475,19 @@ def test_identity_input_reads_back_weights(sd):
     assert got.tobytes() == want.tobytes()
 
 
-@pytest.mark.parametrize("layers", ["gather", "slots"])
+@pytest.mark.parametrize("layers", ["gather", "slots", "narrow"])
 def test_graph_replay_matches_eager(sd, layers):
     """A HIP graph of forward_dense replays the eager result bit for bit, replay after replay, with new inputs
     written into the bound input and unrelated eager work between the replays (both arms); the layers take the
-    gather SpMM (tiny MLP recipe) or the scalar-register LDS-tiled SpMM (d = 0.5)."""
+    gather SpMM (tiny MLP recipe), the scalar-register LDS-tiled SpMM (d = 0.5) or the narrow-chunk gather at
+    a padded activation pitch (n 4200, batch 256 -> 320)."""
     import torch
 
     if layers == "gather":
         p = make_config(1, n=1000, L=3, batch=132)
+    elif layers == "narrow":
+        p = tiny_random(46, 4200, 2, 256, w_density=0.008, y_density=0.6, dense_input=True, bias_lo=-0.3,
+                        bias_hi=0.3)
     else:
         p = tiny_random(45, 1300, 2, 128, w_density=0.5, y_density=0.7, dense_input=True, bias_lo=-1.0,
                         bias_hi=1.0)
