@@ -118,7 +118,7 @@ def spmm_kernel_name(n, nnz, batch=1024):
                 return "spmm_slots_kernel"
         elif 10 * nnz >= 3 * n * n:
             return "spmm_tiled_kernel"
-    if 4096 < n <= 16384 and batch % 4 == 0:
+    if (4096 < n <= 16384 or (batch < 256 and 4096 <= n)) and batch % 4 == 0:
         return "spmm_narrow_kernel"
     return "spmm_fanin_kernel"
 

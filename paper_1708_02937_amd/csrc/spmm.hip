@@ -794,11 +794,15 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, int64_t ld, const int64_t
                 n, batch, ld, (int)chunks, spmm_tile_count(n), fan_ptr, tile_mask, fan, bias, ymax, yt, zt);
         return hipGetLastError();
     }
-    // wide layers whose 64-column slice of Y^T (n x 256 bytes) fits an XCD's 4 MiB L2, with a batch of whole
-    // 16-byte lane loads: the narrow-chunk gather (measured on MI355X at n = 16384, batch 4096: 0.58 ms per
+    // The narrow-chunk gather, for a batch of whole 16-byte lane loads: on wide layers whose 64-column slice
+    // of Y^T (n x 256 bytes) fits an XCD's 4 MiB L2 (measured on MI355X at n = 16384, batch 4096: 0.58 ms per
     // layer against 0.93 for the kernel below; at n = 2^20, where neither slice fits, the kernel below is
-    // slightly faster: 957 against 990 ms per very wide forward)
-    if (n > 4096 && n <= 16384 && batch % 4 == 0 && ld * 4 < (1 << 24)) {
+    // slightly faster: 957 against 990 ms per very wide forward), and on batches under 256 from n = 4096 on,
+    // where the kernel below would take one or two columns per lane (batch 64: 0.52-0.8x the time at
+    // n = 32768, 0.65-0.9x at n = 4096 up to inverse sparsity 1024; below n = 4096 launches dominate and it
+    // measured 1.1-1.3x)
+    if (((n > 4096 && n <= 16384) || (batch < 256 && n >= 4096 && n <= (1 << 24))) && batch % 4 == 0 &&
+        ld * 4 < (1 << 24)) {
         constexpr int V = 4;
         const int64_t chunks = (batch + kNarrowP * V - 1) / (kNarrowP * V);
         const int64_t groups = (n + 4 * (64 / kNarrowP) - 1) / (4 * (64 / kNarrowP));  // 16 neurons per workgroup

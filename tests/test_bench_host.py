@@ -121,3 +121,7 @@ def test_kernel_name_matches_the_selection_rule():
     assert bench.spmm_kernel_name(4097, 10 ** 5, 302) == "spmm_fanin_kernel"
     assert bench.spmm_kernel_name(16385, 524288, 4096) == "spmm_fanin_kernel"
     assert bench.spmm_kernel_name(4096, 3728271, 130) == "spmm_fanin_kernel"  # the tiled kernels need 4 | batch
+    # batches under 256 take the narrow-chunk gather from n = 4096 on
+    assert bench.spmm_kernel_name(32768, 10 ** 6, 64) == "spmm_narrow_kernel"
+    assert bench.spmm_kernel_name(4096, 10 ** 5, 64) == "spmm_narrow_kernel"
+    assert bench.spmm_kernel_name(4095, 10 ** 5, 64) == "spmm_fanin_kernel"
