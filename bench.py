@@ -443,6 +443,9 @@ def run_csr_config(args, torch, sd):
         for _ in range(args.warmup):
             g.replay()
         timed = time_steps(torch, g.replay, args.steps)
+        # the graph holds the net's buffers: release it, with its work finished, before the net is freed
+        torch.cuda.synchronize()
+        del g
         extra = {"eager_ms_per_step": round(ms, 4), "graph_ms_per_step": round(timed[0], 4)}
         log(f"eager {ms:.4f} ms, graph replay {timed[0]:.4f} ms per forward")
         if timed[0] < ms:

@@ -15,6 +15,7 @@ from __future__ import annotations
 import ctypes
 import math
 import os
+import sys
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsdnn.so")
@@ -281,6 +282,10 @@ class Net:
             self._ws.clear()
 
     def __del__(self):
+        # At interpreter shutdown the HIP runtime (and any tool layered on it) may already be torn down, so
+        # no HIP call is made from here then; the process exit releases the device memory.
+        if sys.is_finalizing():
+            return
         try:
             self.free()
         except Exception:

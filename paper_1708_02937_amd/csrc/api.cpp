@@ -448,6 +448,14 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         *out_nnz = in_nnz;
         return SDNN_OK;
     }
+    if (batch == 0) {  // no samples: an empty result (row_ptr = {0})
+        SDNN_HIP(hipMemsetAsync(out_row_ptr, 0, sizeof(int64_t), s));
+        SDNN_HIP(hipStreamSynchronize(s));
+        *out_col = w.col[0];
+        *out_val = w.val[0];
+        *out_nnz = 0;
+        return SDNN_OK;
+    }
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
     SDNN_HIP(hipMemsetAsync(net->d_stats, 0, (size_t)(k1 - k0) * sdnn::kSpgemmStats * sizeof(unsigned long long), s));
 

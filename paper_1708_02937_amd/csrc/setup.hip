@@ -3,9 +3,10 @@
 //
 // Set-up runs once per layer and is not part of the timed forward pass.  The paper's library keeps
 // weights in CSR distributed by rows (Sec. V.A); the dense-Y product instead needs, for every output
-// neuron, the list of its inputs, i.e. W_k^T in CSR.  That list is built here with a counting sort
-// (count, scan, scatter) followed by a per-list sort by input index, so the stored order, and with it
-// the fp64 summation order of the forward pass, does not depend on atomic timing.
+// neuron, the list of its inputs, i.e. W_k^T in CSR.  The lists are built here by a stable LSD radix sort
+// of the entries by column (8-bit digits: tile histograms, a scan per digit, a stable scatter), which
+// leaves every list in ascending input order, so the stored order, and with it the fp64 summation order of
+// the forward pass, does not depend on atomic timing.  List pointers come from a column count and a scan.
 #include "common.h"
 
 namespace sdnn {

@@ -88,3 +88,38 @@ def check_canonical(csr):
         inner = rp[1:-1]
         starts[inner[inner < len(col)]] = True
         assert np.all((np.diff(col) > 0) | starts[1:])
+
+
+def compare_in_chunks(problem, got_csr, rows=None, chunk=512, **kw):
+    """compare() over blocks of `chunk` rows (the oracle and the dense views are built per block, so
+    memory stays bounded at full size).  got_csr holds the rows in the order of `rows` (all rows when
+    None).  Returns the summed entry and ambiguous-entry counts."""
+    nrows = len(got_csr[0]) - 1
+    rows = np.arange(nrows) if rows is None else np.asarray(rows)
+    assert len(rows) == nrows
+    tot = {"entries": 0, "ambiguous": 0}
+    for a in range(0, nrows, chunk):
+        idx = np.arange(a, min(nrows, a + chunk))
+        st = compare(problem, csr_rows(got_csr, idx), rows=rows[idx], **kw)
+        tot["entries"] += st["entries"]
+        tot["ambiguous"] += st["ambiguous"]
+    return tot
+
+
+def compare_exact_csr(problem, got_csr, k0=0, k1=None, chunk=4096, y_in=None):
+    """Bit-for-bit comparison of CSR arrays (row extents, columns, value bits) with the oracle over all
+    rows, in blocks of `chunk` rows, without dense views.  y_in: the CSR taken as Y_{k0} (default Y_0)."""
+    y = problem.y0_as_csr() if y_in is None else y_in
+    nrows = len(y[0]) - 1
+    assert len(got_csr[0]) == nrows + 1
+    total = 0
+    for a in range(0, nrows, chunk):
+        idx = np.arange(a, min(nrows, a + chunk))
+        want = oracle.forward(problem.n, problem.layers, problem.ymax, csr_rows(y, idx), k0=k0, k1=k1)
+        got = csr_rows(got_csr, idx)
+        assert np.array_equal(np.diff(got[0]), np.diff(want[0])), f"row lengths differ in rows {a}.."
+        assert np.array_equal(got[1], want[1]), f"columns differ in rows {a}.."
+        assert got[2].tobytes() == want[2].tobytes(), f"values differ in rows {a}.."
+        total += len(want[1])
+    check_canonical(got_csr)
+    return total

@@ -126,9 +126,11 @@ def test_tiny_csr_batch(sd, seed, n, L, batch):
 
 
 @pytest.mark.parametrize("arm", ARMS)
-@pytest.mark.parametrize("m,S", [(256, 1), (512, 2), (512, 16), (1024, 4), (1024, 1024), (2048, 262144)])
+@pytest.mark.parametrize("m,S", [(256, 1), (512, 2), (512, 16), (1024, 4), (1024, 1024), (2048, 262144),
+                                 (4096, 1), (4096, 64), (8192, 16)])
 def test_paper_grid_points(sd, arm, m, S):
-    """Single layers of the paper's own matrix family (Sec. V.B) on both arms, batch 64."""
+    """Single layers of the paper's own matrix family (Sec. V.B) on both arms, batch 64; from m = 4096 on the
+    sparse arm takes the narrow-chunk gather (batch under 256), up to dense W (S = 1, fan-in 4096)."""
     p = paper_grid(m, S)
     _say("paper grid", arm, m, S)
     parity.compare(p, dense_to_csr(run_dense(sd, p, _arm(sd, arm))))
@@ -216,9 +218,10 @@ def test_semiring_mxm_csr(sd, name):
 
 
 def test_gather_grid_larger_than_one_launch(sd):
-    """n = 2^20 and batch 4098 (the narrow-chunk gather: 129 chunks of 32 columns, 8.45M workgroups) need
-    more than one launch holds, so the gather runs in segments.  Y is drawn on the device from a seeded generator and
-    the sampled rows are handed to the oracle; 68 GB of device memory."""
+    """n = 2^20 and batch 4098 (not a multiple of 4, so the fan-in gather with two columns per lane: 33 chunks
+    of 128 columns x 262144 neuron groups = 8.65M workgroups) need more than one launch holds, so the gather
+    runs in segments.  Y is drawn on the device from a seeded generator and the sampled rows are handed to the
+    oracle; 68 GB of device memory."""
     import torch
 
     n, batch = 1 << 20, 4098
@@ -265,13 +268,16 @@ def _mixed_length_layer(rng, n, lengths):
 
 
 @pytest.mark.parametrize("seed,n,batch,lengths,bias_mode", [
-    (81, 4097, 34, [0, 1, 15, 16, 17, 40, 100], 0), (82, 5003, 96, [3, 0, 0, 33, 8, 9, 64, 1], 0),
-    (83, 6144, 130, [16, 16, 16, 16, 32, 31, 48, 7], 1), (84, 4099, 2, [120, 0, 5, 17], 1),
-    (85, 4500, 300, [2, 30, 31, 33, 0, 64], 0), (86, 16384, 512, [32, 25, 40, 32], 1)])
+    (81, 4097, 36, [0, 1, 15, 16, 17, 40, 100], 0), (82, 5003, 96, [3, 0, 0, 33, 8, 9, 64, 1], 0),
+    (83, 6144, 132, [16, 16, 16, 16, 32, 31, 48, 7], 1), (84, 4099, 4, [120, 0, 5, 17], 1),
+    (85, 4500, 300, [2, 30, 31, 33, 0, 64], 0), (86, 16384, 512, [32, 25, 40, 32], 1),
+    (87, 40000, 60, [33, 2, 0, 17, 64], 0), (88, 4099, 2, [120, 0, 5, 17], 0)])
 def test_narrow_chunk_gather(sd, seed, n, batch, lengths, bias_mode):
-    """Wide layers (n > 4096) with an even batch take the narrow-chunk gather (16 lanes and 32 columns per
-    neuron): ragged n and batch, and list lengths from 0 to 120 side by side in one wave, which exercises
-    the unpredicated prefix, the guarded tail and lists spanning several loads of 16 entries."""
+    """Layers with n > 4096 up to 16384 (any batch that is a multiple of 4), or n >= 4096 and a batch under
+    256 that is a multiple of 4, take the narrow-chunk gather (16 lanes and 64 columns, four per lane, per
+    neuron): ragged n, partial last chunks, and list lengths from 0 to 120 side by side in one wave, which
+    exercises the unpredicated prefix, the guarded tail and lists spanning several loads of 16 entries.  The
+    last case (batch 2, not a multiple of 4) is the fan-in gather fallback with one column per lane."""
     rng = np.random.default_rng(seed)
     layers = [_mixed_length_layer(rng, n, lengths), _mixed_length_layer(rng, n, lengths[::-1])]
     y = rng.random((batch, n), dtype=np.float32)
@@ -383,23 +389,22 @@ def test_config1_csr_path(sd):
 
 
 @pytest.mark.parametrize("d", [0.5, 0.25, 0.1, 0.01, 0.001])
-def test_config2_sparse_arm_sampled(sd, d):
-    """The density-sweep workload at full size through the CSR path, sampled rows; d = 0.25 sits just above the
-    switch to the scalar-register LDS-tiled SpMM."""
+def test_config2_sparse_arm_all_rows(sd, d):
+    """The density-sweep workload at full size through the CSR arm, every row of Y_16 compared; d = 0.25
+    sits just above the switch to the scalar-register LDS-tiled SpMM."""
     p = make_config(2, d)
     _say("config 2 sparse arm", d)
     out = run_dense(sd, p, sd.SDNN_ARM_SPARSE)
-    rows = np.random.default_rng(0).choice(p.batch, 12 if d >= 0.1 else 48, replace=False)
-    parity.compare(p, dense_to_csr(out[rows]), rows=rows)
+    st = parity.compare_in_chunks(p, dense_to_csr(out))
+    assert st["entries"] > 0
 
 
 @pytest.mark.parametrize("d", [0.5, 0.01])
-def test_config2_dense_arm_sampled(sd, d):
+def test_config2_dense_arm_all_rows(sd, d):
     p = make_config(2, d)
     _say("config 2 dense arm", d)
     out = run_dense(sd, p, sd.SDNN_ARM_DENSE)
-    rows = np.random.default_rng(1).choice(p.batch, 12, replace=False)
-    parity.compare(p, dense_to_csr(out[rows]), rows=rows)
+    parity.compare_in_chunks(p, dense_to_csr(out))
 
 
 @pytest.mark.parametrize("n", [700, 701])
@@ -424,12 +429,22 @@ def test_config3_scaled_full_compare(sd):
     parity.compare(p, run_csr(sd, p))
 
 
-def test_config3_full_size_sampled(sd):
+def test_config3_full_size_all_rows(sd):
+    """The sparse-activation workload at full size (n 16384, L 32, batch 4096): every row of Y_32."""
     p = make_config(3)
     _say("config 3 full size")
-    rp, c, v = run_csr(sd, p)
-    rows = np.random.default_rng(2).choice(p.batch, 10, replace=False)
-    parity.compare(p, csr_rows((rp, c, v), rows), rows=rows)
+    st = parity.compare_in_chunks(p, run_csr(sd, p))
+    assert st["entries"] > 0
+
+
+@pytest.fixture(scope="module")
+def config4():
+    return make_config(4)
+
+
+@pytest.fixture(scope="module")
+def config5():
+    return make_config(5)
 
 
 def test_config4_scaled(sd):
@@ -438,26 +453,96 @@ def test_config4_scaled(sd):
     parity.compare(p, run_csr(sd, p))
 
 
-def test_config4_full_size_sampled(sd):
-    p = make_config(4)
-    _say("config 4 full size")
-    rp, c, v = run_csr(sd, p)
-    rows = np.random.default_rng(3).choice(p.batch, 24, replace=False)
-    parity.compare(p, csr_rows((rp, c, v), rows), rows=rows)
+def test_config4_layer0_bit_exact_all_rows(sd, config4):
+    """Deep sparse, full size, the live layer: weights are exactly 1/16 and inputs binary, so every
+    pre-activation is c/16 + b with an integer count c; c/16 is exact and the only rounding is the one to
+    fp32 after the bias, so Y_1 must equal the oracle bit for bit in all 60000 rows (588k entries)."""
+    p = config4
+    _say("config 4 layer 0 exact")
+    got = run_csr(sd, p, k0=0, k1=1)
+    assert parity.compare_exact_csr(p, got, k0=0, k1=1) > 100000
 
 
-def test_config5_full_size_sampled(sd):
-    p = make_config(5)
+def test_config4_two_layers_all_rows(sd, config4):
+    """Layers 0 and 1 of the deep sparse network at full size, all rows, at the tolerance: layer 1 takes
+    the SpGEMM on Y_1 (about 10 entries per sample), whose sums of a few c/16 - 0.3 values stay below the
+    threshold -0.3 leaves, so Y_2 is empty in both."""
+    p = config4
+    _say("config 4 two layers")
+    got = run_csr(sd, p, k0=0, k1=2)
+    want = parity.oracle_rows(p, k1=2)
+    assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+    assert np.all(np.abs(got[2].astype(np.float64) - want[2]) <= parity.ATOL + parity.RTOL * np.abs(want[2]))
+
+
+def config5_rows(batch, seed=4):
+    """One sampled row in each run of 32 consecutive samples: every batch chunk of the dense-Y kernels
+    (32, 64 or 256 columns wide) holds at least one, eight per 256 columns."""
+    rng = np.random.default_rng(seed)
+    return np.arange(0, batch, 32) + rng.integers(0, 32, size=batch // 32)
+
+
+def test_config5_full_size_sampled(sd, config5):
+    """The very wide workload at full size: 256 rows of Y_8 spread over every 32-sample run of the batch."""
+    p = config5
     _say("config 5 full size")
     rp, c, v = run_csr(sd, p)
-    rows = np.random.default_rng(4).choice(p.batch, 6, replace=False)
-    parity.compare(p, csr_rows((rp, c, v), rows), rows=rows)
+    rows = config5_rows(p.batch)
+    st = parity.compare_in_chunks(p, csr_rows((rp, c, v), rows), rows=rows, chunk=64)
+    assert st["entries"] > 0
 
 
 def test_config5_scaled(sd):
     p = make_config(5, n=32768, L=3, batch=24)
     _say("config 5 scaled")
     parity.compare(p, run_csr(sd, p))
+
+
+# ------------------------------------------------------ per layer: the oracle's Y_k through one GPU layer
+
+
+def _one_layer(p, k, y_csr, rows=None):
+    """A one-layer problem: layer k of p applied to the CSR rows y_csr (the oracle's Y_k)."""
+    from workloads import Problem
+
+    nrows = len(y_csr[0]) - 1
+    return Problem(f"{p.name}-layer{k}", p.n, 1, nrows, p.ymax, [p.layers[k]], y0_csr=y_csr)
+
+
+@pytest.mark.parametrize("cfg,kw,k", [(1, {}, 2), (2, {"density": 0.1}, 9), (2, {"density": 0.5}, 15),
+                                      (3, {}, 31)])
+def test_per_layer_from_oracle_input(sd, cfg, kw, k):
+    """The oracle's Y_k (all rows, full size) through GPU layer k alone, against the oracle's layer k:
+    bounds one layer's error independently of the layers before it.  Dense workloads run on the dense-Y
+    path (forward_dense), the sparse-activation one through forward_csr."""
+    p = make_config(cfg, kw.get("density"))
+    yk = parity.oracle_rows(p, k1=k)
+    q = _one_layer(p, k, yk)
+    _say("per layer", cfg, kw, k)
+    if p.y0_dense is not None:
+        got = dense_to_csr(run_dense(sd, q, sd.SDNN_ARM_SPARSE, y0=parity.to_dense(yk, p.n)))
+    else:
+        got = run_csr(sd, q)
+    st = parity.compare_in_chunks(q, got)
+    assert st["entries"] > 0
+
+
+def test_per_layer_config4_and_5(sd, config4, config5):
+    """Deep sparse layer 1 on the oracle's Y_1 (all rows, bit for bit: its inputs are c/16 - 0.3 values and
+    the weights 1/16, so the products and their short sums are exact), and very wide layer 3 on the
+    oracle's Y_3 of 256 sampled rows."""
+    p = config4
+    y1 = parity.oracle_rows(p, k1=1)
+    q = _one_layer(p, 1, y1)
+    _say("per layer config 4")
+    parity.compare_exact_csr(q, run_csr(sd, q), k0=0, k1=1)
+    p = config5
+    rows = config5_rows(p.batch, seed=9)
+    y3 = parity.oracle_rows(p, rows=rows, k1=3)
+    q = _one_layer(p, 3, y3)
+    _say("per layer config 5")
+    st = parity.compare_in_chunks(q, run_csr(sd, q), chunk=64)
+    assert st["entries"] > 0
 
 
 # ------------------------------------------------------------------------------------------ structure
@@ -567,6 +652,14 @@ def test_degenerate_cases(sd):
     p.y0_dense, p.y0_csr = None, (rp, np.zeros(0, np.int32), np.zeros(0, np.float32))
     parity.compare(p, [x.cpu().numpy() for x in out])  # empty samples: h(b) propagates
     net.free()
+    # a CSR batch of no samples through layers, n a multiple of 4 and not
+    for nn in (100, 101):
+        q = tiny_random(5, nn, 2, 3, w_density=0.1)
+        net = sd.net_from_problem(q)
+        rp0 = np.zeros(1, np.int64)
+        orp, oc, ov = net.forward_csr(rp0, np.zeros(0, np.int32), np.zeros(0, np.float32))
+        assert orp.cpu().numpy().tolist() == [0] and oc.numel() == 0 and ov.numel() == 0
+        net.free()
 
 
 def test_errors_leave_net_usable(sd):

@@ -59,6 +59,10 @@ MUTANTS = {
     "pattern_touch_zero_inputs": ("if (job->bias_mode && y != 0.0) touched[W->col[e]] = 1;",
                                   "if (job->bias_mode) touched[W->col[e]] = 1;"),
     "pattern_never_touch": ("if (job->bias_mode && y != 0.0) touched[W->col[e]] = 1;", ""),
+    "scale_signed": ("s[W->col[e]] += fabs(p);", "s[W->col[e]] += p;"),
+    "scale_doubled": ("s[W->col[e]] += fabs(p);", "s[W->col[e]] += 2.0 * fabs(p);"),
+    "scale_no_bias": ("s[j] += fabs((double)W->bias[j]);", ""),
+    "preact_no_bias": ("z[j] += (double)W->bias[j];", ""),
 }
 
 
@@ -101,6 +105,19 @@ def battery(lib):
         out = oracle.forward(3, lay, math.inf, y0, lib=lib, bias_mode=1)
         if not np.array_equal(oracle.csr_to_dense(out, 3), np.array(g["pattern_bias"]["Y2"], np.float32)):
             failed.append("hand_pattern")
+        # pre-activation and its condition scale s = |Y||W| + |b|: hand-worked values, then the exact
+        # integer case against a library matmul of the absolute values
+        z, s = oracle.preact(3, lay[0], y0, lib=lib)
+        if not (np.array_equal(z, np.array(g["Y0W_plus_b"], np.float64))
+                and np.array_equal(s, np.array(g["S_scale"], np.float64))):
+            failed.append("hand_preact")
+        z, s = oracle.preact(256, q.layers[0], q.y0_csr, lib=lib)
+        Yq = oracle.csr_to_dense(q.y0_csr, 256).astype(np.int64)
+        Wq = q.layers[0].to_dense(256).astype(np.int64)
+        bq = q.layers[0].bias.astype(np.int64)
+        if not (np.array_equal(z, (Yq @ Wq + bq).astype(np.float64))
+                and np.array_equal(s, (np.abs(Yq) @ np.abs(Wq) + np.abs(bq)).astype(np.float64))):
+            failed.append("integer_preact")
         for seed in (3, 4):
             p = tiny_random(seed, 19, 3, 5, w_density=0.15, y_density=0.3, bias_lo=-0.2, bias_hi=0.6,
                             explicit_zeros=True)

@@ -262,6 +262,36 @@ def test_preact_consistent_with_forward():
     assert np.all(s >= np.abs(z) - 1e-12)
 
 
+def test_preact_scale_hand_example():
+    """The condition scale s = sum_i |Y(r,i) W(i,j)| + |b_j| of the worked example, computed by hand (the
+    fixture's S_scale), and z = Y W + b beside it."""
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    layers = _layers_from_dense([g["W"]], [g["b"]])
+    z, s = oracle.preact(3, layers[0], dense_to_csr(np.array(g["Y0"], np.float32)))
+    assert np.array_equal(z, np.array(g["Y0W_plus_b"], np.float64))
+    assert np.array_equal(s, np.array(g["S_scale"], np.float64))
+
+
+def test_preact_scale_integer_and_sign_invariance():
+    """Integer-valued inputs make every sum exact: s equals |Y| |W| + |b| from a library matmul of the
+    absolute values; flipping the sign of W or b changes z but leaves s unchanged; with nonnegative operands
+    there is no cancellation, so s equals z."""
+    q = integer_shadow(make_config(3, n=300, L=1, batch=9))
+    l = q.layers[0]
+    z, s = oracle.preact(300, l, q.y0_csr)
+    Y = oracle.csr_to_dense(q.y0_csr, 300).astype(np.int64)
+    W = l.to_dense(300).astype(np.int64)
+    b = l.bias.astype(np.int64)
+    assert np.array_equal(z, (Y @ W + b).astype(np.float64))
+    assert np.array_equal(s, (np.abs(Y) @ np.abs(W) + np.abs(b)).astype(np.float64))
+    neg = Layer(l.row_ptr, l.col, -l.val, -l.bias)
+    z2, s2 = oracle.preact(300, neg, q.y0_csr)
+    assert np.array_equal(z2, -z) and np.array_equal(s2, s)
+    pos = Layer(l.row_ptr, l.col, np.abs(l.val), np.abs(l.bias))
+    z3, s3 = oracle.preact(300, pos, q.y0_csr)
+    assert np.array_equal(z3, s3)
+
+
 def test_rejects_bad_input():
     p = tiny_random(3, 10, 1, 2)
     l = p.layers[0]
