@@ -181,6 +181,23 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
                                float *Y_out, void *ws, int64_t ws_bytes, int32_t arm);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): sdnn_forward_dense without a workspace argument.  Its workspace (the two
+ * activation buffers and the dense arm's partial sums) is a fixed device array of the library, one per
+ * GPU, sdnn_noalloc_scratch_bytes() bytes (64 MiB), held from the first sdnn_net_create on that GPU until
+ * the process ends.  The call itself allocates and frees nothing.  Layers whose workspace
+ * (sdnn_workspace_size(net, batch, 0)) exceeds that size are refused with UNSUPPORTED.  Every call on one
+ * GPU shares the array, which keeps the last call's contents: calls that overlap on one GPU (other host
+ * threads, other nets or streams without ordering between them) race and give undefined results.  Same
+ * arguments, result and errors as sdnn_forward_dense otherwise.
+ */
+sdnn_status sdnn_forward_dense_noalloc(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const float *Y_in,
+                                       float *Y_out, int32_t arm);
+
+/* Size in bytes of the fixed scratch array behind sdnn_forward_dense_noalloc. */
+int64_t sdnn_noalloc_scratch_bytes(void);
+
+/*
  * Layers [k0, k1) on a CSR batch Y_in = (y_row_ptr[batch+1], y_col, y_val),
  * device arrays, columns strictly increasing within a row (not checked; the
  * result is undefined otherwise).  y_col and y_val may be NULL when every row

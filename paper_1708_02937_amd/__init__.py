@@ -61,6 +61,7 @@ _sig = {
     "sdnn_net_build_dense": [_P],
     "sdnn_workspace_size": [_P, _I64, _I32, _c.POINTER(_I64)],
     "sdnn_forward_dense": [_P, _I32, _I32, _I64, _P, _P, _P, _I64, _I32],
+    "sdnn_forward_dense_noalloc": [_P, _I32, _I32, _I64, _P, _P, _I32],
     "sdnn_forward_csr": [_P, _I32, _I32, _I64, _P, _P, _P, _P, _I64, _P, _c.POINTER(_P), _c.POINTER(_P),
                          _c.POINTER(_I64)],
     "sdnn_mxm_dense": [_P, _I32, _I32, _I64, _P, _P, _P, _I64],
@@ -70,6 +71,8 @@ _sig = {
 for _name, _args in _sig.items():
     getattr(lib, _name).argtypes = _args
     getattr(lib, _name).restype = _c.c_int
+lib.sdnn_noalloc_scratch_bytes.argtypes = []
+lib.sdnn_noalloc_scratch_bytes.restype = _I64
 lib.sdnn_status_string.argtypes = [_c.c_int]
 lib.sdnn_status_string.restype = _c.c_char_p
 lib.sdnn_last_error.argtypes = []
@@ -129,6 +132,14 @@ def sdnn_workspace_size(net, batch: int, y_is_csr: int) -> int:
 
 def sdnn_forward_dense(net, k0: int, k1: int, batch: int, y_in, y_out, ws, ws_bytes: int, arm: int = SDNN_ARM_SPARSE):
     _check(lib.sdnn_forward_dense(net, k0, k1, batch, _ptr(y_in), _ptr(y_out), _ptr(ws), ws_bytes, arm))
+
+
+def sdnn_forward_dense_noalloc(net, k0: int, k1: int, batch: int, y_in, y_out, arm: int = SDNN_ARM_SPARSE):
+    _check(lib.sdnn_forward_dense_noalloc(net, k0, k1, batch, _ptr(y_in), _ptr(y_out), arm))
+
+
+def sdnn_noalloc_scratch_bytes() -> int:
+    return int(lib.sdnn_noalloc_scratch_bytes())
 
 
 def sdnn_forward_csr(net, k0: int, k1: int, batch: int, y_row_ptr, y_col, y_val, ws, ws_bytes: int, out_row_ptr):

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -153,6 +154,33 @@ size_t dense_ws_bytes(int64_t n, int64_t batch, int num_cu) {
     return 2 * act_bytes(n, batch) + align_up(sdnn::gemm_partial_bytes(n, batch, num_cu));
 }
 
+// Workspace of sdnn_forward_dense_noalloc: a fixed device array, one copy per GPU, held until the process
+// ends.  In host code the symbol is only a host-side stand-in; kernels get the device address that
+// hipGetSymbolAddress returns for the current device (kept per device in g_scratch).
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+struct ScratchSlot {
+    std::once_flag once;
+    void *ptr = nullptr;
+    hipError_t err = hipErrorNotInitialized;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// Looks up this device's copy of the scratch array once; the device must be current.
+void scratch_init(int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return;
+    ScratchSlot &slot = g_scratch[dev];
+    std::call_once(slot.once, [&slot]() {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        slot.err = e;
+        slot.ptr = e == hipSuccess ? p : nullptr;
+        if (e != hipSuccess) (void)hipGetLastError();
+    });
+}
+
 }  // namespace
 
 struct sdnn_net_s {
@@ -211,6 +239,7 @@ sdnn_status sdnn_net_create(sdnn_net *out, int64_t n, int32_t L, float ymax, voi
     net->device = dev;
     net->num_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
     net->layers.resize((size_t)L);
+    scratch_init(dev);  // this device's copy of the allocation-free entry point's scratch array
     sdnn_status st = dalloc(&net->d_flags, 4, "flags");
     if (st == SDNN_OK) st = dalloc(&net->d_int, 4, "scratch");
     if (st == SDNN_OK) st = dalloc(&net->d_stats, (size_t)(L > 0 ? L : 1) * sdnn::kSpgemmStats, "layer counters");
@@ -364,9 +393,25 @@ static sdnn_status check_range(sdnn_net net, int32_t k0, int32_t k1) {
     return SDNN_OK;
 }
 
+static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const float *Y_in,
+                                      float *Y_out, void *ws, int64_t ws_bytes, int32_t arm, bool static_ws);
+
 sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const float *Y_in, float *Y_out,
                                void *ws, int64_t ws_bytes, int32_t arm) {
     g_last_error.clear();
+    return forward_dense_impl(net, k0, k1, batch, Y_in, Y_out, ws, ws_bytes, arm, false);
+}
+
+sdnn_status sdnn_forward_dense_noalloc(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const float *Y_in,
+                                       float *Y_out, int32_t arm) {
+    g_last_error.clear();
+    return forward_dense_impl(net, k0, k1, batch, Y_in, Y_out, nullptr, 0, arm, true);
+}
+
+int64_t sdnn_noalloc_scratch_bytes(void) { return (int64_t)kScratchBytes; }
+
+static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int64_t batch, const float *Y_in,
+                                      float *Y_out, void *ws, int64_t ws_bytes, int32_t arm, bool static_ws) {
     if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
     sdnn_status st = check_range(net, k0, k1);
     if (st != SDNN_OK) return st;
@@ -383,6 +428,19 @@ sdnn_status sdnn_forward_dense(sdnn_net net, int32_t k0, int32_t k1, int64_t bat
         if (Y_out != Y_in)
             SDNN_HIP(hipMemcpyAsync(Y_out, Y_in, (size_t)batch * (size_t)n * sizeof(float), hipMemcpyDeviceToDevice, s));
         return SDNN_OK;
+    }
+    if (static_ws) {
+        // the library's fixed scratch array of this device replaces the caller's workspace
+        const ScratchSlot *slot = net->device < kMaxDevices ? &g_scratch[net->device] : nullptr;
+        if (!slot || !slot->ptr)
+            return fail(SDNN_ERR_DEVICE, std::string("scratch array of the allocation-free entry point unavailable: ") +
+                                             hipGetErrorString(slot ? slot->err : hipErrorInvalidDevice));
+        if (dense_ws_bytes(n, batch, net->num_cu) > kScratchBytes)
+            return fail(SDNN_ERR_UNSUPPORTED, "batch x n needs " + std::to_string(dense_ws_bytes(n, batch, net->num_cu)) +
+                                                  " bytes of scratch; the allocation-free entry point holds " +
+                                                  std::to_string(kScratchBytes));
+        ws = slot->ptr;
+        ws_bytes = (int64_t)kScratchBytes;
     }
     if (!ws) return fail(SDNN_ERR_NULL_POINTER, "ws is required");
     if (ws_bytes < (int64_t)dense_ws_bytes(n, batch, net->num_cu))
