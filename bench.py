@@ -1,13 +1,15 @@
 """Benchmark: edges/s of the sparse DNN forward pass on one MI355X.
 
-Default workload (the density sweep, n = 4096, L = 16, batch = 1024, fp32 storage): one step is one
-forward pass of all L layers through the CSR (sparse-W) path at each of the four weight densities
-{50%, 10%, 1%, 0.1%}; value = sum over the sweep of batch * nnz(W_k) * L divided by the step time.
-Inputs are resident in HBM before timing starts.  Besides the headline line it measures the dense-W
-arm at every density (the paper's sparse-versus-dense comparison, Sec. V) and reports the crossover
-density, the roofline of the dominant kernel, and the CPU oracle on a bounded sample as a baseline.
+Default workload (the very wide network, n = 2^20, L = 8, batch 8192, the largest configuration): one step
+is one forward pass of all L layers from the CSR input batch Y_0 to the CSR output Y_L through
+sdnn_forward_csr; value = batch * sum_k nnz(W_k) / step time.  Inputs are resident in HBM before timing
+starts.  The line also carries the roofline of the dominant kernel (per-launch GPU time from the library's
+profiling events over the timed steps), its achieved HBM bandwidth (compulsory bytes and, when the committed
+rocprofv3 counters match the kernel's sources, counter bytes), the per-kernel time split, the density sweep
+with the sparse-versus-dense crossover (the paper's Sec. V comparison) as extra keys, and the CPU oracle on
+a bounded sample as a baseline.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..5]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..5] [--no-sweep]
 """
 
 from __future__ import annotations
@@ -97,6 +99,73 @@ def time_calls(torch, fn, reps: int) -> float:
     return a.elapsed_time(b) / reps
 
 
+def kernel_split(records):
+    """Per kernel name: launches, total and average ms, from profiling-log records (layer, name, ms)."""
+    out = {}
+    for layer, name, ms in records:
+        r = out.setdefault(name, {"launches": 0, "total_ms": 0.0, "layers": []})
+        r["launches"] += 1
+        r["total_ms"] += ms
+        r["layers"].append((layer, ms))
+    for r in out.values():
+        r["avg_ms"] = r["total_ms"] / r["launches"]
+    return out
+
+
+SPMM_KERNELS = ("spmm_fanin_kernel", "spmm_narrow_kernel", "spmm_slots_kernel", "spmm_tiled_kernel")
+
+
+def kernel_roofline(name, rec, p, trace=None):
+    """Roofline of one profiled kernel over its launches: algorithmic bytes (flops) per launch, averaged over
+    the launches, divided by the average launch time.  trace: (nnz per Y_k, products per layer) for the
+    sparse-Y product."""
+    launches = rec["layers"]
+    byt = flops = 0.0
+    for layer, _ in launches:
+        nnz = p.layers[layer].nnz if layer >= 0 else 0
+        if name in SPMM_KERNELS:
+            b, f = spmm_algorithmic(p.n, p.batch, nnz)
+        elif name == "gemm_dense_layer_kernel":
+            b, f = 8 * p.n * p.n + 8 * p.n * p.batch, 2.0 * p.batch * p.n * p.n
+        elif name == "spgemm_layer" and trace is not None:
+            ny, prods = trace
+            b = 8 * ny[layer] + 8 * ny[layer + 1] + 8 * p.batch + 8 * nnz + 8 * (p.n + 1) + 4 * p.n
+            f = 2.0 * prods[layer]
+        else:
+            return None
+        byt += b
+        flops += f
+    byt /= len(launches)
+    flops /= len(launches)
+    t_s = rec["avg_ms"] / 1e3
+    if name == "gemm_dense_layer_kernel":
+        roof = {"bound": "mfma", "achieved": round(flops / t_s / 1e12, 3), "peak": FP64_MATRIX_TFLOPS,
+                "unit": "TFLOP/s"}
+    elif flops / byt > FP64_VECTOR_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+        roof = {"bound": "alu", "achieved": round(flops / t_s / 1e12, 3), "peak": FP64_VECTOR_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(byt / t_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof.update({"kernel": name, "launches": len(launches), "avg_launch_ms": round(rec["avg_ms"], 5),
+                 "algorithmic_bytes_per_launch": int(byt), "algorithmic_flops_per_launch": flops})
+    return roof
+
+
+def hbm_fields(roof, traffic):
+    """Achieved HBM bandwidth of the dominant kernel: compulsory bytes per launch / average launch time, and
+    counter bytes (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled) / the same time when the counters are current."""
+    t_s = roof["avg_launch_ms"] / 1e3
+    eff = roof["algorithmic_bytes_per_launch"] / t_s / 1e9
+    out = {"kernel": roof["kernel"], "effective": round(eff, 1), "effective_frac": round(eff / HBM_PEAK_GBS, 4),
+           "counter": None, "counter_frac": None}
+    if traffic:
+        cnt = traffic / t_s / 1e9
+        out.update({"counter": round(cnt, 1), "counter_frac": round(cnt / HBM_PEAK_GBS, 4),
+                    "counter_bytes_per_launch": traffic})
+    return out
+
+
 # ----------------------------------------------------------------------------------- the sweep
 
 
@@ -107,20 +176,6 @@ def spmm_algorithmic(n, batch, nnz):
     write Y_{k+1}^T (4 n batch).  flops: 2 per product, batch * nnz products.
     """
     return 8 * n * batch + 8 * nnz + 8 * (n + 1) + 4 * n, 2.0 * batch * nnz
-
-
-def spmm_kernel_name(n, nnz, batch=1024):
-    """The dense-Y layer kernel the library selects (mirrors spmm_wants_tiles / spmm_wants_slots and the
-    gather's narrow-chunk range in launch_spmm_fanin)."""
-    if n <= 65536 and batch % 4 == 0 and batch >= 128:
-        if -(-n // 16) * 16 * (-(-n // 64) * 64) * 8 <= 2 ** 31:
-            if 9 * nnz >= 2 * n * n:
-                return "spmm_slots_kernel"
-        elif 10 * nnz >= 3 * n * n:
-            return "spmm_tiled_kernel"
-    if (4096 < n <= 16384 or (batch < 256 and 4096 <= n)) and batch % 4 == 0:
-        return "spmm_narrow_kernel"
-    return "spmm_fanin_kernel"
 
 
 def run_sweep(args, torch, sd):
@@ -145,24 +200,28 @@ def run_sweep(args, torch, sd):
 
     for _ in range(args.warmup):
         step()
+    for net in nets:
+        net.set_profiling(True)
     t_wall = time.perf_counter()
     ms_step, ms_med, ms_min = time_steps(torch, step, args.steps)
     t_wall = time.perf_counter() - t_wall
+    splits = []
+    for net in nets:
+        net.set_profiling(False)
+        splits.append(kernel_split(net.read_profile()))
     edges = sum(p.edges() for p in probs)
     value = edges / (ms_step / 1e3)
     log(f"step {ms_step:.3f} ms (wall {1e3 * t_wall / args.steps:.3f} ms), {value:.4g} edges/s")
 
-    # per-density forward time and the per-launch time of the layer kernel
+    # per-density forward time, and the average launch time of the layer kernel over the timed steps
     sweep = {}
-    per_launch = {}
     reps = max(3, args.steps)
-    for d, net, y, o, p in zip(densities, nets, ys, outs, probs):
+    for d, net, y, o, p, sp in zip(densities, nets, ys, outs, probs, splits):
         t_full = time_calls(torch, lambda: net.forward_dense(y, out=o), reps)
-        t_one = time_calls(torch, lambda: net.forward_dense(y, k0=0, k1=1, out=o), reps * 4)
-        launch = (t_full - t_one) / (p.L - 1)  # the two transposes cancel; what is left is L-1 layer launches
-        per_launch[d] = launch
+        kname = next(k for k in sp if k != "transpose_kernel")
         sweep[f"{d:g}"] = {"sparse_ms": round(t_full, 4), "sparse_edges_per_s": p.edges() / (t_full / 1e3),
-                           "layer_launch_ms": round(launch, 5), "nnz_per_layer": int(p.layers[0].nnz)}
+                           "layer_kernel": kname, "layer_launch_ms": round(sp[kname]["avg_ms"], 5),
+                           "nnz_per_layer": int(p.layers[0].nnz)}
 
     # dense-W arm (matrix cores) at every density, one density at a time (n*n fp64 per layer)
     if not args.no_dense:
@@ -208,33 +267,25 @@ def run_sweep(args, torch, sd):
             crossover = find_crossover()
             if crossover is not None:
                 break
-    # dominant kernel: the layer launch with the largest share of the step
-    dom = max(densities, key=lambda d: per_launch[d])
+    # dominant kernel: the layer kernel with the largest share of the step
+    best = None
+    for d, sp in zip(densities, splits):
+        for k, v in sp.items():
+            if k != "transpose_kernel" and (best is None or v["total_ms"] > best[2]["total_ms"]):
+                best = (d, k, v)
+    dom, kernel, rec = best
     p = probs[densities.index(dom)]
-    nnz_avg = sum(l.nnz for l in p.layers) / p.L
-    byt, flops = spmm_algorithmic(p.n, p.batch, nnz_avg)
-    t_s = per_launch[dom] / 1e3
-    intensity = flops / byt
-    if intensity > FP64_VECTOR_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
-        roof = {"bound": "alu", "achieved": round(flops / t_s / 1e12, 3), "peak": FP64_VECTOR_TFLOPS,
-                "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": round(byt / t_s / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    kernel = spmm_kernel_name(p.n, nnz_avg, p.batch)
+    roof = kernel_roofline(kernel, rec, p)
     roof["traffic"] = _pmc_traffic(f"{kernel}_d{dom:g}", ["spmm.hip", "common.h"])
-    roof["kernel"] = kernel
-    roof["per_launch_ms"] = round(per_launch[dom], 5)
     roof["density"] = dom
-    roof["algorithmic_bytes_per_launch"] = int(byt)
-    roof["algorithmic_flops_per_launch"] = flops
+    hbm = hbm_fields(roof, roof["traffic"])
     for net in nets:
         net.free()
     cfg = {"workload": "density-sweep n=4096 L=16 batch=1024 d=" + "/".join(f"{d:g}" for d in densities)
                        + " (CSR sparse-W path; fp32 storage, fp64 accumulate)",
            "n": 4096, "L": 16, "batch": 1024, "densities": densities}
     return dict(value=value, ms_step=ms_step, ms_median=ms_med, ms_min=ms_min, edges=edges, sweep=sweep,
-                crossover=crossover, roofline=roof, config=cfg, probs=probs, densities=densities)
+                crossover=crossover, roofline=roof, hbm=hbm, config=cfg, probs=probs, densities=densities)
 
 
 # oracle sample per workload (rows of the batch): all-core rate, and single-thread rate where the density-sweep
@@ -420,11 +471,19 @@ def layer_trace(torch, net, p, y):
     return nnz, products
 
 
+PMC_TAGS = {1: "tiny-mlp", 3: "sparse-activation", 4: "deep-sparse", 5: "very-wide"}
+
+
 def run_csr_config(args, torch, sd):
-    """Configs 3-5 (sparse Y through the SpGEMM path) and config 1, one forward per step."""
+    """Configs 3-5 (CSR input through sdnn_forward_csr) and config 1 (dense batch), one forward per step.
+    The library's profiling log is on during the timed steps (config 1: during an extra pass of the same
+    steps, so the event records do not weigh on a 30 us forward)."""
     from workloads import make_config
 
+    t0 = time.time()
     p = make_config(args.config)
+    log(f"generated {p.name} in {time.time() - t0:.1f}s")
+    t0 = time.time()
     net = sd.net_from_problem(p)
     if p.y0_csr is not None:
         y = tuple(torch.from_numpy(a).cuda() for a in p.y0_csr)
@@ -433,9 +492,21 @@ def run_csr_config(args, torch, sd):
         y = torch.from_numpy(p.y0_dense).cuda()
         o = torch.empty_like(y)
         fn = lambda: net.forward_dense(y, out=o)
+    fn()
+    torch.cuda.synchronize()
+    log(f"set-up and first forward {time.time() - t0:.1f}s")
     for _ in range(args.warmup):
         fn()
+    profiled_inline = p.y0_csr is not None
+    if profiled_inline:
+        net.set_profiling(True)
     ms, ms_med, ms_min = time_steps(torch, fn, args.steps)
+    if not profiled_inline:
+        net.set_profiling(True)
+        time_steps(torch, fn, args.steps)
+    net.set_profiling(False)
+    split = kernel_split(net.read_profile())
+    log(f"step {ms:.3f} ms; " + ", ".join(f"{k} {v['launches']} x {v['avg_ms']:.4f} ms" for k, v in split.items()))
     extra = {}
     if p.y0_csr is None:
         # a dense batch: the same forward replayed from a HIP graph (launch-bound at small sizes)
@@ -450,15 +521,27 @@ def run_csr_config(args, torch, sd):
         log(f"eager {ms:.4f} ms, graph replay {timed[0]:.4f} ms per forward")
         if timed[0] < ms:
             ms, ms_med, ms_min = timed
-    elif args.config in (3, 4) and not args.no_layer_trace:
+    trace = None
+    if args.config in (3, 4) and not args.no_layer_trace:
         nnz, products = layer_trace(torch, net, p, y)
-        extra = {"nnz_trace": nnz, "products_per_layer": products,
-                 "products_per_s": sum(products) / (ms / 1e3)}
+        trace = (nnz, products)
+        extra.update({"nnz_trace": nnz, "products_per_layer": products,
+                      "products_per_s": sum(products) / (ms / 1e3)})
         log(f"nnz trace {nnz[:4]} ..., {sum(products):.4g} products per forward")
     net.free()
-    cfg = {"workload": f"{p.name} n={p.n} L={p.L} batch={p.batch}", "n": p.n, "L": p.L, "batch": p.batch, **extra}
+    torch.cuda.synchronize()
+    per_step = {k: round(v["total_ms"] / args.steps, 4) for k, v in split.items()}
+    dom = max(split, key=lambda k: split[k]["total_ms"])
+    roof = kernel_roofline(dom, split[dom], p, trace)
+    hbm = None
+    if roof is not None:
+        roof["traffic"] = _pmc_traffic(f"{dom}_{PMC_TAGS.get(args.config, p.name)}", ["spmm.hip", "common.h"]) \
+            if dom in SPMM_KERNELS else None
+        hbm = hbm_fields(roof, roof["traffic"])
+    cfg = {"workload": f"{p.name} n={p.n} L={p.L} batch={p.batch}", "n": p.n, "L": p.L, "batch": p.batch,
+           "nnz_per_layer": int(p.layers[0].nnz), **extra}
     return dict(value=p.edges() / (ms / 1e3), ms_step=ms, ms_median=ms_med, ms_min=ms_min, config=cfg,
-                roofline=None, sweep=None, crossover=None, probs=[p])
+                roofline=roof, hbm=hbm, kernel_ms_per_step=per_step, sweep=None, crossover=None, probs=[p])
 
 
 # ----------------------------------------------------------------------------- profile summaries (no GPU)
@@ -524,7 +607,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--config", type=int, default=5)
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the density sweep (and its crossover) that the default run adds as extra keys")
     ap.add_argument("--densities", default="0.5,0.1,0.01,0.001")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-W arm")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -600,14 +685,28 @@ def main():
         "metric": METRIC, "value": r["value"], "unit": "edges/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(r["ms_step"], 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f64", "data": "synthetic", "config": r["config"],
-        "roofline": r["roofline"], "ms_per_step_median": round(r["ms_median"], 4),
+        "roofline": r["roofline"], "achieved_hbm_gbs": r.get("hbm"), "ms_per_step_median": round(r["ms_median"], 4),
         "ms_per_step_min": round(r["ms_min"], 4),
     }
+    if r.get("kernel_ms_per_step"):
+        out["kernel_ms_per_step"] = r["kernel_ms_per_step"]
     if r.get("sweep"):
         out["sweep"] = r["sweep"]
         out["crossover_density"] = r["crossover"]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args, r["probs"], args.config)
+    if args.config != 2 and not args.no_sweep:
+        # the paper's sparse-versus-dense comparison on the density-sweep workload, as extra keys
+        probs = r.pop("probs")
+        del probs
+        sw_args = argparse.Namespace(**{**vars(args), "steps": min(args.steps, 10), "warmup": min(args.warmup, 2)})
+        t0 = time.time()
+        sw = run_sweep(sw_args, torch, sd)
+        out["density_sweep"] = {"workload": sw["config"]["workload"], "ms_per_step": round(sw["ms_step"], 4),
+                                "value": sw["value"], "unit": "edges/s", "steps": sw_args.steps,
+                                "roofline": sw["roofline"], "achieved_hbm_gbs": sw["hbm"], "sweep": sw["sweep"],
+                                "crossover_density": sw["crossover"]}
+        log(f"density sweep {time.time() - t0:.1f}s")
     print(json.dumps(out), flush=True)
 
 

@@ -225,6 +225,41 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
                              const int32_t *y_col, const float *y_val, void *ws, int64_t ws_bytes,
                              int64_t *out_row_ptr, int32_t **out_col, float **out_val, int64_t *out_nnz);
 
+/*
+ * Profiling log.  While enabled, every forward call records a pair of HIP events on the net's stream around
+ * each layer's product launch(es) and around the format changes, so the log holds the GPU time of each.
+ * The kernel field names what ran (SDNN_KERNEL_*); layer is the layer index, or -1 for a format change.
+ * Recording costs two event records per entry and is not meant for calls under graph capture.
+ */
+enum {
+    SDNN_KERNEL_TRANSPOSE = 0,  /* dense batch-major <-> neuron-major activations (sdnn_forward_dense) */
+    SDNN_KERNEL_GATHER = 1,     /* dense-Y CSR product: fan-in gather (one wavefront per output neuron) */
+    SDNN_KERNEL_NARROW = 2,     /* dense-Y CSR product: narrow-chunk gather (16 lanes per output neuron) */
+    SDNN_KERNEL_SLOTS = 3,      /* dense-Y CSR product: LDS tiles, scalar-register fp64 weights */
+    SDNN_KERNEL_TILED = 4,      /* dense-Y CSR product: LDS tiles */
+    SDNN_KERNEL_DENSE_GEMM = 5, /* dense-W arm on the matrix cores */
+    SDNN_KERNEL_SPGEMM = 6,     /* sparse-Y product: row-wise SpGEMM with fused epilogue and compaction */
+    SDNN_KERNEL_DENSIFY = 7,    /* sparse rows -> dense neuron-major activations (sdnn_forward_csr) */
+    SDNN_KERNEL_PACK = 8,       /* dense activations -> CSR result (sdnn_forward_csr) */
+    SDNN_KERNEL_COMPACT = 9     /* sparse rows -> CSR result (sdnn_forward_csr) */
+};
+
+typedef struct {
+    int32_t layer;  /* layer index, or -1 */
+    int32_t kernel; /* SDNN_KERNEL_* */
+    float ms;       /* GPU time between the two events */
+} sdnn_kernel_time;
+
+/* enable != 0 clears the log and starts recording; 0 stops recording (the log is kept until read). */
+sdnn_status sdnn_net_set_profiling(sdnn_net net, int32_t enable);
+
+/*
+ * Synchronises the net's stream, writes up to max_records entries of the log, oldest first, into out
+ * (host), sets *count (host) to the number of entries the log held, and clears it.
+ * Errors: INVALID_OBJECT, NULL_POINTER, DEVICE.
+ */
+sdnn_status sdnn_net_read_profile(sdnn_net net, sdnn_kernel_time *out, int32_t max_records, int32_t *count);
+
 /* Free the net and the device memory the library allocated for it (synchronises its stream). */
 sdnn_status sdnn_net_free(sdnn_net net);
 

@@ -31,6 +31,13 @@ SDNN_SEMIRING_MAX_MIN = 2
 SDNN_SEMIRING_MIN_MAX = 3
 SDNN_SEMIRING_XOR_AND = 4
 
+# kernel ids of the profiling log (SDNN_KERNEL_*) and the kernels they stand for
+KERNEL_NAMES = {
+    0: "transpose_kernel", 1: "spmm_fanin_kernel", 2: "spmm_narrow_kernel", 3: "spmm_slots_kernel",
+    4: "spmm_tiled_kernel", 5: "gemm_dense_layer_kernel", 6: "spgemm_layer", 7: "densify", 8: "pack_dense_to_csr",
+    9: "compact_rows",
+}
+
 STATUS_NAMES = {
     0: "SDNN_OK", 1: "SDNN_ERR_NULL_POINTER", 2: "SDNN_ERR_INVALID_VALUE", 3: "SDNN_ERR_INVALID_INDEX",
     4: "SDNN_ERR_DIMENSION_MISMATCH", 5: "SDNN_ERR_INVALID_OBJECT", 6: "SDNN_ERR_WORKSPACE_TOO_SMALL",
@@ -67,10 +74,20 @@ _sig = {
     "sdnn_mxm_dense": [_P, _I32, _I32, _I64, _P, _P, _P, _I64],
     "sdnn_mxm_csr": [_P, _I32, _I32, _I64, _P, _P, _P, _P, _P, _I64],
     "sdnn_net_free": [_P],
+    "sdnn_net_set_profiling": [_P, _I32],
 }
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("layer", ctypes.c_int32), ("kernel", ctypes.c_int32), ("ms", ctypes.c_float)]
+
+
+lib_read_profile_args = [_P, _c.POINTER(KernelTime), _I32, _c.POINTER(_I32)]
 for _name, _args in _sig.items():
     getattr(lib, _name).argtypes = _args
     getattr(lib, _name).restype = _c.c_int
+lib.sdnn_net_read_profile.argtypes = lib_read_profile_args
+lib.sdnn_net_read_profile.restype = _c.c_int
 lib.sdnn_noalloc_scratch_bytes.argtypes = []
 lib.sdnn_noalloc_scratch_bytes.restype = _I64
 lib.sdnn_status_string.argtypes = [_c.c_int]
@@ -161,6 +178,18 @@ def sdnn_mxm_csr(net, k: int, semiring: int, batch: int, y_row_ptr, y_col, y_val
 
 def sdnn_net_free(net):
     _check(lib.sdnn_net_free(net))
+
+
+def sdnn_net_set_profiling(net, enable: bool):
+    _check(lib.sdnn_net_set_profiling(net, 1 if enable else 0))
+
+
+def sdnn_net_read_profile(net, max_records: int = 1 << 16):
+    """Up to max_records entries of the profiling log as (layer, kernel id, ms), oldest first; clears it."""
+    buf = (KernelTime * max(1, max_records))()
+    count = _I32()
+    _check(lib.sdnn_net_read_profile(net, buf, max_records, _c.byref(count)))
+    return [(r.layer, r.kernel, r.ms) for r in buf[:min(count.value, max_records)]]
 
 
 class Net:
@@ -284,6 +313,14 @@ class Net:
         col_t = ws[oc - base: oc - base + 4 * nnz].view(t.int32)
         val_t = ws[ov - base: ov - base + 4 * nnz].view(t.float32)
         return out_rp, col_t, val_t
+
+    def set_profiling(self, enable: bool = True):
+        sdnn_net_set_profiling(self.handle, enable)
+
+    def read_profile(self, max_records: int = 1 << 16):
+        """The profiling log as a list of (layer, kernel name, ms); clears it."""
+        return [(layer, KERNEL_NAMES.get(k, str(k)), ms)
+                for layer, k, ms in sdnn_net_read_profile(self.handle, max_records)]
 
     def free(self):
         if getattr(self, "handle", None):

@@ -195,7 +195,70 @@ struct sdnn_net_s {
     int32_t *d_int = nullptr;
     unsigned long long *d_stats = nullptr;  // kSpgemmStats counters per layer of a forward call
     int num_cu = 256;
+    // profiling log (sdnn_net_set_profiling): one pair of events around each timed launch sequence
+    struct ProfRec {
+        int32_t layer, kernel;
+        hipEvent_t a, b;
+    };
+    bool profiling = false;
+    std::vector<ProfRec> prof;
+    std::vector<hipEvent_t> ev_free;
 };
+
+namespace {
+
+hipError_t prof_event(sdnn_net net, hipEvent_t *e) {
+    if (!net->ev_free.empty()) {
+        *e = net->ev_free.back();
+        net->ev_free.pop_back();
+        return hipSuccess;
+    }
+    return hipEventCreate(e);
+}
+
+// Opens a profiling record for the launches that follow (layer -1: not a layer's product); *idx = -1 when
+// profiling is off.
+hipError_t prof_begin(sdnn_net net, int32_t layer, int kind, int *idx) {
+    *idx = -1;
+    if (!net->profiling) return hipSuccess;
+    sdnn_net_s::ProfRec r{layer, kind, nullptr, nullptr};
+    hipError_t e = prof_event(net, &r.a);
+    if (e != hipSuccess) return e;
+    e = prof_event(net, &r.b);
+    if (e == hipSuccess) e = hipEventRecord(r.a, net->stream);
+    if (e != hipSuccess) {
+        net->ev_free.push_back(r.a);
+        if (r.b) net->ev_free.push_back(r.b);
+        return e;
+    }
+    net->prof.push_back(r);
+    *idx = (int)net->prof.size() - 1;
+    return hipSuccess;
+}
+
+// Closes record idx (kind >= 0 replaces the kernel kind given at the start).
+hipError_t prof_end(sdnn_net net, int idx, int kind = -1) {
+    if (idx < 0) return hipSuccess;
+    if (kind >= 0) net->prof[(size_t)idx].kernel = kind;
+    return hipEventRecord(net->prof[(size_t)idx].b, net->stream);
+}
+
+void prof_clear(sdnn_net net) {
+    for (auto &r : net->prof) {
+        net->ev_free.push_back(r.a);
+        net->ev_free.push_back(r.b);
+    }
+    net->prof.clear();
+}
+
+}  // namespace
+
+static_assert(SDNN_KERNEL_TRANSPOSE == sdnn::kKernTranspose && SDNN_KERNEL_GATHER == sdnn::kKernGather &&
+                  SDNN_KERNEL_NARROW == sdnn::kKernNarrow && SDNN_KERNEL_SLOTS == sdnn::kKernSlots &&
+                  SDNN_KERNEL_TILED == sdnn::kKernTiled && SDNN_KERNEL_DENSE_GEMM == sdnn::kKernDenseGemm &&
+                  SDNN_KERNEL_SPGEMM == sdnn::kKernSpgemm && SDNN_KERNEL_DENSIFY == sdnn::kKernDensify &&
+                  SDNN_KERNEL_PACK == sdnn::kKernPack && SDNN_KERNEL_COMPACT == sdnn::kKernCompact,
+              "profiling kernel ids of the header and the library agree");
 
 extern "C" {
 
@@ -454,19 +517,27 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
     buf[0] = (float *)ws;
     buf[1] = (float *)((char *)ws + act_bytes(n, batch));
     double *partial = (double *)((char *)ws + 2 * act_bytes(n, batch));
+    int pr = -1;
+    SDNN_HIP(prof_begin(net, -1, sdnn::kKernTranspose, &pr));
     SDNN_HIP(sdnn::launch_transpose(Y_in, n, buf[0], ld, batch, n, s));  // batch x n -> n x batch
+    SDNN_HIP(prof_end(net, pr));
     int cur = 0;
     for (int32_t k = k0; k < k1; ++k) {
         const Layer &l = net->layers[(size_t)k];
+        int kind = sdnn::kKernDenseGemm;
+        SDNN_HIP(prof_begin(net, k, kind, &pr));
         if (arm == SDNN_ARM_SPARSE)
             SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, ld, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias,
-                                             net->ymax, net->bias_pattern, buf[cur], buf[cur ^ 1], s));
+                                             net->ymax, net->bias_pattern, buf[cur], buf[cur ^ 1], s, &kind));
         else
             SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, ld, l.dense_wt, l.bias, net->ymax, buf[cur],
                                                    buf[cur ^ 1], partial, net->num_cu, s));
+        SDNN_HIP(prof_end(net, pr, kind));
         cur ^= 1;
     }
+    SDNN_HIP(prof_begin(net, -1, sdnn::kKernTranspose, &pr));
     SDNN_HIP(sdnn::launch_transpose(buf[cur], ld, Y_out, n, n, batch, s));  // n x batch -> batch x n
+    SDNN_HIP(prof_end(net, pr));
     return SDNN_OK;
 }
 
@@ -557,11 +628,14 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
             break;
         }
         const bool first = k == k0;
+        int pr = -1;
+        SDNN_HIP(prof_begin(net, k, sdnn::kKernSpgemm, &pr));
         SDNN_HIP(sdnn::launch_spgemm_layer(n, batch, first ? y_row_ptr : nullptr, first ? nullptr : w.cnt[cur ^ 1],
                                            first ? y_col : w.col[cur ^ 1], first ? y_val : w.val[cur ^ 1], l.row_ptr,
                                            l.w_seg, l.w_pack, l.nnz, l.max_fanout, l.bias, l.bias_nonpos ? 1 : 0,
                                            net->bias_pattern, net->ymax, w.cnt[cur], w.col[cur], w.val[cur], w.lists,
                                            net->d_stats + sdnn::kSpgemmStats * (k - k0), net->d_flags, net->num_cu, s));
+        SDNN_HIP(prof_end(net, pr));
         cur ^= 1;
         const double full = (double)batch * (double)n;
         nnz_hi = (l.bias_nonpos || net->bias_pattern) ? std::min(full, nnz_hi * (double)l.max_fanout) : full;
@@ -579,16 +653,23 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         // quarter of batch * n entries (measured on MI355X: 0.34 instead of 0.69 ms for 32M entries into
         // 16384 x 4096; at 2% density the extra transpose costs more than the scattered stores it saves)
         float *stage = nnz_hi >= (double)batch * (double)n / 4.0 ? dense[1] : nullptr;
+        int pr = -1;
+        SDNN_HIP(prof_begin(net, -1, sdnn::kKernDensify, &pr));
         SDNN_HIP(sdnn::launch_densify(n, batch, ld, from_user ? y_row_ptr : nullptr, from_user ? nullptr : w.cnt[cur ^ 1],
                                       from_user ? y_col : w.col[cur ^ 1], from_user ? y_val : w.val[cur ^ 1],
                                       dense[0], stage, net->d_flags, s));
+        SDNN_HIP(prof_end(net, pr));
         int dc = 0;
         for (int32_t k = kd; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
+            int kind = sdnn::kKernGather;
+            SDNN_HIP(prof_begin(net, k, kind, &pr));
             SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, ld, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias,
-                                             net->ymax, net->bias_pattern, dense[dc], dense[dc ^ 1], s));
+                                             net->ymax, net->bias_pattern, dense[dc], dense[dc ^ 1], s, &kind));
+            SDNN_HIP(prof_end(net, pr, kind));
             dc ^= 1;
         }
+        SDNN_HIP(prof_begin(net, -1, sdnn::kKernPack, &pr));
         SDNN_HIP(sdnn::launch_transpose(dense[dc], ld, dense[dc ^ 1], n, n, batch, s));  // -> batch x n
         if (n % 4 == 0) {
             // counted first, then packed straight into the other buffer pair (no slot rows in between)
@@ -602,14 +683,18 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
             last = db ^ 1;
             outb = db;
         }
+        SDNN_HIP(prof_end(net, pr));
     } else {
         last = cur ^ 1;
         outb = cur;
     }
     if (!packed) {
+        int pr = -1;
+        SDNN_HIP(prof_begin(net, -1, sdnn::kKernCompact, &pr));
         SDNN_HIP(sdnn::launch_exclusive_scan_i32_to_i64(batch, w.cnt[last], out_row_ptr, w.scan_tmp, s));
         SDNN_HIP(sdnn::launch_compact_rows(n, batch, w.cnt[last], out_row_ptr, w.col[last], w.val[last],
                                            w.col[outb], w.val[outb], s));
+        SDNN_HIP(prof_end(net, pr));
     }
     int64_t nnz = 0;
     uint32_t flags = 0;
@@ -681,11 +766,39 @@ sdnn_status sdnn_mxm_csr(sdnn_net net, int32_t k, int32_t semiring, int64_t batc
     return SDNN_OK;
 }
 
+sdnn_status sdnn_net_set_profiling(sdnn_net net, int32_t enable) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    if (enable) prof_clear(net);
+    net->profiling = enable != 0;
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_net_read_profile(sdnn_net net, sdnn_kernel_time *out, int32_t max_records, int32_t *count) {
+    g_last_error.clear();
+    if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    if (!count || (max_records > 0 && !out)) return fail(SDNN_ERR_NULL_POINTER, "count (and out) are required");
+    SDNN_ON_DEVICE(net);
+    SDNN_HIP(hipStreamSynchronize(net->stream));
+    *count = (int32_t)std::min<size_t>(net->prof.size(), 0x7fffffff);
+    for (size_t i = 0; i < net->prof.size() && (int64_t)i < (int64_t)max_records; ++i) {
+        float ms = 0.0f;
+        SDNN_HIP(hipEventElapsedTime(&ms, net->prof[i].a, net->prof[i].b));
+        out[i].layer = net->prof[i].layer;
+        out[i].kernel = net->prof[i].kernel;
+        out[i].ms = ms;
+    }
+    prof_clear(net);
+    return SDNN_OK;
+}
+
 sdnn_status sdnn_net_free(sdnn_net net) {
     g_last_error.clear();
     if (!net) return SDNN_OK;
     DeviceScope device_scope(net->device);  // frees on the net's device even if it cannot be made current
     (void)hipStreamSynchronize(net->stream);
+    prof_clear(net);
+    for (hipEvent_t e : net->ev_free) (void)hipEventDestroy(e);
     for (Layer &l : net->layers) release(l);
     dfree(net->d_flags);
     dfree(net->d_int);

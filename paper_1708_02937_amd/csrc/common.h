@@ -14,6 +14,20 @@ struct __align__(8) Edge {
 
 constexpr int kWave = 64;
 
+// The kernels (or kernel sequences) a forward call launches, as the library's profiling log names them.
+enum KernelKind : int {
+    kKernTranspose = 0,   // dense batch-major <-> neuron-major activations
+    kKernGather = 1,      // dense-Y product: fan-in gather, one wave per neuron and 64 to 256 samples
+    kKernNarrow = 2,      // dense-Y product: narrow-chunk gather, 16 lanes per neuron, 64 samples
+    kKernSlots = 3,       // dense-Y product: LDS tiles with scalar-register fp64 weights
+    kKernTiled = 4,       // dense-Y product: LDS tiles, weights broadcast from lanes
+    kKernDenseGemm = 5,   // dense-W arm on the matrix cores
+    kKernSpgemm = 6,      // sparse-Y product: planning, small-sample and workgroup SpGEMM kernels
+    kKernDensify = 7,     // sparse rows -> dense neuron-major activations
+    kKernPack = 8,        // dense activations -> CSR result
+    kKernCompact = 9      // sparse slot rows -> CSR result
+};
+
 // Wave-local exclusive count of set bits below this lane in a 64-bit ballot.
 __device__ __forceinline__ int lane_rank(uint64_t mask) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
@@ -69,9 +83,10 @@ hipError_t launch_spmm_slots(int64_t n, const int64_t *fan_ptr, const Edge *fan,
 // pattern != 0: the bias and h apply only where some fan-in entry meets a nonzero input (else 0).
 // tile_mask / slots: the high fan-in structures when the layer has them (else null).
 // yt, zt: n x batch at row pitch ld (act_ld(n, batch)).
+// kind (may be null) receives which product kernel ran (a KernelKind).
 hipError_t launch_spmm_fanin(int64_t n, int64_t batch, int64_t ld, const int64_t *fan_ptr, const Edge *fan,
                              const uint16_t *tile_mask, const double *slots, const float *bias, double ymax, int pattern,
-                             const float *yt, float *zt, hipStream_t s);
+                             const float *yt, float *zt, hipStream_t s, int *kind = nullptr);
 
 // gemm.hip
 hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *wt, hipStream_t s);

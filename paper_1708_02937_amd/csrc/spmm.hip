@@ -766,9 +766,13 @@ hipError_t launch_spmm_tile_mask(int64_t n, const int64_t *fan_ptr, const Edge *
 
 hipError_t launch_spmm_fanin(int64_t n, int64_t batch, int64_t ld, const int64_t *fan_ptr, const Edge *fan,
                              const uint16_t *tile_mask, const double *slots, const float *bias, double ymax, int pattern,
-                             const float *yt, float *zt, hipStream_t s) {
+                             const float *yt, float *zt, hipStream_t s, int *kind) {
+    int kind_local = kKernGather;
+    if (!kind) kind = &kind_local;
+    *kind = kKernGather;
     if (n == 0 || batch == 0) return hipSuccess;
     if (slots && tile_mask && batch % 4 == 0 && batch >= 128) {
+        *kind = kKernSlots;
         const int64_t chunks = (batch + kTiledCB - 1) / kTiledCB;
         const int64_t groups = mask_pitch(n) / kSlotNJ;
         const int64_t blocks = (groups + 7) / 8 * 8 * chunks;
@@ -782,6 +786,7 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, int64_t ld, const int64_t
         return hipGetLastError();
     }
     if (tile_mask && batch % 4 == 0 && batch >= 128) {
+        *kind = kKernTiled;
         const int64_t chunks = (batch + kTiledCB - 1) / kTiledCB;
         const int64_t groups = (n + kTiledNJ - 1) / kTiledNJ;
         const int64_t blocks = (groups + 7) / 8 * 8 * chunks;
@@ -803,6 +808,7 @@ hipError_t launch_spmm_fanin(int64_t n, int64_t batch, int64_t ld, const int64_t
     // measured 1.1-1.3x)
     if (((n > 4096 && n <= 16384) || (batch < 256 && n >= 4096 && n <= (1 << 24))) && batch % 4 == 0 &&
         ld * 4 < (1 << 24)) {
+        *kind = kKernNarrow;
         constexpr int V = 4;
         const int64_t chunks = (batch + kNarrowP * V - 1) / (kNarrowP * V);
         const int64_t groups = (n + 4 * (64 / kNarrowP) - 1) / (4 * (64 / kNarrowP));  // 16 neurons per workgroup

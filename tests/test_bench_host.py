@@ -105,23 +105,26 @@ def test_summarize_pmc_scales_by_the_copy_probe(tmp_path):
     assert "    cmd one" in out.read_text()
 
 
-def test_kernel_name_matches_the_selection_rule():
-    # scalar-register kernel from density 2/9 (9 nnz >= 2 n^2)
-    assert bench.spmm_kernel_name(4096, 3728271) == "spmm_slots_kernel"
-    assert bench.spmm_kernel_name(4096, 3728270) == "spmm_fanin_kernel"
-    # the slot array (16-row tiles x 64-padded columns, fp64) beyond 2 GiB: readlane-fed tiled kernel from
-    # density 0.3 (10 nnz >= 3 n^2)
-    n = 16448
-    assert math.ceil(n / 16) * 16 * math.ceil(n / 64) * 64 * 8 > 2 ** 31
-    assert bench.spmm_kernel_name(n, 81161012) == "spmm_tiled_kernel"
-    assert bench.spmm_kernel_name(n, 81161011) == "spmm_fanin_kernel"
-    assert bench.spmm_kernel_name(65537, 65537 ** 2) == "spmm_fanin_kernel"
-    # wide layers up to n = 16384 with whole 16-byte lane loads: the narrow-chunk gather
-    assert bench.spmm_kernel_name(16384, 524288, 4096) == "spmm_narrow_kernel"
-    assert bench.spmm_kernel_name(4097, 10 ** 5, 302) == "spmm_fanin_kernel"
-    assert bench.spmm_kernel_name(16385, 524288, 4096) == "spmm_fanin_kernel"
-    assert bench.spmm_kernel_name(4096, 3728271, 130) == "spmm_fanin_kernel"  # the tiled kernels need 4 | batch
-    # batches under 256 take the narrow-chunk gather from n = 4096 on
-    assert bench.spmm_kernel_name(32768, 10 ** 6, 64) == "spmm_narrow_kernel"
-    assert bench.spmm_kernel_name(4096, 10 ** 5, 64) == "spmm_narrow_kernel"
-    assert bench.spmm_kernel_name(4095, 10 ** 5, 64) == "spmm_fanin_kernel"
+def test_kernel_split_and_roofline_from_profile_records():
+    """The dominant kernel's roofline and HBM fields from profiling-log records: algorithmic bytes per launch
+    (averaged over the launches' layers) divided by the average launch time."""
+    from workloads import Layer, Problem
+    import numpy as np
+
+    n, batch = 1000, 256
+    layers = [Layer(np.zeros(n + 1, np.int64), np.zeros(0, np.int32), np.zeros(0, np.float32),
+                    np.zeros(n, np.float32)) for _ in range(2)]
+    layers[0].row_ptr[-1] = 3000  # only nnz is read
+    layers[1].row_ptr[-1] = 5000
+    p = Problem("t", n, 2, batch, math.inf, layers)
+    recs = [(-1, "densify", 0.5), (0, "spmm_fanin_kernel", 2.0), (1, "spmm_fanin_kernel", 4.0), (-1, "pack", 1.0)]
+    split = bench.kernel_split(recs)
+    assert split["spmm_fanin_kernel"]["launches"] == 2 and split["spmm_fanin_kernel"]["avg_ms"] == 3.0
+    roof = bench.kernel_roofline("spmm_fanin_kernel", split["spmm_fanin_kernel"], p)
+    want_bytes = 8 * n * batch + 8 * 4000 + 8 * (n + 1) + 4 * n
+    assert roof["bound"] == "hbm" and roof["algorithmic_bytes_per_launch"] == want_bytes
+    assert roof["achieved"] == pytest.approx(round(want_bytes / 3e-3 / 1e9, 1))
+    hbm = bench.hbm_fields(roof, 2 * want_bytes)
+    assert hbm["effective"] == pytest.approx(want_bytes / 3e-3 / 1e9, abs=0.051)
+    assert hbm["counter"] == pytest.approx(2 * want_bytes / 3e-3 / 1e9, abs=0.051)
+    assert bench.hbm_fields(roof, None)["counter"] is None

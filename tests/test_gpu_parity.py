@@ -708,3 +708,27 @@ def test_errors_leave_net_usable(sd):
     got = net.forward_dense(y).cpu().numpy()  # still usable
     parity.compare(p, dense_to_csr(got))
     net.free()
+
+
+def test_profiling_log_names_each_launch(sd):
+    """The profiling log holds one record per layer product and per format change, in launch order, with
+    the kernel that ran and a positive GPU time; reading clears it, and nothing is recorded while off."""
+    import torch
+
+    p = make_config(1)
+    net = sd.net_from_problem(p)
+    y = torch.from_numpy(p.y0_dense).cuda()
+    net.set_profiling(True)
+    net.forward_dense(y)
+    net.forward_csr(*p.y0_as_csr(), k0=0, k1=2)
+    net.set_profiling(False)
+    rec = net.read_profile()
+    _say("profiling log", rec)
+    names = [r[1] for r in rec]
+    assert names[:6] == ["transpose_kernel"] + ["spmm_fanin_kernel"] * 4 + ["transpose_kernel"]
+    assert [r[0] for r in rec[:6]] == [-1, 0, 1, 2, 3, -1]
+    assert all(r[2] > 0 for r in rec)
+    assert net.read_profile() == []
+    net.forward_dense(y)
+    assert net.read_profile() == []
+    net.free()
