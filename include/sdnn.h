@@ -241,7 +241,8 @@ enum {
     SDNN_KERNEL_SPGEMM = 6,     /* sparse-Y product: row-wise SpGEMM with fused epilogue and compaction */
     SDNN_KERNEL_DENSIFY = 7,    /* sparse rows -> dense neuron-major activations (sdnn_forward_csr) */
     SDNN_KERNEL_PACK = 8,       /* dense activations -> CSR result (sdnn_forward_csr) */
-    SDNN_KERNEL_COMPACT = 9     /* sparse rows -> CSR result (sdnn_forward_csr) */
+    SDNN_KERNEL_COMPACT = 9,    /* sparse rows -> CSR result (sdnn_forward_csr) */
+    SDNN_KERNEL_BLOCKED = 10    /* dense-Y CSR product on the sample-blocked layout of very wide layers */
 };
 
 typedef struct {

@@ -35,7 +35,7 @@ SDNN_SEMIRING_XOR_AND = 4
 KERNEL_NAMES = {
     0: "transpose_kernel", 1: "spmm_fanin_kernel", 2: "spmm_narrow_kernel", 3: "spmm_slots_kernel",
     4: "spmm_tiled_kernel", 5: "gemm_dense_layer_kernel", 6: "spgemm_layer", 7: "densify", 8: "pack_dense_to_csr",
-    9: "compact_rows",
+    9: "compact_rows", 10: "spmm_blocked_kernel",
 }
 
 STATUS_NAMES = {

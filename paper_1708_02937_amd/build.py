@@ -12,7 +12,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsdnn.so")
-SOURCES = ["setup.hip", "spmm.hip", "gemm.hip", "spgemm.hip", "semiring.hip", "api.cpp"]
+SOURCES = ["setup.hip", "spmm.hip", "gemm.hip", "spgemm.hip", "semiring.hip", "blocked.hip", "api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -74,6 +74,7 @@ struct Layer {
     uint16_t *tile_mask = nullptr;  // which rows of each 16-row input tile each fan-in list holds (high fan-in only)
     double *slots = nullptr;        // fp64 weight of every (input, output) pair, tile-major (high fan-in, n^2 fits)
     int32_t *w_seg = nullptr;     // where each fan-out row crosses each accumulator window (wide layers only)
+    sdnn::BlockedSched *sched = nullptr;  // schedule of the blocked product (very wide layers only)
     double *dense_wt = nullptr;  // n x n, W_k row-major in fp64 (zeros explicit), for the dense arm
 };
 
@@ -90,6 +91,7 @@ void release(Layer &l) {
     dfree(l.tile_mask);
     dfree(l.slots);
     dfree(l.w_seg);
+    dfree(l.sched);
     dfree(l.dense_wt);
     l = Layer();
 }
@@ -118,6 +120,7 @@ struct CsrWs {
     float *val[2];
     int32_t *lists;  // 3 * batch: the sample lists of the layer being computed
     int64_t *scan_tmp;
+    int32_t *pcnt;   // per (part, sample) counts of the blocked -> CSR packing
     size_t bytes;
 };
 
@@ -138,6 +141,8 @@ CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
     off = align_up(off + 3 * (size_t)batch * sizeof(int32_t));
     w.scan_tmp = (int64_t *)(p + off);
     off = align_up(off + (size_t)sdnn::scan_tmp_elems(batch) * sizeof(int64_t));
+    w.pcnt = (int32_t *)(p + off);
+    if (sdnn::blocked_wanted(n, batch)) off = align_up(off + sdnn::blocked_pack_elems(n, batch) * sizeof(int32_t));
     w.bytes = off;
     return w;
 }
@@ -257,7 +262,8 @@ static_assert(SDNN_KERNEL_TRANSPOSE == sdnn::kKernTranspose && SDNN_KERNEL_GATHE
                   SDNN_KERNEL_NARROW == sdnn::kKernNarrow && SDNN_KERNEL_SLOTS == sdnn::kKernSlots &&
                   SDNN_KERNEL_TILED == sdnn::kKernTiled && SDNN_KERNEL_DENSE_GEMM == sdnn::kKernDenseGemm &&
                   SDNN_KERNEL_SPGEMM == sdnn::kKernSpgemm && SDNN_KERNEL_DENSIFY == sdnn::kKernDensify &&
-                  SDNN_KERNEL_PACK == sdnn::kKernPack && SDNN_KERNEL_COMPACT == sdnn::kKernCompact,
+                  SDNN_KERNEL_PACK == sdnn::kKernPack && SDNN_KERNEL_COMPACT == sdnn::kKernCompact &&
+                  SDNN_KERNEL_BLOCKED == sdnn::kKernBlocked,
               "profiling kernel ids of the header and the library agree");
 
 extern "C" {
@@ -380,7 +386,7 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     };
     if ((st = dalloc(&nl.w_pack, (size_t)nnz, "packed W_k")) != SDNN_OK) return cleanup(st);
     if ((st = dalloc(&nl.fan_ptr, (size_t)n + 1, "fan-in pointers")) != SDNN_OK) return cleanup(st);
-    if ((st = dalloc(&nl.fan, (size_t)nnz, "fan-in lists")) != SDNN_OK) return cleanup(st);
+    if ((st = dalloc(&nl.fan, (size_t)nnz + 1, "fan-in lists")) != SDNN_OK) return cleanup(st);  // + a zero guard entry
     if ((st = dalloc(&counts, (size_t)n, "fan-in counts")) != SDNN_OK) return cleanup(st);
     if ((st = dalloc(&tmp, (size_t)sdnn::scan_tmp_elems(n), "scan scratch")) != SDNN_OK) return cleanup(st);
     if ((st = dalloc(&sort_scratch, sdnn::fanin_sort_bytes(nnz), "sort scratch")) != SDNN_OK) return cleanup(st);
@@ -396,6 +402,7 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     SETUP_HIP(sdnn::launch_fanin_counts(nnz, col_idx, counts, s));
     SETUP_HIP(sdnn::launch_exclusive_scan_i32_to_i64(n, counts, nl.fan_ptr, tmp, s));
     SETUP_HIP(sdnn::launch_fanin_lists(n, nnz, row_ptr, col_idx, val, nl.fan, sort_scratch, s));
+    SETUP_HIP(hipMemsetAsync(nl.fan + nnz, 0, sizeof(Edge), s));
     SETUP_HIP(hipMemsetAsync(net->d_int, 0, sizeof(int32_t), s));
     SETUP_HIP(sdnn::launch_max_segment(n, row_ptr, net->d_int, s));
     SETUP_HIP(hipMemcpyAsync(&nl.max_fanout, net->d_int, sizeof(int32_t), hipMemcpyDeviceToHost, s));
@@ -403,6 +410,11 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
         if ((st = dalloc(&nl.w_seg, (size_t)n * (size_t)(sdnn::spgemm_windows(n) + 1), "window offsets")) != SDNN_OK)
             return cleanup(st);
         SETUP_HIP(sdnn::launch_window_seg(n, row_ptr, col_idx, nl.w_seg, s));
+    }
+    if (sdnn::blocked_wanted(n, 1 << 20)) {  // a layer wide enough that large batches take the blocked product
+        if ((st = dalloc(&nl.sched, (size_t)sdnn::blocked_sched_elems(n), "blocked schedule")) != SDNN_OK)
+            return cleanup(st);
+        SETUP_HIP(sdnn::launch_blocked_order(n, nl.fan_ptr, nl.sched, s));
     }
     if (sdnn::spmm_wants_tiles(n, nnz)) {
         if ((st = dalloc(&nl.tile_mask, sdnn::spmm_tile_mask_elems(n), "tile masks")) != SDNN_OK)
@@ -518,6 +530,25 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
     buf[1] = (float *)((char *)ws + act_bytes(n, batch));
     double *partial = (double *)((char *)ws + 2 * act_bytes(n, batch));
     int pr = -1;
+    if (arm == SDNN_ARM_SPARSE && sdnn::blocked_wanted(n, batch)) {
+        // very wide layers: the sample-blocked layout (each buffer holds n x ld >= n x round32(batch) floats)
+        SDNN_HIP(prof_begin(net, -1, sdnn::kKernTranspose, &pr));
+        SDNN_HIP(sdnn::launch_to_blocked(n, batch, n, Y_in, buf[0], s));
+        SDNN_HIP(prof_end(net, pr));
+        int cb = 0;
+        for (int32_t k = k0; k < k1; ++k) {
+            const Layer &l = net->layers[(size_t)k];
+            SDNN_HIP(prof_begin(net, k, sdnn::kKernBlocked, &pr));
+            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.fan, l.bias, net->ymax, net->bias_pattern, buf[cb],
+                                               buf[cb ^ 1], s));
+            SDNN_HIP(prof_end(net, pr));
+            cb ^= 1;
+        }
+        SDNN_HIP(prof_begin(net, -1, sdnn::kKernTranspose, &pr));
+        SDNN_HIP(sdnn::launch_from_blocked(n, batch, n, buf[cb], Y_out, s));
+        SDNN_HIP(prof_end(net, pr));
+        return SDNN_OK;
+    }
     SDNN_HIP(prof_begin(net, -1, sdnn::kKernTranspose, &pr));
     SDNN_HIP(sdnn::launch_transpose(Y_in, n, buf[0], ld, batch, n, s));  // batch x n -> n x batch
     SDNN_HIP(prof_end(net, pr));
@@ -643,7 +674,33 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     }
     int last = 0, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
     bool packed = false;  // the CSR is already in buffer outb
-    if (kd < k1) {
+    if (kd < k1 && sdnn::blocked_wanted(n, batch)) {
+        // very wide layers: dense activations in the sample-blocked layout, packed straight into CSR at the end
+        const bool from_user = kd == k0;
+        const int db = from_user ? 0 : cur;  // the input rows (if any) sit in buffer cur ^ 1
+        float *dense[2] = {reinterpret_cast<float *>(w.col[db]), w.val[db]};
+        int pr = -1;
+        SDNN_HIP(prof_begin(net, -1, sdnn::kKernDensify, &pr));
+        SDNN_HIP(sdnn::launch_densify_blocked(n, batch, from_user ? y_row_ptr : nullptr, from_user ? nullptr : w.cnt[cur ^ 1],
+                                              from_user ? y_col : w.col[cur ^ 1], from_user ? y_val : w.val[cur ^ 1],
+                                              dense[0], net->d_flags, s));
+        SDNN_HIP(prof_end(net, pr));
+        int dc = 0;
+        for (int32_t k = kd; k < k1; ++k) {
+            const Layer &l = net->layers[(size_t)k];
+            SDNN_HIP(prof_begin(net, k, sdnn::kKernBlocked, &pr));
+            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.fan, l.bias, net->ymax, net->bias_pattern,
+                                               dense[dc], dense[dc ^ 1], s));
+            SDNN_HIP(prof_end(net, pr));
+            dc ^= 1;
+        }
+        SDNN_HIP(prof_begin(net, -1, sdnn::kKernPack, &pr));
+        SDNN_HIP(sdnn::launch_blocked_to_csr(n, batch, dense[dc], w.pcnt, w.cnt[db ^ 1], out_row_ptr, w.scan_tmp,
+                                             w.col[db ^ 1], w.val[db ^ 1], s));
+        SDNN_HIP(prof_end(net, pr));
+        packed = true;
+        outb = db ^ 1;
+    } else if (kd < k1) {
         const bool from_user = kd == k0;
         const int db = from_user ? 0 : cur;  // the input rows (if any) sit in buffer cur ^ 1
         // two n x batch fp32 buffers at row pitch ld

@@ -1,0 +1,534 @@
+// Dense-Y layer product for very wide layers, on a sample-blocked activation layout (Sec. III batched
+// inference equation; Sec. IV loop body: the +.x product with the bias and ReLU fused into its epilogue).
+//
+// Layout.  The batch is cut into chunks of kBW = 32 samples; chunk c holds, for every neuron j, the 32
+// values of samples 32c .. 32c + 31 in one 128-byte row: element (sample r, neuron i) sits at float
+// ((r / 32) * n + i) * 32 + r % 32.  One chunk is a contiguous n x 128-byte block (128 MiB at n = 2^20),
+// which the 256 MB Infinity Cache and the TLB hold while the whole chip works on it, and a row is one L2
+// line.  With the neuron-major layout (n rows of `batch` samples) a chunk's slice is scattered over the
+// whole activation buffer instead.
+//
+// Product.  Each wavefront owns eight output neurons, eight lanes each, four samples per lane (one 16-byte
+// load of an input row per fan-in entry); all lanes walk their own neuron's fan-in list in step.  The eight
+// neurons of a wave come from a per-layer order (set-up) that sorts every run of 4096 consecutive neurons by
+// fan-in length, so the lists a wave walks together have nearly equal lengths: the common part runs without
+// predication, the few remaining entries with a per-lane guard.  Products are exact in fp64 and summed in
+// list order (ascending input index, as every other dense-Y kernel); bias, h and the single rounding are
+// fused.  XCD-aware order: all workgroups of a chunk are dispatched before the next chunk's, and within a
+// chunk XCD x (workgroup index mod 8) takes the x-th contiguous eighth of the neuron order, so the rows of
+// the 4096-wide neighbourhood a block-structured layer reads stay in that XCD's L2 while the rest of the
+// chunk is read from the Infinity Cache.
+#include <algorithm>
+
+#include "common.h"
+
+namespace sdnn {
+
+namespace {
+
+constexpr int kBW = 32;          // samples per chunk (one 128-byte row per neuron)
+constexpr int kSortSeg = 4096;   // neurons per sort segment of the processing order
+#ifndef SDNN_BLOCKED_GROUPS
+#define SDNN_BLOCKED_GROUPS 2
+#endif
+constexpr int kBWaves = 4;       // waves per workgroup of the product
+constexpr int kBGroups = SDNN_BLOCKED_GROUPS;  // groups of eight neurons each wave takes in turn
+constexpr int kBTile = kBWaves * kBGroups * 8;  // neurons per workgroup and chunk
+#ifndef SDNN_BLOCKED_UNROLL
+#define SDNN_BLOCKED_UNROLL 8
+#endif
+constexpr int kBUnroll = SDNN_BLOCKED_UNROLL;  // list entries per block (rows in flight per lane)
+
+// ------------------------------------------------------------------------------------------ set-up
+
+// Processing order: within each segment of kSortSeg consecutive neurons, by fan-in length (longest first,
+// ties by index), so consecutive groups of eight have nearly equal lists.  One workgroup per segment:
+// bitonic sort of 64-bit keys (complemented length, local index) in LDS.  The result is one schedule entry
+// per position of the order (neuron, list length, list start), so the product reads it with one load;
+// positions past n (up to the padded length) hold an empty list at the guard entry fan[nnz] and neuron -1.
+__global__ __launch_bounds__(256) void blocked_order_kernel(int64_t n, int64_t padded, const int64_t *__restrict__ fan_ptr,
+                                                            BlockedSched *__restrict__ sched) {
+    __shared__ uint64_t key[kSortSeg];
+    const int64_t base = (int64_t)blockIdx.x * kSortSeg;
+    for (int t = threadIdx.x; t < kSortSeg; t += blockDim.x) {
+        const int64_t j = base + t;
+        if (j < n) {
+            const int64_t len = fan_ptr[j + 1] - fan_ptr[j];
+            const uint32_t lc = len > 0xffffffffLL ? 0u : 0xffffffffu - (uint32_t)len;
+            key[t] = ((uint64_t)lc << 32) | (uint32_t)t;
+        } else {
+            key[t] = ~0ull;  // past the end: sorts last
+        }
+    }
+    __syncthreads();
+    for (int k = 2; k <= kSortSeg; k <<= 1) {
+        for (int jj = k >> 1; jj > 0; jj >>= 1) {
+            for (int t = threadIdx.x; t < kSortSeg; t += blockDim.x) {
+                const int u = t ^ jj;
+                if (u > t) {
+                    const uint64_t a = key[t], b = key[u];
+                    const bool up = (t & k) == 0;
+                    if ((a > b) == up) {
+                        key[t] = b;
+                        key[u] = a;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    const int64_t nnz = fan_ptr[n];
+    for (int t = threadIdx.x; t < kSortSeg; t += blockDim.x) {
+        const int64_t pos = base + t;
+        if (pos >= padded) break;
+        BlockedSched e;
+        if (pos < n) {
+            const int64_t j = base + (int64_t)(uint32_t)key[t];
+            const int64_t len = fan_ptr[j + 1] - fan_ptr[j];
+            e.j = (int32_t)j;
+            e.len = (int32_t)len;
+            e.e0 = len > 0 ? fan_ptr[j] : nnz;
+        } else {
+            e.j = -1;
+            e.len = 0;
+            e.e0 = nnz;
+        }
+        sched[pos] = e;
+    }
+}
+
+// ------------------------------------------------------------------------------------------ product
+
+__device__ __forceinline__ float4 load_row(const char *yc, int32_t i, uint32_t lo) {
+    return *reinterpret_cast<const float4 *>(yc + ((uint32_t)i * (uint32_t)(kBW * 4) + lo));
+}
+
+template <bool kPattern>
+__device__ __forceinline__ void fma4(const float4 &y, float w, double (&acc)[4], uint32_t (&hit)[4]) {
+    const double wd = (double)w;
+    acc[0] = __builtin_fma((double)y.x, wd, acc[0]);
+    acc[1] = __builtin_fma((double)y.y, wd, acc[1]);
+    acc[2] = __builtin_fma((double)y.z, wd, acc[2]);
+    acc[3] = __builtin_fma((double)y.w, wd, acc[3]);
+    if constexpr (kPattern) {
+        hit[0] |= __float_as_uint(y.x);
+        hit[1] |= __float_as_uint(y.y);
+        hit[2] |= __float_as_uint(y.z);
+        hit[3] |= __float_as_uint(y.w);
+    }
+}
+
+// Wave-uniform minimum and maximum of a value that is equal within each group of eight lanes.
+__device__ __forceinline__ void group8_min_max(int v, int &mn, int &mx) {
+    int a = v, b = v;
+#pragma unroll
+    for (int off = 8; off < 64; off <<= 1) {
+        a = min(a, __shfl_xor(a, off));
+        b = max(b, __shfl_xor(b, off));
+    }
+    mn = __builtin_amdgcn_readfirstlane(a);
+    mx = __builtin_amdgcn_readfirstlane(b);
+}
+
+// grid: nchunks * 8 * gpx workgroups of kBWaves waves; gpx = workgroups per XCD per chunk, tiles = workgroups
+// per chunk (ceil(n / kBTile)).  Each wave takes kBGroups groups of eight consecutive positions of the
+// schedule in turn (the next group's schedule entry is loaded while the current group runs).  A group's lists
+// are walked in blocks of eight entries: the eight lanes of a neuron load the block's entries with one 8-byte
+// load each (entry t + sub, clamped to the list's last entry), pass them through the wave's LDS slot, and
+// read all eight back (a broadcast read), so the memory path carries each entry once per neuron rather than
+// once per lane; the next block's entries are loaded while the current block's rows are in flight.
+#ifndef SDNN_BLOCKED_WAVES_PER_EU
+#define SDNN_BLOCKED_WAVES_PER_EU 1
+#endif
+template <bool kPattern>
+__global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SDNN_BLOCKED_WAVES_PER_EU, 8))) void spmm_blocked_kernel(
+    int64_t n, int64_t gpx, int64_t tiles, const BlockedSched *__restrict__ sched, const Edge *__restrict__ fan,
+    const float *__restrict__ bias, double ymax, const float *__restrict__ yb, float *__restrict__ zb) {
+    __shared__ __align__(16) Edge ent[kBWaves][kBUnroll * 8];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int q = lane >> 3, sub = lane & 7;
+    const int64_t b = blockIdx.x;
+    const int64_t xcd = b & 7, local = b >> 3;
+    const int64_t c = local / gpx;
+    const int64_t g = xcd * gpx + (local - c * gpx);
+    if (g >= tiles) return;
+    const char *yc = reinterpret_cast<const char *>(yb + c * n * kBW);
+    float *zc = zb + c * n * kBW + sub * 4;
+    const uint32_t lo = (uint32_t)sub * 16u;
+    Edge *slot = &ent[wave][0];
+    const BlockedSched *sp = sched + (g * kBWaves + wave) * (kBGroups * 8) + q;
+    BlockedSched cur = sp[0];
+    for (int gi = 0; gi < kBGroups; ++gi) {
+        const BlockedSched nxt = sp[8 * min(gi + 1, kBGroups - 1)];
+        const float bj = bias[cur.j >= 0 ? cur.j : 0];
+        const int len = cur.len;
+        const Edge *lst = fan + cur.e0;
+        const int last = len > 0 ? len - 1 : 0;
+        int mn, mx;
+        group8_min_max(len, mn, mx);
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
+        uint32_t hit[4] = {0u, 0u, 0u, 0u};
+        constexpr int kR = kBUnroll / 8;  // entries each lane loads per block
+        Edge mine[kR];
+#pragma unroll
+        for (int r = 0; r < kR; ++r) mine[r] = lst[min(8 * r + sub, last)];
+        for (int t = 0; t < mx; t += kBUnroll) {
+            // this block's entries of the lane's neuron: entry t + 8r + u at slot[64r + 8q + u]
+#pragma unroll
+            for (int r = 0; r < kR; ++r) slot[64 * r + lane] = mine[r];
+            __builtin_amdgcn_wave_barrier();
+            Edge e[kBUnroll];
+#pragma unroll
+            for (int r = 0; r < kR; ++r)
+#pragma unroll
+                for (int u = 0; u < 8; ++u) e[8 * r + u] = slot[64 * r + q * 8 + u];
+            __builtin_amdgcn_wave_barrier();
+            float4 y[kBUnroll];
+#pragma unroll
+            for (int u = 0; u < kBUnroll; ++u) y[u] = load_row(yc, e[u].idx, lo);
+#pragma unroll
+            for (int r = 0; r < kR; ++r) mine[r] = lst[min(t + kBUnroll + 8 * r + sub, last)];  // the next block's
+            __builtin_amdgcn_sched_barrier(0);
+            if (t + kBUnroll <= mn) {
+#pragma unroll
+                for (int u = 0; u < kBUnroll; ++u) fma4<kPattern>(y[u], e[u].w, acc, hit);
+            } else {
+                // entries past a lane's end add a zeroed input, which leaves its sum unchanged
+#pragma unroll
+                for (int u = 0; u < kBUnroll; ++u) {
+                    float4 yv = y[u];
+                    if (t + u >= len) yv = make_float4(0.f, 0.f, 0.f, 0.f);
+                    fma4<kPattern>(yv, e[u].w, acc, hit);
+                }
+            }
+        }
+        if (cur.j >= 0) {
+            const double bd = (double)bj;
+            float4 out;
+            out.x = (kPattern && (hit[0] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[0] + bd, ymax);
+            out.y = (kPattern && (hit[1] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[1] + bd, ymax);
+            out.z = (kPattern && (hit[2] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[2] + bd, ymax);
+            out.w = (kPattern && (hit[3] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[3] + bd, ymax);
+            *reinterpret_cast<float4 *>(zc + (int64_t)cur.j * kBW) = out;
+        }
+        cur = nxt;
+    }
+}
+
+// ------------------------------------------------------------------------------------------ format changes
+
+// Sparse rows -> blocked activations.  One workgroup per (chunk, part of the neurons); 16 threads per sample.
+// The part is walked in ranges of kDensR neurons: the range's 32 x kDensR tile is zeroed in LDS, each
+// sample's entries that fall in the range are written into it (the sample's cursor moves forward through
+// its sorted row), and the tile is stored as kDensR whole 128-byte rows.  The first entry of the part is
+// found by a binary search per sample.  Row extents are checked as in the other format changes, and the
+// part-0 workgroups also check every column of their samples.
+constexpr int kDensR = 256;
+constexpr int kDensThreads = 512;
+
+__global__ __launch_bounds__(kDensThreads) void densify_blocked_kernel(
+    int64_t n, int64_t batch, int64_t part_len, const int64_t *__restrict__ in_row_ptr,
+    const int32_t *__restrict__ in_cnt, const int32_t *__restrict__ in_col, const float *__restrict__ in_val,
+    float *__restrict__ yb, uint32_t *err) {
+    __shared__ float tile[kDensR * kBW];
+    const int64_t nparts = (n + part_len - 1) / part_len;
+    const int64_t c = blockIdx.x / nparts, part = blockIdx.x % nparts;
+    const int s = threadIdx.x >> 4, k = threadIdx.x & 15;  // sample of the chunk, thread within the sample
+    const int64_t r = c * kBW + s;
+    const int64_t a0 = part * part_len, a1 = min(n, a0 + part_len);
+    int64_t rb = 0, re = 0;
+    if (r < batch) {
+        if (in_row_ptr) {
+            const int64_t nnz = (in_col && in_val) ? in_row_ptr[batch] : 0;
+            rb = in_row_ptr[r];
+            re = in_row_ptr[r + 1];
+            if (rb < 0 || re < rb || re - rb > n || re > nnz) {
+                if (k == 0 && part == 0) atomicOr(err, 1u);
+                rb = re = 0;
+            }
+        } else {
+            rb = r * n;
+            re = rb + in_cnt[r];
+        }
+    }
+    if (part == 0)
+        for (int64_t t = rb + k; t < re; t += 16) {
+            const int32_t i = in_col[t];
+            if (i < 0 || i >= n) atomicOr(err, 1u);
+        }
+    // first entry with column >= a0 (columns ascending within a row)
+    int64_t lo = rb, hi = re;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (in_col[mid] < a0) lo = mid + 1;
+        else hi = mid;
+    }
+    int64_t cur = lo;  // equal across the sample's 16 threads
+    for (int64_t a = a0; a < a1; a += kDensR) {
+        const int64_t ra = min<int64_t>(kDensR, a1 - a);
+        for (int t = threadIdx.x; t < kDensR * kBW; t += kDensThreads) tile[t] = 0.0f;
+        __syncthreads();
+        // entries of this range: [cur, next) with next the first column >= a + kDensR
+        int64_t next = cur;
+        for (;;) {
+            const int64_t t = next + k;
+            const int32_t i = t < re ? in_col[t] : 0x7fffffff;
+            const bool in = i < a + ra;
+            if (in && i >= a) tile[(i - a) * kBW + s] = in_val[t];
+            // the 16 threads of a sample share one ballot segment: advance past the leading run that is in range
+            const uint64_t m = __ballot(in);
+            const uint32_t seg = (uint32_t)(m >> (threadIdx.x & 48)) & 0xffffu;
+            const int run = __builtin_ctz(~seg | 0x10000u);
+            next += run;
+            if (run < 16) break;
+        }
+        cur = next;
+        __syncthreads();
+        float4 *dst = reinterpret_cast<float4 *>(yb + (c * n + a) * kBW);
+        const float4 *srct = reinterpret_cast<const float4 *>(tile);
+        for (int t = threadIdx.x; t < ra * (kBW / 4); t += kDensThreads) dst[t] = srct[t];
+        __syncthreads();
+    }
+}
+
+// Blocked activations -> CSR rows, in three steps.  Count: one wavefront per (chunk, part of kPackR
+// neurons) counts each sample's nonzeros in the part (lane = neuron, one ballot per sample).  Scan: per
+// sample, the part counts become offsets within the row and the row total goes to cnt.  Pack: the same
+// traversal writes each sample's survivors in ascending neuron order at row_ptr[r] + offset.
+constexpr int kPackR = 2048;
+
+__global__ __launch_bounds__(256) void blocked_count_kernel(int64_t n, int64_t batch, int64_t nparts,
+                                                            const float *__restrict__ yb, int32_t *__restrict__ pcnt) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t nchunks = (batch + kBW - 1) / kBW;
+    if (w >= nchunks * nparts) return;
+    const int64_t c = w / nparts, part = w % nparts;
+    const int64_t a0 = part * kPackR, a1 = min(n, a0 + kPackR);
+    int cnt[kBW];
+#pragma unroll
+    for (int s = 0; s < kBW; ++s) cnt[s] = 0;
+    for (int64_t a = a0; a < a1; a += 64) {
+        const int64_t j = a + lane;
+        float v[kBW];
+        if (j < a1) {
+            const float4 *row = reinterpret_cast<const float4 *>(yb + (c * n + j) * kBW);
+#pragma unroll
+            for (int q = 0; q < kBW / 4; ++q) {
+                const float4 f = row[q];
+                v[4 * q] = f.x;
+                v[4 * q + 1] = f.y;
+                v[4 * q + 2] = f.z;
+                v[4 * q + 3] = f.w;
+            }
+        } else {
+#pragma unroll
+            for (int s = 0; s < kBW; ++s) v[s] = 0.0f;
+        }
+#pragma unroll
+        for (int s = 0; s < kBW; ++s) cnt[s] += __popcll(__ballot(v[s] != 0.0f));
+    }
+#pragma unroll
+    for (int s = 0; s < kBW; ++s) {
+        const int64_t r = c * kBW + s;
+        if (lane == s && r < batch) pcnt[part * batch + r] = cnt[s];
+    }
+}
+
+// per sample: part counts -> exclusive offsets within the row (in place); row totals -> cnt
+__global__ __launch_bounds__(256) void blocked_scan_kernel(int64_t batch, int64_t nparts, int32_t *__restrict__ pcnt,
+                                                           int32_t *__restrict__ cnt) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= batch) return;
+    int32_t run = 0;
+    for (int64_t p = 0; p < nparts; ++p) {
+        const int32_t v = pcnt[p * batch + r];
+        pcnt[p * batch + r] = run;
+        run += v;
+    }
+    cnt[r] = run;
+}
+
+__global__ __launch_bounds__(256) void blocked_pack_kernel(int64_t n, int64_t batch, int64_t nparts,
+                                                           const float *__restrict__ yb,
+                                                           const int32_t *__restrict__ poff,
+                                                           const int64_t *__restrict__ row_ptr,
+                                                           int32_t *__restrict__ out_col, float *__restrict__ out_val) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t nchunks = (batch + kBW - 1) / kBW;
+    if (w >= nchunks * nparts) return;
+    const int64_t c = w / nparts, part = w % nparts;
+    const int64_t a0 = part * kPackR, a1 = min(n, a0 + kPackR);
+    // where each sample's survivors of this part start (lane s holds sample s's position)
+    int64_t pos = 0;
+    if (lane < kBW && c * kBW + lane < batch) pos = row_ptr[c * kBW + lane] + poff[part * batch + c * kBW + lane];
+    for (int64_t a = a0; a < a1; a += 64) {
+        const int64_t j = a + lane;
+        float v[kBW];
+        if (j < a1) {
+            const float4 *row = reinterpret_cast<const float4 *>(yb + (c * n + j) * kBW);
+#pragma unroll
+            for (int q = 0; q < kBW / 4; ++q) {
+                const float4 f = row[q];
+                v[4 * q] = f.x;
+                v[4 * q + 1] = f.y;
+                v[4 * q + 2] = f.z;
+                v[4 * q + 3] = f.w;
+            }
+        } else {
+#pragma unroll
+            for (int s = 0; s < kBW; ++s) v[s] = 0.0f;
+        }
+#pragma unroll
+        for (int s = 0; s < kBW; ++s) {
+            if (c * kBW + s >= batch) break;  // uniform: samples past the batch end hold no output
+            const bool keep = v[s] != 0.0f;
+            const uint64_t m = __ballot(keep);
+            const int64_t base = __shfl(pos, s);
+            if (keep) {
+                const int64_t o = base + lane_rank(m);
+                out_col[o] = (int32_t)j;
+                out_val[o] = v[s];
+            }
+            if (lane == s) pos += __popcll(m);
+        }
+    }
+}
+
+// Batch-major rows (batch x n, row pitch ld_in) <-> blocked.  One workgroup per (chunk, 128 neurons): the
+// 32 x 128 tile goes through LDS; samples past the batch end are written as zeros.
+constexpr int kTrN = 128;
+
+__global__ __launch_bounds__(256) void to_blocked_kernel(int64_t n, int64_t batch, int64_t ld_in,
+                                                         const float *__restrict__ y, float *__restrict__ yb) {
+    __shared__ float tile[kBW][kTrN + 1];
+    const int64_t ntiles = (n + kTrN - 1) / kTrN;
+    const int64_t c = blockIdx.x / ntiles, j0 = (blockIdx.x % ntiles) * kTrN;
+    for (int t = threadIdx.x; t < kBW * kTrN; t += 256) {
+        const int s = t / kTrN, jj = t % kTrN;
+        const int64_t r = c * kBW + s, j = j0 + jj;
+        tile[s][jj] = (r < batch && j < n) ? y[r * ld_in + j] : 0.0f;
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < kBW * kTrN; t += 256) {
+        const int jj = t / kBW, s = t % kBW;
+        const int64_t j = j0 + jj;
+        if (j < n) yb[(c * n + j) * kBW + s] = tile[s][jj];
+    }
+}
+
+__global__ __launch_bounds__(256) void from_blocked_kernel(int64_t n, int64_t batch, int64_t ld_out,
+                                                           const float *__restrict__ yb, float *__restrict__ y) {
+    __shared__ float tile[kBW][kTrN + 1];
+    const int64_t ntiles = (n + kTrN - 1) / kTrN;
+    const int64_t c = blockIdx.x / ntiles, j0 = (blockIdx.x % ntiles) * kTrN;
+    for (int t = threadIdx.x; t < kBW * kTrN; t += 256) {
+        const int jj = t / kBW, s = t % kBW;
+        const int64_t j = j0 + jj;
+        tile[s][jj] = j < n ? yb[(c * n + j) * kBW + s] : 0.0f;
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < kBW * kTrN; t += 256) {
+        const int s = t / kTrN, jj = t % kTrN;
+        const int64_t r = c * kBW + s, j = j0 + jj;
+        if (r < batch && j < n) y[r * ld_out + j] = tile[s][jj];
+    }
+}
+
+}  // namespace
+
+int64_t blocked_chunks(int64_t batch) { return (batch + kBW - 1) / kBW; }
+
+size_t blocked_elems(int64_t n, int64_t batch) { return (size_t)blocked_chunks(batch) * kBW * (size_t)n; }
+
+bool blocked_wanted(int64_t n, int64_t batch) { return n > 16384 && n <= (1 << 24) && batch >= 256; }
+
+size_t blocked_pack_elems(int64_t n, int64_t batch) { return (size_t)((n + kPackR - 1) / kPackR) * (size_t)batch; }
+
+int64_t blocked_sched_elems(int64_t n) { return (n + kBTile - 1) / kBTile * kBTile; }
+
+hipError_t launch_blocked_order(int64_t n, const int64_t *fan_ptr, BlockedSched *sched, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    const int64_t padded = blocked_sched_elems(n);
+    blocked_order_kernel<<<(unsigned)((padded + kSortSeg - 1) / kSortSeg), 256, 0, s>>>(n, padded, fan_ptr, sched);
+    return hipGetLastError();
+}
+
+hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan, const float *bias,
+                               double ymax, int pattern, const float *yb, float *zb, hipStream_t s) {
+    if (n == 0 || batch == 0) return hipSuccess;
+    if (n > (1 << 24)) return hipErrorInvalidValue;  // 32-bit row offsets within a chunk
+    const int64_t nchunks = blocked_chunks(batch);
+    const int64_t groups = (n + kBTile - 1) / kBTile;
+    const int64_t gpx = (groups + 7) / 8;
+    const int64_t per_chunk = 8 * gpx;  // workgroups per chunk (n <= 2^24: at most 2^19 + 8)
+    // launches of whole chunks, at most 2^23 workgroups each; every launch numbers its workgroups from 0, so
+    // the data pointers move to its first chunk
+    const int64_t chunks_per_launch = std::max<int64_t>(1, (int64_t(1) << 23) / per_chunk);
+    for (int64_t c0 = 0; c0 < nchunks; c0 += chunks_per_launch) {
+        const int64_t nc = std::min(chunks_per_launch, nchunks - c0);
+        const unsigned nb = (unsigned)(nc * per_chunk);
+        const float *y0 = yb + c0 * n * kBW;
+        float *z0 = zb + c0 * n * kBW;
+        if (pattern)
+            spmm_blocked_kernel<true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, bias, ymax, y0, z0);
+        else
+            spmm_blocked_kernel<false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, bias, ymax, y0, z0);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_densify_blocked(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
+                                  const int32_t *in_col, const float *in_val, float *yb, uint32_t *err, hipStream_t s) {
+    if (n == 0 || batch == 0) return hipSuccess;
+    const int64_t nchunks = blocked_chunks(batch);
+    // enough parts for about eight workgroups per CU on the widest layers, whole ranges per part
+    int64_t part_len = (n + 7) / 8;
+    part_len = (part_len + kDensR - 1) / kDensR * kDensR;
+    const int64_t nparts = (n + part_len - 1) / part_len;
+    const int64_t blocks = nchunks * nparts;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    densify_blocked_kernel<<<(unsigned)blocks, kDensThreads, 0, s>>>(n, batch, part_len, in_row_ptr, in_cnt, in_col,
+                                                                      in_val, yb, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_blocked_to_csr(int64_t n, int64_t batch, const float *yb, int32_t *pcnt, int32_t *cnt,
+                                 int64_t *row_ptr, int64_t *scan_tmp, int32_t *out_col, float *out_val, hipStream_t s) {
+    if (batch == 0) return hipSuccess;
+    const int64_t nparts = (n + kPackR - 1) / kPackR;
+    const int64_t waves = blocked_chunks(batch) * nparts;
+    const int64_t blocks = (waves + 3) / 4;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    blocked_count_kernel<<<(unsigned)blocks, 256, 0, s>>>(n, batch, nparts, yb, pcnt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    blocked_scan_kernel<<<(unsigned)((batch + 255) / 256), 256, 0, s>>>(batch, nparts, pcnt, cnt);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_exclusive_scan_i32_to_i64(batch, cnt, row_ptr, scan_tmp, s);
+    if (e != hipSuccess) return e;
+    blocked_pack_kernel<<<(unsigned)blocks, 256, 0, s>>>(n, batch, nparts, yb, pcnt, row_ptr, out_col, out_val);
+    return hipGetLastError();
+}
+
+hipError_t launch_to_blocked(int64_t n, int64_t batch, int64_t ld_in, const float *y, float *yb, hipStream_t s) {
+    if (n == 0 || batch == 0) return hipSuccess;
+    const int64_t blocks = blocked_chunks(batch) * ((n + kTrN - 1) / kTrN);
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    to_blocked_kernel<<<(unsigned)blocks, 256, 0, s>>>(n, batch, ld_in, y, yb);
+    return hipGetLastError();
+}
+
+hipError_t launch_from_blocked(int64_t n, int64_t batch, int64_t ld_out, const float *yb, float *y, hipStream_t s) {
+    if (n == 0 || batch == 0) return hipSuccess;
+    const int64_t blocks = blocked_chunks(batch) * ((n + kTrN - 1) / kTrN);
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    from_blocked_kernel<<<(unsigned)blocks, 256, 0, s>>>(n, batch, ld_out, yb, y);
+    return hipGetLastError();
+}
+
+}  // namespace sdnn

@@ -25,7 +25,8 @@ enum KernelKind : int {
     kKernSpgemm = 6,      // sparse-Y product: planning, small-sample and workgroup SpGEMM kernels
     kKernDensify = 7,     // sparse rows -> dense neuron-major activations
     kKernPack = 8,        // dense activations -> CSR result
-    kKernCompact = 9      // sparse slot rows -> CSR result
+    kKernCompact = 9,     // sparse slot rows -> CSR result
+    kKernBlocked = 10     // dense-Y product on the sample-blocked layout (very wide layers)
 };
 
 // Wave-local exclusive count of set bits below this lane in a 64-bit ballot.
@@ -127,6 +128,34 @@ hipError_t launch_dense_to_csr(int64_t n, int64_t batch, const float *y, int32_t
 hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, const int64_t *row_ptr,
                                const int32_t *in_col, const float *in_val, int32_t *out_col, float *out_val,
                                hipStream_t s);
+
+// blocked.hip: the sample-blocked activation layout of very wide layers (chunks of 32 samples, each chunk an
+// n x 32 block: element (r, i) at ((r / 32) * n + i) * 32 + r % 32) and its product.
+int64_t blocked_chunks(int64_t batch);
+size_t blocked_elems(int64_t n, int64_t batch);   // floats of one blocked activation buffer
+bool blocked_wanted(int64_t n, int64_t batch);     // the dense-Y path uses the blocked layout
+size_t blocked_pack_elems(int64_t n, int64_t batch);  // int32 scratch of launch_blocked_to_csr
+// Schedule of the blocked product (set-up): neurons sorted by fan-in length within runs of 4096, one entry
+// per position (neuron or -1, list length, list start; an empty list starts at the guard entry fan[nnz],
+// which set-up zeroes), padded to blocked_sched_elems(n) positions.
+struct __align__(16) BlockedSched {
+    int32_t j;
+    int32_t len;
+    int64_t e0;
+};
+int64_t blocked_sched_elems(int64_t n);
+hipError_t launch_blocked_order(int64_t n, const int64_t *fan_ptr, BlockedSched *sched, hipStream_t s);
+hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan, const float *bias,
+                               double ymax, int pattern, const float *yb, float *zb, hipStream_t s);
+// sparse rows (caller CSR, or slot rows with counts) -> blocked; every element is written
+hipError_t launch_densify_blocked(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
+                                  const int32_t *in_col, const float *in_val, float *yb, uint32_t *err, hipStream_t s);
+// blocked -> CSR: pcnt holds blocked_pack_elems int32, cnt batch int32, row_ptr batch + 1
+hipError_t launch_blocked_to_csr(int64_t n, int64_t batch, const float *yb, int32_t *pcnt, int32_t *cnt,
+                                 int64_t *row_ptr, int64_t *scan_tmp, int32_t *out_col, float *out_val, hipStream_t s);
+// batch-major (row pitch ld) <-> blocked
+hipError_t launch_to_blocked(int64_t n, int64_t batch, int64_t ld_in, const float *y, float *yb, hipStream_t s);
+hipError_t launch_from_blocked(int64_t n, int64_t batch, int64_t ld_out, const float *yb, float *y, hipStream_t s);
 
 // semiring.hip
 enum : int { kSemiringPlusTimes = 0, kSemiringMaxPlus = 1, kSemiringMaxMin = 2, kSemiringMinMax = 3, kSemiringXorAnd = 4 };

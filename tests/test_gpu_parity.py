@@ -217,14 +217,14 @@ def test_semiring_mxm_csr(sd, name):
     assert got.tobytes() == want.tobytes()
 
 
-def test_gather_grid_larger_than_one_launch(sd):
-    """n = 2^20 and batch 4098 (not a multiple of 4, so the fan-in gather with two columns per lane: 33 chunks
-    of 128 columns x 262144 neuron groups = 8.65M workgroups) need more than one launch holds, so the gather
-    runs in segments.  Y is drawn on the device from a seeded generator and the sampled rows are handed to the
-    oracle; 68 GB of device memory."""
+@pytest.mark.parametrize("n,batch", [(1 << 20, 4098), (1 << 23, 1056)])
+def test_blocked_product_very_wide(sd, n, batch):
+    """Very wide layers on the sample-blocked layout: n = 2^20, batch 4098 (129 chunks of 32 samples, the
+    last one partial) and n = 2^23, batch 1056 (33 chunks: more workgroups than one launch holds, so the
+    product runs as two launches of whole chunks).  Y is drawn on the device from a seeded generator and the
+    sampled rows are handed to the oracle; up to 145 GB of device memory."""
     import torch
 
-    n, batch = 1 << 20, 4098
     rng = np.random.default_rng(20170802)
     col = np.sort(rng.integers(0, n, size=(n, 2)), axis=1).astype(np.int32)
     col[:, 1] = np.where(col[:, 1] == col[:, 0], (col[:, 0] + 1) % n, col[:, 1])
@@ -236,9 +236,9 @@ def test_gather_grid_larger_than_one_launch(sd):
     y = torch.rand((batch, n), generator=gen, device="cuda", dtype=torch.float32)
     net = sd.Net(n, 1)
     net.set_layer(0, layer.row_ptr, layer.col, layer.val, layer.bias)
-    _say("segmented gather grid", n, batch)
+    _say("blocked very wide", n, batch)
     out = net.forward_dense(y, arm=sd.SDNN_ARM_SPARSE)
-    rows = [0, 1, 2047, 4096, 4097]
+    rows = [0, 1, 31, 32, 1023, batch - 2, batch - 1]
     got = out[rows].cpu().numpy()
     y_rows = y[rows].cpu().numpy()
     del out, y
@@ -287,6 +287,48 @@ def test_narrow_chunk_gather(sd, seed, n, batch, lengths, bias_mode):
     _say("narrow gather", seed, n, batch, bias_mode)
     parity.compare(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE, bias_mode=bias_mode)),
                    bias_mode=bias_mode)
+
+
+@pytest.mark.parametrize("seed,n,batch,lengths,bias_mode", [
+    (91, 16400, 256, [32, 25, 40, 32, 0, 1, 77, 33], 0), (92, 20000, 300, [3, 0, 0, 33, 8, 9, 64, 1], 1),
+    (93, 17003, 257, [120, 0, 5, 17, 31, 32, 33], 0), (94, 24576, 512, [24, 24, 24, 24, 24, 24, 24, 25], 1)])
+def test_blocked_product(sd, seed, n, batch, lengths, bias_mode):
+    """Layers wider than 16384 with batches of 256 or more take the product on the sample-blocked layout
+    (chunks of 32 samples, eight neurons per wave walking their lists in step): ragged n, a partial last
+    chunk, empty lists and list lengths from 0 to 120 side by side in one wave, both bias readings, every
+    row compared."""
+    rng = np.random.default_rng(seed)
+    layers = [_mixed_length_layer(rng, n, lengths), _mixed_length_layer(rng, n, lengths[::-1])]
+    y = rng.random((batch, n), dtype=np.float32)
+    y[rng.random((batch, n)) < 0.3] = 0.0
+    from workloads import Problem
+    p = Problem(f"blocked-{seed}", n, 2, batch, [math.inf, 2.5][seed % 2], layers, y0_dense=y)
+    _say("blocked product", seed, n, batch, bias_mode)
+    parity.compare_in_chunks(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_SPARSE, bias_mode=bias_mode)),
+                             bias_mode=bias_mode)
+
+
+@pytest.mark.parametrize("case", ["from_input", "after_sparse", "integer", "empty_layer"])
+def test_blocked_csr_path(sd, case):
+    """The CSR path's dense activations on the blocked layout: densify from the caller's CSR (positive bias
+    from layer 0) or from slot rows after sparse layers, the layers, and the packing into CSR; an integer
+    shadow of the very wide recipe (scaled, batch 260) bit for bit; a layer with no weights."""
+    if case == "integer":
+        q = integer_shadow(make_config(5, n=20480, L=3, batch=260, block=4096))
+        for l in q.layers:  # positive biases everywhere: dense activations from layer 0
+            l.bias = np.ones(q.n, np.float32)
+        _say("blocked csr integer")
+        parity.compare(q, run_csr(sd, q), exact=True)
+        return
+    p = tiny_random(95, 20000, 3, 300, w_density=0.0016, y_density=0.02, bias_lo=-0.2,
+                    bias_hi=0.0 if case == "after_sparse" else 0.3)
+    if case == "after_sparse":
+        p.layers[2].bias = np.full(p.n, 0.02, np.float32)
+    if case == "empty_layer":
+        p.layers[1] = Layer(np.zeros(p.n + 1, np.int64), np.zeros(0, np.int32), np.zeros(0, np.float32),
+                            np.linspace(-0.5, 0.5, p.n).astype(np.float32))
+    _say("blocked csr", case)
+    parity.compare_in_chunks(p, run_csr(sd, p))
 
 
 def test_long_fanin_lists(sd):
