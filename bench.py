@@ -31,6 +31,8 @@ METRIC = "edges/sec (batch × nnz(W_k) × L / time) at 1 MI355X; achieved HBM GB
 HBM_PEAK_GBS = 8000.0
 FP64_VECTOR_TFLOPS = 78.6  # MI355X fp64 vector peak: the sparse kernels multiply-add in fp64
 FP64_MATRIX_TFLOPS = 78.6  # MI355X fp64 matrix-core peak (dense-W arm)
+FP32_MATRIX_TFLOPS = 157.3  # MI355X fp32 matrix-core peak (fp32 dense-W arm)
+DENSE_BOTH = 3  # SDNN_ARENA_DENSE_F64 | SDNN_ARENA_DENSE_F32
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -112,7 +114,16 @@ def kernel_split(records):
     return out
 
 
-SPMM_KERNELS = ("spmm_fanin_kernel", "spmm_narrow_kernel", "spmm_slots_kernel", "spmm_tiled_kernel")
+SPMM_KERNELS = ("spmm_fanin_kernel", "spmm_narrow_kernel", "spmm_slots_kernel", "spmm_tiled_kernel", "spmm_blocked_kernel")
+
+
+def kernel_sources(kernel):
+    """The library sources a kernel's counters depend on (their hash marks a counter summary as current)."""
+    if kernel.startswith("spmm_blocked"):
+        return ["blocked.hip", "common.h"]
+    if kernel.startswith("gemm"):
+        return ["gemm.hip", "common.h"]
+    return ["spmm.hip", "common.h"]
 
 
 def kernel_roofline(name, rec, p, trace=None):
@@ -186,7 +197,7 @@ def run_sweep(args, torch, sd):
     for d in densities:
         t0 = time.time()
         p = make_config(2, d)
-        net = sd.net_from_problem(p)
+        net = sd.net_from_problem(p, dense=0 if args.no_dense else DENSE_BOTH)
         nets.append(net)
         probs.append(p)
         ys.append(torch.from_numpy(p.y0_dense).cuda())
@@ -223,20 +234,19 @@ def run_sweep(args, torch, sd):
                            "layer_kernel": kname, "layer_launch_ms": round(sp[kname]["avg_ms"], 5),
                            "nnz_per_layer": int(p.layers[0].nnz)}
 
-    # dense-W arm (matrix cores) at every density, one density at a time (n*n fp64 per layer)
+    # dense-W arms at every density: fp64 matrix cores (the sparse paths' arithmetic) and fp32 matrix cores (an
+    # sgemm's arithmetic, the paper's comparison)
     if not args.no_dense:
         for d, net, y, o, p in zip(densities, nets, ys, outs, probs):
-            net.build_dense()
-            t_dense = time_calls(torch, lambda: net.forward_dense(y, out=o, arm=sd.SDNN_ARM_DENSE), max(2, reps // 2))
-            sweep[f"{d:g}"]["dense_ms"] = round(t_dense, 4)
-            # release the dense copies by re-uploading the layer set (drops dense_wt)
-            for k, l in enumerate(p.layers):
-                net.set_layer(k, l.row_ptr, l.col, l.val, l.bias)
+            for key, arm in (("dense_ms", sd.SDNN_ARM_DENSE), ("dense32_ms", sd.SDNN_ARM_DENSE_F32)):
+                net.forward_dense(y, out=o, arm=arm)
+                t_dense = time_calls(torch, lambda: net.forward_dense(y, out=o, arm=arm), max(2, reps // 2))
+                sweep[f"{d:g}"][key] = round(t_dense, 4)
             torch.cuda.synchronize()
 
-    def find_crossover():
-        pts = sorted((d, v["sparse_ms"], v.get("dense_ms")) for d, v in
-                     ((float(k), v) for k, v in sweep.items()) if v.get("dense_ms"))
+    def find_crossover(key="dense_ms"):
+        pts = sorted((d, v["sparse_ms"], v.get(key)) for d, v in
+                     ((float(k), v) for k, v in sweep.items()) if v.get(key))
         for (d0, s0, q0), (d1, s1, q1) in zip(pts, pts[1:]):
             r0, r1 = math.log(s0 / q0), math.log(s1 / q1)
             if r0 <= 0 <= r1 and r1 != r0:  # sparse faster at d0, slower at d1
@@ -245,28 +255,29 @@ def run_sweep(args, torch, sd):
         return None
 
     crossover = find_crossover()
-    if crossover is None and not args.no_dense and max(densities) < 1.0:
+    if (crossover is None or find_crossover("dense32_ms") is None) and not args.no_dense and max(densities) < 1.0:
         # the sparse arm wins at every sweep density: bracket the crossover with denser weights (same recipe,
         # same L); these points inform the crossover only and are not part of the step
         for d in (0.75, 1.0):
             if d <= max(densities):
                 continue
             q = make_config(2, d)
-            net = sd.net_from_problem(q)
+            net = sd.net_from_problem(q, dense=DENSE_BOTH)
             y = torch.from_numpy(q.y0_dense).cuda()
             o = torch.empty_like(y)
             net.workspace(q.batch, 0)
             t_sp = time_calls(torch, lambda: net.forward_dense(y, out=o), max(2, reps // 2))
-            net.build_dense()
             t_dn = time_calls(torch, lambda: net.forward_dense(y, out=o, arm=sd.SDNN_ARM_DENSE), max(2, reps // 2))
+            t_d32 = time_calls(torch, lambda: net.forward_dense(y, out=o, arm=sd.SDNN_ARM_DENSE_F32), max(2, reps // 2))
             net.free()
-            sweep[f"{d:g}"] = {"sparse_ms": round(t_sp, 4), "dense_ms": round(t_dn, 4),
+            sweep[f"{d:g}"] = {"sparse_ms": round(t_sp, 4), "dense_ms": round(t_dn, 4), "dense32_ms": round(t_d32, 4),
                                "nnz_per_layer": int(q.layers[0].nnz), "bracket": True}
-            log(f"bracket density {d}: sparse {t_sp:.3f} ms, dense {t_dn:.3f} ms")
+            log(f"bracket density {d}: sparse {t_sp:.3f} ms, dense fp64 {t_dn:.3f} ms, fp32 {t_d32:.3f} ms")
             del q
             crossover = find_crossover()
-            if crossover is not None:
+            if crossover is not None and find_crossover("dense32_ms") is not None:
                 break
+    crossover32 = find_crossover("dense32_ms")
     # dominant kernel: the layer kernel with the largest share of the step
     best = None
     for d, sp in zip(densities, splits):
@@ -276,7 +287,7 @@ def run_sweep(args, torch, sd):
     dom, kernel, rec = best
     p = probs[densities.index(dom)]
     roof = kernel_roofline(kernel, rec, p)
-    roof["traffic"] = _pmc_traffic(f"{kernel}_d{dom:g}", ["spmm.hip", "common.h"])
+    roof["traffic"] = _pmc_traffic(f"{kernel}_d{dom:g}", kernel_sources(kernel))
     roof["density"] = dom
     hbm = hbm_fields(roof, roof["traffic"])
     for net in nets:
@@ -285,7 +296,8 @@ def run_sweep(args, torch, sd):
                        + " (CSR sparse-W path; fp32 storage, fp64 accumulate)",
            "n": 4096, "L": 16, "batch": 1024, "densities": densities}
     return dict(value=value, ms_step=ms_step, ms_median=ms_med, ms_min=ms_min, edges=edges, sweep=sweep,
-                crossover=crossover, roofline=roof, hbm=hbm, config=cfg, probs=probs, densities=densities)
+                crossover=crossover, crossover32=crossover32, roofline=roof, hbm=hbm, config=cfg, probs=probs,
+                densities=densities)
 
 
 # oracle sample per workload (rows of the batch): all-core rate, and single-thread rate where the density-sweep
@@ -382,7 +394,7 @@ def run_paper_grid(args, torch, sd):
             L = 2 if m >= 8192 else 17
             p = paper_grid(m, S, L=L)
             l0 = p.layers[0]
-            net = sd.Net(m, L)
+            net = sd.Net(m, L, nnz_per_layer=int(l0.nnz), dense=0 if args.no_dense else DENSE_BOTH)
             dev = [torch.from_numpy(a).cuda() for a in (l0.row_ptr, l0.col, l0.val, l0.bias)]
             del p.layers[:]
             for k in range(L):
@@ -393,7 +405,7 @@ def run_paper_grid(args, torch, sd):
             arms = [("sparse", sd.SDNN_ARM_SPARSE)]
             if not args.no_dense:
                 net.build_dense()
-                arms.append(("dense", sd.SDNN_ARM_DENSE))
+                arms += [("dense", sd.SDNN_ARM_DENSE), ("dense32", sd.SDNN_ARM_DENSE_F32)]
             for name, arm in arms:
                 for k1 in (1, L):
                     net.forward_dense(y, k1=k1, arm=arm, out=o)
@@ -418,9 +430,9 @@ def run_paper_grid(args, torch, sd):
             q["sparse_slope_per_nnz"] = (g[1]["sparse_ms"] - g[4]["sparse_ms"]) / (0.75 * m * m)
         if 262144 in g:
             q["saturation_per_row"] = g[262144]["sparse_ms"] / m
-        pts = [(S, v["sparse_ms"], v["dense_ms"]) for S, v in sorted(g.items())
-               if v.get("dense_ms") and v["sparse_ms"] > 0]
-        q["crossover_inv_sparsity"] = _crossover(pts)
+        for key, dk in (("crossover_inv_sparsity", "dense_ms"), ("crossover_inv_sparsity_f32", "dense32_ms")):
+            pts = [(S, v["sparse_ms"], v[dk]) for S, v in sorted(g.items()) if v.get(dk) and v["sparse_ms"] > 0]
+            q[key] = _crossover(pts)
         params[m] = q
     if 4096 in params:
         ref = params[4096]
@@ -535,7 +547,7 @@ def run_csr_config(args, torch, sd):
     roof = kernel_roofline(dom, split[dom], p, trace)
     hbm = None
     if roof is not None:
-        roof["traffic"] = _pmc_traffic(f"{dom}_{PMC_TAGS.get(args.config, p.name)}", ["spmm.hip", "common.h"]) \
+        roof["traffic"] = _pmc_traffic(f"{dom}_{PMC_TAGS.get(args.config, p.name)}", kernel_sources(dom)) \
             if dom in SPMM_KERNELS else None
         hbm = hbm_fields(roof, roof["traffic"])
     cfg = {"workload": f"{p.name} n={p.n} L={p.L} batch={p.batch}", "n": p.n, "L": p.L, "batch": p.batch,
@@ -636,7 +648,7 @@ def main():
         return
     if args.summarize_pmc:
         a = args.summarize_pmc
-        summarize_pmc(a[0], a[1], a[2:6], int(a[6]), a[7].split("|"), a[8], ["spmm.hip", "common.h"])
+        summarize_pmc(a[0], a[1], a[2:6], int(a[6]), a[7].split("|"), a[8], kernel_sources(a[0]))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the library has no multi-GPU path (batch rows would shard "
@@ -693,6 +705,7 @@ def main():
     if r.get("sweep"):
         out["sweep"] = r["sweep"]
         out["crossover_density"] = r["crossover"]
+        out["crossover_density_f32"] = r.get("crossover32")
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args, r["probs"], args.config)
     if args.config != 2 and not args.no_sweep:
@@ -705,7 +718,7 @@ def main():
         out["density_sweep"] = {"workload": sw["config"]["workload"], "ms_per_step": round(sw["ms_step"], 4),
                                 "value": sw["value"], "unit": "edges/s", "steps": sw_args.steps,
                                 "roofline": sw["roofline"], "achieved_hbm_gbs": sw["hbm"], "sweep": sw["sweep"],
-                                "crossover_density": sw["crossover"]}
+                                "crossover_density": sw["crossover"], "crossover_density_f32": sw["crossover32"]}
         log(f"density sweep {time.time() - t0:.1f}s")
     print(json.dumps(out), flush=True)
 

@@ -19,7 +19,7 @@
  * exactly and accumulate in fp64, add the bias and apply h in fp64, and round
  * once to fp32 per layer; the dense-W path (the comparison arm for the paper's
  * sparse-versus-dense experiment, Sec. V) does the same on the fp64 matrix
- * cores.  Output entries equal to zero are not stored in CSR results (Sec. II,
+ * cores, or, as SDNN_ARM_DENSE_F32, computes in fp32 on the fp32 matrix cores.  Output entries equal to zero are not stored in CSR results (Sec. II,
  * 0-element).
  *
  * Conventions for every call:
@@ -27,7 +27,9 @@
  *     net's device (the HIP device current when the net was created); "host"
  *     pointers to host memory.  A call that does device work makes the net's
  *     device current while it runs and restores the caller's device before it
- *     returns.  The library never frees memory it did not allocate.
+ *     returns.  All device memory is the caller's (the net arena, workspaces,
+ *     operands); the library allocates none, apart from the fixed scratch array
+ *     behind sdnn_forward_dense_noalloc, and frees none.
  *   - CSR matrices use int64 row_ptr (rows + 1 entries, row_ptr[0] = 0),
  *     int32 column indices strictly increasing within a row, fp32 values.
  *   - Work is enqueued on the net's HIP stream and is asynchronous unless the
@@ -55,15 +57,25 @@ typedef enum {
     SDNN_ERR_DIMENSION_MISMATCH = 4, /* layer range outside [0, L] or batch / nnz inconsistent */
     SDNN_ERR_INVALID_OBJECT = 5,     /* NULL net, layer not set, dense arm not built */
     SDNN_ERR_WORKSPACE_TOO_SMALL = 6,/* ws_bytes below sdnn_workspace_size() */
-    SDNN_ERR_OUT_OF_MEMORY = 7,      /* device allocation by the library failed */
+    SDNN_ERR_OUT_OF_MEMORY = 7,      /* a host allocation by the library failed */
     SDNN_ERR_DEVICE = 8,             /* a HIP call failed; detail in sdnn_last_error() */
     SDNN_ERR_UNSUPPORTED = 9         /* a size the library does not handle (see the message) */
 } sdnn_status;
 
 /* Which product a dense-Y forward uses for Y_k W_k. */
 enum {
-    SDNN_ARM_SPARSE = 0, /* CSR W_k: each output neuron gathers its fan-in (row-per-wavefront SpMM) */
-    SDNN_ARM_DENSE = 1   /* dense W_k with explicit zeros on the matrix cores (Sec. V dense baseline) */
+    SDNN_ARM_SPARSE = 0,    /* CSR W_k: each output neuron gathers its fan-in (row-per-wavefront SpMM) */
+    SDNN_ARM_DENSE = 1,     /* dense W_k with explicit zeros on the fp64 matrix cores (Sec. V dense baseline,
+                               the sparse paths' arithmetic: exact products, fp64 sums, one rounding) */
+    SDNN_ARM_DENSE_F32 = 2  /* the same dense product in fp32 on the fp32 matrix cores, the arithmetic of the
+                               single-precision BLAS the paper compares with (Sec. V.A): fp32 products and
+                               sums, so results differ from the others by fp32 rounding of the sums */
+};
+
+/* Dense copies an arena holds (sdnn_net_arena_size / sdnn_net_create dense_flags). */
+enum {
+    SDNN_ARENA_DENSE_F64 = 1, /* an n x n fp64 copy of every layer, for SDNN_ARM_DENSE */
+    SDNN_ARENA_DENSE_F32 = 2  /* an n x n fp32 copy of every layer, for SDNN_ARM_DENSE_F32 */
 };
 
 /* Where the bias b_k is added (sdnn_net_set_bias_mode). */
@@ -79,14 +91,31 @@ enum {
 typedef struct sdnn_net_s *sdnn_net;
 
 /*
- * Create a net of L layers of width n (every layer is n x n, Sec. IV: all
- * layers have the same number of neurons).  ymax > 0 is the clamp of h
- * (+INFINITY for plain ReLU).  `stream` is a hipStream_t (NULL = the default
- * stream).  *net receives a host handle owned by the caller; release it with
- * sdnn_net_free.  Checks the device is a gfx950 part.
- * Errors: NULL_POINTER, INVALID_VALUE (n < 1, n > 2^31-1, L < 0, ymax <= 0 or NaN), DEVICE.
+ * Bytes of device memory (the net arena) a net of L layers of width n needs, when layer k will hold at
+ * most nnz_per_layer[k] weight entries (host array of L values) and dense_flags (SDNN_ARENA_DENSE_*) names
+ * the dense copies wanted.  The arena holds every derived copy the library keeps: per layer the packed
+ * fan-out rows, the fan-in (transposed) lists, and, as n and the capacity call for them, the tile masks and
+ * fp64 weight slots of near-dense layers, the window offsets of wide sparse-activation layers, the schedule
+ * of the very wide product and the dense copies; plus the set-up scratch and the per-forward flags.
+ * Errors: NULL_POINTER, INVALID_VALUE (n, L, a capacity outside [0, 2^31-1], unknown flags).
  */
-sdnn_status sdnn_net_create(sdnn_net *net, int64_t n, int32_t L, float ymax, void *stream);
+sdnn_status sdnn_net_arena_size(int64_t n, int32_t L, const int64_t *nnz_per_layer, int32_t dense_flags,
+                                int64_t *bytes);
+
+/*
+ * Create a net of L layers of width n (every layer is n x n, Sec. IV: all
+ * layers have the same number of neurons), the shape of the paper's dnn(Y, W, B, L) (Fig. 4), whose
+ * operands all belong to the caller.  ymax > 0 is the clamp of h (+INFINITY for plain ReLU).
+ * nnz_per_layer (host, L values) caps each layer's entries and dense_flags selects the dense copies, as for
+ * sdnn_net_arena_size; `arena` is device memory of at least that many bytes, 256-byte aligned, owned by the
+ * caller, which must keep it alive and untouched until sdnn_net_free: the library allocates no device
+ * memory for the net, now or later.  `stream` is a hipStream_t (NULL = the default stream).  *net receives
+ * a host handle owned by the caller; release it with sdnn_net_free.  Checks the device is a gfx950 part.
+ * Errors: NULL_POINTER, INVALID_VALUE (n < 1, n > 2^31-1, L < 0, ymax <= 0 or NaN, bad capacities or
+ * flags, arena misaligned), WORKSPACE_TOO_SMALL (arena_bytes below sdnn_net_arena_size), UNSUPPORTED, DEVICE.
+ */
+sdnn_status sdnn_net_create(sdnn_net *net, int64_t n, int32_t L, float ymax, const int64_t *nnz_per_layer,
+                            int32_t dense_flags, void *arena, int64_t arena_bytes, void *stream);
 
 /* Replace the stream later work is enqueued on. */
 sdnn_status sdnn_net_set_stream(sdnn_net net, void *stream);
@@ -107,21 +136,25 @@ sdnn_status sdnn_net_set_bias_mode(sdnn_net net, int32_t mode);
  * replicated over the batch).  All four arrays are device memory that the
  * caller keeps alive and unchanged until the net is freed or the layer is set
  * again.  The call validates the CSR and the values on the device, builds the
- * library-owned fan-in (transposed) copy used by the dense-Y path, and
- * synchronises the net's stream once (the fan-in lists come from a stable
- * radix sort of the entries by column, so each is sorted by input index).
- * Layers wider than n = 2^24 are rejected with UNSUPPORTED.
+ * fan-in (transposed) copy used by the dense-Y path and the layer's other
+ * derived structures in its region of the arena (a dense copy is rebuilt by
+ * the next sdnn_net_build_dense), and synchronises the net's stream once (the
+ * fan-in lists come from a stable radix sort of the entries by column, so each
+ * is sorted by input index).  Layers wider than n = 2^24 are rejected with
+ * UNSUPPORTED.  On a validation error the layer keeps its previous contents;
+ * on a device error it is left unset.
  * Errors: INVALID_OBJECT, NULL_POINTER (nnz > 0 and col/val NULL), INVALID_VALUE
- * (nnz < 0 or >= 2^31, non-finite value), INVALID_INDEX, UNSUPPORTED, OUT_OF_MEMORY, DEVICE.
+ * (nnz < 0 or >= 2^31, non-finite value), INVALID_INDEX, WORKSPACE_TOO_SMALL (nnz above the layer's
+ * capacity in the arena), UNSUPPORTED, DEVICE.
  */
 sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64_t *row_ptr,
                                const int32_t *col_idx, const float *val, const float *bias);
 
 /*
- * Build, for every layer that is set, a library-owned dense copy of W_k with
- * explicit zeros (n*n values each, held in fp64, Sec. V.B: the dense version
- * stores zeros explicitly) for SDNN_ARM_DENSE.  Synchronises once.
- * Errors: INVALID_OBJECT (a layer not set), OUT_OF_MEMORY, DEVICE.
+ * Build, for every layer, the dense copies of W_k with explicit zeros that the arena holds (Sec. V.B: the
+ * dense version stores zeros explicitly): n*n fp64 values for SDNN_ARM_DENSE and/or n*n fp32 values for
+ * SDNN_ARM_DENSE_F32, in the layer's region of the arena.  Synchronises once.
+ * Errors: INVALID_OBJECT (a layer not set, or an arena without dense copies), DEVICE.
  */
 sdnn_status sdnn_net_build_dense(sdnn_net net);
 
@@ -242,7 +275,8 @@ enum {
     SDNN_KERNEL_DENSIFY = 7,    /* sparse rows -> dense neuron-major activations (sdnn_forward_csr) */
     SDNN_KERNEL_PACK = 8,       /* dense activations -> CSR result (sdnn_forward_csr) */
     SDNN_KERNEL_COMPACT = 9,    /* sparse rows -> CSR result (sdnn_forward_csr) */
-    SDNN_KERNEL_BLOCKED = 10    /* dense-Y CSR product on the sample-blocked layout of very wide layers */
+    SDNN_KERNEL_BLOCKED = 10,   /* dense-Y CSR product on the sample-blocked layout of very wide layers */
+    SDNN_KERNEL_DENSE_GEMM32 = 11 /* dense-W arm on the fp32 matrix cores */
 };
 
 typedef struct {
@@ -261,7 +295,7 @@ sdnn_status sdnn_net_set_profiling(sdnn_net net, int32_t enable);
  */
 sdnn_status sdnn_net_read_profile(sdnn_net net, sdnn_kernel_time *out, int32_t max_records, int32_t *count);
 
-/* Free the net and the device memory the library allocated for it (synchronises its stream). */
+/* Free the net's host handle (synchronises its stream); the arena is the caller's to release afterwards. */
 sdnn_status sdnn_net_free(sdnn_net net);
 
 /* Static text for a status code. */

@@ -23,6 +23,9 @@ LIB_PATH = os.path.join(_HERE, "libsdnn.so")
 SDNN_OK = 0
 SDNN_ARM_SPARSE = 0
 SDNN_ARM_DENSE = 1
+SDNN_ARM_DENSE_F32 = 2
+SDNN_ARENA_DENSE_F64 = 1
+SDNN_ARENA_DENSE_F32 = 2
 SDNN_BIAS_EVERYWHERE = 0
 SDNN_BIAS_PATTERN = 1
 SDNN_SEMIRING_PLUS_TIMES = 0
@@ -35,7 +38,7 @@ SDNN_SEMIRING_XOR_AND = 4
 KERNEL_NAMES = {
     0: "transpose_kernel", 1: "spmm_fanin_kernel", 2: "spmm_narrow_kernel", 3: "spmm_slots_kernel",
     4: "spmm_tiled_kernel", 5: "gemm_dense_layer_kernel", 6: "spgemm_layer", 7: "densify", 8: "pack_dense_to_csr",
-    9: "compact_rows", 10: "spmm_blocked_kernel",
+    9: "compact_rows", 10: "spmm_blocked_kernel", 11: "gemm32_dense_layer_kernel",
 }
 
 STATUS_NAMES = {
@@ -61,7 +64,8 @@ _P = _c.c_void_p
 _I64 = _c.c_int64
 _I32 = _c.c_int32
 _sig = {
-    "sdnn_net_create": [_c.POINTER(_P), _I64, _I32, _c.c_float, _P],
+    "sdnn_net_create": [_c.POINTER(_P), _I64, _I32, _c.c_float, _c.POINTER(_I64), _I32, _P, _I64, _P],
+    "sdnn_net_arena_size": [_I64, _I32, _c.POINTER(_I64), _I32, _c.POINTER(_I64)],
     "sdnn_net_set_stream": [_P, _P],
     "sdnn_net_set_bias_mode": [_P, _I32],
     "sdnn_net_set_layer": [_P, _I32, _I64, _P, _P, _P, _P],
@@ -118,10 +122,23 @@ def sdnn_last_error() -> str:
     return lib.sdnn_last_error().decode()
 
 
-def sdnn_net_create(n: int, L: int, ymax: float = math.inf, stream=None):
-    """Returns the opaque net handle (an int)."""
+def _caps(nnz_per_layer):
+    arr = (_I64 * max(1, len(nnz_per_layer)))(*[int(x) for x in nnz_per_layer])
+    return arr
+
+
+def sdnn_net_arena_size(n: int, L: int, nnz_per_layer, dense_flags: int = 0) -> int:
+    out = _I64()
+    _check(lib.sdnn_net_arena_size(n, L, _caps(nnz_per_layer), dense_flags, _c.byref(out)))
+    return out.value
+
+
+def sdnn_net_create(n: int, L: int, ymax: float, nnz_per_layer, dense_flags: int, arena, arena_bytes: int,
+                    stream=None):
+    """Returns the opaque net handle (an int); arena: device memory of at least sdnn_net_arena_size bytes."""
     h = _P()
-    _check(lib.sdnn_net_create(_c.byref(h), n, L, ymax, _ptr(stream)))
+    _check(lib.sdnn_net_create(_c.byref(h), n, L, ymax, _caps(nnz_per_layer), dense_flags, _ptr(arena), arena_bytes,
+                               _ptr(stream)))
     return h.value
 
 
@@ -193,16 +210,26 @@ def sdnn_net_read_profile(net, max_records: int = 1 << 16):
 
 
 class Net:
-    """Owns a net handle and the device tensors its layers reference (they must outlive it)."""
+    """Owns a net handle, its arena (a torch uint8 tensor) and the device tensors its layers reference (they
+    must outlive it).  nnz_per_layer: the most entries each layer will hold (an int applies to every layer);
+    dense: SDNN_ARENA_DENSE_* flags (True means the fp64 copy) for the dense arms."""
 
-    def __init__(self, n: int, L: int, ymax: float = math.inf, device: str = "cuda:0"):
+    def __init__(self, n: int, L: int, ymax: float = math.inf, device: str = "cuda:0", nnz_per_layer=None,
+                 dense=0):
         import torch
 
         self.torch = torch
         self.device = torch.device(device)
         self.n, self.L, self.ymax = n, L, ymax
+        if nnz_per_layer is None:
+            raise ValueError("nnz_per_layer (the entry capacity of each layer) is required")
+        caps = [int(nnz_per_layer)] * L if isinstance(nnz_per_layer, int) else [int(x) for x in nnz_per_layer]
+        flags = SDNN_ARENA_DENSE_F64 if dense is True else int(dense or 0)
+        self.arena_bytes = sdnn_net_arena_size(n, L, caps, flags)
+        self.arena = torch.empty(max(self.arena_bytes, 1), dtype=torch.uint8, device=self.device)
         with torch.cuda.device(self.device):
-            self.handle = sdnn_net_create(n, L, ymax, torch.cuda.current_stream(self.device).cuda_stream)
+            self.handle = sdnn_net_create(n, L, ymax, caps, flags, self.arena, self.arena_bytes,
+                                          torch.cuda.current_stream(self.device).cuda_stream)
         self._keep = [None] * L
         self._ws = {}
 
@@ -328,6 +355,7 @@ class Net:
             self.handle = None
             self._keep = []
             self._ws.clear()
+            self.arena = None
 
     def __del__(self):
         # At interpreter shutdown the HIP runtime (and any tool layered on it) may already be torn down, so
@@ -340,9 +368,11 @@ class Net:
             pass
 
 
-def net_from_problem(problem, device: str = "cuda:0", dense: bool = False, bias_mode: int = SDNN_BIAS_EVERYWHERE) -> Net:
-    """Upload every layer of a workloads.Problem."""
-    net = Net(problem.n, problem.L, problem.ymax, device)
+def net_from_problem(problem, device: str = "cuda:0", dense=0, bias_mode: int = SDNN_BIAS_EVERYWHERE) -> Net:
+    """Upload every layer of a workloads.Problem (dense: SDNN_ARENA_DENSE_* flags, True for the fp64 copy;
+    the dense copies are built)."""
+    net = Net(problem.n, problem.L, problem.ymax, device, nnz_per_layer=[l.nnz for l in problem.layers],
+              dense=dense)
     if bias_mode != SDNN_BIAS_EVERYWHERE:
         net.set_bias_mode(bias_mode)
     for k, l in enumerate(problem.layers):

@@ -75,42 +75,95 @@ struct Layer {
     double *slots = nullptr;        // fp64 weight of every (input, output) pair, tile-major (high fan-in, n^2 fits)
     int32_t *w_seg = nullptr;     // where each fan-out row crosses each accumulator window (wide layers only)
     sdnn::BlockedSched *sched = nullptr;  // schedule of the blocked product (very wide layers only)
-    double *dense_wt = nullptr;  // n x n, W_k row-major in fp64 (zeros explicit), for the dense arm
+    double *dense_wt = nullptr;  // n x n, W_k k-major in fp64 (zeros explicit), for the fp64 dense arm
+    float *dense_wt32 = nullptr; // the same in fp32, for the fp32 dense arm
+    bool dense_ready = false, dense32_ready = false;  // the dense copies hold the current W_k
 };
-
-template <typename T>
-void dfree(T *&p) {
-    if (p) (void)hipFree((void *)p);
-    p = nullptr;
-}
-
-void release(Layer &l) {
-    dfree(l.w_pack);
-    dfree(l.fan_ptr);
-    dfree(l.fan);
-    dfree(l.tile_mask);
-    dfree(l.slots);
-    dfree(l.w_seg);
-    dfree(l.sched);
-    dfree(l.dense_wt);
-    l = Layer();
-}
-
-template <typename T>
-sdnn_status dalloc(T **p, size_t count, const char *what) {
-    *p = nullptr;
-    if (count == 0) count = 1;
-    hipError_t e = hipMalloc((void **)p, count * sizeof(T));
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        *p = nullptr;
-        return fail(SDNN_ERR_OUT_OF_MEMORY, std::string("hipMalloc failed for ") + what);
-    }
-    return SDNN_OK;
-}
 
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// ---------------------------------------------------------------------------------------- net arena
+// All device memory a net keeps lives in one caller-owned arena, laid out once at creation from n, L, the
+// entry capacity of every layer and which dense copies are wanted.  Per layer, at fixed offsets: the packed
+// fan-out rows, the fan-in (W_k^T) pointers and lists (plus a zero guard entry), and the optional structures
+// whose need follows from n and the capacity (tile masks and fp64 weight slots for dense-ish layers, window
+// offsets for the SpGEMM of wide layers, the blocked product's schedule for very wide layers, the dense
+// copies).  Shared: the set-up scratch (counts, scan, radix-sort buffers, sized for the largest layer) and
+// the small per-forward flags and counters.
+constexpr size_t kAbsent = ~size_t(0);
+
+struct LayerPlan {
+    size_t w_pack = kAbsent, fan_ptr = kAbsent, fan = kAbsent, tile_mask = kAbsent, slots = kAbsent,
+           w_seg = kAbsent, sched = kAbsent, dense64 = kAbsent, dense32 = kAbsent;
+    size_t bytes = 0;
+};
+
+struct NetPlan {
+    size_t flags = 0, d_int = 0, stats = 0, counts = 0, tmp = 0, sort = 0;
+    std::vector<size_t> layer_off;
+    std::vector<LayerPlan> layer;
+    size_t bytes = 0;
+};
+
+size_t take(size_t &off, size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+}
+
+LayerPlan plan_layer(int64_t n, int64_t cap, int32_t dense_flags) {
+    LayerPlan lp;
+    size_t off = 0;
+    lp.w_pack = take(off, (size_t)std::max<int64_t>(cap, 1) * sizeof(Edge));
+    lp.fan_ptr = take(off, (size_t)(n + 1) * sizeof(int64_t));
+    lp.fan = take(off, (size_t)(cap + 1) * sizeof(Edge));
+    if (sdnn::spmm_wants_tiles(n, cap)) lp.tile_mask = take(off, sdnn::spmm_tile_mask_elems(n) * sizeof(uint16_t));
+    if (sdnn::spmm_wants_slots(n, cap)) lp.slots = take(off, sdnn::spmm_slot_elems(n) * sizeof(double));
+    if (sdnn::spgemm_wants_window_index(n))
+        lp.w_seg = take(off, (size_t)n * (size_t)(sdnn::spgemm_windows(n) + 1) * sizeof(int32_t));
+    if (sdnn::blocked_wanted(n, 1 << 20))
+        lp.sched = take(off, (size_t)sdnn::blocked_sched_elems(n) * sizeof(sdnn::BlockedSched));
+    if (dense_flags & SDNN_ARENA_DENSE_F64) lp.dense64 = take(off, (size_t)n * (size_t)n * sizeof(double));
+    if (dense_flags & SDNN_ARENA_DENSE_F32) lp.dense32 = take(off, (size_t)n * (size_t)n * sizeof(float));
+    lp.bytes = off;
+    return lp;
+}
+
+NetPlan plan_net(int64_t n, int32_t L, const int64_t *caps, int32_t dense_flags) {
+    NetPlan np;
+    size_t off = 0;
+    int64_t max_cap = 0;
+    for (int32_t k = 0; k < L; ++k) max_cap = std::max(max_cap, caps[k]);
+    np.flags = take(off, 4 * sizeof(uint32_t));
+    np.d_int = take(off, 4 * sizeof(int32_t));
+    np.stats = take(off, (size_t)std::max<int32_t>(L, 1) * sdnn::kSpgemmStats * sizeof(unsigned long long));
+    np.counts = take(off, (size_t)n * sizeof(int32_t));
+    np.tmp = take(off, (size_t)sdnn::scan_tmp_elems(n) * sizeof(int64_t));
+    np.sort = take(off, sdnn::fanin_sort_bytes(max_cap));
+    for (int32_t k = 0; k < L; ++k) {
+        np.layer.push_back(plan_layer(n, caps[k], dense_flags));
+        np.layer_off.push_back(take(off, np.layer.back().bytes));
+    }
+    np.bytes = off;
+    return np;
+}
+
+template <typename T>
+T *at(char *base, size_t off) {
+    return off == kAbsent ? nullptr : reinterpret_cast<T *>(base + off);
+}
+
+sdnn_status check_plan_args(int64_t n, int32_t L, const int64_t *caps, int32_t dense_flags) {
+    if (n < 1 || n > 0x7fffffffLL) return fail(SDNN_ERR_INVALID_VALUE, "n must be in [1, 2^31-1]");
+    if (L < 0) return fail(SDNN_ERR_INVALID_VALUE, "L must be >= 0");
+    if (L > 0 && !caps) return fail(SDNN_ERR_NULL_POINTER, "nnz_per_layer is required when L > 0");
+    if (dense_flags & ~(SDNN_ARENA_DENSE_F64 | SDNN_ARENA_DENSE_F32))
+        return fail(SDNN_ERR_INVALID_VALUE, "unknown dense-copy flags");
+    for (int32_t k = 0; k < L; ++k)
+        if (caps[k] < 0 || caps[k] > 0x7fffffffLL) return fail(SDNN_ERR_INVALID_VALUE, "layer capacities must be in [0, 2^31-1]");
+    return SDNN_OK;
+}
 
 // Workspace of a CSR forward: two slot buffers (count[batch], col[n*ld], val[n*ld] with ld = act_ld(n, batch)
 // >= batch, so that a pair of them also holds two n x batch activation buffers at row pitch ld) and a scan area.
@@ -200,6 +253,10 @@ struct sdnn_net_s {
     int32_t *d_int = nullptr;
     unsigned long long *d_stats = nullptr;  // kSpgemmStats counters per layer of a forward call
     int num_cu = 256;
+    char *arena = nullptr;  // caller-owned device memory holding everything above and every layer's copies
+    NetPlan plan;
+    std::vector<int64_t> caps;  // entry capacity of each layer
+    int32_t dense_flags = 0;
     // profiling log (sdnn_net_set_profiling): one pair of events around each timed launch sequence
     struct ProfRec {
         int32_t layer, kernel;
@@ -263,7 +320,7 @@ static_assert(SDNN_KERNEL_TRANSPOSE == sdnn::kKernTranspose && SDNN_KERNEL_GATHE
                   SDNN_KERNEL_TILED == sdnn::kKernTiled && SDNN_KERNEL_DENSE_GEMM == sdnn::kKernDenseGemm &&
                   SDNN_KERNEL_SPGEMM == sdnn::kKernSpgemm && SDNN_KERNEL_DENSIFY == sdnn::kKernDensify &&
                   SDNN_KERNEL_PACK == sdnn::kKernPack && SDNN_KERNEL_COMPACT == sdnn::kKernCompact &&
-                  SDNN_KERNEL_BLOCKED == sdnn::kKernBlocked,
+                  SDNN_KERNEL_BLOCKED == sdnn::kKernBlocked && SDNN_KERNEL_DENSE_GEMM32 == sdnn::kKernDenseGemm32,
               "profiling kernel ids of the header and the library agree");
 
 extern "C" {
@@ -286,13 +343,30 @@ const char *sdnn_status_string(sdnn_status s) {
 
 const char *sdnn_last_error(void) { return g_last_error.c_str(); }
 
-sdnn_status sdnn_net_create(sdnn_net *out, int64_t n, int32_t L, float ymax, void *stream) {
+sdnn_status sdnn_net_arena_size(int64_t n, int32_t L, const int64_t *nnz_per_layer, int32_t dense_flags,
+                                int64_t *bytes) {
+    g_last_error.clear();
+    if (!bytes) return fail(SDNN_ERR_NULL_POINTER, "bytes is NULL");
+    sdnn_status st = check_plan_args(n, L, nnz_per_layer, dense_flags);
+    if (st != SDNN_OK) return st;
+    *bytes = (int64_t)plan_net(n, L, nnz_per_layer, dense_flags).bytes;
+    return SDNN_OK;
+}
+
+sdnn_status sdnn_net_create(sdnn_net *out, int64_t n, int32_t L, float ymax, const int64_t *nnz_per_layer,
+                            int32_t dense_flags, void *arena, int64_t arena_bytes, void *stream) {
     g_last_error.clear();
     if (!out) return fail(SDNN_ERR_NULL_POINTER, "net is NULL");
     *out = nullptr;
-    if (n < 1 || n > 0x7fffffffLL) return fail(SDNN_ERR_INVALID_VALUE, "n must be in [1, 2^31-1]");
-    if (L < 0) return fail(SDNN_ERR_INVALID_VALUE, "L must be >= 0");
+    sdnn_status st = check_plan_args(n, L, nnz_per_layer, dense_flags);
+    if (st != SDNN_OK) return st;
     if (!(ymax > 0.0f)) return fail(SDNN_ERR_INVALID_VALUE, "ymax must be > 0 (INFINITY for plain ReLU)");
+    if (!arena) return fail(SDNN_ERR_NULL_POINTER, "arena is NULL");
+    if (((uintptr_t)arena) % kAlign != 0) return fail(SDNN_ERR_INVALID_VALUE, "arena must be 256-byte aligned");
+    NetPlan plan = plan_net(n, L, nnz_per_layer, dense_flags);
+    if (arena_bytes < (int64_t)plan.bytes)
+        return fail(SDNN_ERR_WORKSPACE_TOO_SMALL, "arena smaller than sdnn_net_arena_size(): need " +
+                                                      std::to_string(plan.bytes) + " bytes");
     int dev = 0;
     SDNN_HIP(hipGetDevice(&dev));
     hipDeviceProp_t prop;
@@ -308,17 +382,14 @@ sdnn_status sdnn_net_create(sdnn_net *out, int64_t n, int32_t L, float ymax, voi
     net->device = dev;
     net->num_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
     net->layers.resize((size_t)L);
+    net->arena = (char *)arena;
+    net->plan = std::move(plan);
+    net->caps.assign(nnz_per_layer, nnz_per_layer + L);
+    net->dense_flags = dense_flags;
+    net->d_flags = at<uint32_t>(net->arena, net->plan.flags);
+    net->d_int = at<int32_t>(net->arena, net->plan.d_int);
+    net->d_stats = at<unsigned long long>(net->arena, net->plan.stats);
     scratch_init(dev);  // this device's copy of the allocation-free entry point's scratch array
-    sdnn_status st = dalloc(&net->d_flags, 4, "flags");
-    if (st == SDNN_OK) st = dalloc(&net->d_int, 4, "scratch");
-    if (st == SDNN_OK) st = dalloc(&net->d_stats, (size_t)(L > 0 ? L : 1) * sdnn::kSpgemmStats, "layer counters");
-    if (st != SDNN_OK) {
-        dfree(net->d_flags);
-        dfree(net->d_int);
-        dfree(net->d_stats);
-        delete net;
-        return st;
-    }
     *out = net;
     return SDNN_OK;
 }
@@ -346,6 +417,9 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     if (!row_ptr || !bias) return fail(SDNN_ERR_NULL_POINTER, "row_ptr and bias are required");
     if (nnz < 0 || nnz > 0x7fffffffLL) return fail(SDNN_ERR_INVALID_VALUE, "nnz must be in [0, 2^31-1]");
     if (nnz > 0 && (!col_idx || !val)) return fail(SDNN_ERR_NULL_POINTER, "col_idx and val are required when nnz > 0");
+    if (nnz > net->caps[(size_t)k])
+        return fail(SDNN_ERR_WORKSPACE_TOO_SMALL, "the arena holds " + std::to_string(net->caps[(size_t)k]) +
+                                                      " entries for this layer (sdnn_net_create's nnz_per_layer)");
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     if (n > kMaxScan) return fail(SDNN_ERR_UNSUPPORTED, "layers wider than 2^24 neurons are not supported");
@@ -363,7 +437,12 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
                     "W_k is not valid CSR (row_ptr monotone from 0 to nnz, columns in [0,n) strictly increasing)");
     if (flags & 2u) return fail(SDNN_ERR_INVALID_VALUE, "W_k or b_k holds a non-finite value");
 
-    // 2. derived copies
+    // 2. derived copies, built in the layer's region of the arena (its previous copies are overwritten; any
+    //    forward that still reads them was enqueued earlier on the same stream)
+    Layer &l = net->layers[(size_t)k];
+    l = Layer();  // not set until the build below completes
+    char *base = net->arena + net->plan.layer_off[(size_t)k];
+    const LayerPlan &lp = net->plan.layer[(size_t)k];
     Layer nl;
     nl.set = true;
     nl.nnz = nnz;
@@ -373,29 +452,25 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     nl.bias = bias;
     nl.bias_nonpos = (flags & 4u) == 0;
     nl.pos_bias = (int64_t)fl[1];
-    int32_t *counts = nullptr;
-    int64_t *tmp = nullptr;
-    char *sort_scratch = nullptr;
-    sdnn_status st = SDNN_OK;
-    auto cleanup = [&](sdnn_status r) {
-        dfree(counts);
-        dfree(tmp);
-        dfree(sort_scratch);
-        if (r != SDNN_OK) release(nl);
-        return r;
-    };
-    if ((st = dalloc(&nl.w_pack, (size_t)nnz, "packed W_k")) != SDNN_OK) return cleanup(st);
-    if ((st = dalloc(&nl.fan_ptr, (size_t)n + 1, "fan-in pointers")) != SDNN_OK) return cleanup(st);
-    if ((st = dalloc(&nl.fan, (size_t)nnz + 1, "fan-in lists")) != SDNN_OK) return cleanup(st);  // + a zero guard entry
-    if ((st = dalloc(&counts, (size_t)n, "fan-in counts")) != SDNN_OK) return cleanup(st);
-    if ((st = dalloc(&tmp, (size_t)sdnn::scan_tmp_elems(n), "scan scratch")) != SDNN_OK) return cleanup(st);
-    if ((st = dalloc(&sort_scratch, sdnn::fanin_sort_bytes(nnz), "sort scratch")) != SDNN_OK) return cleanup(st);
+    nl.w_pack = at<Edge>(base, lp.w_pack);
+    nl.fan_ptr = at<int64_t>(base, lp.fan_ptr);
+    nl.fan = at<Edge>(base, lp.fan);
+    // optional structures: present when this layer's density (not only the capacity) wants them
+    nl.w_seg = at<int32_t>(base, lp.w_seg);
+    nl.sched = at<sdnn::BlockedSched>(base, lp.sched);
+    nl.tile_mask = sdnn::spmm_wants_tiles(n, nnz) ? at<uint16_t>(base, lp.tile_mask) : nullptr;
+    nl.slots = sdnn::spmm_wants_slots(n, nnz) ? at<double>(base, lp.slots) : nullptr;
+    nl.dense_wt = at<double>(base, lp.dense64);
+    nl.dense_wt32 = at<float>(base, lp.dense32);
+    int32_t *counts = at<int32_t>(net->arena, net->plan.counts);
+    int64_t *tmp = at<int64_t>(net->arena, net->plan.tmp);
+    char *sort_scratch = net->arena + net->plan.sort;
 
     hipError_t e;
-#define SETUP_HIP(call)                                            \
-    do {                                                           \
-        e = (call);                                                \
-        if (e != hipSuccess) return cleanup(fail_hip(e, #call));   \
+#define SETUP_HIP(call)                                  \
+    do {                                                 \
+        e = (call);                                      \
+        if (e != hipSuccess) return fail_hip(e, #call);  \
     } while (0)
     SETUP_HIP(sdnn::launch_pack_edges(nnz, col_idx, val, nl.w_pack, s));
     SETUP_HIP(hipMemsetAsync(counts, 0, (size_t)n * sizeof(int32_t), s));
@@ -406,47 +481,33 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     SETUP_HIP(hipMemsetAsync(net->d_int, 0, sizeof(int32_t), s));
     SETUP_HIP(sdnn::launch_max_segment(n, row_ptr, net->d_int, s));
     SETUP_HIP(hipMemcpyAsync(&nl.max_fanout, net->d_int, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-    if (sdnn::spgemm_wants_window_index(n)) {
-        if ((st = dalloc(&nl.w_seg, (size_t)n * (size_t)(sdnn::spgemm_windows(n) + 1), "window offsets")) != SDNN_OK)
-            return cleanup(st);
-        SETUP_HIP(sdnn::launch_window_seg(n, row_ptr, col_idx, nl.w_seg, s));
-    }
-    if (sdnn::blocked_wanted(n, 1 << 20)) {  // a layer wide enough that large batches take the blocked product
-        if ((st = dalloc(&nl.sched, (size_t)sdnn::blocked_sched_elems(n), "blocked schedule")) != SDNN_OK)
-            return cleanup(st);
-        SETUP_HIP(sdnn::launch_blocked_order(n, nl.fan_ptr, nl.sched, s));
-    }
-    if (sdnn::spmm_wants_tiles(n, nnz)) {
-        if ((st = dalloc(&nl.tile_mask, sdnn::spmm_tile_mask_elems(n), "tile masks")) != SDNN_OK)
-            return cleanup(st);
-        SETUP_HIP(sdnn::launch_spmm_tile_mask(n, nl.fan_ptr, nl.fan, nl.tile_mask, s));
-    }
-    if (sdnn::spmm_wants_slots(n, nnz)) {
-        if ((st = dalloc(&nl.slots, sdnn::spmm_slot_elems(n), "weight slots")) != SDNN_OK) return cleanup(st);
-        SETUP_HIP(sdnn::launch_spmm_slots(n, nl.fan_ptr, nl.fan, nl.slots, s));
-    }
+    if (nl.w_seg) SETUP_HIP(sdnn::launch_window_seg(n, row_ptr, col_idx, nl.w_seg, s));
+    if (nl.sched) SETUP_HIP(sdnn::launch_blocked_order(n, nl.fan_ptr, nl.sched, s));
+    if (nl.tile_mask) SETUP_HIP(sdnn::launch_spmm_tile_mask(n, nl.fan_ptr, nl.fan, nl.tile_mask, s));
+    if (nl.slots) SETUP_HIP(sdnn::launch_spmm_slots(n, nl.fan_ptr, nl.fan, nl.slots, s));
     SETUP_HIP(hipStreamSynchronize(s));
 #undef SETUP_HIP
-    cleanup(SDNN_OK);
-    Layer &slot = net->layers[(size_t)k];
-    release(slot);  // the stream was synchronised above, so nothing still reads the old copies
-    slot = nl;
+    l = nl;
     return SDNN_OK;
 }
 
 sdnn_status sdnn_net_build_dense(sdnn_net net) {
     g_last_error.clear();
     if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
+    if (!net->dense_flags) return fail(SDNN_ERR_INVALID_OBJECT, "the arena holds no dense copies (dense_flags 0)");
     SDNN_ON_DEVICE(net);
     const int64_t n = net->n;
     for (int32_t k = 0; k < net->L; ++k) {
         Layer &l = net->layers[(size_t)k];
         if (!l.set) return fail(SDNN_ERR_INVALID_OBJECT, "every layer must be set before build_dense");
-        if (l.dense_wt) continue;
-        sdnn_status st = dalloc(&l.dense_wt, (size_t)n * (size_t)n, "dense W_k");
-        if (st != SDNN_OK) return st;
-        hipError_t e = sdnn::launch_dense_from_fanin(n, l.fan_ptr, l.fan, l.dense_wt, net->stream);
-        if (e != hipSuccess) return fail_hip(e, "launch_dense_from_fanin");
+        if (l.dense_wt && !l.dense_ready) {
+            SDNN_HIP(sdnn::launch_dense_from_fanin(n, l.fan_ptr, l.fan, l.dense_wt, net->stream));
+            l.dense_ready = true;
+        }
+        if (l.dense_wt32 && !l.dense32_ready) {
+            SDNN_HIP(sdnn::launch_dense32_from_fanin(n, l.fan_ptr, l.fan, l.dense_wt32, net->stream));
+            l.dense32_ready = true;
+        }
     }
     SDNN_HIP(hipStreamSynchronize(net->stream));
     return SDNN_OK;
@@ -491,9 +552,10 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
     sdnn_status st = check_range(net, k0, k1);
     if (st != SDNN_OK) return st;
     if (batch < 0) return fail(SDNN_ERR_DIMENSION_MISMATCH, "batch must be >= 0");
-    if (arm != SDNN_ARM_SPARSE && arm != SDNN_ARM_DENSE) return fail(SDNN_ERR_INVALID_VALUE, "unknown arm");
-    if (arm == SDNN_ARM_DENSE && net->bias_pattern)
-        return fail(SDNN_ERR_UNSUPPORTED, "the dense arm stores every zero of W_k, so it has no bias pattern");
+    if (arm != SDNN_ARM_SPARSE && arm != SDNN_ARM_DENSE && arm != SDNN_ARM_DENSE_F32)
+        return fail(SDNN_ERR_INVALID_VALUE, "unknown arm");
+    if (arm != SDNN_ARM_SPARSE && net->bias_pattern)
+        return fail(SDNN_ERR_UNSUPPORTED, "the dense arms store every zero of W_k, so they have no bias pattern");
     if (batch == 0) return SDNN_OK;
     if (!Y_in || !Y_out) return fail(SDNN_ERR_NULL_POINTER, "Y_in and Y_out are required");
     SDNN_ON_DEVICE(net);
@@ -520,10 +582,12 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
     if (!ws) return fail(SDNN_ERR_NULL_POINTER, "ws is required");
     if (ws_bytes < (int64_t)dense_ws_bytes(n, batch, net->num_cu))
         return fail(SDNN_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than sdnn_workspace_size(net, batch, 0)");
-    if (arm == SDNN_ARM_DENSE)
-        for (int32_t k = k0; k < k1; ++k)
-            if (!net->layers[(size_t)k].dense_wt)
-                return fail(SDNN_ERR_INVALID_OBJECT, "dense arm requested before sdnn_net_build_dense");
+    for (int32_t k = k0; k < k1; ++k) {
+        const Layer &l = net->layers[(size_t)k];
+        if ((arm == SDNN_ARM_DENSE && !l.dense_ready) || (arm == SDNN_ARM_DENSE_F32 && !l.dense32_ready))
+            return fail(SDNN_ERR_INVALID_OBJECT, "dense arm requested before sdnn_net_build_dense (or without its copy "
+                                                 "in the arena)");
+    }
     const int64_t ld = sdnn::act_ld(n, batch);
     float *buf[2];
     buf[0] = (float *)ws;
@@ -560,9 +624,14 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
         if (arm == SDNN_ARM_SPARSE)
             SDNN_HIP(sdnn::launch_spmm_fanin(n, batch, ld, l.fan_ptr, l.fan, l.tile_mask, l.slots, l.bias,
                                              net->ymax, net->bias_pattern, buf[cur], buf[cur ^ 1], s, &kind));
-        else
+        else if (arm == SDNN_ARM_DENSE)
             SDNN_HIP(sdnn::launch_gemm_dense_layer(n, batch, ld, l.dense_wt, l.bias, net->ymax, buf[cur],
                                                    buf[cur ^ 1], partial, net->num_cu, s));
+        else {
+            kind = sdnn::kKernDenseGemm32;
+            SDNN_HIP(sdnn::launch_gemm32_dense_layer(n, batch, ld, l.dense_wt32, l.bias, net->ymax, buf[cur],
+                                                     buf[cur ^ 1], reinterpret_cast<float *>(partial), net->num_cu, s));
+        }
         SDNN_HIP(prof_end(net, pr, kind));
         cur ^= 1;
     }
@@ -856,11 +925,7 @@ sdnn_status sdnn_net_free(sdnn_net net) {
     (void)hipStreamSynchronize(net->stream);
     prof_clear(net);
     for (hipEvent_t e : net->ev_free) (void)hipEventDestroy(e);
-    for (Layer &l : net->layers) release(l);
-    dfree(net->d_flags);
-    dfree(net->d_int);
-    dfree(net->d_stats);
-    delete net;
+    delete net;  // the arena belongs to the caller
     return SDNN_OK;
 }
 

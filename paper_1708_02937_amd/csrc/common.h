@@ -21,12 +21,13 @@ enum KernelKind : int {
     kKernNarrow = 2,      // dense-Y product: narrow-chunk gather, 16 lanes per neuron, 64 samples
     kKernSlots = 3,       // dense-Y product: LDS tiles with scalar-register fp64 weights
     kKernTiled = 4,       // dense-Y product: LDS tiles, weights broadcast from lanes
-    kKernDenseGemm = 5,   // dense-W arm on the matrix cores
+    kKernDenseGemm = 5,   // dense-W arm on the fp64 matrix cores
     kKernSpgemm = 6,      // sparse-Y product: planning, small-sample and workgroup SpGEMM kernels
     kKernDensify = 7,     // sparse rows -> dense neuron-major activations
     kKernPack = 8,        // dense activations -> CSR result
     kKernCompact = 9,     // sparse slot rows -> CSR result
-    kKernBlocked = 10     // dense-Y product on the sample-blocked layout (very wide layers)
+    kKernBlocked = 10,    // dense-Y product on the sample-blocked layout (very wide layers)
+    kKernDenseGemm32 = 11 // dense-W arm on the fp32 matrix cores
 };
 
 // Wave-local exclusive count of set bits below this lane in a 64-bit ballot.
@@ -96,6 +97,11 @@ size_t gemm_partial_bytes(int64_t n, int64_t batch, int num_cu);
 // partial: gemm_partial_bytes(n, batch, num_cu) bytes of scratch (unused when that is 0).
 hipError_t launch_gemm_dense_layer(int64_t n, int64_t batch, int64_t ld, const double *wt, const float *bias, double ymax,
                                    const float *yt, float *zt, double *partial, int num_cu, hipStream_t s);
+
+// fp32 copy and the fp32 matrix-core arm (partial: gemm_partial_bytes scratch, used as fp32)
+hipError_t launch_dense32_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge *fan, float *wt, hipStream_t s);
+hipError_t launch_gemm32_dense_layer(int64_t n, int64_t batch, int64_t ld, const float *wt, const float *bias,
+                                     double ymax, const float *yt, float *zt, float *partial, int num_cu, hipStream_t s);
 
 // spgemm.hip
 size_t spgemm_lds_bytes(int64_t n);

@@ -179,7 +179,164 @@ __global__ void dense_from_fanin_kernel(int64_t n, const int64_t *__restrict__ f
     }
 }
 
+// ---------------------------------------------------------------------------- fp32 matrix-core arm
+// The same product with fp32 operands and fp32 accumulation on v_mfma_f32_16x16x4_f32, the arithmetic of a
+// single-precision BLAS sgemm (the dense library of the paper's comparison, Sec. V.A).  Same 128 x 64 tiles,
+// four waves of 64 x 32 (4 x 2 blocks of 16 x 16), double-buffered LDS with K steps of 16 and the
+// split-K scheme for small batches (fp32 partials, summed in split order).  Output layout of the 16 x 16
+// f32 MFMA: lane l holds column l % 16 and, in element v, row 4 * (l / 16) + v.
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+constexpr int kPad32 = 4;
+
+template <bool kFast>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm32_dense_layer_kernel(
+    int64_t M, int64_t N, int64_t K, int64_t ld, int64_t kc, const float *__restrict__ Wk, const float *__restrict__ B,
+    const float *__restrict__ bias, double ymax, float *__restrict__ C, float *__restrict__ partial) {
+    __shared__ __align__(16) float As[2][BK][BM + kPad32];
+    __shared__ __align__(16) float Bs[2][BK][BN + kPad32];
+    constexpr int kNB = BN / 32;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t m0 = (int64_t)blockIdx.x * BM;
+    const int64_t n0 = (int64_t)blockIdx.y * BN;
+    const int64_t kb = (int64_t)blockIdx.z * kc;
+    const int64_t ke = kb + kc < K ? kb + kc : K;
+
+    // staging: thread -> k row tid / 16, A columns (tid % 16) * 8 .. + 7, B columns (tid % 16) * 4 .. + 3
+    const int s_k = tid >> 4, s_a = (tid & 15) * 8, s_b = (tid & 15) * 4;
+    float ra[8], rb[4];
+    auto load_tiles = [&](int64_t k0) {
+        const int64_t gk = k0 + s_k;
+        if constexpr (kFast) {
+            const float4 v0 = *reinterpret_cast<const float4 *>(Wk + gk * M + m0 + s_a);
+            const float4 v1 = *reinterpret_cast<const float4 *>(Wk + gk * M + m0 + s_a + 4);
+            ra[0] = v0.x; ra[1] = v0.y; ra[2] = v0.z; ra[3] = v0.w;
+            ra[4] = v1.x; ra[5] = v1.y; ra[6] = v1.z; ra[7] = v1.w;
+            const float4 u = *reinterpret_cast<const float4 *>(B + gk * ld + n0 + s_b);
+            rb[0] = u.x; rb[1] = u.y; rb[2] = u.z; rb[3] = u.w;
+        } else {
+#pragma unroll
+            for (int h = 0; h < 8; ++h) {
+                const int64_t gm = m0 + s_a + h;
+                ra[h] = (gk < ke && gm < M) ? Wk[gk * M + gm] : 0.0f;
+            }
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+                const int64_t gc = n0 + s_b + h;
+                rb[h] = (gk < ke && gc < N) ? B[gk * ld + gc] : 0.0f;
+            }
+        }
+    };
+    auto store_tiles = [&](int buf) {
+        *reinterpret_cast<float4 *>(&As[buf][s_k][s_a]) = make_float4(ra[0], ra[1], ra[2], ra[3]);
+        *reinterpret_cast<float4 *>(&As[buf][s_k][s_a + 4]) = make_float4(ra[4], ra[5], ra[6], ra[7]);
+        *reinterpret_cast<float4 *>(&Bs[buf][s_k][s_b]) = make_float4(rb[0], rb[1], rb[2], rb[3]);
+    };
+
+    floatx4 acc[4][kNB];
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < kNB; ++ni) acc[mi][ni] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    const int rc = lane & 15, kq = lane >> 4;
+    auto compute = [&](int cur) {
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 4) {
+            float a[4], b[kNB];
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi) a[mi] = As[cur][kk + kq][wm * 64 + mi * 16 + rc];
+#pragma unroll
+            for (int ni = 0; ni < kNB; ++ni) b[ni] = Bs[cur][kk + kq][wn * (BN / 2) + ni * 16 + rc];
+#pragma unroll
+            for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < kNB; ++ni)
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
+        }
+    };
+
+    const int64_t ktiles = (ke - kb + BK - 1) / BK;
+    load_tiles(kb);
+    store_tiles(0);
+    __syncthreads();
+    for (int64_t kt = 0; kt + 1 < ktiles; ++kt) {
+        const int cur = (int)(kt & 1);
+        load_tiles(kb + (kt + 1) * BK);
+        compute(cur);
+        store_tiles(cur ^ 1);
+        __syncthreads();
+    }
+    compute((int)((ktiles - 1) & 1));
+
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < kNB; ++ni)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int64_t m = m0 + wm * 64 + mi * 16 + 4 * kq + v;
+                const int64_t col = n0 + wn * (BN / 2) + ni * 16 + rc;
+                if (kFast || (m < M && col < N)) {
+                    if (partial)
+                        partial[((int64_t)blockIdx.z * M + m) * N + col] = acc[mi][ni][v];
+                    else
+                        C[m * ld + col] = activate((double)(acc[mi][ni][v] + bias[m]), ymax);
+                }
+            }
+}
+
+__global__ void gemm32_split_reduce_kernel(int64_t M, int64_t N, int64_t ld, int splits, const float *__restrict__ partial,
+                                           const float *__restrict__ bias, double ymax, float *__restrict__ C) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= M * N) return;
+    float z = 0.0f;
+    for (int sp = 0; sp < splits; ++sp) z += partial[(int64_t)sp * M * N + e];
+    C[(e / N) * ld + e % N] = activate((double)(z + bias[e / N]), ymax);
+}
+
+__global__ void dense32_from_fanin_kernel(int64_t n, const int64_t *__restrict__ fan_ptr, const Edge *__restrict__ fan,
+                                          float *__restrict__ wk) {
+    const int64_t j = blockIdx.x;
+    for (int64_t e = fan_ptr[j] + threadIdx.x; e < fan_ptr[j + 1]; e += blockDim.x) {
+        const Edge ed = fan[e];
+        wk[(int64_t)ed.idx * n + j] = ed.w;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_dense32_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge *fan, float *wt, hipStream_t s) {
+    hipError_t err = hipMemsetAsync(wt, 0, (size_t)n * (size_t)n * sizeof(float), s);
+    if (err != hipSuccess) return err;
+    dense32_from_fanin_kernel<<<(unsigned)n, 256, 0, s>>>(n, fan_ptr, fan, wt);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm32_dense_layer(int64_t n, int64_t batch, int64_t ld, const float *wt, const float *bias,
+                                     double ymax, const float *yt, float *zt, float *partial, int num_cu, hipStream_t s) {
+    if (n == 0 || batch == 0) return hipSuccess;
+    const int64_t gx = (n + BM - 1) / BM, gy = (batch + BN - 1) / BN;
+    if (gx > 0x7fffffffLL || gy > 65535) return hipErrorInvalidValue;
+    int sp = gemm_splits(n, batch, num_cu);
+    const int64_t steps = (n + BK - 1) / BK;
+    const int64_t kc = ((steps + sp - 1) / sp) * BK;
+    sp = (int)((n + kc - 1) / kc);
+    float *part = sp > 1 ? partial : nullptr;
+    const bool fast = n % BM == 0 && batch % BN == 0 && n % BK == 0 && ld % 4 == 0;
+    const dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)sp);
+    if (fast)
+        gemm32_dense_layer_kernel<true><<<grid, 256, 0, s>>>(n, batch, n, ld, kc, wt, yt, bias, ymax, zt, part);
+    else
+        gemm32_dense_layer_kernel<false><<<grid, 256, 0, s>>>(n, batch, n, ld, kc, wt, yt, bias, ymax, zt, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || sp == 1) return e;
+    gemm32_split_reduce_kernel<<<(unsigned)((n * batch + 255) / 256), 256, 0, s>>>(n, batch, ld, sp, partial, bias,
+                                                                                  ymax, zt);
+    return hipGetLastError();
+}
 
 hipError_t launch_dense_from_fanin(int64_t n, const int64_t *fan_ptr, const Edge *fan, double *wt, hipStream_t s) {
     hipError_t err = hipMemsetAsync(wt, 0, (size_t)n * (size_t)n * sizeof(double), s);

@@ -33,7 +33,7 @@ def _say(*a):
 def run_dense(sd, p, arm, y0=None, bias_mode=0):
     import torch
 
-    net = sd.net_from_problem(p, dense=(arm == sd.SDNN_ARM_DENSE), bias_mode=bias_mode)
+    net = sd.net_from_problem(p, dense={sd.SDNN_ARM_DENSE: 1, sd.SDNN_ARM_DENSE_F32: 2}.get(arm, 0), bias_mode=bias_mode)
     y = torch.from_numpy(p.y0_dense if y0 is None else y0).cuda()
     out = net.forward_dense(y, arm=arm).cpu().numpy()
     net.free()
@@ -52,7 +52,7 @@ ARMS = ["sparse", "dense"]
 
 
 def _arm(sd, name):
-    return sd.SDNN_ARM_SPARSE if name == "sparse" else sd.SDNN_ARM_DENSE
+    return {"sparse": sd.SDNN_ARM_SPARSE, "dense": sd.SDNN_ARM_DENSE, "dense32": sd.SDNN_ARM_DENSE_F32}[name]
 
 
 # ------------------------------------------------------------------------------------------ small shapes
@@ -234,7 +234,7 @@ def test_blocked_product_very_wide(sd, n, batch):
                   rng.uniform(-0.1, 0.1, size=n).astype(np.float32))
     gen = torch.Generator(device="cuda").manual_seed(20170802)
     y = torch.rand((batch, n), generator=gen, device="cuda", dtype=torch.float32)
-    net = sd.Net(n, 1)
+    net = sd.Net(n, 1, nnz_per_layer=layer.nnz)
     net.set_layer(0, layer.row_ptr, layer.col, layer.val, layer.bias)
     _say("blocked very wide", n, batch)
     out = net.forward_dense(y, arm=sd.SDNN_ARM_SPARSE)
@@ -620,7 +620,7 @@ def test_graph_replay_matches_eager(sd, layers):
                         bias_hi=1.0)
         assert 9 * p.layers[0].nnz >= 2 * p.n * p.n
     for arm in ARMS:
-        net = sd.net_from_problem(p, dense=(arm == "dense"))
+        net = sd.net_from_problem(p, dense={"dense": 1, "dense32": 2}.get(arm, 0))
         rng = np.random.default_rng(5)
         inputs = [p.y0_dense] + [rng.random((p.batch, p.n), dtype=np.float32) for _ in range(3)]
         want = [net.forward_dense(torch.from_numpy(x).cuda(), arm=_arm(sd, arm)).cpu().numpy() for x in inputs]
@@ -708,7 +708,7 @@ def test_errors_leave_net_usable(sd):
     import torch
 
     p = tiny_random(4, 50, 2, 6, w_density=0.2, dense_input=True)
-    net = sd.Net(50, 2)
+    net = sd.Net(50, 2, nnz_per_layer=[l.nnz for l in p.layers])
     l = p.layers[0]
     bad_cols = l.col.copy()
     r = int(np.argmax(np.diff(l.row_ptr) >= 2))
@@ -774,3 +774,82 @@ def test_profiling_log_names_each_launch(sd):
     net.forward_dense(y)
     assert net.read_profile() == []
     net.free()
+
+
+# ------------------------------------------------------------------ fp32 dense arm (sgemm arithmetic)
+
+
+@pytest.mark.parametrize("seed,n,batch,d", [(101, 1, 1, 1.0), (102, 63, 65, 0.3), (103, 130, 200, 0.2),
+                                            (104, 1000, 300, 0.05), (105, 4096, 64, 0.5), (106, 700, 1024, 1.0)])
+def test_fp32_dense_arm_one_layer(sd, seed, n, batch, d):
+    """The fp32 matrix-core arm against the oracle within its derived bound: products and sums rounded to
+    fp32 over n terms, |g - o| <= 1e-6 + 1e-5 |o| + gamma_{n+2} s (s = sum |y w| + |b|); ragged tiles, the
+    split-K path at small batch and fully dense W."""
+    p = tiny_random(seed, n, 1, batch, w_density=d, y_density=0.6, dense_input=True, bias_lo=-0.5, bias_hi=0.5)
+    _say("fp32 dense arm", seed, n, batch, d)
+    out = run_dense(sd, p, sd.SDNN_ARM_DENSE_F32)
+    st = parity.compare_in_chunks(p, dense_to_csr(out), scale_tol=parity.fp32_sum_scale(n))
+    assert st["entries"] > 0 or n == 1
+
+
+@pytest.mark.parametrize("d", [0.5, 0.01])
+def test_fp32_dense_arm_density_sweep_layer(sd, d):
+    """One full-size density-sweep layer (n 4096, batch 1024) on the fp32 arm, every row, and the oracle's
+    Y_9 through layer 9 (d = 0.01)."""
+    p = make_config(2, d, L=1)
+    _say("fp32 dense arm sweep", d)
+    parity.compare_in_chunks(p, dense_to_csr(run_dense(sd, p, sd.SDNN_ARM_DENSE_F32)),
+                             scale_tol=parity.fp32_sum_scale(p.n))
+    if d == 0.01:
+        q = make_config(2, d)
+        yk = parity.oracle_rows(q, k1=9)
+        one = _one_layer(q, 9, yk)
+        got = dense_to_csr(run_dense(sd, one, sd.SDNN_ARM_DENSE_F32, y0=parity.to_dense(yk, q.n)))
+        parity.compare_in_chunks(one, got, scale_tol=parity.fp32_sum_scale(q.n))
+
+
+# ------------------------------------------------------------------ caller-owned arena
+
+
+def test_arena_is_the_only_device_memory(sd):
+    """The net keeps everything in the caller's arena: an arena one byte short is refused, a layer above
+    its capacity is refused, and set-up, dense copies and forwards leave the device's free memory unchanged
+    (the arena and workspace are allocated by the caller beforehand)."""
+    import torch
+
+    p = make_config(2, 0.01, n=20000, L=2, batch=256)
+    caps = [l.nnz for l in p.layers]
+    need = sd.sdnn_net_arena_size(p.n, p.L, caps, 3)
+    assert need > sd.sdnn_net_arena_size(p.n, p.L, caps, 0)
+    small = torch.empty(need - 1, dtype=torch.uint8, device="cuda")
+    with pytest.raises(sd.SdnnError) as e:
+        sd.sdnn_net_create(p.n, p.L, math.inf, caps, 3, small, need - 1)
+    assert e.value.status == 6
+    del small
+    for rep in range(2):  # the first pass loads the code objects
+        torch.cuda.synchronize()
+        net = sd.Net(p.n, p.L, nnz_per_layer=caps, dense=3)
+        y = torch.from_numpy(p.y0_dense).cuda()
+        out = torch.empty_like(y)
+        ws = net.workspace(p.batch, 0)
+        torch.cuda.synchronize()
+        free0 = torch.cuda.mem_get_info()[0]
+        for k, l in enumerate(p.layers):
+            net.set_layer(k, l.row_ptr, l.col, l.val, l.bias)
+        net.build_dense()
+        for arm in (sd.SDNN_ARM_SPARSE, sd.SDNN_ARM_DENSE, sd.SDNN_ARM_DENSE_F32):
+            net.forward_dense(y, arm=arm, out=out)
+        torch.cuda.synchronize()
+        free1 = torch.cuda.mem_get_info()[0]
+        _say("arena free memory", rep, free0, free1)
+        if rep == 1:
+            assert free0 - free1 < (2 << 20), "device memory was allocated outside the arena"
+            l = p.layers[0]
+            big = make_config(2, 0.02, n=20000, L=1, batch=8).layers[0]
+            assert big.nnz > caps[0]
+            with pytest.raises(sd.SdnnError) as e:
+                net.set_layer(0, big.row_ptr, big.col, big.val, big.bias)
+            assert e.value.status == 6
+            parity.compare(p, dense_to_csr(net.forward_dense(y).cpu().numpy()))  # still usable
+        net.free()
+        del ws

@@ -55,12 +55,19 @@ def test_host_side_argument_errors():
     import paper_1708_02937_amd as sd
 
     lib = sd.lib
-    assert lib.sdnn_net_create(None, 8, 1, 1.0, None) == 1  # NULL out pointer
+    caps = (ctypes.c_int64 * 1)(10)
+    fake = 1 << 20  # an aligned non-null address: every call below fails its argument checks first
+    assert lib.sdnn_net_create(None, 8, 1, 1.0, caps, 0, fake, 1 << 20, None) == 1  # NULL out pointer
     h = ctypes.c_void_p()
-    assert lib.sdnn_net_create(ctypes.byref(h), 0, 1, 1.0, None) == 2  # n < 1
-    assert lib.sdnn_net_create(ctypes.byref(h), 8, -1, 1.0, None) == 2  # L < 0
-    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, 0.0, None) == 2  # ymax <= 0
-    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, float("nan"), None) == 2
+    assert lib.sdnn_net_create(ctypes.byref(h), 0, 1, 1.0, caps, 0, fake, 1 << 20, None) == 2  # n < 1
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, -1, 1.0, caps, 0, fake, 1 << 20, None) == 2  # L < 0
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, 0.0, caps, 0, fake, 1 << 20, None) == 2  # ymax <= 0
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, float("nan"), caps, 0, fake, 1 << 20, None) == 2
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, 1.0, None, 0, fake, 1 << 20, None) == 1  # no capacities
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, 1.0, caps, 4, fake, 1 << 20, None) == 2  # unknown flags
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, 1.0, caps, 0, None, 1 << 20, None) == 1  # no arena
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, 1.0, caps, 0, fake + 8, 1 << 20, None) == 2  # misaligned
+    assert lib.sdnn_net_create(ctypes.byref(h), 8, 1, 1.0, caps, 0, fake, 16, None) == 6  # arena too small
     out = ctypes.c_int64()
     assert lib.sdnn_workspace_size(None, 4, 0, ctypes.byref(out)) == 5  # NULL net
     assert lib.sdnn_net_set_layer(None, 0, 0, None, None, None, None) == 5
@@ -77,3 +84,24 @@ def test_oracle_and_library_share_no_code():
             if f.endswith((".hip", ".cpp", ".h", ".py")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in text.lower(), f
+
+
+def test_arena_size_accounts_for_every_copy():
+    """sdnn_net_arena_size (host-only arithmetic): grows with the layers' capacities, with the dense copies
+    (at least n^2 x 8 and n^2 x 4 bytes per layer) and with the near-dense structures a high capacity calls
+    for; bad arguments are refused."""
+    import paper_1708_02937_amd as sd
+
+    n = 1000
+    base = sd.sdnn_net_arena_size(n, 2, [5000, 5000], 0)
+    assert base >= 2 * (5000 * 8 + (n + 1) * 8 + 5001 * 8)
+    assert sd.sdnn_net_arena_size(n, 2, [5000, 9000], 0) > base
+    assert sd.sdnn_net_arena_size(n, 2, [5000, 5000], 1) >= base + 2 * n * n * 8
+    assert sd.sdnn_net_arena_size(n, 2, [5000, 5000], 2) >= base + 2 * n * n * 4
+    assert sd.sdnn_net_arena_size(n, 2, [5000, 5000], 3) >= base + 2 * n * n * 12
+    dense_ish = sd.sdnn_net_arena_size(n, 1, [n * n // 2], 0)  # density 1/2: tile masks and fp64 weight slots
+    assert dense_ish >= (n * n // 2) * 16 + n * n * 8
+    assert sd.sdnn_net_arena_size(n, 0, [], 0) > 0
+    for args in [(0, 1, [1], 0), (n, -1, [1], 0), (n, 1, [-1], 0), (n, 1, [1], 8)]:
+        with pytest.raises(sd.SdnnError):
+            sd.sdnn_net_arena_size(*args)
