@@ -614,6 +614,51 @@ def summarize_pmc(kernel, tag, dirs, copy_bytes, commands, out, src_names):
         f.write("\n".join(lines) + "\n")
 
 
+def summarize_counters(dirs, title, commands, out):
+    """Per kernel, the mean of every counter over its dispatches, from rocprofv3 --pmc runs (counter_collection
+    CSVs under each of dirs; runs of the same command, merged by kernel name), with busy fractions against the
+    dispatch's cycles (GRBM_GUI_ACTIVE, summed over the 8 XCDs): VALU issue (4 cycles per wave64 instruction
+    on a 16-lane SIMD, 1024 SIMDs), MFMA busy (per SIMD) and TA / TD busy (per CU)."""
+    import csv
+    import glob
+    from collections import defaultdict
+
+    agg = defaultdict(lambda: defaultdict(list))
+    for d in dirs:
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(path)):
+                k = _short_name(r["Kernel_Name"])
+                if k.startswith(("at::", "__amd")):
+                    continue
+                agg[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    lines = [f"# rocprofv3 counters: {title}", "", "commands (from the repository root on the MI355X box):", ""]
+    lines += [f"    {c}" for c in commands]
+    lines += ["", "| kernel | counter | dispatches | mean per dispatch |", "|---|---|---|---|"]
+    derived = []
+    for k in sorted(agg):
+        m = {c: sum(v) / len(v) for c, v in agg[k].items()}
+        for c in sorted(m):
+            lines.append(f"| {k} | {c} | {len(agg[k][c])} | {m[c]:.6g} |")
+        cyc = m.get("GRBM_GUI_ACTIVE", 0) / 8  # GUI-active cycles are summed over the 8 XCDs
+        if cyc <= 0:
+            continue
+        if "SQ_INSTS_VALU" in m:  # a wave64 VALU instruction occupies its 16-lane SIMD for 4 cycles
+            derived.append(f"| {k} | VALU issue: SQ_INSTS_VALU x 4 / (1024 SIMDs x cycles) | "
+                           f"{m['SQ_INSTS_VALU'] * 4 / (1024 * cyc):.3f} |")
+        if m.get("SQ_VALU_MFMA_BUSY_CYCLES"):
+            derived.append(f"| {k} | MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x cycles) | "
+                           f"{m['SQ_VALU_MFMA_BUSY_CYCLES'] / (1024 * cyc):.3f} |")
+        for c in ("TA_TA_BUSY_sum", "TD_TD_BUSY_sum"):
+            if c in m:
+                derived.append(f"| {k} | {c} / (256 CUs x cycles) | {m[c] / (256 * cyc):.3f} |")
+        derived.append(f"| {k} | dispatch cycles (GRBM_GUI_ACTIVE / 8 XCDs) | {cyc:.4g} |")
+    if derived:
+        lines += ["", "derived (busy fractions; 1.0 = every unit busy for the whole dispatch):", "",
+                  "| kernel | ratio | value |", "|---|---|---|"] + derived
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -638,6 +683,9 @@ def main():
                     help="only run a plain device copy of BYTES bytes 5 times (counter calibration)")
     ap.add_argument("--summarize-stats", nargs=4, metavar=("CSV_DIR", "TITLE", "COMMAND", "OUT"),
                     help="write a profiles/ table from a rocprofv3 --stats run (no GPU needed)")
+    ap.add_argument("--summarize-counters", nargs=4, metavar=("DIRS", "TITLE", "COMMANDS", "OUT"),
+                    help="write a profiles/ table of per-kernel counter means from rocprofv3 --pmc runs "
+                         "('|'-separated directories and commands)")
     ap.add_argument("--summarize-pmc", nargs=9,
                     metavar=("KERNEL", "WORKLOAD", "FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR",
                              "COPY_BYTES", "COMMANDS", "OUT"),
@@ -645,6 +693,10 @@ def main():
     args = ap.parse_args()
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats)
+        return
+    if args.summarize_counters:
+        a = args.summarize_counters
+        summarize_counters(a[0].split("|"), a[1], a[2].split("|"), a[3])
         return
     if args.summarize_pmc:
         a = args.summarize_pmc
