@@ -118,6 +118,13 @@ __device__ __forceinline__ void fma4(const float4 &y, float w, double (&acc)[4],
     }
 }
 
+// Orders LDS writes and reads among the lanes of one wave (no other wave touches the region).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Wave-uniform minimum and maximum of a value that is equal within each group of eight lanes.
 __device__ __forceinline__ void group8_min_max(int v, int &mn, int &mx) {
     int a = v, b = v;
@@ -176,13 +183,13 @@ __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SD
             // this block's entries of the lane's neuron: entry t + 8r + u at slot[64r + 8q + u]
 #pragma unroll
             for (int r = 0; r < kR; ++r) slot[64 * r + lane] = mine[r];
-            __builtin_amdgcn_wave_barrier();
+            wave_lds_sync();
             Edge e[kBUnroll];
 #pragma unroll
             for (int r = 0; r < kR; ++r)
 #pragma unroll
                 for (int u = 0; u < 8; ++u) e[8 * r + u] = slot[64 * r + q * 8 + u];
-            __builtin_amdgcn_wave_barrier();
+            wave_lds_sync();
             float4 y[kBUnroll];
 #pragma unroll
             for (int u = 0; u < kBUnroll; ++u) y[u] = load_row(yc, e[u].idx, lo);
@@ -296,35 +303,48 @@ __global__ __launch_bounds__(kDensThreads) void densify_blocked_kernel(
 // sample, the part counts become offsets within the row and the row total goes to cnt.  Pack: the same
 // traversal writes each sample's survivors in ascending neuron order at row_ptr[r] + offset.
 constexpr int kPackR = 2048;
+constexpr int kTileLd = kBW + 1;  // LDS row pitch of a transposed 64 x 32 tile (conflict-free column reads)
+
+// Rows a .. a + 63 of chunk c (rows from a1 on read as zero) into v: lane l gets row a + l, all 32 samples.
+// The global reads are coalesced (each instruction takes eight whole rows, 1 KiB) and the transpose goes
+// through the wave's LDS tile.
+__device__ __forceinline__ void load_tile(const float *yb, int64_t c, int64_t n, int64_t a, int64_t a1, float *tile,
+                                          int lane, float (&v)[kBW]) {
+    const float4 *src = reinterpret_cast<const float4 *>(yb + (c * n + a) * kBW);
+    const int64_t rows = a1 - a < 64 ? a1 - a : 64;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int r = 8 * u + (lane >> 3);
+        float4 f = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (r < rows) f = src[64 * u + lane];
+        float *d = tile + r * kTileLd + (lane & 7) * 4;
+        d[0] = f.x;
+        d[1] = f.y;
+        d[2] = f.z;
+        d[3] = f.w;
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int s = 0; s < kBW; ++s) v[s] = tile[lane * kTileLd + s];
+    wave_lds_sync();
+}
 
 __global__ __launch_bounds__(256) void blocked_count_kernel(int64_t n, int64_t batch, int64_t nparts,
                                                             const float *__restrict__ yb, int32_t *__restrict__ pcnt) {
+    __shared__ float tiles[4][64 * kTileLd];
     const int lane = threadIdx.x & 63;
     const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int64_t nchunks = (batch + kBW - 1) / kBW;
     if (w >= nchunks * nparts) return;
+    float *tile = tiles[threadIdx.x >> 6];
     const int64_t c = w / nparts, part = w % nparts;
     const int64_t a0 = part * kPackR, a1 = min(n, a0 + kPackR);
     int cnt[kBW];
 #pragma unroll
     for (int s = 0; s < kBW; ++s) cnt[s] = 0;
     for (int64_t a = a0; a < a1; a += 64) {
-        const int64_t j = a + lane;
         float v[kBW];
-        if (j < a1) {
-            const float4 *row = reinterpret_cast<const float4 *>(yb + (c * n + j) * kBW);
-#pragma unroll
-            for (int q = 0; q < kBW / 4; ++q) {
-                const float4 f = row[q];
-                v[4 * q] = f.x;
-                v[4 * q + 1] = f.y;
-                v[4 * q + 2] = f.z;
-                v[4 * q + 3] = f.w;
-            }
-        } else {
-#pragma unroll
-            for (int s = 0; s < kBW; ++s) v[s] = 0.0f;
-        }
+        load_tile(yb, c, n, a, a1, tile, lane, v);
 #pragma unroll
         for (int s = 0; s < kBW; ++s) cnt[s] += __popcll(__ballot(v[s] != 0.0f));
     }
@@ -354,10 +374,12 @@ __global__ __launch_bounds__(256) void blocked_pack_kernel(int64_t n, int64_t ba
                                                            const int32_t *__restrict__ poff,
                                                            const int64_t *__restrict__ row_ptr,
                                                            int32_t *__restrict__ out_col, float *__restrict__ out_val) {
+    __shared__ float tiles[4][64 * kTileLd];
     const int lane = threadIdx.x & 63;
     const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int64_t nchunks = (batch + kBW - 1) / kBW;
     if (w >= nchunks * nparts) return;
+    float *tile = tiles[threadIdx.x >> 6];
     const int64_t c = w / nparts, part = w % nparts;
     const int64_t a0 = part * kPackR, a1 = min(n, a0 + kPackR);
     // where each sample's survivors of this part start (lane s holds sample s's position)
@@ -366,20 +388,7 @@ __global__ __launch_bounds__(256) void blocked_pack_kernel(int64_t n, int64_t ba
     for (int64_t a = a0; a < a1; a += 64) {
         const int64_t j = a + lane;
         float v[kBW];
-        if (j < a1) {
-            const float4 *row = reinterpret_cast<const float4 *>(yb + (c * n + j) * kBW);
-#pragma unroll
-            for (int q = 0; q < kBW / 4; ++q) {
-                const float4 f = row[q];
-                v[4 * q] = f.x;
-                v[4 * q + 1] = f.y;
-                v[4 * q + 2] = f.z;
-                v[4 * q + 3] = f.w;
-            }
-        } else {
-#pragma unroll
-            for (int s = 0; s < kBW; ++s) v[s] = 0.0f;
-        }
+        load_tile(yb, c, n, a, a1, tile, lane, v);
 #pragma unroll
         for (int s = 0; s < kBW; ++s) {
             if (c * kBW + s >= batch) break;  // uniform: samples past the batch end hold no output
