@@ -375,8 +375,9 @@ def run_paper_grid(args, torch, sd):
     """The paper's own experiment (Sec. V.B-D) on one MI355X: one layer of m x m weights with inverse
     sparsity S (Bernoulli pattern, values U[-1,3)) applied to 64 dense samples, through the CSR arm and the
     dense-W arm.  Per-layer time = (T(L identical layers) - T(1 layer)) / (L - 1), so the entry and exit
-    transposes cancel (the paper times one iteration of its layer loop); L = 2 for m >= 8192 and 17 below,
-    so that for small layers the GPU time, not the host's launch time, is what remains.  Also the analogues
+    transposes cancel (the paper times one iteration of its layer loop); L = 17 below m = 8192, then 9, 5
+    and 3 (the dense copies take m^2 x 12 bytes per layer), so that the GPU time, not the host's launch
+    time, is what remains.  Also the analogues
     of the paper's scaling parameters (Fig. 7), each normalised to m = 4096: dense time per element,
     sparse/dense ratio at S = 1, sparse slope per nonzero between S = 1 and S = 4, and the saturation time
     per row at S = 262144."""
@@ -390,8 +391,9 @@ def run_paper_grid(args, torch, sd):
         grid[m] = {}
         for S in invs:
             t0 = time.time()
-            # enough identical layers that GPU time, not host launch time, dominates the difference
-            L = 2 if m >= 8192 else 17
+            # enough identical layers that GPU time, not host launch time, dominates the difference, within the
+            # memory the dense copies take (m^2 x 12 bytes per layer)
+            L = 17 if m < 8192 else {8192: 9, 16384: 5}.get(m, 3)
             p = paper_grid(m, S, L=L)
             l0 = p.layers[0]
             net = sd.Net(m, L, nnz_per_layer=int(l0.nnz), dense=0 if args.no_dense else DENSE_BOTH)
@@ -459,11 +461,19 @@ def run_semiring(args, torch, sd):
         y = torch.from_numpy(p.y0_dense).cuda()
         z = torch.empty_like(y)
         out[f"{d:g}"] = {}
+        # a CSR batch of the same shape with 10% of its entries stored (the rest are the 0-element)
+        yc = p.y0_dense.copy()
+        yc[np.random.default_rng(11).random(yc.shape) >= 0.1] = 0.0
+        from workloads import dense_to_csr
+        crs = [torch.from_numpy(a).cuda() for a in dense_to_csr(yc)]
         for sr, name in enumerate(names):
             net.mxm(0, sr, y, out=z)
             ms = time_calls(torch, lambda: net.mxm(0, sr, y, out=z), reps)
-            out[f"{d:g}"][name] = {"ms": round(ms, 5), "edges_per_s": p.edges() / (ms / 1e3)}
-            log(f"semiring {name} d {d}: {ms:.4f} ms")
+            net.mxm_csr(0, sr, *crs)
+            ms_csr = time_calls(torch, lambda: net.mxm_csr(0, sr, *crs), reps)
+            out[f"{d:g}"][name] = {"ms": round(ms, 5), "edges_per_s": p.edges() / (ms / 1e3),
+                                   "csr_10pct_ms": round(ms_csr, 5)}
+            log(f"semiring {name} d {d}: {ms:.4f} ms dense input, {ms_csr:.4f} ms CSR input (10% stored)")
         net.free()
     return out
 

@@ -186,10 +186,16 @@ sdnn_status sdnn_mxm_dense(sdnn_net net, int32_t k, int32_t semiring, int64_t ba
  * The same product for a CSR batch Y (y_row_ptr[batch+1], y_col, y_val; device
  * arrays, columns in [0, n)): entries Y does not store are the semiring's
  * 0-element (the additive identity and multiplicative annihilator, Sec. II.E,
- * so they contribute nothing).  Z (device, batch x n fp32, row-major) receives
- * every entry.  Synchronises the stream once to report invalid CSR extents or
- * columns (INVALID_INDEX; the offending rows are skipped).
- * Errors: as sdnn_mxm_dense, plus INVALID_INDEX.
+ * so they contribute nothing), and the product is computed row by row over the
+ * stored entries only (the row-wise form of Sec. II.D): each stored Y(r, i)
+ * folds Y(r, i) (x) W_k(i, :) into an accumulator window of row r, so Y is never
+ * densified.  Z (device, batch x n fp32, row-major) receives every entry.
+ * + . x adds the exact products in fp64 in the order the accumulator's atomic
+ * adds land and rounds once (within one fp32 rounding of the ordered sum, not
+ * fixed bit for bit); the other semirings are exact.  ws and ws_bytes are not
+ * used (may be NULL / 0).  Synchronises the stream once to report invalid CSR
+ * extents or columns (INVALID_INDEX; the offending rows or entries are skipped).
+ * Errors: INVALID_OBJECT, NULL_POINTER, DIMENSION_MISMATCH, INVALID_VALUE, INVALID_INDEX, DEVICE.
  */
 sdnn_status sdnn_mxm_csr(sdnn_net net, int32_t k, int32_t semiring, int64_t batch, const int64_t *y_row_ptr,
                          const int32_t *y_col, const float *y_val, float *Z, void *ws, int64_t ws_bytes);

@@ -319,9 +319,8 @@ class Net:
         v = self._dev(val, t.float32)
         batch = rp.numel() - 1
         out = t.empty((batch, self.n), dtype=t.float32, device=self.device)
-        ws = self.workspace(batch, 0)
         sdnn_mxm_csr(self.handle, k, semiring, batch, rp, c if c.numel() else None, v if v.numel() else None,
-                     out, ws, ws.numel())
+                     out, None, 0)
         return out
 
     def forward_csr(self, row_ptr, col, val, k0: int = 0, k1: int | None = None):

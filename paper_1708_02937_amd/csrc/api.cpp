@@ -835,13 +835,15 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     return SDNN_OK;
 }
 
-static sdnn_status mxm_common(sdnn_net net, int32_t k, int32_t semiring, int64_t batch, void *ws, int64_t ws_bytes) {
+static sdnn_status mxm_common(sdnn_net net, int32_t k, int32_t semiring, int64_t batch, void *ws, int64_t ws_bytes,
+                              bool needs_ws) {
     if (!net) return fail(SDNN_ERR_INVALID_OBJECT, "net is NULL");
     if (k < 0 || k >= net->L) return fail(SDNN_ERR_DIMENSION_MISMATCH, "layer index outside [0, L)");
     if (!net->layers[(size_t)k].set) return fail(SDNN_ERR_INVALID_OBJECT, "layer k is not set");
     if (semiring < SDNN_SEMIRING_PLUS_TIMES || semiring > SDNN_SEMIRING_XOR_AND)
         return fail(SDNN_ERR_INVALID_VALUE, "unknown semiring");
     if (batch < 0) return fail(SDNN_ERR_DIMENSION_MISMATCH, "batch must be >= 0");
+    if (!needs_ws) return SDNN_OK;
     if (batch > 0 && !ws) return fail(SDNN_ERR_NULL_POINTER, "ws is required");
     if (batch > 0 && ws_bytes < (int64_t)dense_ws_bytes(net->n, batch, net->num_cu))
         return fail(SDNN_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than sdnn_workspace_size(net, batch, 0)");
@@ -851,7 +853,7 @@ static sdnn_status mxm_common(sdnn_net net, int32_t k, int32_t semiring, int64_t
 sdnn_status sdnn_mxm_dense(sdnn_net net, int32_t k, int32_t semiring, int64_t batch, const float *Y, float *Z,
                            void *ws, int64_t ws_bytes) {
     g_last_error.clear();
-    sdnn_status st = mxm_common(net, k, semiring, batch, ws, ws_bytes);
+    sdnn_status st = mxm_common(net, k, semiring, batch, ws, ws_bytes, true);
     if (st != SDNN_OK || batch == 0) return st;
     if (!Y || !Z) return fail(SDNN_ERR_NULL_POINTER, "Y and Z are required");
     SDNN_ON_DEVICE(net);
@@ -870,21 +872,19 @@ sdnn_status sdnn_mxm_dense(sdnn_net net, int32_t k, int32_t semiring, int64_t ba
 sdnn_status sdnn_mxm_csr(sdnn_net net, int32_t k, int32_t semiring, int64_t batch, const int64_t *y_row_ptr,
                          const int32_t *y_col, const float *y_val, float *Z, void *ws, int64_t ws_bytes) {
     g_last_error.clear();
-    sdnn_status st = mxm_common(net, k, semiring, batch, ws, ws_bytes);
+    (void)ws;
+    (void)ws_bytes;
+    sdnn_status st = mxm_common(net, k, semiring, batch, ws, ws_bytes, false);
     if (st != SDNN_OK || batch == 0) return st;
     if (!y_row_ptr || !Z) return fail(SDNN_ERR_NULL_POINTER, "y_row_ptr and Z are required");
     SDNN_ON_DEVICE(net);
     const int64_t n = net->n;
     hipStream_t s = net->stream;
     const Layer &l = net->layers[(size_t)k];
-    const int64_t ld = sdnn::act_ld(n, batch);
-    float *yt = (float *)ws;
-    float *zt = (float *)((char *)ws + act_bytes(n, batch));
     SDNN_HIP(hipMemsetAsync(net->d_flags, 0, sizeof(uint32_t), s));
-    SDNN_HIP(sdnn::launch_semiring_densify(n, batch, ld, sdnn::semiring_zero(semiring), y_row_ptr, y_col, y_val, yt,
-                                           net->d_flags, s));
-    SDNN_HIP(sdnn::launch_semiring_mxm(semiring, n, batch, ld, l.fan_ptr, l.fan, yt, zt, s));
-    SDNN_HIP(sdnn::launch_transpose(zt, ld, Z, n, n, batch, s));
+    // row by row over the stored entries (the SpGEMM skeleton): Y is never densified
+    SDNN_HIP(sdnn::launch_semiring_rows(semiring, n, batch, y_row_ptr, y_col, y_val, l.row_ptr, l.w_pack, Z,
+                                        net->d_flags, s));
     uint32_t flags = 0;
     SDNN_HIP(hipMemcpyAsync(&flags, net->d_flags, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
     SDNN_HIP(hipStreamSynchronize(s));

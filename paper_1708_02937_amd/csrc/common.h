@@ -169,9 +169,9 @@ float semiring_zero(int semiring);
 // Z^T = (Y (+).(x) W)^T from Y^T (n x batch, row pitch ld) over the fan-in lists; no bias, no activation.
 hipError_t launch_semiring_mxm(int semiring, int64_t n, int64_t batch, int64_t ld, const int64_t *fan_ptr, const Edge *fan,
                                const float *yt, float *zt, hipStream_t s);
-// Y^T (n x batch, row pitch ld) = `fill` everywhere, then the stored entries of the CSR rows (extents checked,
-// flagged in err).
-hipError_t launch_semiring_densify(int64_t n, int64_t batch, int64_t ld, float fill, const int64_t *row_ptr, const int32_t *col,
-                                   const float *val, float *yt, uint32_t *err, hipStream_t s);
-
+// Z (batch x n, row-major) = Y (+).(x) W for CSR rows Y, row by row from W's packed fan-out rows (w_ptr = W's
+// row pointers, w = (column, weight) pairs), without densifying Y (extents and columns checked, flagged in err).
+hipError_t launch_semiring_rows(int semiring, int64_t n, int64_t batch, const int64_t *row_ptr, const int32_t *col,
+                                const float *val, const int64_t *w_ptr, const Edge *w, float *z, uint32_t *err,
+                                hipStream_t s);
 }  // namespace sdnn

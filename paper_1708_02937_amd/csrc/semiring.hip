@@ -7,37 +7,67 @@
 // ascending input order), broadcasting each entry with readlane.  Values are carried in fp64 and rounded
 // once to fp32: +.x multiplies exactly and sums in fp64 as the forward pass does; max.+ adds in fp64 and
 // max.min, min.max and xor.and only select or compare, so those four are exact.
+#include <type_traits>
+
 #include "common.h"
 
 namespace sdnn {
 
 namespace {
 
+// Each semiring also says how a product is folded into an LDS accumulator slot (an atomic (+) on fp64,
+// or for GF(2) an exclusive or on the slot's low word) for the row-wise product on CSR input.
 struct PlusTimes {
     static __device__ double zero() { return 0.0; }
     static __device__ double add(double a, double b) { return a + b; }
     static __device__ double mul(double y, double w) { return y * w; }  // exact for fp32 operands
+    static __device__ void fold(double *slot, double p) { atomicAdd(slot, p); }
 };
 struct MaxPlus {
     static __device__ double zero() { return -__builtin_huge_val(); }
     static __device__ double add(double a, double b) { return a > b ? a : b; }
     static __device__ double mul(double y, double w) { return y + w; }
+    static __device__ void fold(double *slot, double p) {
+        __hip_atomic_fetch_max(slot, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
 };
 struct MaxMin {
     static __device__ double zero() { return -__builtin_huge_val(); }
     static __device__ double add(double a, double b) { return a > b ? a : b; }
     static __device__ double mul(double y, double w) { return y < w ? y : w; }
+    static __device__ void fold(double *slot, double p) {
+        __hip_atomic_fetch_max(slot, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
 };
 struct MinMax {
     static __device__ double zero() { return __builtin_huge_val(); }
     static __device__ double add(double a, double b) { return a < b ? a : b; }
     static __device__ double mul(double y, double w) { return y > w ? y : w; }
+    static __device__ void fold(double *slot, double p) {
+        __hip_atomic_fetch_min(slot, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
 };
 struct XorAnd {  // GF(2): a value counts as 1 when it is nonzero
     static __device__ double zero() { return 0.0; }
     static __device__ double add(double a, double b) { return (double)((a != 0.0) != (b != 0.0)); }
     static __device__ double mul(double y, double w) { return (double)(y != 0.0 && w != 0.0); }
+    // the slot holds a parity counter in its low 32 bits (the accumulator is read back through value())
+    static __device__ void fold(double *slot, double p) {
+        if (p != 0.0) atomicXor(reinterpret_cast<unsigned *>(slot), 1u);
+    }
 };
+
+// The accumulator slot's value for the result: GF(2) reads its parity word, the others the fp64 value.
+template <class SR>
+__device__ __forceinline__ double slot_value(const double *slot) {
+    if constexpr (std::is_same<SR, XorAnd>::value) return (double)(*reinterpret_cast<const unsigned *>(slot) & 1u);
+    else return *slot;
+}
+template <class SR>
+__device__ __forceinline__ void slot_init(double *slot) {
+    if constexpr (std::is_same<SR, XorAnd>::value) *slot = 0.0;  // parity word 0
+    else *slot = SR::zero();
+}
 
 constexpr int kSrUnroll = 8;
 
@@ -92,32 +122,82 @@ __global__ __launch_bounds__(256) void semiring_gather_kernel(int64_t n, int64_t
     for (int v = 0; v < V; ++v) zt[j * ld + col + v] = (float)acc[v];
 }
 
-// Y^T (n x batch, row pitch ld) filled with `fill`, then the stored entries of CSR rows scattered into it.
-__global__ void semiring_fill_kernel(int64_t count, float fill, float *__restrict__ yt) {
-    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e < count) yt[e] = fill;
-}
+// Row-wise product on CSR input (the SpGEMM skeleton of the forward pass, Sec. II.D computed row by row):
+// one workgroup per sample keeps a window of kSrWin output columns in LDS, initialised to the 0-element;
+// each wave takes one stored entry (i, y) of the sample at a time and its lanes walk the window's part of
+// W_k's fan-out row i (rows are sorted by column, so the part is found by binary search), folding y (x) w
+// into the column's slot with an LDS atomic ((+) is an fp64 add, max, min or, for GF(2), an exclusive or).
+// Unstored entries are the 0-element, which changes nothing, so only stored ones are visited; the window
+// is written to Z's row (batch-major) as fp32.  +.x sums exact products in fp64 in the order the atomics
+// land and rounds once; the other semirings only select, compare or count, so they are exact.  Row extents
+// and columns are checked as in the forward pass (flagged, offending rows or entries skipped).
+constexpr int kSrWin = 16384;
+constexpr int kSrThreads = 512;
 
-__global__ __launch_bounds__(256) void semiring_scatter_kernel(int64_t n, int64_t batch, int64_t ld,
-                                                               const int64_t *__restrict__ row_ptr,
-                                                               const int32_t *__restrict__ col,
-                                                               const float *__restrict__ val, float *__restrict__ yt,
-                                                               uint32_t *err) {
+template <class SR>
+__global__ __launch_bounds__(kSrThreads) void semiring_rows_kernel(int64_t n, int64_t batch,
+                                                                   const int64_t *__restrict__ row_ptr,
+                                                                   const int32_t *__restrict__ col,
+                                                                   const float *__restrict__ val,
+                                                                   const int64_t *__restrict__ w_ptr,
+                                                                   const Edge *__restrict__ w, float *__restrict__ z,
+                                                                   uint32_t *err) {
+    __shared__ double acc[kSrWin];
     const int64_t r = blockIdx.x;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int kW = kSrThreads / 64;
     const int64_t nnz = (col && val) ? row_ptr[batch] : 0;
-    const int64_t b = row_ptr[r], len = row_ptr[r + 1] - b;
+    int64_t b = row_ptr[r], len = row_ptr[r + 1] - b;
     if (b < 0 || len < 0 || len > n || b + len > nnz) {
         if (threadIdx.x == 0) atomicOr(err, 1u);
-        return;
+        len = 0;
     }
-    for (int64_t t = threadIdx.x; t < len; t += blockDim.x) {
-        const int32_t i = col[b + t];
-        if (i < 0 || i >= n) {
-            atomicOr(err, 1u);
-            continue;
+    for (int64_t w0 = 0; w0 < n; w0 += kSrWin) {
+        const int64_t wn = n - w0 < kSrWin ? n - w0 : kSrWin;
+        for (int64_t c = threadIdx.x; c < wn; c += kSrThreads) slot_init<SR>(&acc[c]);
+        __syncthreads();
+        for (int64_t t = wave; t < len; t += kW) {
+            const int32_t i = col[b + t];
+            if (i < 0 || i >= n) {
+                if (lane == 0 && w0 == 0) atomicOr(err, 1u);
+                continue;
+            }
+            const double y = (double)val[b + t];
+            int64_t lo = w_ptr[i], hi = w_ptr[(int64_t)i + 1];
+            if (w0 > 0 || wn < n) {  // the window's part of the sorted row: [first col >= w0, first col >= w0 + wn)
+                int64_t a = lo, e = hi;
+                while (a < e) {
+                    const int64_t m = (a + e) >> 1;
+                    if (w[m].idx < w0) a = m + 1;
+                    else e = m;
+                }
+                int64_t a2 = a, e2 = hi;
+                while (a2 < e2) {
+                    const int64_t m = (a2 + e2) >> 1;
+                    if (w[m].idx < w0 + wn) a2 = m + 1;
+                    else e2 = m;
+                }
+                lo = a;
+                hi = a2;
+            }
+            for (int64_t q = lo + lane; q < hi; q += 64) {
+                const Edge ed = w[q];
+                SR::fold(&acc[ed.idx - w0], SR::mul(y, (double)ed.w));
+            }
         }
-        yt[(int64_t)i * ld + r] = val[b + t];
+        __syncthreads();
+        float *zr = z + r * n + w0;
+        for (int64_t c = threadIdx.x; c < wn; c += kSrThreads) zr[c] = (float)slot_value<SR>(&acc[c]);
+        __syncthreads();
     }
+}
+
+template <class SR>
+hipError_t launch_sr_rows(int64_t n, int64_t batch, const int64_t *row_ptr, const int32_t *col, const float *val,
+                          const int64_t *w_ptr, const Edge *w, float *z, uint32_t *err, hipStream_t s) {
+    if (batch > 0x7fffffffLL) return hipErrorInvalidValue;
+    semiring_rows_kernel<SR><<<(unsigned)batch, kSrThreads, 0, s>>>(n, batch, row_ptr, col, val, w_ptr, w, z, err);
+    return hipGetLastError();
 }
 
 template <class SR>
@@ -167,13 +247,18 @@ hipError_t launch_semiring_mxm(int semiring, int64_t n, int64_t batch, int64_t l
     }
 }
 
-hipError_t launch_semiring_densify(int64_t n, int64_t batch, int64_t ld, float fill, const int64_t *row_ptr, const int32_t *col,
-                                   const float *val, float *yt, uint32_t *err, hipStream_t s) {
+hipError_t launch_semiring_rows(int semiring, int64_t n, int64_t batch, const int64_t *row_ptr, const int32_t *col,
+                                const float *val, const int64_t *w_ptr, const Edge *w, float *z, uint32_t *err,
+                                hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
-    const int64_t count = n * ld;
-    semiring_fill_kernel<<<(unsigned)((count + 255) / 256), 256, 0, s>>>(count, fill, yt);
-    semiring_scatter_kernel<<<(unsigned)batch, 256, 0, s>>>(n, batch, ld, row_ptr, col, val, yt, err);
-    return hipGetLastError();
+    switch (semiring) {
+        case kSemiringPlusTimes: return launch_sr_rows<PlusTimes>(n, batch, row_ptr, col, val, w_ptr, w, z, err, s);
+        case kSemiringMaxPlus: return launch_sr_rows<MaxPlus>(n, batch, row_ptr, col, val, w_ptr, w, z, err, s);
+        case kSemiringMaxMin: return launch_sr_rows<MaxMin>(n, batch, row_ptr, col, val, w_ptr, w, z, err, s);
+        case kSemiringMinMax: return launch_sr_rows<MinMax>(n, batch, row_ptr, col, val, w_ptr, w, z, err, s);
+        case kSemiringXorAnd: return launch_sr_rows<XorAnd>(n, batch, row_ptr, col, val, w_ptr, w, z, err, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace sdnn

@@ -198,23 +198,38 @@ def test_semiring_mxm_dense(sd, name, seed, n, batch, d):
 
 
 @pytest.mark.parametrize("name", SEMIRINGS)
-def test_semiring_mxm_csr(sd, name):
-    """The CSR form: entries Y does not store are the 0-element (they contribute nothing)."""
+@pytest.mark.parametrize("seed,n,batch,wd,yd", [(85, 500, 97, 0.02, 0.05), (86, 3000, 40, 0.3, 0.2),
+                                                (87, 40000, 9, 0.0005, 0.002), (88, 64, 5, 0.5, 0.0)])
+def test_semiring_mxm_csr(sd, name, seed, n, batch, wd, yd):
+    """The CSR form, row by row over the stored entries: entries Y does not store are the 0-element (they
+    contribute nothing); one and three accumulator windows, long fan-out rows, empty rows, explicit zeros in
+    W.  Every semiring but +.x is exact; +.x sums in fp64 in atomic order, so it is held to the tolerance, and
+    an integer-valued +.x product (exact in any order) bit for bit."""
     import oracle
 
-    n, batch = 500, 97
-    p = tiny_random(85, n, 1, batch, w_density=0.02, y_density=0.05)
+    p = tiny_random(seed, n, 1, batch, w_density=wd, y_density=yd, explicit_zeros=True)
     zero = {"max_plus": -math.inf, "max_min": -math.inf, "min_max": math.inf}.get(name, 0.0)
-    yd = np.full((batch, n), zero, np.float32)
+    ydn = np.full((batch, n), zero, np.float32)
     rp, c, v = p.y0_csr
     rows = np.repeat(np.arange(batch), np.diff(rp))
-    yd[rows, c] = v
-    want = oracle.mxm(name, n, p.layers[0], yd)
+    ydn[rows, c] = v
+    want = oracle.mxm(name, n, p.layers[0], ydn)
     net = sd.net_from_problem(p)
-    _say("semiring csr", name)
+    _say("semiring csr", name, seed, n)
     got = net.mxm_csr(0, oracle.SEMIRINGS[name], rp, c, v).cpu().numpy()
+    if name == "plus_times":
+        assert np.all(np.abs(got.astype(np.float64) - want) <= 1e-6 + 1e-5 * np.abs(want.astype(np.float64)))
+        q = integer_shadow(p)
+        net2 = sd.net_from_problem(q)
+        qrp, qc, qv = q.y0_csr
+        qd = np.zeros((batch, n), np.float32)
+        qd[np.repeat(np.arange(batch), np.diff(qrp)), qc] = qv
+        got2 = net2.mxm_csr(0, 0, qrp, qc, qv).cpu().numpy()
+        net2.free()
+        assert got2.tobytes() == oracle.mxm(name, n, q.layers[0], qd).tobytes()
+    else:
+        assert got.tobytes() == want.tobytes()
     net.free()
-    assert got.tobytes() == want.tobytes()
 
 
 @pytest.mark.parametrize("n,batch", [(1 << 20, 4098), (1 << 23, 1056)])
@@ -410,7 +425,11 @@ def test_semiring_mxm_padded_pitch(sd, name):
     yd[np.repeat(np.arange(batch), np.diff(rp)), c] = v
     got = net.mxm_csr(0, oracle.SEMIRINGS[name], rp, c, v).cpu().numpy()
     net.free()
-    assert got.tobytes() == oracle.mxm(name, n, p.layers[0], yd).tobytes()
+    want = oracle.mxm(name, n, p.layers[0], yd)
+    if name == "plus_times":  # summed in atomic order on the CSR path
+        assert np.all(np.abs(got.astype(np.float64) - want) <= 1e-6 + 1e-5 * np.abs(want.astype(np.float64)))
+    else:
+        assert got.tobytes() == want.tobytes()
 
 
 # ------------------------------------------------------------------------------------------ the workloads
