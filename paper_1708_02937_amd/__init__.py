@@ -356,10 +356,11 @@ class Net:
             self._ws.clear()
             self.arena = None
 
-    def __del__(self):
+    def __del__(self, _finalizing=sys.is_finalizing):
         # At interpreter shutdown the HIP runtime (and any tool layered on it) may already be torn down, so
-        # no HIP call is made from here then; the process exit releases the device memory.
-        if sys.is_finalizing():
+        # no HIP call is made from here then; the process exit releases the device memory.  (The check is
+        # bound at definition: module globals such as sys may already be cleared when this runs.)
+        if _finalizing():
             return
         try:
             self.free()

@@ -503,11 +503,14 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                         written += tot;
                     }
                 } else if (touched || !bias_nonpos) {
-                    // epilogue over the whole window in column order: in round rd thread t owns columns
-                    // rd * 4096 + 4t .. +3; reads and zeroes the accumulator.  One scan covers all
-                    // rounds: the survivor counts of the rounds travel in 16-bit fields of one integer.
-                    float f[kRounds][4];
+                    // epilogue over the whole window in column order (round rd: thread t owns columns
+                    // rd * 4096 + 4t .. +3), in two passes so that no output value is held across the scan:
+                    // the first counts the survivors of each round (the counts travel in 16-bit fields of
+                    // one integer, one scan for all rounds), marks them in a per-thread mask and clears
+                    // every other slot it found nonzero; the second writes the marked columns in order and
+                    // clears them.
                     unsigned long long packed = 0;
+                    uint32_t smask = 0;  // bit 4 rd + v: column rd * 4096 + 4 tid + v survives
 #pragma unroll
                     for (int rd = 0; rd < kRounds; ++rd) {
                         int keep = 0;
@@ -515,12 +518,15 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                         for (int v = 0; v < 4; ++v) {
                             const int t = rd * 4 * kThreads + 4 * tid + v;
                             const int at = rd * kRoundCols + v * kThreads + tid;  // acc_pos(t)
-                            f[rd][v] = 0.0f;
                             if (t < width) {
-                                f[rd][v] = activate(acc[at] + (double)bias[c0 + t], ymax);
-                                acc[at] = 0.0;
+                                const double a = acc[at];
+                                if (activate(a + (double)bias[c0 + t], ymax) != 0.0f) {
+                                    ++keep;
+                                    smask |= 1u << (4 * rd + v);
+                                } else if (__double_as_longlong(a) != 0) {
+                                    acc[at] = 0.0;
+                                }
                             }
-                            keep += f[rd][v] != 0.0f;
                         }
                         packed |= (unsigned long long)keep << (16 * rd);
                     }
@@ -541,16 +547,20 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                     }
                     const unsigned long long excl = incl - packed;
                     int64_t round_base = ob + written;
-#pragma unroll
                     for (int rd = 0; rd < kRounds; ++rd) {
                         const int sh = 16 * rd;
-                        int64_t pos = round_base + (int64_t)((before >> sh) & 0xffff) + (int64_t)((excl >> sh) & 0xffff);
+                        if ((smask >> (4 * rd)) & 15u) {
+                            int64_t pos = round_base + (int64_t)((before >> sh) & 0xffff) + (int64_t)((excl >> sh) & 0xffff);
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            if (f[rd][v] != 0.0f) {
-                                out_col[pos] = (int32_t)(c0 + rd * 4 * kThreads + 4 * tid + v);
-                                out_val[pos] = f[rd][v];
-                                ++pos;
+                            for (int v = 0; v < 4; ++v) {
+                                if ((smask >> (4 * rd + v)) & 1u) {
+                                    const int t = rd * 4 * kThreads + 4 * tid + v;
+                                    const int at = rd * kRoundCols + v * kThreads + tid;
+                                    out_col[pos] = (int32_t)(c0 + t);
+                                    out_val[pos] = activate(acc[at] + (double)bias[c0 + t], ymax);
+                                    ++pos;
+                                    acc[at] = 0.0;
+                                }
                             }
                         }
                         round_base += (int64_t)((all >> sh) & 0xffff);
