@@ -75,6 +75,8 @@ struct Layer {
     double *slots = nullptr;        // fp64 weight of every (input, output) pair, tile-major (high fan-in, n^2 fits)
     int32_t *w_seg = nullptr;     // where each fan-out row crosses each accumulator window (wide layers only)
     sdnn::BlockedSched *sched = nullptr;  // schedule of the blocked product (very wide layers only)
+    Edge *stage = nullptr;                 // its lists in schedule order, one region per workgroup
+    sdnn::BlockedRegion *regions = nullptr;  // the regions (null when one exceeds the product's LDS capacity)
     double *dense_wt = nullptr;  // n x n, W_k k-major in fp64 (zeros explicit), for the fp64 dense arm
     float *dense_wt32 = nullptr; // the same in fp32, for the fp32 dense arm
     bool dense_ready = false, dense32_ready = false;  // the dense copies hold the current W_k
@@ -95,7 +97,8 @@ constexpr size_t kAbsent = ~size_t(0);
 
 struct LayerPlan {
     size_t w_pack = kAbsent, fan_ptr = kAbsent, fan = kAbsent, tile_mask = kAbsent, slots = kAbsent,
-           w_seg = kAbsent, sched = kAbsent, dense64 = kAbsent, dense32 = kAbsent;
+           w_seg = kAbsent, sched = kAbsent, stage = kAbsent, regions = kAbsent, starts = kAbsent,
+           dense64 = kAbsent, dense32 = kAbsent;
     size_t bytes = 0;
 };
 
@@ -122,8 +125,12 @@ LayerPlan plan_layer(int64_t n, int64_t cap, int32_t dense_flags) {
     if (sdnn::spmm_wants_slots(n, cap)) lp.slots = take(off, sdnn::spmm_slot_elems(n) * sizeof(double));
     if (sdnn::spgemm_wants_window_index(n))
         lp.w_seg = take(off, (size_t)n * (size_t)(sdnn::spgemm_windows(n) + 1) * sizeof(int32_t));
-    if (sdnn::blocked_wanted(n, 1 << 20))
+    if (sdnn::blocked_wanted(n, 1 << 20)) {
         lp.sched = take(off, (size_t)sdnn::blocked_sched_elems(n) * sizeof(sdnn::BlockedSched));
+        lp.stage = take(off, sdnn::blocked_stage_elems(n, cap) * sizeof(Edge));
+        lp.regions = take(off, (size_t)sdnn::blocked_regions(n) * sizeof(sdnn::BlockedRegion));
+        lp.starts = take(off, (size_t)(sdnn::blocked_regions(n) + 1) * sizeof(int64_t));
+    }
     if (dense_flags & SDNN_ARENA_DENSE_F64) lp.dense64 = take(off, (size_t)n * (size_t)n * sizeof(double));
     if (dense_flags & SDNN_ARENA_DENSE_F32) lp.dense32 = take(off, (size_t)n * (size_t)n * sizeof(float));
     lp.bytes = off;
@@ -458,6 +465,9 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     // optional structures: present when this layer's density (not only the capacity) wants them
     nl.w_seg = at<int32_t>(base, lp.w_seg);
     nl.sched = at<sdnn::BlockedSched>(base, lp.sched);
+    nl.stage = at<Edge>(base, lp.stage);
+    sdnn::BlockedRegion *regions = at<sdnn::BlockedRegion>(base, lp.regions);
+    int64_t *starts = at<int64_t>(base, lp.starts);
     nl.tile_mask = sdnn::spmm_wants_tiles(n, nnz) ? at<uint16_t>(base, lp.tile_mask) : nullptr;
     nl.slots = sdnn::spmm_wants_slots(n, nnz) ? at<double>(base, lp.slots) : nullptr;
     nl.dense_wt = at<double>(base, lp.dense64);
@@ -482,11 +492,20 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     SETUP_HIP(sdnn::launch_max_segment(n, row_ptr, net->d_int, s));
     SETUP_HIP(hipMemcpyAsync(&nl.max_fanout, net->d_int, sizeof(int32_t), hipMemcpyDeviceToHost, s));
     if (nl.w_seg) SETUP_HIP(sdnn::launch_window_seg(n, row_ptr, col_idx, nl.w_seg, s));
-    if (nl.sched) SETUP_HIP(sdnn::launch_blocked_order(n, nl.fan_ptr, nl.sched, s));
+    int32_t region_max = 0;
+    if (nl.sched) {
+        SETUP_HIP(sdnn::launch_blocked_order(n, nl.fan_ptr, nl.sched, s));
+        SETUP_HIP(sdnn::launch_blocked_stage(n, nnz, nl.fan, nl.sched, nl.stage, regions, counts, starts, tmp,
+                                             net->d_int + 1, s));
+        SETUP_HIP(hipMemcpyAsync(&region_max, net->d_int + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    }
     if (nl.tile_mask) SETUP_HIP(sdnn::launch_spmm_tile_mask(n, nl.fan_ptr, nl.fan, nl.tile_mask, s));
     if (nl.slots) SETUP_HIP(sdnn::launch_spmm_slots(n, nl.fan_ptr, nl.fan, nl.slots, s));
     SETUP_HIP(hipStreamSynchronize(s));
 #undef SETUP_HIP
+    // the product stages each workgroup's lists in LDS when the longest region fits; otherwise it reads the
+    // same staged copy entry by entry
+    if (nl.sched && region_max <= sdnn::blocked_stage_cap()) nl.regions = regions;
     l = nl;
     return SDNN_OK;
 }
@@ -603,7 +622,7 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
         for (int32_t k = k0; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
             SDNN_HIP(prof_begin(net, k, sdnn::kKernBlocked, &pr));
-            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.fan, l.bias, net->ymax, net->bias_pattern, buf[cb],
+            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.stage, l.regions, l.bias, net->ymax, net->bias_pattern, buf[cb],
                                                buf[cb ^ 1], s));
             SDNN_HIP(prof_end(net, pr));
             cb ^= 1;
@@ -758,7 +777,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         for (int32_t k = kd; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
             SDNN_HIP(prof_begin(net, k, sdnn::kKernBlocked, &pr));
-            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.fan, l.bias, net->ymax, net->bias_pattern,
+            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.stage, l.regions, l.bias, net->ymax, net->bias_pattern,
                                                dense[dc], dense[dc ^ 1], s));
             SDNN_HIP(prof_end(net, pr));
             dc ^= 1;

@@ -38,6 +38,7 @@ constexpr int kBTile = kBWaves * kBGroups * 8;  // neurons per workgroup and chu
 #define SDNN_BLOCKED_UNROLL 8
 #endif
 constexpr int kBUnroll = SDNN_BLOCKED_UNROLL;  // list entries per block (rows in flight per lane)
+constexpr int kStageCap = 4096;  // entries of a workgroup's staged lists (32 KiB of LDS: five workgroups per CU)
 
 // ------------------------------------------------------------------------------------------ set-up
 
@@ -97,6 +98,50 @@ __global__ __launch_bounds__(256) void blocked_order_kernel(int64_t n, int64_t p
     }
 }
 
+// The workgroups' list regions: the padded size of each (its kBTile positions' lists, rounded up to an even
+// entry count so that every region starts 16-byte aligned), then, after a scan of the sizes, one 64-thread
+// workgroup per region copies its lists in schedule order (a wave prefix sum of the lengths places them),
+// writes a zero entry into the padding, repoints the schedule's list starts and records the region.
+__global__ __launch_bounds__(256) void blocked_region_size_kernel(int64_t nreg, const BlockedSched *__restrict__ sched,
+                                                                  int32_t *__restrict__ sizes) {
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g >= nreg) return;
+    int64_t cnt = 0;
+    for (int k = 0; k < kBTile; ++k) cnt += sched[g * kBTile + k].len;
+    sizes[g] = (int32_t)((cnt + 1) & ~1LL);
+}
+
+static_assert(kBTile == 64, "one wave per region in blocked_stage_kernel");
+
+__global__ __launch_bounds__(64) void blocked_stage_kernel(const Edge *__restrict__ fan, BlockedSched *__restrict__ sched,
+                                                           const int64_t *__restrict__ starts, Edge *__restrict__ stage,
+                                                           BlockedRegion *__restrict__ regions, int32_t *region_max) {
+    const int64_t g = blockIdx.x;
+    const int lane = threadIdx.x;
+    BlockedSched e = sched[g * kBTile + lane];
+    int incl = e.len;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int v = __shfl_up(incl, d);
+        if (lane >= d) incl += v;
+    }
+    const int cnt = __shfl(incl, 63);
+    const int64_t base = starts[g];
+    const int64_t dst = base + (incl - e.len);
+    for (int i = 0; i < e.len; ++i) stage[dst + i] = fan[e.e0 + i];
+    e.e0 = dst;
+    sched[g * kBTile + lane] = e;
+    if (lane == 0) {
+        if (cnt & 1) stage[base + cnt] = Edge{0, 0.0f};
+        BlockedRegion r;
+        r.e0 = base;
+        r.cnt = cnt;
+        r.pad = 0;
+        regions[g] = r;
+        atomicMax(region_max, (cnt + 1) & ~1);
+    }
+}
+
 // ------------------------------------------------------------------------------------------ product
 
 __device__ __forceinline__ float4 load_row(const char *yc, int32_t i, uint32_t lo) {
@@ -147,11 +192,16 @@ __device__ __forceinline__ void group8_min_max(int v, int &mn, int &mx) {
 #ifndef SDNN_BLOCKED_WAVES_PER_EU
 #define SDNN_BLOCKED_WAVES_PER_EU 1
 #endif
-template <bool kPattern>
+// kStaged: the workgroup's lists sit in one region of the staged copy (`fan` then points to that copy); the
+// workgroup loads the whole region into LDS at once (16 bytes per lane, straight to LDS) and reads every
+// entry from there, so the only global loads of the loop are the rows.  Measured on the very wide layer: the
+// per-block entry loads from HBM sat on each block's critical path (94 -> 79 ms per layer without them).
+template <bool kPattern, bool kStaged>
 __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SDNN_BLOCKED_WAVES_PER_EU, 8))) void spmm_blocked_kernel(
     int64_t n, int64_t gpx, int64_t tiles, const BlockedSched *__restrict__ sched, const Edge *__restrict__ fan,
-    const float *__restrict__ bias, double ymax, const float *__restrict__ yb, float *__restrict__ zb) {
-    __shared__ __align__(16) Edge ent[kBWaves][kBUnroll * 8];
+    const BlockedRegion *__restrict__ regions, const float *__restrict__ bias, double ymax,
+    const float *__restrict__ yb, float *__restrict__ zb) {
+    __shared__ __align__(16) Edge ent[kStaged ? kStageCap : kBWaves * kBUnroll * 8];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q = lane >> 3, sub = lane & 7;
     const int64_t b = blockIdx.x;
@@ -162,8 +212,65 @@ __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SD
     const char *yc = reinterpret_cast<const char *>(yb + c * n * kBW);
     float *zc = zb + c * n * kBW + sub * 4;
     const uint32_t lo = (uint32_t)sub * 16u;
-    Edge *slot = &ent[wave][0];
     const BlockedSched *sp = sched + (g * kBWaves + wave) * (kBGroups * 8) + q;
+    if constexpr (kStaged) {
+        // the region (at most kStageCap - 128 entries, padded to an even count, 16-byte aligned); each load
+        // instruction moves 128 entries, the last one up to 127 entries past the region (into the next region
+        // or the zeroed tail of the copy), all within ent
+        const BlockedRegion rg = regions[g];
+        const Edge *src = fan + rg.e0;
+        for (int base = wave * 128; base < rg.cnt; base += kBWaves * 128)
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(src + base + 2 * lane),
+                                             (__attribute__((address_space(3))) void *)(&ent[base]), 16,
+                                             0, 0);
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's loads into LDS have landed
+        __syncthreads();
+        for (int gi = 0; gi < kBGroups; ++gi) {
+            const BlockedSched cur = sp[8 * gi];
+            const int len = cur.len;
+            const Edge *lst = ent + (cur.e0 - rg.e0);
+            const int last = len > 0 ? len - 1 : 0;
+            int mn, mx;
+            group8_min_max(len, mn, mx);
+            double acc[4] = {0.0, 0.0, 0.0, 0.0};
+            uint32_t hit[4] = {0u, 0u, 0u, 0u};
+            for (int t = 0; t < mx; t += kBUnroll) {
+                Edge e[kBUnroll];
+#pragma unroll
+                for (int u = 0; u < kBUnroll; ++u) e[u] = lst[min(t + u, last)];
+                float4 y[kBUnroll];
+#pragma unroll
+                for (int u = 0; u < kBUnroll; ++u) y[u] = load_row(yc, e[u].idx, lo);
+                if (t + kBUnroll <= mn) {
+#pragma unroll
+                    for (int u = 0; u < kBUnroll; ++u) fma4<kPattern>(y[u], e[u].w, acc, hit);
+                } else {
+                    // entries past a lane's end add a zeroed input times a zero weight
+#pragma unroll
+                    for (int u = 0; u < kBUnroll; ++u) {
+                        float4 yv = y[u];
+                        float wv = e[u].w;
+                        if (t + u >= len) {
+                            yv = make_float4(0.f, 0.f, 0.f, 0.f);
+                            wv = 0.0f;
+                        }
+                        fma4<kPattern>(yv, wv, acc, hit);
+                    }
+                }
+            }
+            if (cur.j >= 0) {
+                const double bd = (double)bias[cur.j];
+                float4 out;
+                out.x = (kPattern && (hit[0] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[0] + bd, ymax);
+                out.y = (kPattern && (hit[1] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[1] + bd, ymax);
+                out.z = (kPattern && (hit[2] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[2] + bd, ymax);
+                out.w = (kPattern && (hit[3] & 0x7fffffffu) == 0u) ? 0.0f : activate(acc[3] + bd, ymax);
+                *reinterpret_cast<float4 *>(zc + (int64_t)cur.j * kBW) = out;
+            }
+        }
+        return;
+    }
+    Edge *slot = &ent[wave * kBUnroll * 8];
     BlockedSched cur = sp[0];
     for (int gi = 0; gi < kBGroups; ++gi) {
         const BlockedSched nxt = sp[8 * min(gi + 1, kBGroups - 1)];
@@ -464,8 +571,36 @@ hipError_t launch_blocked_order(int64_t n, const int64_t *fan_ptr, BlockedSched 
     return hipGetLastError();
 }
 
-hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan, const float *bias,
-                               double ymax, int pattern, const float *yb, float *zb, hipStream_t s) {
+int64_t blocked_regions(int64_t n) { return blocked_sched_elems(n) / kBTile; }
+
+size_t blocked_stage_elems(int64_t n, int64_t nnz) { return (size_t)nnz + (size_t)blocked_regions(n) + 128; }
+
+int32_t blocked_stage_cap() { return kStageCap - 128; }
+
+hipError_t launch_blocked_stage(int64_t n, int64_t nnz, const Edge *fan, BlockedSched *sched, Edge *stage,
+                                BlockedRegion *regions, int32_t *sizes, int64_t *starts, int64_t *scan_tmp,
+                                int32_t *region_max, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    const int64_t nreg = blocked_regions(n);
+    blocked_region_size_kernel<<<(unsigned)((nreg + 255) / 256), 256, 0, s>>>(nreg, sched, sizes);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_exclusive_scan_i32_to_i64(nreg, sizes, starts, scan_tmp, s);
+    if (e != hipSuccess) return e;
+    // the regions end between nnz and nnz + nreg entries (one padding entry at most per region): zeroing from
+    // nnz to the end of the copy leaves zeros in the 128 entries after the last region, which the staging
+    // loads of the last regions may read
+    e = hipMemsetAsync(stage + nnz, 0, ((size_t)nreg + 128) * sizeof(Edge), s);
+    if (e != hipSuccess) return e;
+    e = hipMemsetAsync(region_max, 0, sizeof(int32_t), s);
+    if (e != hipSuccess) return e;
+    blocked_stage_kernel<<<(unsigned)nreg, 64, 0, s>>>(fan, sched, starts, stage, regions, region_max);
+    return hipGetLastError();
+}
+
+hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan,
+                               const BlockedRegion *regions, const float *bias, double ymax, int pattern,
+                               const float *yb, float *zb, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
     if (n > (1 << 24)) return hipErrorInvalidValue;  // 32-bit row offsets within a chunk
     const int64_t nchunks = blocked_chunks(batch);
@@ -480,10 +615,16 @@ hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sch
         const unsigned nb = (unsigned)(nc * per_chunk);
         const float *y0 = yb + c0 * n * kBW;
         float *z0 = zb + c0 * n * kBW;
-        if (pattern)
-            spmm_blocked_kernel<true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, bias, ymax, y0, z0);
-        else
-            spmm_blocked_kernel<false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, bias, ymax, y0, z0);
+        if (regions) {
+            if (pattern)
+                spmm_blocked_kernel<true, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, regions, bias, ymax, y0, z0);
+            else
+                spmm_blocked_kernel<false, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, regions, bias, ymax, y0, z0);
+        } else if (pattern) {
+            spmm_blocked_kernel<true, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, nullptr, bias, ymax, y0, z0);
+        } else {
+            spmm_blocked_kernel<false, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, nullptr, bias, ymax, y0, z0);
+        }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

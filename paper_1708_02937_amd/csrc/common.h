@@ -151,8 +151,27 @@ struct __align__(16) BlockedSched {
 };
 int64_t blocked_sched_elems(int64_t n);
 hipError_t launch_blocked_order(int64_t n, const int64_t *fan_ptr, BlockedSched *sched, hipStream_t s);
-hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan, const float *bias,
-                               double ymax, int pattern, const float *yb, float *zb, hipStream_t s);
+// The lists of each workgroup of the product (kBlockedTile consecutive schedule positions) copied into one
+// contiguous region, in schedule order, so that the product stages them into LDS at once (set-up).  A
+// region starts 16-byte aligned (its length is padded to an even count with a zero entry); stage holds
+// blocked_stage_elems(n, nnz) entries (the last 128, zeroed, cover the staging loads' overrun).  The schedule's
+// list starts are rewritten to point into stage; region_max receives the longest padded region (entries).
+// sizes: blocked_regions(n) int32 of scratch; starts: blocked_regions(n) + 1 int64.
+struct __align__(16) BlockedRegion {
+    int64_t e0;   // first entry of the region in the staged copy
+    int32_t cnt;  // entries of the region (unpadded)
+    int32_t pad;
+};
+int64_t blocked_regions(int64_t n);
+size_t blocked_stage_elems(int64_t n, int64_t nnz);
+int32_t blocked_stage_cap();  // longest padded region the product stages in LDS
+hipError_t launch_blocked_stage(int64_t n, int64_t nnz, const Edge *fan, BlockedSched *sched, Edge *stage,
+                                BlockedRegion *regions, int32_t *sizes, int64_t *starts, int64_t *scan_tmp,
+                                int32_t *region_max, hipStream_t s);
+// regions: the staged lists (null when a region exceeds blocked_stage_cap(): entries come from fan instead)
+hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan,
+                               const BlockedRegion *regions, const float *bias, double ymax, int pattern,
+                               const float *yb, float *zb, hipStream_t s);
 // sparse rows (caller CSR, or slot rows with counts) -> blocked; every element is written
 hipError_t launch_densify_blocked(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                   const int32_t *in_col, const float *in_val, float *yb, uint32_t *err, hipStream_t s);

@@ -306,12 +306,15 @@ def test_narrow_chunk_gather(sd, seed, n, batch, lengths, bias_mode):
 
 @pytest.mark.parametrize("seed,n,batch,lengths,bias_mode", [
     (91, 16400, 256, [32, 25, 40, 32, 0, 1, 77, 33], 0), (92, 20000, 300, [3, 0, 0, 33, 8, 9, 64, 1], 1),
-    (93, 17003, 257, [120, 0, 5, 17, 31, 32, 33], 0), (94, 24576, 512, [24, 24, 24, 24, 24, 24, 24, 25], 1)])
+    (93, 17003, 257, [120, 0, 5, 17, 31, 32, 33], 0), (94, 24576, 512, [24, 24, 24, 24, 24, 24, 24, 25], 1),
+    (95, 16900, 288, [100, 90, 110, 64], 0), (96, 18000, 256, [95, 0, 120, 101], 1)])
 def test_blocked_product(sd, seed, n, batch, lengths, bias_mode):
     """Layers wider than 16384 with batches of 256 or more take the product on the sample-blocked layout
     (chunks of 32 samples, eight neurons per wave walking their lists in step): ragged n, a partial last
     chunk, empty lists and list lengths from 0 to 120 side by side in one wave, both bias readings, every
-    row compared."""
+    row compared.  Each workgroup stages its 64 neurons' lists in LDS while they fit (up to about 3968
+    entries: the cases with lists of about 100 entries exceed it, and their layers read the staged copy
+    entry by entry instead)."""
     rng = np.random.default_rng(seed)
     layers = [_mixed_length_layer(rng, n, lengths), _mixed_length_layer(rng, n, lengths[::-1])]
     y = rng.random((batch, n), dtype=np.float32)
