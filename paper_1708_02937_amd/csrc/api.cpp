@@ -181,6 +181,7 @@ struct CsrWs {
     int32_t *lists;  // 3 * batch: the sample lists of the layer being computed
     int64_t *scan_tmp;
     int32_t *pcnt;   // per (part, sample) counts of the blocked -> CSR packing
+    uint32_t *nzrows;  // nonzero-row maps of a sparse input in the blocked layout
     size_t bytes;
 };
 
@@ -202,7 +203,12 @@ CsrWs carve_csr(void *base, int64_t n, int64_t batch) {
     w.scan_tmp = (int64_t *)(p + off);
     off = align_up(off + (size_t)sdnn::scan_tmp_elems(batch) * sizeof(int64_t));
     w.pcnt = (int32_t *)(p + off);
-    if (sdnn::blocked_wanted(n, batch)) off = align_up(off + sdnn::blocked_pack_elems(n, batch) * sizeof(int32_t));
+    w.nzrows = nullptr;
+    if (sdnn::blocked_wanted(n, batch)) {
+        off = align_up(off + sdnn::blocked_pack_elems(n, batch) * sizeof(int32_t));
+        w.nzrows = (uint32_t *)(p + off);
+        off = align_up(off + (size_t)sdnn::blocked_chunks(batch) * (size_t)sdnn::blocked_nz_words(n) * sizeof(uint32_t));
+    }
     w.bytes = off;
     return w;
 }
@@ -622,7 +628,7 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
         for (int32_t k = k0; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
             SDNN_HIP(prof_begin(net, k, sdnn::kKernBlocked, &pr));
-            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.stage, l.regions, l.bias, net->ymax, net->bias_pattern, buf[cb],
+            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.stage, l.regions, nullptr, l.bias, net->ymax, net->bias_pattern, buf[cb],
                                                buf[cb ^ 1], s));
             SDNN_HIP(prof_end(net, pr));
             cb ^= 1;
@@ -767,18 +773,21 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         const bool from_user = kd == k0;
         const int db = from_user ? 0 : cur;  // the input rows (if any) sit in buffer cur ^ 1
         float *dense[2] = {reinterpret_cast<float *>(w.col[db]), w.val[db]};
+        // a sparse input (at most 1/16 of batch * n entries: a 32-sample row is then entirely zero with
+        // probability >= (15/16)^32, about 13%, at uniform density): the first product skips the zero rows
+        uint32_t *nz = nnz_hi <= (double)batch * (double)n / 16.0 ? w.nzrows : nullptr;
         int pr = -1;
         SDNN_HIP(prof_begin(net, -1, sdnn::kKernDensify, &pr));
         SDNN_HIP(sdnn::launch_densify_blocked(n, batch, from_user ? y_row_ptr : nullptr, from_user ? nullptr : w.cnt[cur ^ 1],
                                               from_user ? y_col : w.col[cur ^ 1], from_user ? y_val : w.val[cur ^ 1],
-                                              dense[0], net->d_flags, s));
+                                              dense[0], nz, net->d_flags, s));
         SDNN_HIP(prof_end(net, pr));
         int dc = 0;
         for (int32_t k = kd; k < k1; ++k) {
             const Layer &l = net->layers[(size_t)k];
             SDNN_HIP(prof_begin(net, k, sdnn::kKernBlocked, &pr));
-            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.stage, l.regions, l.bias, net->ymax, net->bias_pattern,
-                                               dense[dc], dense[dc ^ 1], s));
+            SDNN_HIP(sdnn::launch_spmm_blocked(n, batch, l.sched, l.stage, l.regions, k == kd ? nz : nullptr, l.bias,
+                                               net->ymax, net->bias_pattern, dense[dc], dense[dc ^ 1], s));
             SDNN_HIP(prof_end(net, pr));
             dc ^= 1;
         }

@@ -199,8 +199,8 @@ __device__ __forceinline__ void group8_min_max(int v, int &mn, int &mx) {
 template <bool kPattern, bool kStaged>
 __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SDNN_BLOCKED_WAVES_PER_EU, 8))) void spmm_blocked_kernel(
     int64_t n, int64_t gpx, int64_t tiles, const BlockedSched *__restrict__ sched, const Edge *__restrict__ fan,
-    const BlockedRegion *__restrict__ regions, const float *__restrict__ bias, double ymax,
-    const float *__restrict__ yb, float *__restrict__ zb) {
+    const BlockedRegion *__restrict__ regions, const uint32_t *__restrict__ nzrows, int64_t nz_words,
+    const float *__restrict__ bias, double ymax, const float *__restrict__ yb, float *__restrict__ zb) {
     __shared__ __align__(16) Edge ent[kStaged ? kStageCap : kBWaves * kBUnroll * 8];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q = lane >> 3, sub = lane & 7;
@@ -225,38 +225,62 @@ __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SD
                                              0, 0);
         __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's loads into LDS have landed
         __syncthreads();
+        if (nzrows) {
+            // a sparse input: entries whose input row is zero in this chunk are marked (bit 31 of the index;
+            // n <= 2^24) and read nothing below
+            const uint32_t *nzc = nzrows + c * nz_words;
+            for (int k = threadIdx.x; k < rg.cnt; k += kBWaves * 64) {
+                const int32_t i = ent[k].idx;
+                if (!((nzc[i >> 5] >> (i & 31)) & 1u)) ent[k].idx = (int32_t)((uint32_t)i | 0x80000000u);
+            }
+            __syncthreads();
+        }
+        // rows through buffer loads: an entry past its list's end, or marked, gets an offset past the chunk,
+        // which reads zero without a memory access
+        const uint32_t nrec = (uint32_t)n * (uint32_t)(kBW * 4);
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc((void *)yc, (short)0, (int)nrec, 0x00020000);
         for (int gi = 0; gi < kBGroups; ++gi) {
             const BlockedSched cur = sp[8 * gi];
-            const int len = cur.len;
-            const Edge *lst = ent + (cur.e0 - rg.e0);
-            const int last = len > 0 ? len - 1 : 0;
+            int len = cur.len;
+            Edge *lst = ent + (cur.e0 - rg.e0);
             int mn, mx;
             group8_min_max(len, mn, mx);
+            if (nzrows) {
+                // drop the marked entries: each neuron's 8 lanes move its unmarked ones to the front of its
+                // list, in order (reads of a block happen before its writes, which land at or before them)
+                int kept = 0;
+                for (int t = 0; t < mx; t += 8) {
+                    const int tt = t + sub;
+                    Edge e;
+                    e.idx = -1;
+                    e.w = 0.0f;
+                    if (tt < len) e = lst[tt];
+                    const bool keep = tt < len && e.idx >= 0;
+                    const uint32_t seg = (uint32_t)(__ballot(keep) >> (8 * q)) & 0xffu;
+                    wave_lds_sync();
+                    if (keep) lst[kept + __popc(seg & ((1u << sub) - 1u))] = e;
+                    kept += __popc(seg);
+                    wave_lds_sync();
+                }
+                len = kept;
+                group8_min_max(len, mn, mx);
+            }
+            const int last = len > 0 ? len - 1 : 0;
             double acc[4] = {0.0, 0.0, 0.0, 0.0};
             uint32_t hit[4] = {0u, 0u, 0u, 0u};
             for (int t = 0; t < mx; t += kBUnroll) {
-                Edge e[kBUnroll];
-#pragma unroll
-                for (int u = 0; u < kBUnroll; ++u) e[u] = lst[min(t + u, last)];
                 float4 y[kBUnroll];
+                float w[kBUnroll];
 #pragma unroll
-                for (int u = 0; u < kBUnroll; ++u) y[u] = load_row(yc, e[u].idx, lo);
-                if (t + kBUnroll <= mn) {
-#pragma unroll
-                    for (int u = 0; u < kBUnroll; ++u) fma4<kPattern>(y[u], e[u].w, acc, hit);
-                } else {
-                    // entries past a lane's end add a zeroed input times a zero weight
-#pragma unroll
-                    for (int u = 0; u < kBUnroll; ++u) {
-                        float4 yv = y[u];
-                        float wv = e[u].w;
-                        if (t + u >= len) {
-                            yv = make_float4(0.f, 0.f, 0.f, 0.f);
-                            wv = 0.0f;
-                        }
-                        fma4<kPattern>(yv, wv, acc, hit);
-                    }
+                for (int u = 0; u < kBUnroll; ++u) {
+                    const Edge e = lst[min(t + u, last)];
+                    const bool in = t + u < len && e.idx >= 0;
+                    w[u] = e.w;
+                    y[u] = __builtin_bit_cast(
+                        float4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (uint32_t)e.idx * (uint32_t)(kBW * 4) + lo : nrec, 0, 0));
                 }
+#pragma unroll
+                for (int u = 0; u < kBUnroll; ++u) fma4<kPattern>(y[u], w[u], acc, hit);
             }
             if (cur.j >= 0) {
                 const double bd = (double)bias[cur.j];
@@ -343,8 +367,9 @@ constexpr int kDensThreads = 512;
 __global__ __launch_bounds__(kDensThreads) void densify_blocked_kernel(
     int64_t n, int64_t batch, int64_t part_len, const int64_t *__restrict__ in_row_ptr,
     const int32_t *__restrict__ in_cnt, const int32_t *__restrict__ in_col, const float *__restrict__ in_val,
-    float *__restrict__ yb, uint32_t *err) {
-    __shared__ float tile[kDensR * kBW];
+    float *__restrict__ yb, uint32_t *__restrict__ nzrows, int64_t nz_words, uint32_t *err) {
+    __shared__ __align__(16) float tile[kDensR * kBW];
+    __shared__ uint32_t rowbits[kDensR / 32];  // rows of the range that receive a nonzero
     const int64_t nparts = (n + part_len - 1) / part_len;
     const int64_t c = blockIdx.x / nparts, part = blockIdx.x % nparts;
     const int s = threadIdx.x >> 4, k = threadIdx.x & 15;  // sample of the chunk, thread within the sample
@@ -381,6 +406,7 @@ __global__ __launch_bounds__(kDensThreads) void densify_blocked_kernel(
     for (int64_t a = a0; a < a1; a += kDensR) {
         const int64_t ra = min<int64_t>(kDensR, a1 - a);
         for (int t = threadIdx.x; t < kDensR * kBW; t += kDensThreads) tile[t] = 0.0f;
+        if (threadIdx.x < kDensR / 32) rowbits[threadIdx.x] = 0u;
         __syncthreads();
         // entries of this range: [cur, next) with next the first column >= a + kDensR
         int64_t next = cur;
@@ -388,7 +414,11 @@ __global__ __launch_bounds__(kDensThreads) void densify_blocked_kernel(
             const int64_t t = next + k;
             const int32_t i = t < re ? in_col[t] : 0x7fffffff;
             const bool in = i < a + ra;
-            if (in && i >= a) tile[(i - a) * kBW + s] = in_val[t];
+            if (in && i >= a) {
+                const float v = in_val[t];
+                tile[(i - a) * kBW + s] = v;
+                if (nzrows && v != 0.0f) atomicOr(&rowbits[(i - a) >> 5], 1u << ((i - a) & 31));
+            }
             // the 16 threads of a sample share one ballot segment: advance past the leading run that is in range
             const uint64_t m = __ballot(in);
             const uint32_t seg = (uint32_t)(m >> (threadIdx.x & 48)) & 0xffffu;
@@ -398,6 +428,8 @@ __global__ __launch_bounds__(kDensThreads) void densify_blocked_kernel(
         }
         cur = next;
         __syncthreads();
+        // bit i of the chunk's map: row a + i holds a nonzero
+        if (nzrows && threadIdx.x < kDensR / 32) nzrows[c * nz_words + (a >> 5) + threadIdx.x] = rowbits[threadIdx.x];
         float4 *dst = reinterpret_cast<float4 *>(yb + (c * n + a) * kBW);
         const float4 *srct = reinterpret_cast<const float4 *>(tile);
         for (int t = threadIdx.x; t < ra * (kBW / 4); t += kDensThreads) dst[t] = srct[t];
@@ -573,6 +605,8 @@ hipError_t launch_blocked_order(int64_t n, const int64_t *fan_ptr, BlockedSched 
 
 int64_t blocked_regions(int64_t n) { return blocked_sched_elems(n) / kBTile; }
 
+int64_t blocked_nz_words(int64_t n) { return (n + kDensR - 1) / kDensR * (kDensR / 32); }
+
 size_t blocked_stage_elems(int64_t n, int64_t nnz) { return (size_t)nnz + (size_t)blocked_regions(n) + 128; }
 
 int32_t blocked_stage_cap() { return kStageCap - 128; }
@@ -599,8 +633,8 @@ hipError_t launch_blocked_stage(int64_t n, int64_t nnz, const Edge *fan, Blocked
 }
 
 hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan,
-                               const BlockedRegion *regions, const float *bias, double ymax, int pattern,
-                               const float *yb, float *zb, hipStream_t s) {
+                               const BlockedRegion *regions, const uint32_t *nzrows, const float *bias, double ymax,
+                               int pattern, const float *yb, float *zb, hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
     if (n > (1 << 24)) return hipErrorInvalidValue;  // 32-bit row offsets within a chunk
     const int64_t nchunks = blocked_chunks(batch);
@@ -615,15 +649,17 @@ hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sch
         const unsigned nb = (unsigned)(nc * per_chunk);
         const float *y0 = yb + c0 * n * kBW;
         float *z0 = zb + c0 * n * kBW;
+        const int64_t words = blocked_nz_words(n);
+        const uint32_t *nz0 = (regions && nzrows) ? nzrows + c0 * words : nullptr;
         if (regions) {
             if (pattern)
-                spmm_blocked_kernel<true, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, regions, bias, ymax, y0, z0);
+                spmm_blocked_kernel<true, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, regions, nz0, words, bias, ymax, y0, z0);
             else
-                spmm_blocked_kernel<false, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, regions, bias, ymax, y0, z0);
+                spmm_blocked_kernel<false, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, regions, nz0, words, bias, ymax, y0, z0);
         } else if (pattern) {
-            spmm_blocked_kernel<true, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, nullptr, bias, ymax, y0, z0);
+            spmm_blocked_kernel<true, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, nullptr, nullptr, 0, bias, ymax, y0, z0);
         } else {
-            spmm_blocked_kernel<false, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, nullptr, bias, ymax, y0, z0);
+            spmm_blocked_kernel<false, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, nullptr, nullptr, 0, bias, ymax, y0, z0);
         }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -632,7 +668,8 @@ hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sch
 }
 
 hipError_t launch_densify_blocked(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
-                                  const int32_t *in_col, const float *in_val, float *yb, uint32_t *err, hipStream_t s) {
+                                  const int32_t *in_col, const float *in_val, float *yb, uint32_t *nzrows, uint32_t *err,
+                                  hipStream_t s) {
     if (n == 0 || batch == 0) return hipSuccess;
     const int64_t nchunks = blocked_chunks(batch);
     // enough parts for about eight workgroups per CU on the widest layers, whole ranges per part
@@ -642,7 +679,7 @@ hipError_t launch_densify_blocked(int64_t n, int64_t batch, const int64_t *in_ro
     const int64_t blocks = nchunks * nparts;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
     densify_blocked_kernel<<<(unsigned)blocks, kDensThreads, 0, s>>>(n, batch, part_len, in_row_ptr, in_cnt, in_col,
-                                                                      in_val, yb, err);
+                                                                      in_val, yb, nzrows, blocked_nz_words(n), err);
     return hipGetLastError();
 }
 

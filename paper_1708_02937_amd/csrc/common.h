@@ -168,13 +168,18 @@ int32_t blocked_stage_cap();  // longest padded region the product stages in LDS
 hipError_t launch_blocked_stage(int64_t n, int64_t nnz, const Edge *fan, BlockedSched *sched, Edge *stage,
                                 BlockedRegion *regions, int32_t *sizes, int64_t *starts, int64_t *scan_tmp,
                                 int32_t *region_max, hipStream_t s);
-// regions: the staged lists (null when a region exceeds blocked_stage_cap(): entries come from fan instead)
+// regions: the staged lists (null when a region exceeds blocked_stage_cap(): entries come from fan instead).
+// nzrows (with regions only, may be null): per chunk a map of blocked_nz_words(n) words, bit i set when
+// input row i holds a nonzero; the product then reads no row that is zero in its chunk.
+int64_t blocked_nz_words(int64_t n);
 hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan,
-                               const BlockedRegion *regions, const float *bias, double ymax, int pattern,
-                               const float *yb, float *zb, hipStream_t s);
-// sparse rows (caller CSR, or slot rows with counts) -> blocked; every element is written
+                               const BlockedRegion *regions, const uint32_t *nzrows, const float *bias, double ymax,
+                               int pattern, const float *yb, float *zb, hipStream_t s);
+// sparse rows (caller CSR, or slot rows with counts) -> blocked; every element is written, and when nzrows is
+// not null the nonzero-row map of every chunk (blocked_chunks(batch) * blocked_nz_words(n) words)
 hipError_t launch_densify_blocked(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
-                                  const int32_t *in_col, const float *in_val, float *yb, uint32_t *err, hipStream_t s);
+                                  const int32_t *in_col, const float *in_val, float *yb, uint32_t *nzrows, uint32_t *err,
+                                  hipStream_t s);
 // blocked -> CSR: pcnt holds blocked_pack_elems int32, cnt batch int32, row_ptr batch + 1
 hipError_t launch_blocked_to_csr(int64_t n, int64_t batch, const float *yb, int32_t *pcnt, int32_t *cnt,
                                  int64_t *row_ptr, int64_t *scan_tmp, int32_t *out_col, float *out_val, hipStream_t s);
