@@ -125,7 +125,7 @@ LayerPlan plan_layer(int64_t n, int64_t cap, int32_t dense_flags) {
     if (sdnn::spmm_wants_slots(n, cap)) lp.slots = take(off, sdnn::spmm_slot_elems(n) * sizeof(double));
     if (sdnn::spgemm_wants_window_index(n))
         lp.w_seg = take(off, (size_t)n * (size_t)(sdnn::spgemm_windows(n) + 1) * sizeof(int32_t));
-    if (sdnn::blocked_wanted(n, 1 << 20)) {
+    if (sdnn::blocked_planned(n, cap)) {
         lp.sched = take(off, (size_t)sdnn::blocked_sched_elems(n) * sizeof(sdnn::BlockedSched));
         lp.stage = take(off, sdnn::blocked_stage_elems(n, cap) * sizeof(Edge));
         lp.regions = take(off, (size_t)sdnn::blocked_regions(n) * sizeof(sdnn::BlockedRegion));
@@ -281,6 +281,17 @@ struct sdnn_net_s {
 };
 
 namespace {
+
+// Whether dense-Y layers [k0, k1) run on the sample-blocked layout: always beyond 16384 neurons; from 4097 to
+// 16384 only when every layer of the range stages its lists (short lists), since the other dense-Y products
+// share the neuron-major layout and the forward keeps one layout throughout.
+bool use_blocked(const sdnn_net_s *net, int32_t k0, int32_t k1, int64_t batch) {
+    if (!sdnn::blocked_wanted(net->n, batch)) return false;
+    if (sdnn::blocked_only(net->n)) return true;
+    for (int32_t k = k0; k < k1; ++k)
+        if (!net->layers[(size_t)k].regions) return false;
+    return true;
+}
 
 hipError_t prof_event(sdnn_net net, hipEvent_t *e) {
     if (!net->ev_free.empty()) {
@@ -619,7 +630,7 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
     buf[1] = (float *)((char *)ws + act_bytes(n, batch));
     double *partial = (double *)((char *)ws + 2 * act_bytes(n, batch));
     int pr = -1;
-    if (arm == SDNN_ARM_SPARSE && sdnn::blocked_wanted(n, batch)) {
+    if (arm == SDNN_ARM_SPARSE && use_blocked(net, k0, k1, batch)) {
         // very wide layers: the sample-blocked layout (each buffer holds n x ld >= n x round32(batch) floats)
         SDNN_HIP(prof_begin(net, -1, sdnn::kKernTranspose, &pr));
         SDNN_HIP(sdnn::launch_to_blocked(n, batch, n, Y_in, buf[0], s));
@@ -768,7 +779,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     }
     int last = 0, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
     bool packed = false;  // the CSR is already in buffer outb
-    if (kd < k1 && sdnn::blocked_wanted(n, batch)) {
+    if (kd < k1 && use_blocked(net, kd, k1, batch)) {
         // very wide layers: dense activations in the sample-blocked layout, packed straight into CSR at the end
         const bool from_user = kd == k0;
         const int db = from_user ? 0 : cur;  // the input rows (if any) sit in buffer cur ^ 1

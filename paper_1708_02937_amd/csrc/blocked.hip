@@ -198,17 +198,26 @@ __device__ __forceinline__ void group8_min_max(int v, int &mn, int &mx) {
 // per-block entry loads from HBM sat on each block's critical path (94 -> 79 ms per layer without them).
 template <bool kPattern, bool kStaged>
 __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SDNN_BLOCKED_WAVES_PER_EU, 8))) void spmm_blocked_kernel(
-    int64_t n, int64_t gpx, int64_t tiles, const BlockedSched *__restrict__ sched, const Edge *__restrict__ fan,
-    const BlockedRegion *__restrict__ regions, const uint32_t *__restrict__ nzrows, int64_t nz_words,
-    const float *__restrict__ bias, double ymax, const float *__restrict__ yb, float *__restrict__ zb) {
+    int64_t n, int64_t gpx, int64_t tiles, int64_t nchunk, int xcd_chunks, const BlockedSched *__restrict__ sched,
+    const Edge *__restrict__ fan, const BlockedRegion *__restrict__ regions, const uint32_t *__restrict__ nzrows,
+    int64_t nz_words, const float *__restrict__ bias, double ymax, const float *__restrict__ yb, float *__restrict__ zb) {
     __shared__ __align__(16) Edge ent[kStaged ? kStageCap : kBWaves * kBUnroll * 8];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q = lane >> 3, sub = lane & 7;
     const int64_t b = blockIdx.x;
     const int64_t xcd = b & 7, local = b >> 3;
-    const int64_t c = local / gpx;
-    const int64_t g = xcd * gpx + (local - c * gpx);
-    if (g >= tiles) return;
+    int64_t c, g;
+    if (xcd_chunks) {
+        // whole chunks per XCD (chunk c on XCD c mod 8, its workgroups in schedule order), for chunks small
+        // enough that one, with the next, stays in that XCD's L2
+        c = xcd + 8 * (local / tiles);
+        g = local - (local / tiles) * tiles;
+        if (c >= nchunk) return;
+    } else {
+        c = local / gpx;
+        g = xcd * gpx + (local - c * gpx);
+        if (g >= tiles) return;
+    }
     const char *yc = reinterpret_cast<const char *>(yb + c * n * kBW);
     float *zc = zb + c * n * kBW + sub * 4;
     const uint32_t lo = (uint32_t)sub * 16u;
@@ -590,7 +599,14 @@ int64_t blocked_chunks(int64_t batch) { return (batch + kBW - 1) / kBW; }
 
 size_t blocked_elems(int64_t n, int64_t batch) { return (size_t)blocked_chunks(batch) * kBW * (size_t)n; }
 
-bool blocked_wanted(int64_t n, int64_t batch) { return n > 16384 && n <= (1 << 24) && batch >= 256; }
+bool blocked_wanted(int64_t n, int64_t batch) { return n > 4096 && n <= (1 << 24) && batch >= 256; }
+
+bool blocked_only(int64_t n) { return n > 16384 && n <= (1 << 24); }
+
+// Up to 16384 neurons the blocked product pays only on short lists (measured at n 16384, 32 entries per
+// neuron, batch 4096: 0.43 ms per layer against 0.53 in the narrow-chunk gather); dense-ish layers keep the
+// scalar-register and tiled products, so only layers averaging at most 48 entries per neuron get the schedule.
+bool blocked_planned(int64_t n, int64_t nnz) { return blocked_only(n) || (n > 4096 && nnz <= 48 * n); }
 
 size_t blocked_pack_elems(int64_t n, int64_t batch) { return (size_t)((n + kPackR - 1) / kPackR) * (size_t)batch; }
 
@@ -640,26 +656,33 @@ hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sch
     const int64_t nchunks = blocked_chunks(batch);
     const int64_t groups = (n + kBTile - 1) / kBTile;
     const int64_t gpx = (groups + 7) / 8;
-    const int64_t per_chunk = 8 * gpx;  // workgroups per chunk (n <= 2^24: at most 2^19 + 8)
-    // launches of whole chunks, at most 2^23 workgroups each; every launch numbers its workgroups from 0, so
+    // chunks of at most 2 MiB (n <= 16384) go whole to one XCD each (measured on n = 16384, batch 4096: all 8
+    // XCDs sharing each chunk keep about 2.5 chunks in flight, more than one XCD's 4 MB L2 holds); wider
+    // chunks are split over the XCDs as above
+    const int xcd_chunks = n * kBW * 4 <= (int64_t(2) << 20) ? 1 : 0;
+    // workgroups per chunk (n <= 2^24: at most 2^19 + 8); in the XCD-chunk order 8 chunks are launched as a
+    // unit, the workgroups of missing chunks of the last unit return at once
+    const int64_t per_chunk = xcd_chunks ? groups : 8 * gpx;
+    const int64_t unit = xcd_chunks ? 8 : 1;
+    // launches of whole units, at most 2^23 workgroups each; every launch numbers its workgroups from 0, so
     // the data pointers move to its first chunk
-    const int64_t chunks_per_launch = std::max<int64_t>(1, (int64_t(1) << 23) / per_chunk);
+    const int64_t chunks_per_launch = std::max<int64_t>(unit, (int64_t(1) << 23) / (per_chunk * unit) * unit);
     for (int64_t c0 = 0; c0 < nchunks; c0 += chunks_per_launch) {
         const int64_t nc = std::min(chunks_per_launch, nchunks - c0);
-        const unsigned nb = (unsigned)(nc * per_chunk);
+        const unsigned nb = (unsigned)((nc + unit - 1) / unit * unit * per_chunk);
         const float *y0 = yb + c0 * n * kBW;
         float *z0 = zb + c0 * n * kBW;
         const int64_t words = blocked_nz_words(n);
         const uint32_t *nz0 = (regions && nzrows) ? nzrows + c0 * words : nullptr;
         if (regions) {
             if (pattern)
-                spmm_blocked_kernel<true, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, regions, nz0, words, bias, ymax, y0, z0);
+                spmm_blocked_kernel<true, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, nc, xcd_chunks, sched, fan, regions, nz0, words, bias, ymax, y0, z0);
             else
-                spmm_blocked_kernel<false, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, regions, nz0, words, bias, ymax, y0, z0);
+                spmm_blocked_kernel<false, true><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, nc, xcd_chunks, sched, fan, regions, nz0, words, bias, ymax, y0, z0);
         } else if (pattern) {
-            spmm_blocked_kernel<true, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, nullptr, nullptr, 0, bias, ymax, y0, z0);
+            spmm_blocked_kernel<true, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, nc, xcd_chunks, sched, fan, nullptr, nullptr, 0, bias, ymax, y0, z0);
         } else {
-            spmm_blocked_kernel<false, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, sched, fan, nullptr, nullptr, 0, bias, ymax, y0, z0);
+            spmm_blocked_kernel<false, false><<<nb, kBWaves * 64, 0, s>>>(n, gpx, groups, nc, xcd_chunks, sched, fan, nullptr, nullptr, 0, bias, ymax, y0, z0);
         }
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;

@@ -139,7 +139,9 @@ hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, con
 // n x 32 block: element (r, i) at ((r / 32) * n + i) * 32 + r % 32) and its product.
 int64_t blocked_chunks(int64_t batch);
 size_t blocked_elems(int64_t n, int64_t batch);   // floats of one blocked activation buffer
-bool blocked_wanted(int64_t n, int64_t batch);     // the dense-Y path uses the blocked layout
+bool blocked_wanted(int64_t n, int64_t batch);     // the dense-Y path can use the blocked layout
+bool blocked_only(int64_t n);                      // ... and always does (no other dense-Y product this wide)
+bool blocked_planned(int64_t n, int64_t nnz);      // set-up builds a layer's schedule and staged lists
 size_t blocked_pack_elems(int64_t n, int64_t batch);  // int32 scratch of launch_blocked_to_csr
 // Schedule of the blocked product (set-up): neurons sorted by fan-in length within runs of 4096, one entry
 // per position (neuron or -1, list length, list start; an empty list starts at the guard entry fan[nnz],

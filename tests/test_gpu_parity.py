@@ -285,12 +285,13 @@ def _mixed_length_layer(rng, n, lengths):
 @pytest.mark.parametrize("seed,n,batch,lengths,bias_mode", [
     (81, 4097, 36, [0, 1, 15, 16, 17, 40, 100], 0), (82, 5003, 96, [3, 0, 0, 33, 8, 9, 64, 1], 0),
     (83, 6144, 132, [16, 16, 16, 16, 32, 31, 48, 7], 1), (84, 4099, 4, [120, 0, 5, 17], 1),
-    (85, 4500, 300, [2, 30, 31, 33, 0, 64], 0), (86, 16384, 512, [32, 25, 40, 32], 1),
+    (85, 4500, 300, [2, 30, 31, 33, 0, 64, 120, 130], 0), (86, 16384, 512, [32, 25, 40, 32, 100, 120], 1),
     (87, 40000, 60, [33, 2, 0, 17, 64], 0), (88, 4099, 2, [120, 0, 5, 17], 0)])
 def test_narrow_chunk_gather(sd, seed, n, batch, lengths, bias_mode):
-    """Layers with n > 4096 up to 16384 (any batch that is a multiple of 4), or n >= 4096 and a batch under
-    256 that is a multiple of 4, take the narrow-chunk gather (16 lanes and 64 columns, four per lane, per
-    neuron): ragged n, partial last chunks, and list lengths from 0 to 120 side by side in one wave, which
+    """Layers with n >= 4096 and a batch under 256 that is a multiple of 4, or n > 4096 up to 16384 with
+    lists too long for the blocked product (over 48 entries per neuron on average; cases 85 and 86, at a
+    batch of 256 or more), take the narrow-chunk gather (16 lanes and 64 columns, four per lane, per
+    neuron): ragged n, partial last chunks, and list lengths from 0 to 130 side by side in one wave, which
     exercises the unpredicated prefix, the guarded tail and lists spanning several loads of 16 entries.  The
     last case (batch 2, not a multiple of 4) is the fan-in gather fallback with one column per lane."""
     rng = np.random.default_rng(seed)
@@ -307,12 +308,15 @@ def test_narrow_chunk_gather(sd, seed, n, batch, lengths, bias_mode):
 @pytest.mark.parametrize("seed,n,batch,lengths,bias_mode", [
     (91, 16400, 256, [32, 25, 40, 32, 0, 1, 77, 33], 0), (92, 20000, 300, [3, 0, 0, 33, 8, 9, 64, 1], 1),
     (93, 17003, 257, [120, 0, 5, 17, 31, 32, 33], 0), (94, 24576, 512, [24, 24, 24, 24, 24, 24, 24, 25], 1),
-    (95, 16900, 288, [100, 90, 110, 64], 0), (96, 18000, 256, [95, 0, 120, 101], 1)])
+    (95, 16900, 288, [100, 90, 110, 64], 0), (96, 18000, 256, [95, 0, 120, 101], 1),
+    (97, 4500, 300, [2, 30, 31, 33, 0, 64], 0), (98, 16384, 512, [32, 25, 40, 32], 1),
+    (99, 8192, 256, [0, 1, 15, 16, 17, 40, 100], 0)])
 def test_blocked_product(sd, seed, n, batch, lengths, bias_mode):
-    """Layers wider than 16384 with batches of 256 or more take the product on the sample-blocked layout
-    (chunks of 32 samples, eight neurons per wave walking their lists in step): ragged n, a partial last
-    chunk, empty lists and list lengths from 0 to 120 side by side in one wave, both bias readings, every
-    row compared.  Each workgroup stages its 64 neurons' lists in LDS while they fit (up to about 3968
+    """Layers wider than 16384, or from 4097 to 16384 neurons with short lists (at most 48 entries per neuron
+    on average: cases 97-99, whose 2 MiB or smaller chunks go whole to one XCD each, 10, 16 and 8 chunks),
+    with batches of 256 or more take the product on the sample-blocked layout (chunks of 32 samples, eight
+    neurons per wave walking their lists in step): ragged n, a partial last chunk, empty lists and list
+    lengths from 0 to 120 side by side in one wave, both bias readings, every row compared.  Each workgroup stages its 64 neurons' lists in LDS while they fit (up to about 3968
     entries: the cases with lists of about 100 entries exceed it, and their layers read the staged copy
     entry by entry instead)."""
     rng = np.random.default_rng(seed)
@@ -394,7 +398,8 @@ def test_padded_pitch_every_kernel(sd, case, batch):
     split sum) and the CSR path's switch to dense activations (densify, gather, transpose and compaction) at a
     padded pitch, ragged in n and batch."""
     n = 4500
-    d = {"gather": 0.01, "slots": 0.3, "dense_arm": 0.05, "csr_switch": 0.02}[case]
+    # the gather case averages 67 entries per neuron: short lists would take the sample-blocked layout
+    d = {"gather": 0.015, "slots": 0.3, "dense_arm": 0.05, "csr_switch": 0.02}[case]
     if case == "csr_switch":
         p = tiny_random(90, n, 3, batch, w_density=d, y_density=0.3, bias_lo=0.0, bias_hi=0.2)
         _say("padded pitch", case, batch)
@@ -624,19 +629,20 @@ def test_identity_input_reads_back_weights(sd):
     assert got.tobytes() == want.tobytes()
 
 
-@pytest.mark.parametrize("layers", ["gather", "slots", "narrow"])
+@pytest.mark.parametrize("layers", ["gather", "slots", "narrow", "blocked"])
 def test_graph_replay_matches_eager(sd, layers):
     """A HIP graph of forward_dense replays the eager result bit for bit, replay after replay, with new inputs
     written into the bound input and unrelated eager work between the replays (both arms); the layers take the
-    gather SpMM (tiny MLP recipe), the scalar-register LDS-tiled SpMM (d = 0.5) or the narrow-chunk gather at
-    a padded activation pitch (n 4200, batch 256 -> 320)."""
+    gather SpMM (tiny MLP recipe), the scalar-register LDS-tiled SpMM (d = 0.5), the narrow-chunk gather at
+    a padded activation pitch (n 4200, batch 256 -> 320, 63 entries per neuron) or the product on the
+    sample-blocked layout (the same shape with 34 entries per neuron)."""
     import torch
 
     if layers == "gather":
         p = make_config(1, n=1000, L=3, batch=132)
-    elif layers == "narrow":
-        p = tiny_random(46, 4200, 2, 256, w_density=0.008, y_density=0.6, dense_input=True, bias_lo=-0.3,
-                        bias_hi=0.3)
+    elif layers in ("narrow", "blocked"):
+        p = tiny_random(46, 4200, 2, 256, w_density=0.015 if layers == "narrow" else 0.008, y_density=0.6,
+                        dense_input=True, bias_lo=-0.3, bias_hi=0.3)
     else:
         p = tiny_random(45, 1300, 2, 128, w_density=0.5, y_density=0.7, dense_input=True, bias_lo=-1.0,
                         bias_hi=1.0)
