@@ -163,6 +163,27 @@ __device__ __forceinline__ void fma4(const float4 &y, float w, double (&acc)[4],
     }
 }
 
+// K entries t .. t + K - 1 of the lane's staged list (clamped to its last entry): the K row loads are issued
+// together, then the K products added in list order.  Entries past the list's end, or marked (negative
+// index), load from an offset past the chunk, which reads zero without a memory access.
+template <int K, bool kPattern>
+__device__ __forceinline__ void staged_block(const Edge *lst, int t, int len, int last, __amdgpu_buffer_rsrc_t rs,
+                                             uint32_t lo, uint32_t nrec, double (&acc)[4], uint32_t (&hit)[4]) {
+    static_assert(K <= kBUnroll, "rows in flight per lane");
+    float4 y[K];
+    float w[K];
+#pragma unroll
+    for (int u = 0; u < K; ++u) {
+        const Edge e = lst[min(t + u, last)];
+        const bool in = t + u < len && e.idx >= 0;
+        w[u] = e.w;
+        y[u] = __builtin_bit_cast(
+            float4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (uint32_t)e.idx * (uint32_t)(kBW * 4) + lo : nrec, 0, 0));
+    }
+#pragma unroll
+    for (int u = 0; u < K; ++u) fma4<kPattern>(y[u], w[u], acc, hit);
+}
+
 // Orders LDS writes and reads among the lanes of one wave (no other wave touches the region).
 __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -277,20 +298,19 @@ __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SD
             const int last = len > 0 ? len - 1 : 0;
             double acc[4] = {0.0, 0.0, 0.0, 0.0};
             uint32_t hit[4] = {0u, 0u, 0u, 0u};
-            for (int t = 0; t < mx; t += kBUnroll) {
-                float4 y[kBUnroll];
-                float w[kBUnroll];
-#pragma unroll
-                for (int u = 0; u < kBUnroll; ++u) {
-                    const Edge e = lst[min(t + u, last)];
-                    const bool in = t + u < len && e.idx >= 0;
-                    w[u] = e.w;
-                    y[u] = __builtin_bit_cast(
-                        float4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (uint32_t)e.idx * (uint32_t)(kBW * 4) + lo : nrec, 0, 0));
-                }
-#pragma unroll
-                for (int u = 0; u < kBUnroll; ++u) fma4<kPattern>(y[u], w[u], acc, hit);
-            }
+            int t = 0;
+            for (; t + kBUnroll <= mx; t += kBUnroll) staged_block<kBUnroll, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+            // the last mx - t (< kBUnroll, the same for the whole wave) entries: one block of the smallest even
+            // size that covers them, since loads past the longest list still occupy the address and data units
+            const int rem = mx - t;
+            if (rem > 6)
+                staged_block<8, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+            else if (rem > 4)
+                staged_block<6, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+            else if (rem > 2)
+                staged_block<4, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+            else if (rem > 0)
+                staged_block<2, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
             if (cur.j >= 0) {
                 const double bd = (double)bias[cur.j];
                 float4 out;
