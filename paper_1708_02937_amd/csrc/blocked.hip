@@ -39,6 +39,7 @@ constexpr int kBTile = kBWaves * kBGroups * 8;  // neurons per workgroup and chu
 #endif
 constexpr int kBUnroll = SDNN_BLOCKED_UNROLL;  // list entries per block (rows in flight per lane)
 constexpr int kStageCap = 4096;  // entries of a workgroup's staged lists (32 KiB of LDS: five workgroups per CU)
+constexpr int kStageAhead = 128;  // longest list the staged product walks; also how far past its region it loads
 
 // ------------------------------------------------------------------------------------------ set-up
 
@@ -101,7 +102,10 @@ __global__ __launch_bounds__(256) void blocked_order_kernel(int64_t n, int64_t p
 // The workgroups' list regions: the padded size of each (its kBTile positions' lists, rounded up to an even
 // entry count so that every region starts 16-byte aligned), then, after a scan of the sizes, one 64-thread
 // workgroup per region copies its lists in schedule order (a wave prefix sum of the lengths places them),
-// writes a zero entry into the padding, repoints the schedule's list starts and records the region.
+// writes a zero entry into the padding, repoints the schedule's list starts and records the region.  The
+// region's extent, its entries plus 2 * kStageAhead (the product loads kStageAhead entries past the region and
+// reads up to a list's length past the last list's end), goes into region_max, or 2^30 when a list is longer
+// than kStageAhead: the product stages the layer's lists only when every extent fits its LDS.
 __global__ __launch_bounds__(256) void blocked_region_size_kernel(int64_t nreg, const BlockedSched *__restrict__ sched,
                                                                   int32_t *__restrict__ sizes) {
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -126,6 +130,9 @@ __global__ __launch_bounds__(64) void blocked_stage_kernel(const Edge *__restric
         if (lane >= d) incl += v;
     }
     const int cnt = __shfl(incl, 63);
+    int longest = e.len;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) longest = max(longest, __shfl_xor(longest, d));
     const int64_t base = starts[g];
     const int64_t dst = base + (incl - e.len);
     for (int i = 0; i < e.len; ++i) stage[dst + i] = fan[e.e0 + i];
@@ -138,7 +145,7 @@ __global__ __launch_bounds__(64) void blocked_stage_kernel(const Edge *__restric
         r.cnt = cnt;
         r.pad = 0;
         regions[g] = r;
-        atomicMax(region_max, (cnt + 1) & ~1);
+        atomicMax(region_max, longest > kStageAhead ? (1 << 30) : ((cnt + 1) & ~1) + 2 * kStageAhead);
     }
 }
 
@@ -163,19 +170,20 @@ __device__ __forceinline__ void fma4(const float4 &y, float w, double (&acc)[4],
     }
 }
 
-// K entries t .. t + K - 1 of the lane's staged list (clamped to its last entry): the K row loads are issued
-// together, then the K products added in list order.  Entries past the list's end, or marked (negative
-// index), load from an offset past the chunk, which reads zero without a memory access.
+// K entries t .. t + K - 1 of the lane's staged list: the K row loads are issued together, then the K
+// products added in list order.  Entries past the list's end (up to kStageAhead of them: the next lists, or
+// what was loaded after the region, all finite) load from an offset past the chunk, which reads zero without a
+// memory access, so their products add zero.  No marked entry lies within a list's length.
 template <int K, bool kPattern>
-__device__ __forceinline__ void staged_block(const Edge *lst, int t, int len, int last, __amdgpu_buffer_rsrc_t rs,
+__device__ __forceinline__ void staged_block(const Edge *lst, int t, int len, __amdgpu_buffer_rsrc_t rs,
                                              uint32_t lo, uint32_t nrec, double (&acc)[4], uint32_t (&hit)[4]) {
     static_assert(K <= kBUnroll, "rows in flight per lane");
     float4 y[K];
     float w[K];
 #pragma unroll
     for (int u = 0; u < K; ++u) {
-        const Edge e = lst[min(t + u, last)];
-        const bool in = t + u < len && e.idx >= 0;
+        const Edge e = lst[t + u];
+        const bool in = t + u < len;
         w[u] = e.w;
         y[u] = __builtin_bit_cast(
             float4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (uint32_t)e.idx * (uint32_t)(kBW * 4) + lo : nrec, 0, 0));
@@ -244,12 +252,15 @@ __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SD
     const uint32_t lo = (uint32_t)sub * 16u;
     const BlockedSched *sp = sched + (g * kBWaves + wave) * (kBGroups * 8) + q;
     if constexpr (kStaged) {
-        // the region (at most kStageCap - 128 entries, padded to an even count, 16-byte aligned); each load
-        // instruction moves 128 entries, the last one up to 127 entries past the region (into the next region
-        // or the zeroed tail of the copy), all within ent
+        // the region (padded to an even count, 16-byte aligned) and more than kStageAhead entries after it (the
+        // next regions, or the zeroed tail of the copy): a lane reads at most to index mx of its list (a tail
+        // block's last slot), mx <= kStageAhead, so never past entry cnt + kStageAhead.  Each load instruction
+        // moves 128 entries; the last ends before entry cnt + 2 * kStageAhead, within ent (the region's
+        // extent, checked at set-up, is at most kStageCap) and within the copy (zeroed 2 * kStageAhead entries
+        // past its last region)
         const BlockedRegion rg = regions[g];
         const Edge *src = fan + rg.e0;
-        for (int base = wave * 128; base < rg.cnt; base += kBWaves * 128)
+        for (int base = wave * 128; base <= rg.cnt + kStageAhead; base += kBWaves * 128)
             __builtin_amdgcn_global_load_lds(reinterpret_cast<const void *>(src + base + 2 * lane),
                                              (__attribute__((address_space(3))) void *)(&ent[base]), 16,
                                              0, 0);
@@ -295,22 +306,21 @@ __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SD
                 len = kept;
                 group8_min_max(len, mn, mx);
             }
-            const int last = len > 0 ? len - 1 : 0;
             double acc[4] = {0.0, 0.0, 0.0, 0.0};
             uint32_t hit[4] = {0u, 0u, 0u, 0u};
             int t = 0;
-            for (; t + kBUnroll <= mx; t += kBUnroll) staged_block<kBUnroll, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+            for (; t + kBUnroll <= mx; t += kBUnroll) staged_block<kBUnroll, kPattern>(lst, t, len, rs, lo, nrec, acc, hit);
             // the last mx - t (< kBUnroll, the same for the whole wave) entries: one block of the smallest even
             // size that covers them, since loads past the longest list still occupy the address and data units
             const int rem = mx - t;
             if (rem > 6)
-                staged_block<8, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+                staged_block<8, kPattern>(lst, t, len, rs, lo, nrec, acc, hit);
             else if (rem > 4)
-                staged_block<6, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+                staged_block<6, kPattern>(lst, t, len, rs, lo, nrec, acc, hit);
             else if (rem > 2)
-                staged_block<4, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+                staged_block<4, kPattern>(lst, t, len, rs, lo, nrec, acc, hit);
             else if (rem > 0)
-                staged_block<2, kPattern>(lst, t, len, last, rs, lo, nrec, acc, hit);
+                staged_block<2, kPattern>(lst, t, len, rs, lo, nrec, acc, hit);
             if (cur.j >= 0) {
                 const double bd = (double)bias[cur.j];
                 float4 out;
@@ -643,9 +653,11 @@ int64_t blocked_regions(int64_t n) { return blocked_sched_elems(n) / kBTile; }
 
 int64_t blocked_nz_words(int64_t n) { return (n + kDensR - 1) / kDensR * (kDensR / 32); }
 
-size_t blocked_stage_elems(int64_t n, int64_t nnz) { return (size_t)nnz + (size_t)blocked_regions(n) + 128; }
+size_t blocked_stage_elems(int64_t n, int64_t nnz) {
+    return (size_t)nnz + (size_t)blocked_regions(n) + 2 * kStageAhead;
+}
 
-int32_t blocked_stage_cap() { return kStageCap - 128; }
+int32_t blocked_stage_cap() { return kStageCap; }
 
 hipError_t launch_blocked_stage(int64_t n, int64_t nnz, const Edge *fan, BlockedSched *sched, Edge *stage,
                                 BlockedRegion *regions, int32_t *sizes, int64_t *starts, int64_t *scan_tmp,
@@ -658,9 +670,9 @@ hipError_t launch_blocked_stage(int64_t n, int64_t nnz, const Edge *fan, Blocked
     e = launch_exclusive_scan_i32_to_i64(nreg, sizes, starts, scan_tmp, s);
     if (e != hipSuccess) return e;
     // the regions end between nnz and nnz + nreg entries (one padding entry at most per region): zeroing from
-    // nnz to the end of the copy leaves zeros in the 128 entries after the last region, which the staging
-    // loads of the last regions may read
-    e = hipMemsetAsync(stage + nnz, 0, ((size_t)nreg + 128) * sizeof(Edge), s);
+    // nnz to the end of the copy leaves zeros in the 2 * kStageAhead entries after the last region, which the
+    // staging loads of the last regions may read
+    e = hipMemsetAsync(stage + nnz, 0, ((size_t)nreg + 2 * kStageAhead) * sizeof(Edge), s);
     if (e != hipSuccess) return e;
     e = hipMemsetAsync(region_max, 0, sizeof(int32_t), s);
     if (e != hipSuccess) return e;

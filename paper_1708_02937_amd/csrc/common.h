@@ -157,7 +157,8 @@ hipError_t launch_blocked_order(int64_t n, const int64_t *fan_ptr, BlockedSched 
 // contiguous region, in schedule order, so that the product stages them into LDS at once (set-up).  A
 // region starts 16-byte aligned (its length is padded to an even count with a zero entry); stage holds
 // blocked_stage_elems(n, nnz) entries (the last 128, zeroed, cover the staging loads' overrun).  The schedule's
-// list starts are rewritten to point into stage; region_max receives the longest padded region (entries).
+// list starts are rewritten to point into stage; region_max receives the largest region extent (entries the
+// product needs in LDS, 2^30 when a list is too long to stage).
 // sizes: blocked_regions(n) int32 of scratch; starts: blocked_regions(n) + 1 int64.
 struct __align__(16) BlockedRegion {
     int64_t e0;   // first entry of the region in the staged copy
@@ -166,7 +167,7 @@ struct __align__(16) BlockedRegion {
 };
 int64_t blocked_regions(int64_t n);
 size_t blocked_stage_elems(int64_t n, int64_t nnz);
-int32_t blocked_stage_cap();  // longest padded region the product stages in LDS
+int32_t blocked_stage_cap();  // largest region extent the product stages in LDS
 hipError_t launch_blocked_stage(int64_t n, int64_t nnz, const Edge *fan, BlockedSched *sched, Edge *stage,
                                 BlockedRegion *regions, int32_t *sizes, int64_t *starts, int64_t *scan_tmp,
                                 int32_t *region_max, hipStream_t s);
