@@ -789,7 +789,9 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         float *dense[2] = {reinterpret_cast<float *>(w.col[db]), w.val[db]};
         // a sparse input (at most 1/16 of batch * n entries: a 32-sample row is then entirely zero with
         // probability >= (15/16)^32, about 13%, at uniform density): the first product skips the zero rows
-        uint32_t *nz = nnz_hi <= (double)batch * (double)n / 16.0 ? w.nzrows : nullptr;
+        // (only when the first layer stages its lists: the product reads the map only then, and densify does
+        // not store the zero rows when it writes one)
+        uint32_t *nz = (nnz_hi <= (double)batch * (double)n / 16.0 && net->layers[(size_t)kd].regions) ? w.nzrows : nullptr;
         int pr = -1;
         SDNN_HIP(prof_begin(net, -1, sdnn::kKernDensify, &pr));
         SDNN_HIP(sdnn::launch_densify_blocked(n, batch, from_user ? y_row_ptr : nullptr, from_user ? nullptr : w.cnt[cur ^ 1],

@@ -178,8 +178,10 @@ int64_t blocked_nz_words(int64_t n);
 hipError_t launch_spmm_blocked(int64_t n, int64_t batch, const BlockedSched *sched, const Edge *fan,
                                const BlockedRegion *regions, const uint32_t *nzrows, const float *bias, double ymax,
                                int pattern, const float *yb, float *zb, hipStream_t s);
-// sparse rows (caller CSR, or slot rows with counts) -> blocked; every element is written, and when nzrows is
-// not null the nonzero-row map of every chunk (blocked_chunks(batch) * blocked_nz_words(n) words)
+// sparse rows (caller CSR, or slot rows with counts) -> blocked; every element is written, except that when
+// nzrows is not null the rows of a chunk that hold no nonzero are not stored (only a product given the same map,
+// which reads no such row, may consume the result), and the nonzero-row map of every chunk
+// (blocked_chunks(batch) * blocked_nz_words(n) words) is written
 hipError_t launch_densify_blocked(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                   const int32_t *in_col, const float *in_val, float *yb, uint32_t *nzrows, uint32_t *err,
                                   hipStream_t s);

@@ -330,11 +330,26 @@ def test_blocked_product(sd, seed, n, batch, lengths, bias_mode):
                              bias_mode=bias_mode)
 
 
-@pytest.mark.parametrize("case", ["from_input", "after_sparse", "integer", "empty_layer"])
+@pytest.mark.parametrize("case", ["from_input", "after_sparse", "integer", "empty_layer", "unstaged"])
 def test_blocked_csr_path(sd, case):
     """The CSR path's dense activations on the blocked layout: densify from the caller's CSR (positive bias
     from layer 0) or from slot rows after sparse layers, the layers, and the packing into CSR; an integer
-    shadow of the very wide recipe (scaled, batch 260) bit for bit; a layer with no weights."""
+    shadow of the very wide recipe (scaled, batch 260) bit for bit; a layer with no weights; a 2%-dense input
+    whose first layer cannot stage its lists (one list of 150 entries), so densify stores every row, zero
+    rows included, for a product that reads them all."""
+    if case == "unstaged":
+        rng = np.random.default_rng(97)
+        n, batch = 17000, 288
+        layers = [_mixed_length_layer(rng, n, [150, 10, 20, 30, 0, 33]), _mixed_length_layer(rng, n, [33, 2, 40])]
+        for l in layers:
+            l.bias = rng.uniform(0.0, 0.2, size=n).astype(np.float32)
+        y = rng.random((batch, n), dtype=np.float32)
+        y[rng.random((batch, n)) >= 0.02] = 0.0
+        from workloads import Problem
+        p = Problem("blocked-unstaged", n, 2, batch, math.inf, layers, y0_dense=y)
+        _say("blocked csr", case)
+        parity.compare_in_chunks(p, run_csr(sd, p))
+        return
     if case == "integer":
         q = integer_shadow(make_config(5, n=20480, L=3, batch=260, block=4096))
         for l in q.layers:  # positive biases everywhere: dense activations from layer 0
