@@ -330,6 +330,39 @@ def test_blocked_product(sd, seed, n, batch, lengths, bias_mode):
                              bias_mode=bias_mode)
 
 
+@pytest.mark.parametrize("longest,want", [(150, "spmm_narrow_kernel"), (120, "spmm_blocked_kernel")])
+def test_mid_width_layout_choice(sd, longest, want):
+    """From 4097 to 16384 neurons a forward takes the sample-blocked layout only when every layer stages its
+    lists: layers of 20-entry lists with one longer list per 4096 neurons (which the schedule's sort puts in
+    its run's first workgroup region, still small enough for LDS) stay neuron-major on the narrow-chunk
+    gather when that list holds 150 entries (more than the staged product walks), and take the blocked
+    product at 120; both paths (dense and CSR input) against the oracle, the kernel that ran read from the
+    library's profiling log."""
+    import torch
+
+    rng = np.random.default_rng(71)
+    n, batch = 6000, 300
+    lengths = [20] * 4095 + [longest]
+    layers = [_mixed_length_layer(rng, n, lengths), _mixed_length_layer(rng, n, lengths[::-1])]
+    assert all(l.nnz <= 48 * n for l in layers)
+    y = rng.random((batch, n), dtype=np.float32)
+    y[rng.random((batch, n)) < 0.5] = 0.0
+    from workloads import Problem
+    p = Problem(f"mid-width-{longest}", n, 2, batch, math.inf, layers, y0_dense=y)
+    net = sd.net_from_problem(p)
+    net.set_profiling(True)
+    _say("mid-width layout", longest)
+    out = net.forward_dense(torch.from_numpy(y).cuda()).cpu().numpy()
+    rp, c, v = net.forward_csr(*(torch.from_numpy(a).cuda() for a in p.y0_as_csr()))
+    got_csr = (rp.cpu().numpy(), c.cpu().numpy(), v.cpu().numpy())
+    torch.cuda.synchronize()
+    ran = {k for _, k, _ in net.read_profile()}
+    net.free()
+    assert want in ran and ({"spmm_blocked_kernel", "spmm_narrow_kernel"} - {want}).isdisjoint(ran), ran
+    parity.compare(p, dense_to_csr(out))
+    parity.compare(p, got_csr)
+
+
 @pytest.mark.parametrize("case", ["from_input", "after_sparse", "integer", "empty_layer", "unstaged"])
 def test_blocked_csr_path(sd, case):
     """The CSR path's dense activations on the blocked layout: densify from the caller's CSR (positive bias

@@ -38,6 +38,26 @@ def test_noalloc_matches_workspace_entry_point(arm):
     net.free()
 
 
+def test_noalloc_blocked_layout():
+    """At 4097-16384 neurons with short lists the forward runs on the sample-blocked layout: the same two
+    calls in a row (batch 300, then 256) on the fixed array, bit for bit against the workspace entry point."""
+    import torch
+
+    import paper_1708_02937_amd as sd
+
+    p = tiny_random(8, 4500, 2, 300, w_density=0.006, dense_input=True, y_density=0.5, bias_lo=-0.2, bias_hi=0.2)
+    net = sd.net_from_problem(p)
+    for batch in (300, 256):
+        y = torch.from_numpy(np.ascontiguousarray(p.y0_dense[:batch])).cuda()
+        want = net.forward_dense(y).cpu().numpy()
+        got = torch.full_like(y, float("nan"))
+        _say("noalloc blocked", batch)
+        sd.sdnn_forward_dense_noalloc(net.handle, 0, p.L, batch, y, got, sd.SDNN_ARM_SPARSE)
+        torch.cuda.synchronize()
+        assert got.cpu().numpy().tobytes() == want.tobytes()
+    net.free()
+
+
 def test_noalloc_layer_range_and_limits():
     import torch
 
