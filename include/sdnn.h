@@ -281,7 +281,7 @@ enum {
     SDNN_KERNEL_DENSIFY = 7,    /* sparse rows -> dense neuron-major activations (sdnn_forward_csr) */
     SDNN_KERNEL_PACK = 8,       /* dense activations -> CSR result (sdnn_forward_csr) */
     SDNN_KERNEL_COMPACT = 9,    /* sparse rows -> CSR result (sdnn_forward_csr) */
-    SDNN_KERNEL_BLOCKED = 10,   /* dense-Y CSR product on the sample-blocked layout of very wide layers */
+    SDNN_KERNEL_BLOCKED = 10,   /* dense-Y CSR product on the sample-blocked layout (wide layers, short lists) */
     SDNN_KERNEL_DENSE_GEMM32 = 11 /* dense-W arm on the fp32 matrix cores */
 };
 
