@@ -269,10 +269,25 @@ __global__ __launch_bounds__(kBWaves * 64) __attribute__((amdgpu_waves_per_eu(SD
         if (nzrows) {
             // a sparse input: entries whose input row is zero in this chunk are marked (bit 31 of the index;
             // n <= 2^24) and read nothing below
+            // Eight entries per thread at a time, their map words loaded together (one round trip per eight
+            // entries rather than per entry: the map is read at the start of every workgroup)
             const uint32_t *nzc = nzrows + c * nz_words;
-            for (int k = threadIdx.x; k < rg.cnt; k += kBWaves * 64) {
-                const int32_t i = ent[k].idx;
-                if (!((nzc[i >> 5] >> (i & 31)) & 1u)) ent[k].idx = (int32_t)((uint32_t)i | 0x80000000u);
+            constexpr int kMarkU = 8;
+            for (int k0 = threadIdx.x; k0 < rg.cnt; k0 += kMarkU * kBWaves * 64) {
+                int32_t iv[kMarkU];
+                uint32_t wv[kMarkU];
+#pragma unroll
+                for (int u = 0; u < kMarkU; ++u) {
+                    const int k = k0 + u * kBWaves * 64;
+                    iv[u] = k < rg.cnt ? ent[k].idx : 0;
+                }
+#pragma unroll
+                for (int u = 0; u < kMarkU; ++u) wv[u] = nzc[iv[u] >> 5];
+#pragma unroll
+                for (int u = 0; u < kMarkU; ++u) {
+                    const int k = k0 + u * kBWaves * 64;
+                    if (k < rg.cnt && !((wv[u] >> (iv[u] & 31)) & 1u)) ent[k].idx = (int32_t)((uint32_t)iv[u] | 0x80000000u);
+                }
             }
             __syncthreads();
         }
