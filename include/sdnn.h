@@ -96,7 +96,9 @@ typedef struct sdnn_net_s *sdnn_net;
  * the dense copies wanted.  The arena holds every derived copy the library keeps: per layer the packed
  * fan-out rows, the fan-in (transposed) lists, and, as n and the capacity call for them, the tile masks and
  * fp64 weight slots of near-dense layers, the window offsets of wide sparse-activation layers, the schedule
- * of the very wide product and the dense copies; plus the set-up scratch and the per-forward flags.
+ * and staged lists of the sample-blocked product (layers wider than 16384 neurons, and from 4097 on layers
+ * averaging at most 48 entries per neuron) and the dense copies; plus the set-up scratch and the per-forward
+ * flags.
  * Errors: NULL_POINTER, INVALID_VALUE (n, L, a capacity outside [0, 2^31-1], unknown flags).
  */
 sdnn_status sdnn_net_arena_size(int64_t n, int32_t L, const int64_t *nnz_per_layer, int32_t dense_flags,

@@ -74,7 +74,7 @@ struct Layer {
     uint16_t *tile_mask = nullptr;  // which rows of each 16-row input tile each fan-in list holds (high fan-in only)
     double *slots = nullptr;        // fp64 weight of every (input, output) pair, tile-major (high fan-in, n^2 fits)
     int32_t *w_seg = nullptr;     // where each fan-out row crosses each accumulator window (wide layers only)
-    sdnn::BlockedSched *sched = nullptr;  // schedule of the blocked product (very wide layers only)
+    sdnn::BlockedSched *sched = nullptr;  // schedule of the blocked product (wide layers, short lists)
     Edge *stage = nullptr;                 // its lists in schedule order, one region per workgroup
     sdnn::BlockedRegion *regions = nullptr;  // the regions (null when one exceeds the product's LDS capacity)
     double *dense_wt = nullptr;  // n x n, W_k k-major in fp64 (zeros explicit), for the fp64 dense arm
@@ -90,7 +90,7 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // entry capacity of every layer and which dense copies are wanted.  Per layer, at fixed offsets: the packed
 // fan-out rows, the fan-in (W_k^T) pointers and lists (plus a zero guard entry), and the optional structures
 // whose need follows from n and the capacity (tile masks and fp64 weight slots for dense-ish layers, window
-// offsets for the SpGEMM of wide layers, the blocked product's schedule for very wide layers, the dense
+// offsets for the SpGEMM of wide layers, the blocked product's schedule and staged lists, the dense
 // copies).  Shared: the set-up scratch (counts, scan, radix-sort buffers, sized for the largest layer) and
 // the small per-forward flags and counters.
 constexpr size_t kAbsent = ~size_t(0);
@@ -631,7 +631,7 @@ static sdnn_status forward_dense_impl(sdnn_net net, int32_t k0, int32_t k1, int6
     double *partial = (double *)((char *)ws + 2 * act_bytes(n, batch));
     int pr = -1;
     if (arm == SDNN_ARM_SPARSE && use_blocked(net, k0, k1, batch)) {
-        // very wide layers: the sample-blocked layout (each buffer holds n x ld >= n x round32(batch) floats)
+        // the sample-blocked layout (each buffer holds n x ld >= n x round32(batch) floats)
         SDNN_HIP(prof_begin(net, -1, sdnn::kKernTranspose, &pr));
         SDNN_HIP(sdnn::launch_to_blocked(n, batch, n, Y_in, buf[0], s));
         SDNN_HIP(prof_end(net, pr));
@@ -783,7 +783,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     int last = 0, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
     bool packed = false;  // the CSR is already in buffer outb
     if (kd < k1 && use_blocked(net, kd, k1, batch)) {
-        // very wide layers: dense activations in the sample-blocked layout, packed straight into CSR at the end
+        // dense activations in the sample-blocked layout, packed straight into CSR at the end
         const bool from_user = kd == k0;
         const int db = from_user ? 0 : cur;  // the input rows (if any) sit in buffer cur ^ 1
         float *dense[2] = {reinterpret_cast<float *>(w.col[db]), w.val[db]};

@@ -1,5 +1,6 @@
-// Dense-Y layer product for very wide layers, on a sample-blocked activation layout (Sec. III batched
-// inference equation; Sec. IV loop body: the +.x product with the bias and ReLU fused into its epilogue).
+// Dense-Y layer product for wide layers (and narrower ones with short lists), on a sample-blocked activation
+// layout (Sec. III batched inference equation; Sec. IV loop body: the +.x product with the bias and ReLU fused
+// into its epilogue).
 //
 // Layout.  The batch is cut into chunks of kBW = 32 samples; chunk c holds, for every neuron j, the 32
 // values of samples 32c .. 32c + 31 in one 128-byte row: element (sample r, neuron i) sits at float

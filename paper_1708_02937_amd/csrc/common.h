@@ -26,7 +26,7 @@ enum KernelKind : int {
     kKernDensify = 7,     // sparse rows -> dense neuron-major activations
     kKernPack = 8,        // dense activations -> CSR result
     kKernCompact = 9,     // sparse slot rows -> CSR result
-    kKernBlocked = 10,    // dense-Y product on the sample-blocked layout (very wide layers)
+    kKernBlocked = 10,    // dense-Y product on the sample-blocked layout
     kKernDenseGemm32 = 11 // dense-W arm on the fp32 matrix cores
 };
 
@@ -135,7 +135,7 @@ hipError_t launch_compact_rows(int64_t n, int64_t batch, const int32_t *cnt, con
                                const int32_t *in_col, const float *in_val, int32_t *out_col, float *out_val,
                                hipStream_t s);
 
-// blocked.hip: the sample-blocked activation layout of very wide layers (chunks of 32 samples, each chunk an
+// blocked.hip: the sample-blocked activation layout of wide layers (chunks of 32 samples, each chunk an
 // n x 32 block: element (r, i) at ((r / 32) * n + i) * 32 + r % 32) and its product.
 int64_t blocked_chunks(int64_t batch);
 size_t blocked_elems(int64_t n, int64_t batch);   // floats of one blocked activation buffer

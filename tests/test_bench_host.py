@@ -105,6 +105,14 @@ def test_summarize_pmc_scales_by_the_copy_probe(tmp_path):
     assert "    cmd one" in out.read_text()
 
 
+def test_source_hash_ignores_comments_only():
+    """Counters stay current across comment edits and go stale on a change of code."""
+    a = "int x = 1; // one\n/* a block\n   comment */ int y;\n"
+    b = "int x = 1;   // another comment\nint y;"
+    assert bench._code_only(a) == bench._code_only(b) == "int x = 1; int y;"
+    assert bench._code_only(a) != bench._code_only("int x = 2; int y;")
+
+
 def test_kernel_split_and_roofline_from_profile_records():
     """The dominant kernel's roofline and HBM fields from profiling-log records: algorithmic bytes per launch
     (averaged over the launches' layers) divided by the average launch time."""
