@@ -310,10 +310,11 @@ def test_narrow_chunk_gather(sd, seed, n, batch, lengths, bias_mode):
     (93, 17003, 257, [120, 0, 5, 17, 31, 32, 33], 0), (94, 24576, 512, [24, 24, 24, 24, 24, 24, 24, 25], 1),
     (95, 16900, 288, [100, 90, 110, 64], 0), (96, 18000, 256, [95, 0, 120, 101], 1),
     (97, 4500, 300, [2, 30, 31, 33, 0, 64], 0), (98, 16384, 512, [32, 25, 40, 32], 1),
-    (99, 8192, 256, [0, 1, 15, 16, 17, 40, 100], 0)])
+    (99, 8192, 256, [0, 1, 15, 16, 17, 40, 100], 0), (100, 5000, 257, [3, 0, 17, 33, 64], 1)])
 def test_blocked_product(sd, seed, n, batch, lengths, bias_mode):
     """Layers wider than 16384, or from 4097 to 16384 neurons with short lists (at most 48 entries per neuron
-    on average: cases 97-99, whose 2 MiB or smaller chunks go whole to one XCD each, 10, 16 and 8 chunks),
+    on average: cases 97-100, whose 2 MiB or smaller chunks go whole to one XCD each, 10, 16, 8 and 9 chunks,
+    the last of one sample),
     with batches of 256 or more take the product on the sample-blocked layout (chunks of 32 samples, eight
     neurons per wave walking their lists in step): ragged n, a partial last chunk, empty lists and list
     lengths from 0 to 120 side by side in one wave, both bias readings, every row compared.  Each workgroup stages its 64 neurons' lists in LDS while they fit (up to about 3968
