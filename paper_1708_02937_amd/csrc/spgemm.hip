@@ -266,13 +266,16 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, hl = lane & 31;
+    // this instance's list was filled by the planning pass of the layer; chunks of it are taken in turn.  An
+    // empty list (every later layer of a net whose activations have died out) ends the workgroup before it
+    // clears its accumulator (the same count in every workgroup)
+    const int64_t count = (int64_t)stats[kResident ? kStatResident : kStatLarge];
+    if (count == 0) return;
     // the accumulator covers whole rounds (the positions of a partial round's columns spread over the round)
     const int width0 = (int)(n < kTile ? (n + kRoundCols - 1) / kRoundCols * kRoundCols : kTile);
     for (int t = tid; t < width0; t += kThreads) acc[t] = 0.0;
     for (int t = tid; t < kBitWords; t += kThreads) bits[t] = 0u;
     if (tid == 0) any = 0;
-    // this instance's list was filled by the planning pass of the layer; chunks of it are taken in turn
-    const int64_t count = (int64_t)stats[kResident ? kStatResident : kStatLarge];
     int64_t chunk = count / ((int64_t)gridDim.x * 16);
     chunk = chunk < 1 ? 1 : (chunk > 64 ? 64 : chunk);
     const unsigned long long nchunks = (unsigned long long)((count + chunk - 1) / chunk);
