@@ -67,6 +67,7 @@ struct Layer {
     const float *bias = nullptr;
     bool bias_nonpos = true;
     int64_t pos_bias = 0;      // neurons with b_j > 0
+    double zero_below = -INFINITY;  // every b_j <= 0: -max_j b_j (a sum at most this is zero after h), else -inf
     int32_t max_fanout = 0;    // longest fan-out row of W_k
     Edge *w_pack = nullptr;    // fan-out entries packed as (column, weight)
     int64_t *fan_ptr = nullptr;  // fan-in CSR (W_k^T)
@@ -450,10 +451,10 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     SDNN_ON_DEVICE(net);
 
     // 1. validate on the device
-    SDNN_HIP(hipMemsetAsync(net->d_flags, 0, 2 * sizeof(uint32_t), s));
+    SDNN_HIP(hipMemsetAsync(net->d_flags, 0, 3 * sizeof(uint32_t), s));
     SDNN_HIP(sdnn::launch_validate_layer(n, nnz, row_ptr, col_idx, val, bias, net->d_flags, s));
-    uint32_t fl[2] = {0, 0};
-    SDNN_HIP(hipMemcpyAsync(fl, net->d_flags, 2 * sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    uint32_t fl[3] = {0, 0, 0};
+    SDNN_HIP(hipMemcpyAsync(fl, net->d_flags, 3 * sizeof(uint32_t), hipMemcpyDeviceToHost, s));
     SDNN_HIP(hipStreamSynchronize(s));
     const uint32_t flags = fl[0];
     if (flags & 1u)
@@ -476,6 +477,14 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     nl.bias = bias;
     nl.bias_nonpos = (flags & 4u) == 0;
     nl.pos_bias = (int64_t)fl[1];
+    {
+        // with every b_j <= 0, an accumulated sum at most -max_j b_j gives h(sum + b_j) = 0 for every j
+        const uint32_t key = fl[2];
+        const uint32_t u = (key & 0x80000000u) ? (key & 0x7fffffffu) : ~key;
+        float bmax;
+        std::memcpy(&bmax, &u, sizeof(bmax));
+        nl.zero_below = nl.bias_nonpos ? -(double)bmax : -INFINITY;
+    }
     nl.w_pack = at<Edge>(base, lp.w_pack);
     nl.fan_ptr = at<int64_t>(base, lp.fan_ptr);
     nl.fan = at<Edge>(base, lp.fan);
@@ -771,7 +780,7 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         SDNN_HIP(prof_begin(net, k, sdnn::kKernSpgemm, &pr));
         SDNN_HIP(sdnn::launch_spgemm_layer(n, batch, first ? y_row_ptr : nullptr, first ? nullptr : w.cnt[cur ^ 1],
                                            first ? y_col : w.col[cur ^ 1], first ? y_val : w.val[cur ^ 1], l.row_ptr,
-                                           l.w_seg, l.w_pack, l.nnz, l.max_fanout, l.bias, l.bias_nonpos ? 1 : 0,
+                                           l.w_seg, l.w_pack, l.nnz, l.max_fanout, l.bias, l.bias_nonpos ? 1 : 0, l.zero_below,
                                            net->bias_pattern, net->ymax, w.cnt[cur], w.col[cur], w.val[cur], w.lists,
                                            net->d_stats + sdnn::kSpgemmStats * (k - k0), net->d_flags, net->num_cu, s));
         SDNN_HIP(prof_end(net, pr));

@@ -18,7 +18,9 @@
 // per-thread survivor counts and a scan of the wave totals.  It zeroes what it reads, so the
 // accumulator needs no separate clearing.  When every b_j <= 0 only touched columns can survive: for
 // samples with few products the scatter also marks a bitmap and the epilogue walks only marked columns;
-// windows that received no product are skipped.  Rows go to fixed slots of the output buffer (row r
+// windows that received no product are skipped.  Then also a sum z <= -max_j b_j is zero after h for every
+// column, so the bias of such a column (in practice nearly all of them once the bias is negative) is never
+// read.  Rows go to fixed slots of the output buffer (row r
 // starts at r * n, its length goes to cnt[r]), so the next layer reads them without a global scan; only
 // the final layer is packed into contiguous CSR.
 #include <atomic>
@@ -251,8 +253,8 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
     int64_t n, int64_t batch, int nwin, const int64_t *__restrict__ in_row_ptr,
     const int32_t *__restrict__ in_cnt, const int32_t *__restrict__ in_col, const float *__restrict__ in_val,
     const int64_t *__restrict__ w_ptr, const int32_t *__restrict__ w_seg, const Edge *__restrict__ w,
-    const float *__restrict__ bias, int bias_nonpos, int pattern, int64_t sparse_limit, int lane_segments,
-    double ymax, const int32_t *__restrict__ list, unsigned long long *stats, int32_t *__restrict__ out_cnt,
+    const float *__restrict__ bias, int bias_nonpos, double zero_below, int pattern, int64_t sparse_limit,
+    int lane_segments, double ymax, const int32_t *__restrict__ list, unsigned long long *stats, int32_t *__restrict__ out_cnt,
     int32_t *__restrict__ out_col, float *__restrict__ out_val, uint32_t *err) {
     // bias_nonpos: only touched columns can be nonzero (every b_j <= 0, or pattern mode); pattern: the
     // bias applies only on the structural pattern, so the touched-column bitmap is always kept
@@ -474,7 +476,8 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                         int keep = 0;
                         for (uint32_t m = word; m; m &= m - 1) {
                             const int col = tid * 32 + __builtin_ctz(m);
-                            keep += activate(acc[acc_pos(col)] + (double)bias[c0 + col], ymax) != 0.0f;
+                            const double a = acc[acc_pos(col)];
+                            keep += a > zero_below && activate(a + (double)bias[c0 + col], ymax) != 0.0f;
                         }
                         int incl = keep;
 #pragma unroll
@@ -494,7 +497,8 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                         int64_t pos = ob + written + off + incl - keep;
                         for (uint32_t m = word; m; m &= m - 1) {
                             const int col = tid * 32 + __builtin_ctz(m);
-                            const float f = activate(acc[acc_pos(col)] + (double)bias[c0 + col], ymax);
+                            const double a = acc[acc_pos(col)];
+                            const float f = a > zero_below ? activate(a + (double)bias[c0 + col], ymax) : 0.0f;
                             acc[acc_pos(col)] = 0.0;
                             if (f != 0.0f) {
                                 out_col[pos] = (int32_t)(c0 + col);
@@ -523,7 +527,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                             const int at = rd * kRoundCols + v * kThreads + tid;  // acc_pos(t)
                             if (t < width) {
                                 const double a = acc[at];
-                                if (activate(a + (double)bias[c0 + t], ymax) != 0.0f) {
+                                if (a > zero_below && activate(a + (double)bias[c0 + t], ymax) != 0.0f) {
                                     ++keep;
                                     smask |= 1u << (4 * rd + v);
                                 } else if (__double_as_longlong(a) != 0) {
@@ -778,7 +782,7 @@ int64_t spgemm_small_len(int64_t n, int32_t max_fanout) {
 hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const int32_t *w_seg,
                                const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
-                               int pattern, double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val,
+                               double zero_below, int pattern, double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val,
                                int32_t *lists, unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s) {
     if (batch == 0) return hipSuccess;
     const int only_touched = bias_nonpos || pattern;
@@ -823,14 +827,14 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     const int64_t grid = batch < num_cu ? batch : num_cu;
     if (resident_len > 0) {
         spgemm_row_kernel<true><<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
-            n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, only_touched, pattern,
-            sparse_limit, lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
+            n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, only_touched, zero_below,
+            pattern, sparse_limit, lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     spgemm_row_kernel<false><<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
-        n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, only_touched, pattern,
-        sparse_limit, lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
+        n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, only_touched, zero_below,
+        pattern, sparse_limit, lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);
     return hipGetLastError();
 }
 

@@ -413,6 +413,45 @@ def test_long_fanin_lists(sd):
         parity.compare(p, dense_to_csr(out[rows]), rows=rows)
 
 
+@pytest.mark.parametrize("n", [3000, 20000])
+def test_spgemm_negative_bias_threshold(sd, n):
+    """Every b_j < 0 but of different sizes: an accumulated sum at most -max_j b_j is zero after h in every
+    column, so the SpGEMM epilogues read no bias for it; integer weights, inputs and biases put sums exactly
+    on both thresholds (-max_j b_j and the column's own -b_j), compared bit for bit, with samples short enough
+    for the one-wave kernel and long ones for the workgroup kernels (one accumulator window at n = 3000, two
+    at 20000, dense and bitmap epilogues)."""
+    rng = np.random.default_rng(13 + n)
+    batch = 300
+    layers = []
+    for _ in range(2):
+        ii, jj = [], []
+        for i in range(n):
+            k = int(rng.integers(4, 24))
+            ii.append(np.full(k, i))
+            jj.append(np.sort(rng.choice(n, size=k, replace=False)))
+        i = np.concatenate(ii).astype(np.int64)
+        j = np.concatenate(jj).astype(np.int32)
+        row_ptr = np.zeros(n + 1, np.int64)
+        np.add.at(row_ptr, i + 1, 1)
+        vals = rng.choice(np.array([1.0, 2.0], np.float32), size=len(j))
+        bias = -rng.choice(np.array([1.0, 2.0, 3.0, 5.0], np.float32), size=n)
+        layers.append(Layer(np.cumsum(row_ptr), j, vals, bias))
+    rows, cols = [], []
+    for r in range(batch):
+        ylen = int(rng.integers(1, 12)) if r % 3 else int(rng.integers(60, 160))
+        rows.append(np.full(ylen, r))
+        cols.append(np.sort(rng.choice(n, size=ylen, replace=False)))
+    r_all = np.concatenate(rows).astype(np.int64)
+    c_all = np.concatenate(cols).astype(np.int32)
+    y_ptr = np.zeros(batch + 1, np.int64)
+    np.add.at(y_ptr, r_all + 1, 1)
+    y_val = rng.choice(np.array([1.0, 2.0], np.float32), size=len(c_all))
+    from workloads import Problem
+    p = Problem(f"neg-bias-{n}", n, 2, batch, math.inf, layers, y0_csr=(np.cumsum(y_ptr), c_all, y_val))
+    _say("negative bias threshold", n)
+    parity.compare(p, run_csr(sd, p), exact=True)
+
+
 @pytest.mark.parametrize("seed,n,L,batch,wd,yd", [(41, 5000, 3, 300, 0.0024, 0.008), (42, 3000, 2, 257, 0.003, 0.015),
                                                   (43, 40000, 2, 64, 0.0002, 0.0012)])
 def test_small_and_large_samples_mixed(sd, seed, n, L, batch, wd, yd):
