@@ -127,9 +127,9 @@ __device__ __forceinline__ void wave_lds_sync() {
 __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
     int64_t n, int64_t batch, const int64_t *__restrict__ in_row_ptr, const int32_t *__restrict__ in_cnt,
     const int32_t *__restrict__ in_col, const float *__restrict__ in_val, const int64_t *__restrict__ w_ptr,
-    const Edge *__restrict__ w, const float *__restrict__ bias, double ymax, const int32_t *__restrict__ list,
-    unsigned long long *stats, int32_t *__restrict__ out_cnt, int32_t *__restrict__ out_col,
-    float *__restrict__ out_val, uint32_t *err) {
+    const Edge *__restrict__ w, const float *__restrict__ bias, double zero_below, double ymax,
+    const int32_t *__restrict__ list, unsigned long long *stats, int32_t *__restrict__ out_cnt,
+    int32_t *__restrict__ out_col, float *__restrict__ out_val, uint32_t *err) {
     __shared__ int32_t keys_all[kSmallWaves][kSmallCap];
     __shared__ double vals_all[kSmallWaves][kSmallCap];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -214,7 +214,7 @@ __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
                 if (e == 0 || keys[e - 1] != key) {
                     double z = 0.0;
                     for (int u = e; u < total && keys[u] == key; ++u) z += vals[u];
-                    f = activate(z + (double)bias[key], ymax);
+                    f = z > zero_below ? activate(z + (double)bias[key], ymax) : 0.0f;
                 }
             }
             const bool keep = f != 0.0f;
@@ -819,8 +819,8 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
         // enough waves to cover every CU several times; each wave strides through the small list
         const int64_t waves = (batch < (int64_t)num_cu * 16 ? batch : (int64_t)num_cu * 16);
         spgemm_small_kernel<<<(unsigned)((waves + kSmallWaves - 1) / kSmallWaves), kSmallWaves * 64, 0, s>>>(
-            n, batch, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w, bias, ymax, lists, stats, out_cnt, out_col,
-            out_val, err);
+            n, batch, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w, bias, zero_below, ymax, lists, stats, out_cnt,
+            out_col, out_val, err);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
