@@ -633,7 +633,7 @@ def summarize_pmc(kernel, tag, dirs, copy_bytes, commands, out, src_names):
         f.write("\n".join(lines) + "\n")
 
 
-def summarize_counters(dirs, title, commands, out):
+def summarize_counters(dirs, title, commands, out, longest=False):
     """Per kernel, the mean of every counter over its dispatches, from rocprofv3 --pmc runs (counter_collection
     CSVs under each of dirs; runs of the same command, merged by kernel name), with busy fractions against the
     dispatch's cycles (GRBM_GUI_ACTIVE, summed over the 8 XCDs): VALU issue (4 cycles per wave64 instruction
@@ -645,11 +645,18 @@ def summarize_counters(dirs, title, commands, out):
     agg = defaultdict(lambda: defaultdict(list))
     for d in dirs:
         for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
-            for r in csv.DictReader(open(path)):
-                k = _short_name(r["Kernel_Name"])
-                if k.startswith(("at::", "__amd")):
-                    continue
-                agg[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+            rows = [r for r in csv.DictReader(open(path)) if not _short_name(r["Kernel_Name"]).startswith(("at::", "__amd"))]
+            if longest:
+                # only each kernel's longest dispatch of this run (e.g. the one layer that does the work)
+                dur = {}
+                for r in rows:
+                    k = _short_name(r["Kernel_Name"])
+                    t = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+                    if t > dur.get(k, (-1, None))[0]:
+                        dur[k] = (t, r["Dispatch_Id"])
+                rows = [r for r in rows if dur[_short_name(r["Kernel_Name"])][1] == r["Dispatch_Id"]]
+            for r in rows:
+                agg[_short_name(r["Kernel_Name"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
     lines = [f"# rocprofv3 counters: {title}", "", "commands (from the repository root on the MI355X box):", ""]
     lines += [f"    {c}" for c in commands]
     lines += ["", "| kernel | counter | dispatches | mean per dispatch |", "|---|---|---|---|"]
@@ -705,6 +712,8 @@ def main():
     ap.add_argument("--summarize-counters", nargs=4, metavar=("DIRS", "TITLE", "COMMANDS", "OUT"),
                     help="write a profiles/ table of per-kernel counter means from rocprofv3 --pmc runs "
                          "('|'-separated directories and commands)")
+    ap.add_argument("--longest-dispatch", action="store_true",
+                    help="with --summarize-counters: only each kernel's longest dispatch of every run")
     ap.add_argument("--summarize-pmc", nargs=9,
                     metavar=("KERNEL", "WORKLOAD", "FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR",
                              "COPY_BYTES", "COMMANDS", "OUT"),
@@ -715,7 +724,7 @@ def main():
         return
     if args.summarize_counters:
         a = args.summarize_counters
-        summarize_counters(a[0].split("|"), a[1], a[2].split("|"), a[3])
+        summarize_counters(a[0].split("|"), a[1], a[2].split("|"), a[3], longest=args.longest_dispatch)
         return
     if args.summarize_pmc:
         a = args.summarize_pmc

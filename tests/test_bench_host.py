@@ -105,6 +105,22 @@ def test_summarize_pmc_scales_by_the_copy_probe(tmp_path):
     assert "    cmd one" in out.read_text()
 
 
+def test_summarize_counters_longest_dispatch(tmp_path):
+    """--longest-dispatch keeps each kernel's longest dispatch of a run and drops the others."""
+    d = tmp_path / "run"
+    d.mkdir()
+    with open(d / "x_counter_collection.csv", "w") as f:
+        f.write("Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value,Start_Timestamp,End_Timestamp\n")
+        f.write('1,"k(int)",SQ_WAVES,10,0,100\n')
+        f.write('2,"k(int)",SQ_WAVES,99,0,5000\n')
+        f.write('3,"k(int)",SQ_WAVES,20,0,200\n')
+    out = tmp_path / "s.md"
+    bench.summarize_counters([str(d)], "t", ["cmd"], str(out), longest=True)
+    assert "| k | SQ_WAVES | 1 | 99 |" in out.read_text()
+    bench.summarize_counters([str(d)], "t", ["cmd"], str(out))
+    assert "| k | SQ_WAVES | 3 | 43 |" in out.read_text()
+
+
 def test_source_hash_ignores_comments_only():
     """Counters stay current across comment edits and go stale on a change of code."""
     a = "int x = 1; // one\n/* a block\n   comment */ int y;\n"
