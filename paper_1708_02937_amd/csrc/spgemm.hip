@@ -18,9 +18,10 @@
 // per-thread survivor counts and a scan of the wave totals.  It zeroes what it reads, so the
 // accumulator needs no separate clearing.  When every b_j <= 0 only touched columns can survive: for
 // samples with few products the scatter also marks a bitmap and the epilogue walks only marked columns;
-// windows that received no product are skipped.  Then also a sum z <= -max_j b_j is zero after h for every
-// column, so the bias of such a column (in practice nearly all of them once the bias is negative) is never
-// read.  Rows go to fixed slots of the output buffer (row r
+// windows that received no product are skipped.  Then also a sum at most -max_j b_j is zero after h in every
+// column, so for the other samples the scatter's atomics return the previous sum and mark a column when an
+// addition lifts it above that bound: the epilogue reads only the marked columns (a handful per window on a
+// sparse network) and clears the window with 16-byte stores.  Rows go to fixed slots of the output buffer (row r
 // starts at r * n, its length goes to cnt[r]), so the next layer reads them without a global scan; only
 // the final layer is packed into contiguous CSR.
 #include <atomic>
@@ -245,6 +246,31 @@ static_assert(kTile % kRoundCols == 0, "whole rounds per window");
 __device__ __forceinline__ int acc_pos(int col) {
     return (col & ~(kRoundCols - 1)) | ((col & 3) * kThreads) | ((col & (kRoundCols - 1)) >> 2);
 }
+// Add product v to column col of the window.  mark_all (bitmap epilogue): mark every column a nonzero entry
+// touches.  cross (every b_j <= 0, dense samples): the sum starts at 0 <= zero_below, so a column whose final
+// sum exceeds zero_below was pushed across it by some addition; that addition reads the previous sum back and
+// marks the column, and only marked columns can survive.  The thread's add rounds like the LDS unit's, so no
+// crossing goes unmarked; a column that crosses and falls back is marked and dropped by the epilogue.
+template <int K>
+__device__ __forceinline__ void add_products(double *acc, uint32_t *bits, const int (&col)[K], const double (&v)[K],
+                                             const bool (&ok)[K], bool mark_all, bool cross, double zero_below) {
+    if (cross) {
+        double old[K];
+#pragma unroll
+        for (int u = 0; u < K; ++u) old[u] = ok[u] ? atomicAdd(&acc[acc_pos(col[u])], v[u]) : 0.0;
+#pragma unroll
+        for (int u = 0; u < K; ++u)
+            if (ok[u] && old[u] <= zero_below && old[u] + v[u] > zero_below)
+                atomicOr(&bits[col[u] >> 5], 1u << (col[u] & 31));
+    } else {
+#pragma unroll
+        for (int u = 0; u < K; ++u)
+            if (ok[u]) {
+                atomicAdd(&acc[acc_pos(col[u])], v[u]);
+                if (mark_all) atomicOr(&bits[col[u] >> 5], 1u << (col[u] & 31));
+            }
+    }
+}
 constexpr int kRes = 1;                           // stored entries a thread keeps in registers (resident mode)
 constexpr int kResLoads = 4;                      // weight loads in flight per resident entry
 
@@ -258,7 +284,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
     int32_t *__restrict__ out_col, float *__restrict__ out_val, uint32_t *err) {
     // bias_nonpos: only touched columns can be nonzero (every b_j <= 0, or pattern mode); pattern: the
     // bias applies only on the structural pattern, so the touched-column bitmap is always kept
-    extern __shared__ double acc[];
+    extern __shared__ __align__(16) double acc[];
     __shared__ RowRef refs[kThreads];
     __shared__ uint32_t bits[kBitWords];
     __shared__ int wave_tot[kWaves];
@@ -295,6 +321,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
             const RowIn ri = input_row(r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err);
             const int64_t yb = ri.yb, ylen = ri.ylen;
             const bool sparse = pattern || (bias_nonpos && ylen <= sparse_limit);
+            const bool cross = !sparse && zero_below >= 0.0;
             // resident instance: up to kRes stored entries per thread, kept in registers across the
             // windows; the thread's fan-out segment for window w is [s_lo, s_hi), and the next window's
             // segment starts where this one ends, so each window costs one more offset load, issued a
@@ -343,14 +370,17 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                         }
                         int64_t e = lo;
                         if (have_pre) {
+                            int col[kResLoads];
+                            double v[kResLoads];
+                            bool ok[kResLoads];
 #pragma unroll
-                            for (int u = 0; u < kResLoads; ++u)
-                                if (e + u < hi) {
-                                    const int col = pre[k][u].idx - (int)c0;
-                                    atomicAdd(&acc[acc_pos(col)], my_y[k] * (double)pre[k][u].w);
-                                    if (sparse && my_y[k] != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
-                                    mine_any = true;
-                                }
+                            for (int u = 0; u < kResLoads; ++u) {
+                                ok[u] = e + u < hi;
+                                col[u] = pre[k][u].idx - (int)c0;
+                                v[u] = my_y[k] * (double)pre[k][u].w;
+                                mine_any |= ok[u];
+                            }
+                            add_products(acc, bits, col, v, ok, sparse && my_y[k] != 0.0, cross, zero_below);
                             e += kResLoads;
                         }
                         for (; e < hi; e += kResLoads) {
@@ -358,14 +388,17 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
 #pragma unroll
                             for (int u = 0; u < kResLoads; ++u)
                                 if (e + u < hi) ed[u] = w[e + u];
+                            int col[kResLoads];
+                            double v[kResLoads];
+                            bool ok[kResLoads];
 #pragma unroll
-                            for (int u = 0; u < kResLoads; ++u)
-                                if (e + u < hi) {
-                                    const int col = ed[u].idx - (int)c0;
-                                    atomicAdd(&acc[acc_pos(col)], my_y[k] * (double)ed[u].w);
-                                    if (sparse && my_y[k] != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
-                                    mine_any = true;
-                                }
+                            for (int u = 0; u < kResLoads; ++u) {
+                                ok[u] = e + u < hi;
+                                col[u] = ed[u].idx - (int)c0;
+                                v[u] = my_y[k] * (double)ed[u].w;
+                                mine_any |= ok[u];
+                            }
+                            add_products(acc, bits, col, v, ok, sparse && my_y[k] != 0.0, cross, zero_below);
                         }
                         // the next window's segment is [s_lo, s_hi) now: start its loads
                         have_pre = win + 1 < nwin;
@@ -418,15 +451,17 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                                     ed[u].w = 0.0f;
                                     if (cc + u < ref.len) ed[u] = w[ref.start + cc + u];
                                 }
+                                int col[8];
+                                double v[8];
+                                bool ok[8];
 #pragma unroll
                                 for (int u = 0; u < 8; ++u) {
-                                    if (ed[u].idx >= c0 && ed[u].idx < c1) {
-                                        const int col = ed[u].idx - (int)c0;
-                                        atomicAdd(&acc[acc_pos(col)], ref.y * (double)ed[u].w);
-                                        if (sparse && ref.y != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
-                                        mine_any = true;
-                                    }
+                                    ok[u] = ed[u].idx >= c0 && ed[u].idx < c1;
+                                    col[u] = ed[u].idx - (int)c0;
+                                    v[u] = ref.y * (double)ed[u].w;
+                                    mine_any |= ok[u];
                                 }
+                                add_products(acc, bits, col, v, ok, sparse && ref.y != 0.0, cross, zero_below);
                             }
                             continue;
                         }
@@ -452,14 +487,25 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                                     ed[p].w = 0.0f;
                                     if (cc + hl < rr[p].len) ed[p] = w[rr[p].start + cc + hl];
                                 }
+                                int col[4];
+                                double v[4];
+                                bool ok[4];
 #pragma unroll
                                 for (int p = 0; p < 4; ++p) {
-                                    if (ed[p].idx >= c0 && ed[p].idx < c1) {
-                                        const int col = ed[p].idx - (int)c0;
-                                        atomicAdd(&acc[acc_pos(col)], rr[p].y * (double)ed[p].w);
-                                        if (sparse && rr[p].y != 0.0) atomicOr(&bits[col >> 5], 1u << (col & 31));
-                                        mine_any = true;
-                                    }
+                                    ok[p] = ed[p].idx >= c0 && ed[p].idx < c1;
+                                    col[p] = ed[p].idx - (int)c0;
+                                    v[p] = rr[p].y * (double)ed[p].w;
+                                    mine_any |= ok[p];
+                                }
+                                if (cross) {
+                                    add_products(acc, bits, col, v, ok, false, true, zero_below);
+                                } else {
+#pragma unroll
+                                    for (int p = 0; p < 4; ++p)
+                                        if (ok[p]) {
+                                            atomicAdd(&acc[acc_pos(col[p])], v[p]);
+                                            if (sparse && rr[p].y != 0.0) atomicOr(&bits[col[p] >> 5], 1u << (col[p] & 31));
+                                        }
                                 }
                             }
                         }
@@ -468,9 +514,10 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                 if (mine_any) any = 1;
                 __syncthreads();
                 const bool touched = any != 0;
-                if (sparse) {
+                if (sparse || cross) {
                     if (touched) {
-                        // epilogue over marked columns: count survivors per bitmap word, scan, write
+                        // epilogue over marked columns (every touched column, or in cross mode those whose
+                        // sum crossed zero_below): count survivors per bitmap word, scan, write
                         const int nw = (width + 31) >> 5;
                         uint32_t word = tid < nw ? bits[tid] : 0u;
                         int keep = 0;
@@ -499,7 +546,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                             const int col = tid * 32 + __builtin_ctz(m);
                             const double a = acc[acc_pos(col)];
                             const float f = a > zero_below ? activate(a + (double)bias[c0 + col], ymax) : 0.0f;
-                            acc[acc_pos(col)] = 0.0;
+                            if (!cross) acc[acc_pos(col)] = 0.0;
                             if (f != 0.0f) {
                                 out_col[pos] = (int32_t)(c0 + col);
                                 out_val[pos] = f;
@@ -576,6 +623,11 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                 }
                 __syncthreads();
                 if (tid == 0) any = 0;
+                if (cross && touched) {
+                    // cross mode leaves the unmarked sums in place: clear the window with 16-byte stores
+                    double2 *acc2 = reinterpret_cast<double2 *>(acc);
+                    for (int t = tid; t < width0 / 2; t += kThreads) acc2[t] = make_double2(0.0, 0.0);
+                }
                 __syncthreads();
             }
             if (tid == 0) {

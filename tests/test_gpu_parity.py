@@ -452,6 +452,49 @@ def test_spgemm_negative_bias_threshold(sd, n):
     parity.compare(p, run_csr(sd, p), exact=True)
 
 
+@pytest.mark.parametrize("n,fan,lens,biases", [(3000, (4, 24), (150, 300), (0.0, -1.0, -2.0)),
+                                               (40000, (4, 24), (450, 1000), (-1.0, -2.0, -3.0)),
+                                               (3000, (30, 50), (60, 300), (-1.0, -2.0))])
+def test_spgemm_crossing_marks(sd, n, fan, lens, biases):
+    """Every b_j <= 0 and samples too long for the bitmap epilogue: the scatter marks the columns whose sum
+    rises above -max_j b_j and the epilogue reads only those.  Weights of both signs make sums cross the
+    threshold and fall back in any order of the additions; integer values keep every sum exact, so the
+    output is compared bit for bit.  Samples longer than the bitmap epilogue takes (one in eight beyond 1024
+    entries) use the register-resident and the general workgroup instances (lane-walked segments with short
+    fan-out rows, half-wave segments with long ones), over one and three accumulator windows, with the input
+    sparse enough to stay on the SpGEMM; a threshold of 0 comes from b_j = 0."""
+    rng = np.random.default_rng(17 + n + fan[0])
+    batch = 160
+    layers = []
+    for _ in range(2):
+        ii, jj = [], []
+        for i in range(n):
+            k = int(rng.integers(fan[0], fan[1]))
+            ii.append(np.full(k, i))
+            jj.append(np.sort(rng.choice(n, size=k, replace=False)))
+        i = np.concatenate(ii).astype(np.int64)
+        j = np.concatenate(jj).astype(np.int32)
+        row_ptr = np.zeros(n + 1, np.int64)
+        np.add.at(row_ptr, i + 1, 1)
+        vals = rng.choice(np.array([1.0, 2.0, -1.0, -2.0, -3.0], np.float32), size=len(j))
+        bias = rng.choice(np.array(biases, np.float32), size=n)
+        layers.append(Layer(np.cumsum(row_ptr), j, vals, bias))
+    rows, cols = [], []
+    for r in range(batch):
+        ylen = int(rng.integers(*lens)) if r % 8 else int(rng.integers(1025, 1100))
+        rows.append(np.full(ylen, r))
+        cols.append(np.sort(rng.choice(n, size=ylen, replace=False)))
+    r_all = np.concatenate(rows).astype(np.int64)
+    c_all = np.concatenate(cols).astype(np.int32)
+    y_ptr = np.zeros(batch + 1, np.int64)
+    np.add.at(y_ptr, r_all + 1, 1)
+    y_val = rng.choice(np.array([1.0, 2.0], np.float32), size=len(c_all))
+    from workloads import Problem
+    p = Problem(f"crossing-{n}-{fan[0]}", n, 2, batch, math.inf, layers, y0_csr=(np.cumsum(y_ptr), c_all, y_val))
+    _say("crossing marks", n, fan, biases)
+    parity.compare(p, run_csr(sd, p), exact=True)
+
+
 @pytest.mark.parametrize("seed,n,L,batch,wd,yd", [(41, 5000, 3, 300, 0.0024, 0.008), (42, 3000, 2, 257, 0.003, 0.015),
                                                   (43, 40000, 2, 64, 0.0002, 0.0012)])
 def test_small_and_large_samples_mixed(sd, seed, n, L, batch, wd, yd):
