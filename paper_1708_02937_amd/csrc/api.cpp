@@ -119,7 +119,8 @@ size_t take(size_t &off, size_t bytes) {
 LayerPlan plan_layer(int64_t n, int64_t cap, int32_t dense_flags) {
     LayerPlan lp;
     size_t off = 0;
-    lp.w_pack = take(off, (size_t)std::max<int64_t>(cap, 1) * sizeof(Edge));
+    // one entry more than the layer's: 16-byte loads of entry pairs may read one entry past a row's end
+    lp.w_pack = take(off, (size_t)(std::max<int64_t>(cap, 1) + 1) * sizeof(Edge));
     lp.fan_ptr = take(off, (size_t)(n + 1) * sizeof(int64_t));
     lp.fan = take(off, (size_t)(cap + 1) * sizeof(Edge));
     if (sdnn::spmm_wants_tiles(n, cap)) lp.tile_mask = take(off, sdnn::spmm_tile_mask_elems(n) * sizeof(uint16_t));

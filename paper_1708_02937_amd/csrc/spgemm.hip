@@ -11,7 +11,9 @@
 // empty sample stays empty (h(b_j) = 0) and costs one store; a sample whose products fit a wave's share of
 // LDS (at most 1024) goes to the small-sample kernel, one wavefront per sample; every other sample goes to
 // the workgroup kernel below, where one persistent workgroup per CU takes chunks of the list from a device
-// counter (every workgroup leaves once the counter passes the last chunk).
+// counter (every workgroup leaves once the counter passes the last chunk).  Samples of at most 1024 entries
+// keep them in registers (one per thread); with three or four windows and only marked columns to read, they
+// go to a pipelined instance that loads every window's data a window ahead (described at that kernel).
 //
 // The epilogue visits the window in column order: z = acc + b_j, h(z), one rounding to fp32, and the
 // entries that are not zero (Sec. II.E: zeros are not stored) are compacted with a wave prefix sum of
@@ -273,6 +275,7 @@ __device__ __forceinline__ void add_products(double *acc, uint32_t *bits, const 
 }
 constexpr int kRes = 1;                           // stored entries a thread keeps in registers (resident mode)
 constexpr int kResLoads = 4;                      // weight loads in flight per resident entry
+constexpr int kPre = 8;                           // entries of each window's segment loaded a window ahead
 
 template <bool kResident>
 __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
@@ -351,10 +354,20 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
             }
             const int64_t ob = r * n;
             int64_t written = 0;
-            // resident instance: the first kResLoads entries of the next window's segment, loaded before this
-            // window's epilogue so that their latency is covered by it
-            Edge pre[kRes][kResLoads];
-            bool have_pre = false;
+            // resident instance: the first kPre entries of each window's segment are loaded a window ahead
+            // (the first window's right after the set-up), so that the previous window's epilogue covers
+            // their latency; longer segments load the rest kResLoads at a time
+            Edge pre[kRes][kPre];
+            if constexpr (kResident) {
+#pragma unroll
+                for (int k = 0; k < kRes; ++k)
+#pragma unroll
+                    for (int u = 0; u < kPre; ++u) {
+                        pre[k][u].idx = 0;
+                        pre[k][u].w = 0.0f;
+                        if (s_lo[k] + u < s_hi[k]) pre[k][u] = w[s_lo[k] + u];
+                    }
+            }
             for (int win = 0; win < nwin; ++win) {
                 const int64_t c0 = (int64_t)win * kTile;
                 const int64_t c1 = (c0 + kTile < n) ? c0 + kTile : n;
@@ -369,19 +382,19 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                             s_hi[k] = my_rb[k] + w_seg[(int64_t)my_i[k] * (nwin + 1) + win + 2];
                         }
                         int64_t e = lo;
-                        if (have_pre) {
-                            int col[kResLoads];
-                            double v[kResLoads];
-                            bool ok[kResLoads];
+                        {
+                            int col[kPre];
+                            double v[kPre];
+                            bool ok[kPre];
 #pragma unroll
-                            for (int u = 0; u < kResLoads; ++u) {
+                            for (int u = 0; u < kPre; ++u) {
                                 ok[u] = e + u < hi;
                                 col[u] = pre[k][u].idx - (int)c0;
                                 v[u] = my_y[k] * (double)pre[k][u].w;
                                 mine_any |= ok[u];
                             }
                             add_products(acc, bits, col, v, ok, sparse && my_y[k] != 0.0, cross, zero_below);
-                            e += kResLoads;
+                            e += kPre;
                         }
                         for (; e < hi; e += kResLoads) {
                             Edge ed[kResLoads];
@@ -401,10 +414,9 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
                             add_products(acc, bits, col, v, ok, sparse && my_y[k] != 0.0, cross, zero_below);
                         }
                         // the next window's segment is [s_lo, s_hi) now: start its loads
-                        have_pre = win + 1 < nwin;
-                        if (have_pre) {
+                        if (win + 1 < nwin) {
 #pragma unroll
-                            for (int u = 0; u < kResLoads; ++u)
+                            for (int u = 0; u < kPre; ++u)
                                 if (s_lo[k] + u < s_hi[k]) pre[k][u] = w[s_lo[k] + u];
                         }
                     }
@@ -639,6 +651,285 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
     }
 }
 
+// Pipelined register-resident instance, for layers whose windows only marked columns leave (every b_j <= 0,
+// so the scatter marks threshold crossings, or the bias on the structural pattern, so it marks every touched
+// column) and three or four accumulator windows (per-row window offsets).  Per sample and window the work is
+// short (a few products per thread), so what bounds it is the chain of dependent loads: the sample's entry,
+// its fan-out row's window offsets, the segment itself, each a round trip to memory.  Here every load is
+// issued at least one window before its value is read.  Workgroup g takes the samples g, g + G, g + 2G, ...
+// of the list (G workgroups).  Every window issues the same loads in the same order: the entries of its own
+// segment beyond the buffered ones; the first kPipePre entries of the next window's segment (in the last
+// window, of the next sample's first window) into the other of two register buffers; the fan-out row starts
+// and window offsets of the next sample's entries (read a window earlier); the next sample's entries.  The
+// last two are real in one window each (the entries in the first, the rows in the second, kept from the
+// third on) and read one shared address in the others, so the instruction stream, and with it the count of
+// loads issued after each one, is the same in every window (each wait is for its own load only) while the
+// memory requests stay those the sample needs.  Lanes with nothing to load read w[0] and ignore it (the
+// layer has at least one weight).
+constexpr int kPipeWin = 4;   // accumulator windows (n <= 4 * 16384)
+constexpr int kPipePre = 8;   // entries of a window's segment loaded a window ahead
+constexpr int kPipeRem = 4;   // entries beyond those, loaded at the start of their window
+
+// Two consecutive fan-out entries, read with one 16-byte load (8-byte aligned; the packed array has one
+// entry of padding, so the pair that starts at a row's last entry stays inside it).
+struct __attribute__((aligned(8))) EdgePair {
+    Edge e[2];
+};
+
+// One stored entry of a sample as the pipelined instance keeps it: the value, the start of the neuron's
+// fan-out row, and the offsets of the row's window segments from the current window on (shifted down one
+// place per window, so that every index is a constant).  ok = false: no entry (or an invalid one); its
+// offsets are then ignored.
+struct PipeEntry {
+    double y;
+    int64_t rb;
+    int32_t so[kPipeWin + 1];
+    bool ok;
+};
+
+__global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
+    int64_t n, int64_t batch, int nwin, const int64_t *__restrict__ in_row_ptr, const int32_t *__restrict__ in_cnt,
+    const int32_t *__restrict__ in_col, const float *__restrict__ in_val, const int64_t *__restrict__ w_ptr,
+    const int32_t *__restrict__ w_seg, const Edge *__restrict__ w, const float *__restrict__ bias, double zero_below,
+    int pattern, int64_t sparse_limit, double ymax, const int32_t *__restrict__ list, unsigned long long *stats,
+    int32_t *__restrict__ out_cnt, int32_t *__restrict__ out_col, float *__restrict__ out_val, uint32_t *err) {
+    extern __shared__ __align__(16) double acc[];
+    __shared__ uint32_t bits[kBitWords];
+    __shared__ int wave_tot[kWaves];
+    __shared__ int any;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t count = (int64_t)stats[kStatResident];
+    const int64_t grid = gridDim.x;
+    if ((int64_t)blockIdx.x >= count) return;  // uniform: no sample for this workgroup
+    const int width0 = (int)(n < kTile ? (n + kRoundCols - 1) / kRoundCols * kRoundCols : kTile);
+    for (int t = tid; t < width0; t += kThreads) acc[t] = 0.0;
+    for (int t = tid; t < kBitWords; t += kThreads) bits[t] = 0u;
+    if (tid == 0) any = 0;
+    const int32_t *res = list + 2 * batch;
+
+    // the samples' rows, 64 at a time: lane l of every wave holds sample s0 + l of this workgroup
+    int32_t ref_r = 0, ref_len = 0;
+    int64_t ref_yb = 0;
+    auto load_refs = [&](int64_t s0) {
+        const int64_t j = (int64_t)blockIdx.x + (s0 + lane) * grid;
+        ref_r = 0;
+        ref_yb = 0;
+        ref_len = 0;
+        if (j < count) {
+            ref_r = res[j];
+            const RowIn ri = input_row(ref_r, n, batch, in_row_ptr, in_cnt, in_col, in_val, err);
+            ref_yb = ri.yb;
+            ref_len = (int32_t)ri.ylen;
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // once per 64 samples: read at once
+    };
+    struct Sample {
+        int64_t r, yb, ylen;
+    };
+    auto sample_at = [&](int64_t s) {
+        const int k = (int)(s & 63);
+        Sample sm;
+        sm.r = __builtin_amdgcn_readlane(ref_r, k);
+        sm.ylen = __builtin_amdgcn_readlane(ref_len, k);
+        sm.yb = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(ref_yb >> 32), k) << 32) |
+                          (uint32_t)__builtin_amdgcn_readlane((int)ref_yb, k));
+        return sm;
+    };
+    // this thread's stored entry of a sample (the row's first entry for lanes past its end; the planning pass
+    // sends no empty sample here, and the input then has an entry 0)
+    auto entry_load = [&](const Sample &sm, int32_t &ri, float &ry, bool real) {
+        const int64_t t = real && sm.ylen > 0 ? sm.yb + (tid < sm.ylen ? tid : 0) : 0;
+        ri = in_col[t];
+        ry = in_val[t];
+    };
+    // the entry's fan-out row start and window offsets (row 0 for lanes without a valid entry)
+    auto entry_rows = [&](const Sample &sm, int32_t ri, float ry, PipeEntry &e, bool real) {
+        const bool has = tid < sm.ylen;
+        e.ok = has && ri >= 0 && ri < n;
+        if (real && has && !e.ok) atomicOr(err, 1u);
+        const int64_t i = real && e.ok ? ri : 0;
+        e.y = e.ok ? (double)ry : 0.0;
+        e.rb = w_ptr[i];
+        const int32_t *sg = w_seg + i * (nwin + 1);  // nwin + 1 = 4 or 5 offsets
+#pragma unroll
+        for (int t = 0; t < 4; ++t) e.so[t] = sg[t];
+        e.so[4] = sg[nwin == 4 ? 4 : 3];
+    };
+    // entries u < kPipePre of the segment [lo, lo + len) of the row starting at rb, in pairs (w[0], w[1]
+    // past its end)
+    auto prefetch = [&](int64_t rb, int32_t lo, int32_t len, EdgePair(&buf)[kPipePre / 2]) {
+        const Edge *row = w + rb + lo;
+#pragma unroll
+        for (int u = 0; u < kPipePre / 2; ++u)
+            buf[u] = *reinterpret_cast<const EdgePair *>(2 * u < len ? row + 2 * u : w);
+    };
+
+    int64_t s = 0;
+    load_refs(0);
+    Sample cur = sample_at(0), nxt = cur;
+    PipeEntry E, N;
+    int32_t ni = 0;
+    float ny = 0.0f;
+    entry_load(cur, ni, ny, true);
+    entry_rows(cur, ni, ny, E, true);
+    N = E;
+    PipeEntry T = E;
+    EdgePair bufA[kPipePre / 2], bufB[kPipePre / 2];
+    prefetch(E.rb, E.so[0], E.ok ? E.so[1] - E.so[0] : 0, bufA);
+    int win = 0;
+    int64_t written = 0;
+    bool has_next = false;
+
+    auto step = [&](EdgePair(&cb)[kPipePre / 2], EdgePair(&pb)[kPipePre / 2]) -> bool {
+        const int64_t c0 = (int64_t)win * kTile;
+        const int64_t c1 = (c0 + kTile < n) ? c0 + kTile : n;
+        const int width = (int)(c1 - c0);
+        const bool mark_all = pattern || cur.ylen <= sparse_limit;
+        const bool last = win + 1 == nwin;
+        if (win == 0) {
+            has_next = (int64_t)blockIdx.x + (s + 1) * grid < count;
+            if (has_next && ((s + 1) & 63) == 0) load_refs(s + 1);
+            nxt = has_next ? sample_at(s + 1) : cur;
+        }
+        const int32_t lo = E.so[0], len = E.ok ? E.so[1] - lo : 0;
+        const Edge *row = w + E.rb + lo;
+        if (win == 2) N = T;  // the next sample's rows, loaded in the second window
+        // the loads of every window, in this order (see above)
+        EdgePair rem[kPipeRem / 2];
+#pragma unroll
+        for (int u = 0; u < kPipeRem / 2; ++u)
+            rem[u] = *reinterpret_cast<const EdgePair *>(kPipePre + 2 * u < len ? row + kPipePre + 2 * u : w);
+        {
+            const bool nx = last && has_next;
+            const int64_t rb = last ? N.rb : E.rb;
+            const int32_t plo = last ? N.so[0] : E.so[1];
+            const int32_t plen = (last ? (nx && N.ok) : E.ok) ? (last ? N.so[1] : E.so[2]) - plo : 0;
+            prefetch(rb, plo, plen, pb);
+        }
+        entry_rows(nxt, ni, ny, T, win == 1);
+        entry_load(nxt, ni, ny, win == 0);
+        // the products of this window's segment (buffered ones four at a time)
+        const bool mine_any = len > 0;
+#pragma unroll
+        for (int h = 0; h < kPipePre; h += 4) {
+            int col[4];
+            double v[4];
+            bool ok[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const Edge &ed = cb[(h + u) >> 1].e[(h + u) & 1];
+                ok[u] = h + u < len;
+                col[u] = ed.idx - (int)c0;
+                v[u] = E.y * (double)ed.w;
+            }
+            add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
+        }
+        {
+            int col[kPipeRem];
+            double v[kPipeRem];
+            bool ok[kPipeRem];
+#pragma unroll
+            for (int u = 0; u < kPipeRem; ++u) {
+                const Edge &ed = rem[u >> 1].e[u & 1];
+                ok[u] = kPipePre + u < len;
+                col[u] = ed.idx - (int)c0;
+                v[u] = E.y * (double)ed.w;
+            }
+            add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
+        }
+        for (int e = kPipePre + kPipeRem; e < len; e += kPipeRem) {
+            EdgePair ep[kPipeRem / 2];
+#pragma unroll
+            for (int u = 0; u < kPipeRem / 2; ++u)
+                ep[u] = *reinterpret_cast<const EdgePair *>(e + 2 * u < len ? row + e + 2 * u : w);
+            int col[kPipeRem];
+            double v[kPipeRem];
+            bool ok[kPipeRem];
+#pragma unroll
+            for (int u = 0; u < kPipeRem; ++u) {
+                const Edge &ed = ep[u >> 1].e[u & 1];
+                ok[u] = e + u < len;
+                col[u] = ed.idx - (int)c0;
+                v[u] = E.y * (double)ed.w;
+            }
+            add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
+        }
+        if (mine_any) any = 1;
+        __syncthreads();
+        const bool touched = any != 0;
+        if (touched) {
+            // survivors among the marked columns: count per bitmap word, scan, write in column order
+            const int nw = (width + 31) >> 5;
+            const uint32_t word = tid < nw ? bits[tid] : 0u;
+            int keep = 0;
+            for (uint32_t m = word; m; m &= m - 1) {
+                const int col = tid * 32 + __builtin_ctz(m);
+                const double a = acc[acc_pos(col)];
+                keep += a > zero_below && activate(a + (double)bias[c0 + col], ymax) != 0.0f;
+            }
+            int incl = keep;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int v = __shfl_up(incl, d);
+                if (lane >= d) incl += v;
+            }
+            if (lane == 63) wave_tot[wave] = incl;
+            __syncthreads();
+            int off = 0, tot = 0;
+#pragma unroll
+            for (int u = 0; u < kWaves; ++u) {
+                const int v = wave_tot[u];
+                off += (u < wave) ? v : 0;
+                tot += v;
+            }
+            int64_t pos = cur.r * n + written + off + incl - keep;
+            for (uint32_t m = word; m; m &= m - 1) {
+                const int col = tid * 32 + __builtin_ctz(m);
+                const double a = acc[acc_pos(col)];
+                const float f = a > zero_below ? activate(a + (double)bias[c0 + col], ymax) : 0.0f;
+                if (mark_all) acc[acc_pos(col)] = 0.0;
+                if (f != 0.0f) {
+                    out_col[pos] = (int32_t)(c0 + col);
+                    out_val[pos] = f;
+                    ++pos;
+                }
+            }
+            if (tid < nw) bits[tid] = 0u;
+            written += tot;
+        }
+        __syncthreads();
+        if (tid == 0) any = 0;
+        if (!mark_all && touched) {
+            // crossing marks leave the other sums in place: clear the window with 16-byte stores
+            double2 *acc2 = reinterpret_cast<double2 *>(acc);
+            for (int t = tid; t < width0 / 2; t += kThreads) acc2[t] = make_double2(0.0, 0.0);
+        }
+        __syncthreads();
+        if (!last) {
+#pragma unroll
+            for (int t = 0; t < kPipeWin; ++t) E.so[t] = E.so[t + 1];
+            ++win;
+            return true;
+        }
+        if (tid == 0) {
+            out_cnt[cur.r] = (int32_t)written;
+            if (written) atomicAdd(&stats[kStatNnz], (unsigned long long)written);
+        }
+        if (!has_next) return false;
+        ++s;
+        cur = nxt;
+        E = N;
+        win = 0;
+        written = 0;
+        return true;
+    };
+    for (;;) {
+        if (!step(bufA, bufB)) break;
+        if (!step(bufB, bufA)) break;
+    }
+}
+
 // w_seg[i * (nwin + 1) + t] = offset, within fan-out row i, of its first column >= t * kTile.
 __global__ void window_seg_kernel(int64_t n, int nwin, const int64_t *__restrict__ w_ptr,
                                   const int32_t *__restrict__ col, int32_t *__restrict__ w_seg) {
@@ -847,7 +1138,8 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     if (ed != hipSuccess) return ed;
     const unsigned long long bit = dev >= 0 && dev < 64 ? 1ull << dev : 0ull;
     if (!bit || !(attr_devices.load(std::memory_order_acquire) & bit)) {
-        for (const void *f : {(const void *)spgemm_row_kernel<true>, (const void *)spgemm_row_kernel<false>}) {
+        for (const void *f : {(const void *)spgemm_row_kernel<true>, (const void *)spgemm_row_kernel<false>,
+                              (const void *)spgemm_pipe_kernel}) {
             hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
                                                (int)((size_t)kTile * sizeof(double)));
             if (e != hipSuccess) return e;
@@ -877,7 +1169,15 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
         if (e != hipSuccess) return e;
     }
     const int64_t grid = batch < num_cu ? batch : num_cu;
-    if (resident_len > 0) {
+    // the pipelined instance: three or four windows, and only marked columns leave them
+    const bool pipe = w_seg && nwin >= 3 && nwin <= kPipeWin && w_nnz > 0 && (pattern || zero_below >= 0.0);
+    if (resident_len > 0 && pipe) {
+        spgemm_pipe_kernel<<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
+            n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, zero_below, pattern,
+            sparse_limit, ymax, lists, stats, out_cnt, out_col, out_val, err);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    } else if (resident_len > 0) {
         spgemm_row_kernel<true><<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
             n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, only_touched, zero_below,
             pattern, sparse_limit, lane_segments, ymax, lists, stats, out_cnt, out_col, out_val, err);

@@ -141,10 +141,11 @@ def test_paper_grid_points(sd, arm, m, S):
 
 @pytest.mark.parametrize("seed,n,L,batch,wd,yd", [(61, 300, 3, 40, 0.02, 0.05), (62, 3000, 2, 257, 0.003, 0.015),
                                                   (63, 40000, 2, 24, 0.0002, 0.0012), (64, 500, 3, 64, 0.05, 0.3),
-                                                  (65, 2000, 2, 100, 0.016, 0.1)])
+                                                  (65, 2000, 2, 100, 0.016, 0.1), (72, 40000, 2, 700, 0.0002, 0.008)])
 def test_pattern_bias_csr_path(sd, seed, n, L, batch, wd, yd):
     """SDNN_BIAS_PATTERN with positive biases through the CSR path: small-sample and workgroup SpGEMM
-    (one and three windows), and the density-driven switch to dense activations (denser cases)."""
+    (one and three windows; the last case gives the pipelined instance several samples per workgroup), and
+    the density-driven switch to dense activations (denser cases)."""
     p = tiny_random(seed, n, L, batch, w_density=wd, y_density=yd, bias_lo=-0.2, bias_hi=0.6,
                     explicit_zeros=seed % 2 == 1, ymax=[math.inf, 2.0][seed % 2])
     _say("pattern csr", seed, n, L, batch)
@@ -452,19 +453,23 @@ def test_spgemm_negative_bias_threshold(sd, n):
     parity.compare(p, run_csr(sd, p), exact=True)
 
 
-@pytest.mark.parametrize("n,fan,lens,biases", [(3000, (4, 24), (150, 300), (0.0, -1.0, -2.0)),
-                                               (40000, (4, 24), (450, 1000), (-1.0, -2.0, -3.0)),
-                                               (3000, (30, 50), (60, 300), (-1.0, -2.0))])
-def test_spgemm_crossing_marks(sd, n, fan, lens, biases):
+@pytest.mark.parametrize("n,fan,lens,biases,batch", [(3000, (4, 24), (150, 300), (0.0, -1.0, -2.0), 160),
+                                                     (40000, (4, 24), (450, 1000), (-1.0, -2.0, -3.0), 160),
+                                                     (3000, (30, 50), (60, 300), (-1.0, -2.0), 160),
+                                                     (40000, (4, 24), (300, 900), (0.0, -1.0), 1100),
+                                                     (60000, (4, 24), (400, 1000), (-1.0, -2.0), 1500)])
+def test_spgemm_crossing_marks(sd, n, fan, lens, biases, batch):
     """Every b_j <= 0 and samples too long for the bitmap epilogue: the scatter marks the columns whose sum
     rises above -max_j b_j and the epilogue reads only those.  Weights of both signs make sums cross the
     threshold and fall back in any order of the additions; integer values keep every sum exact, so the
     output is compared bit for bit.  Samples longer than the bitmap epilogue takes (one in eight beyond 1024
     entries) use the register-resident and the general workgroup instances (lane-walked segments with short
-    fan-out rows, half-wave segments with long ones), over one and three accumulator windows, with the input
-    sparse enough to stay on the SpGEMM; a threshold of 0 comes from b_j = 0."""
-    rng = np.random.default_rng(17 + n + fan[0])
-    batch = 160
+    fan-out rows, half-wave segments with long ones), over one, three and four accumulator windows, with the
+    input sparse enough to stay on the SpGEMM; a threshold of 0 comes from b_j = 0.  With three or four
+    windows the register-resident samples take the pipelined instance; the two larger batches give each
+    workgroup several samples in turn, mixing samples short enough for the bitmap epilogue with longer
+    ones (all rows compared bit for bit, in blocks)."""
+    rng = np.random.default_rng(17 + n + fan[0] + batch)
     layers = []
     for _ in range(2):
         ii, jj = [], []
@@ -491,8 +496,11 @@ def test_spgemm_crossing_marks(sd, n, fan, lens, biases):
     y_val = rng.choice(np.array([1.0, 2.0], np.float32), size=len(c_all))
     from workloads import Problem
     p = Problem(f"crossing-{n}-{fan[0]}", n, 2, batch, math.inf, layers, y0_csr=(np.cumsum(y_ptr), c_all, y_val))
-    _say("crossing marks", n, fan, biases)
-    parity.compare(p, run_csr(sd, p), exact=True)
+    _say("crossing marks", n, fan, biases, batch)
+    if batch > 500:
+        assert parity.compare_exact_csr(p, run_csr(sd, p)) > 0
+    else:
+        parity.compare(p, run_csr(sd, p), exact=True)
 
 
 @pytest.mark.parametrize("seed,n,L,batch,wd,yd", [(41, 5000, 3, 300, 0.0024, 0.008), (42, 3000, 2, 257, 0.003, 0.015),
