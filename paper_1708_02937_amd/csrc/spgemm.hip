@@ -668,7 +668,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
 // layer has at least one weight).
 constexpr int kPipeWin = 4;   // accumulator windows (n <= 4 * 16384)
 constexpr int kPipePre = 8;   // entries of a window's segment loaded a window ahead
-constexpr int kPipeRem = 4;   // entries beyond those, loaded at the start of their window
+constexpr int kPipeRem = 8;   // entries beyond those, loaded at the start of their window
 
 // Two consecutive fan-out entries, read with one 16-byte load (8-byte aligned; the packed array has one
 // entry of padding, so the pair that starts at a row's last entry stays inside it).
@@ -825,29 +825,31 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
             }
             add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
         }
-        {
-            int col[kPipeRem];
-            double v[kPipeRem];
-            bool ok[kPipeRem];
 #pragma unroll
-            for (int u = 0; u < kPipeRem; ++u) {
-                const Edge &ed = rem[u >> 1].e[u & 1];
-                ok[u] = kPipePre + u < len;
+        for (int h = 0; h < kPipeRem; h += 4) {
+            int col[4];
+            double v[4];
+            bool ok[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const Edge &ed = rem[(h + u) >> 1].e[(h + u) & 1];
+                ok[u] = kPipePre + h + u < len;
                 col[u] = ed.idx - (int)c0;
                 v[u] = E.y * (double)ed.w;
             }
             add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
         }
-        for (int e = kPipePre + kPipeRem; e < len; e += kPipeRem) {
-            EdgePair ep[kPipeRem / 2];
+        // rare: segments longer than kPipePre + kPipeRem
+        for (int e = kPipePre + kPipeRem; e < len; e += 4) {
+            EdgePair ep[2];
 #pragma unroll
-            for (int u = 0; u < kPipeRem / 2; ++u)
+            for (int u = 0; u < 2; ++u)
                 ep[u] = *reinterpret_cast<const EdgePair *>(e + 2 * u < len ? row + e + 2 * u : w);
-            int col[kPipeRem];
-            double v[kPipeRem];
-            bool ok[kPipeRem];
+            int col[4];
+            double v[4];
+            bool ok[4];
 #pragma unroll
-            for (int u = 0; u < kPipeRem; ++u) {
+            for (int u = 0; u < 4; ++u) {
                 const Edge &ed = ep[u >> 1].e[u & 1];
                 ok[u] = e + u < len;
                 col[u] = ed.idx - (int)c0;
