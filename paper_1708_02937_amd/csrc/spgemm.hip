@@ -121,10 +121,98 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Value of lane (l ^ M) for lane l of the wave: DPP quad permutations for M = 1, 2, DPP row shifts (lanes
+// l - M and l + M within each row of 16) for M = 4, 8, a swizzle within 32 lanes for M = 16, a permute for
+// M = 32.
+template <int M>
+__device__ __forceinline__ int xor_lanes(int v, int lane) {
+    if constexpr (M == 1) {
+        return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);  // quad_perm [1, 0, 3, 2]
+    } else if constexpr (M == 2) {
+        return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);  // quad_perm [2, 3, 0, 1]
+    } else if constexpr (M == 4 || M == 8) {
+        const int hi = __builtin_amdgcn_update_dpp(0, v, 0x100 + M, 0xF, 0xF, false);  // row_shl: lane l + M
+        const int lo = __builtin_amdgcn_update_dpp(0, v, 0x110 + M, 0xF, 0xF, false);  // row_shr: lane l - M
+        return (lane & M) ? lo : hi;
+    } else if constexpr (M == 16) {
+        return __builtin_amdgcn_ds_swizzle(v, (16 << 10) | 0x1F);  // and 0x1f, or 0, xor 16
+    } else {
+        return __builtin_amdgcn_ds_bpermute((lane ^ M) << 2, v);
+    }
+}
+template <int M>
+__device__ __forceinline__ double xor_lanes(double v, int lane) {
+    const long long b = __double_as_longlong(v);
+    const int lo = xor_lanes<M>((int)b, lane), hi = xor_lanes<M>((int)(b >> 32), lane);
+    return __longlong_as_double(((long long)hi << 32) | (uint32_t)lo);
+}
+
+// One stage (block size KK, distance J) of a bitonic sort of 64 * P (key, value) pairs held by a wave, lane
+// l holding elements l * P .. l * P + P - 1: distances below P stay inside a lane, the others exchange with
+// lane l ^ (J / P).  Equal keys keep their places within each compared pair, so every element survives.
+template <int P, int KK, int J>
+__device__ __forceinline__ void bitonic_stages(int32_t (&k)[P], double (&v)[P], int lane) {
+    if constexpr (J >= P) {
+        constexpr int LJ = J / P;
+        const bool lower = (lane & LJ) == 0;
+#pragma unroll
+        for (int r = 0; r < P; ++r) {
+            const bool up = ((lane * P + r) & KK) == 0;
+            const int32_t pk = xor_lanes<LJ>(k[r], lane);
+            const double pv = xor_lanes<LJ>(v[r], lane);
+            const bool take = (lower == up) ? pk < k[r] : pk > k[r];
+            if (take) {
+                k[r] = pk;
+                v[r] = pv;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < P; ++r) {
+            const int r2 = r ^ J;
+            if (r2 > r) {
+                const bool up = ((lane * P + r) & KK) == 0;
+                if (up ? k[r] > k[r2] : k[r] < k[r2]) {
+                    const int32_t tk = k[r];
+                    k[r] = k[r2];
+                    k[r2] = tk;
+                    const double tv = v[r];
+                    v[r] = v[r2];
+                    v[r2] = tv;
+                }
+            }
+        }
+    }
+    if constexpr (J > 1) bitonic_stages<P, KK, J / 2>(k, v, lane);
+}
+template <int P, int KK>
+__device__ __forceinline__ void bitonic_blocks(int32_t (&k)[P], double (&v)[P], int lane) {
+    bitonic_stages<P, KK, KK / 2>(k, v, lane);
+    if constexpr (KK < 64 * P) bitonic_blocks<P, KK * 2>(k, v, lane);
+}
+
+// Bitonic sort by key of the 64 * P pairs in keys/vals (one wave), in registers.
+template <int P>
+__device__ __forceinline__ void wave_sort_pairs(int32_t *keys, double *vals, int lane) {
+    int32_t k[P];
+    double v[P];
+#pragma unroll
+    for (int r = 0; r < P; ++r) {
+        k[r] = keys[lane * P + r];
+        v[r] = vals[lane * P + r];
+    }
+    bitonic_blocks<P, 2>(k, v, lane);
+#pragma unroll
+    for (int r = 0; r < P; ++r) {
+        keys[lane * P + r] = k[r];
+        vals[lane * P + r] = v[r];
+    }
+}
+
 // Small samples (every b_j <= 0, at most kSmallCap products): one wavefront per sample, no accumulator
 // window.  The wave expands the sample's products (column, exact fp64 product) into its own LDS area
 // (a wave prefix sum of the fan-out row lengths gives each entry its place), sorts them by column with a
-// bitonic network, then each run of equal columns is summed, biased, activated and rounded once, and the
+// bitonic network held in registers, then each run of equal columns is summed, biased, activated and rounded once, and the
 // survivors are compacted in column order with a ballot.  Only touched columns can survive when
 // b_j <= 0 or when the bias applies only on the structural pattern, so nothing else is visited.
 __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
@@ -186,25 +274,36 @@ __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
         while (size < total) size <<= 1;
         for (int e = total + lane; e < size; e += 64) keys[e] = 0x7fffffff;
         wave_lds_sync();
-        // bitonic sort of (key, value) pairs by key over [0, size)
-        for (int k = 2; k <= size; k <<= 1) {
-            for (int j = k >> 1; j > 0; j >>= 1) {
-                for (int p = lane; p < (size >> 1); p += 64) {
-                    const int i = ((p & ~(j - 1)) << 1) | (p & (j - 1));
-                    const int l = i + j;
-                    const int32_t ki = keys[i], kl = keys[l];
-                    const bool up = (i & k) == 0;
-                    if ((ki > kl) == up && ki != kl) {
-                        keys[i] = kl;
-                        keys[l] = ki;
-                        const double vi = vals[i];
-                        vals[i] = vals[l];
-                        vals[l] = vi;
+        // bitonic sort of (key, value) pairs by key over [0, size): in registers up to 512 pairs (more would
+        // cost the kernel's occupancy), through LDS beyond
+        if (size <= 512) {
+            switch (size) {
+                case 64: wave_sort_pairs<1>(keys, vals, lane); break;
+                case 128: wave_sort_pairs<2>(keys, vals, lane); break;
+                case 256: wave_sort_pairs<4>(keys, vals, lane); break;
+                default: wave_sort_pairs<8>(keys, vals, lane); break;
+            }
+        } else {
+            for (int k = 2; k <= size; k <<= 1) {
+                for (int j = k >> 1; j > 0; j >>= 1) {
+                    for (int p = lane; p < (size >> 1); p += 64) {
+                        const int i = ((p & ~(j - 1)) << 1) | (p & (j - 1));
+                        const int l = i + j;
+                        const int32_t ki = keys[i], kl = keys[l];
+                        const bool up = (i & k) == 0;
+                        if ((ki > kl) == up && ki != kl) {
+                            keys[i] = kl;
+                            keys[l] = ki;
+                            const double vi = vals[i];
+                            vals[i] = vals[l];
+                            vals[l] = vi;
+                        }
                     }
+                    wave_lds_sync();
                 }
-                wave_lds_sync();
             }
         }
+        wave_lds_sync();
         // runs of equal columns: the first element of a run sums it, then h, one rounding, compaction
         const int64_t ob = r * n;
         int written = 0;

@@ -453,6 +453,45 @@ def test_spgemm_negative_bias_threshold(sd, n):
     parity.compare(p, run_csr(sd, p), exact=True)
 
 
+def test_small_sample_sort_sizes(sd):
+    """The one-wave small-sample kernel sorts each sample's products by column: in registers for up to 512
+    products (64, 128, 256 or 512 slots), through LDS beyond.  A narrow layer (300 neurons, fan-out rows of
+    8-40) gives samples of 1 to about 1000 products with many equal columns (ties inside the sort), integer
+    weights of both signs, inputs and non-positive biases keep every sum exact: compared bit for bit."""
+    rng = np.random.default_rng(29)
+    n, batch = 300, 700
+    ii, jj = [], []
+    for i in range(n):
+        k = int(rng.integers(8, 41))
+        ii.append(np.full(k, i))
+        jj.append(np.sort(rng.choice(n, size=k, replace=False)))
+    i = np.concatenate(ii).astype(np.int64)
+    j = np.concatenate(jj).astype(np.int32)
+    row_ptr = np.zeros(n + 1, np.int64)
+    np.add.at(row_ptr, i + 1, 1)
+    vals = rng.choice(np.array([1.0, 2.0, -1.0, -3.0], np.float32), size=len(j))
+    bias = rng.choice(np.array([0.0, -1.0, -2.0], np.float32), size=n)
+    layer = Layer(np.cumsum(row_ptr), j, vals, bias)
+    longest = int(np.diff(layer.row_ptr).max())
+    rows, cols = [], []
+    for r in range(batch):
+        ylen = 1 + r % (1024 // longest)
+        rows.append(np.full(ylen, r))
+        cols.append(np.sort(rng.choice(n, size=ylen, replace=False)))
+    r_all = np.concatenate(rows).astype(np.int64)
+    c_all = np.concatenate(cols).astype(np.int32)
+    y_ptr = np.zeros(batch + 1, np.int64)
+    np.add.at(y_ptr, r_all + 1, 1)
+    y_val = rng.choice(np.array([1.0, 2.0], np.float32), size=len(c_all))
+    from workloads import Problem
+    p = Problem("small-sort-sizes", n, 1, batch, math.inf, [layer], y0_csr=(np.cumsum(y_ptr), c_all, y_val))
+    fan = np.diff(layer.row_ptr)
+    products = np.array([fan[c].sum() for c in cols])
+    assert products.min() <= 64 and products.max() > 512
+    _say("small-sample sort sizes")
+    parity.compare(p, run_csr(sd, p), exact=True)
+
+
 @pytest.mark.parametrize("n,fan,lens,biases,batch", [(3000, (4, 24), (150, 300), (0.0, -1.0, -2.0), 160),
                                                      (40000, (4, 24), (450, 1000), (-1.0, -2.0, -3.0), 160),
                                                      (3000, (30, 50), (60, 300), (-1.0, -2.0), 160),
