@@ -21,6 +21,8 @@
 // chunk is read from the Infinity Cache.
 #include <algorithm>
 
+#include <atomic>
+
 #include "common.h"
 
 namespace sdnn {
@@ -499,9 +501,12 @@ __global__ __launch_bounds__(kDensThreads) void densify_blocked_kernel(
 
 // Blocked activations -> CSR rows, in three steps.  Count: one wavefront per (chunk, part of kPackR
 // neurons) counts each sample's nonzeros in the part (lane = neuron, one ballot per sample).  Scan: per
-// sample, the part counts become offsets within the row and the row total goes to cnt.  Pack: the same
-// traversal writes each sample's survivors in ascending neuron order at row_ptr[r] + offset.
-constexpr int kPackR = 2048;
+// sample, the part counts become offsets within the row and the row total goes to cnt.  Pack: one
+// workgroup per (chunk, part) moves the part's 32 x kPackR values into LDS transposed, and each wave, for
+// each of its samples, compacts the survivors in ascending neuron order into its LDS area and then writes
+// the run at row_ptr[r] + offset with whole-wave stores aligned to 128-byte lines (a run of a few hundred
+// entries is written in whole lines but for its two ends).
+constexpr int kPackR = 512;
 constexpr int kTileLd = kBW + 1;  // LDS row pitch of a transposed 64 x 32 tile (conflict-free column reads)
 
 // Rows a .. a + 63 of chunk c (rows from a1 on read as zero) into v: lane l gets row a + l, all 32 samples.
@@ -568,39 +573,63 @@ __global__ __launch_bounds__(256) void blocked_scan_kernel(int64_t batch, int64_
     cnt[r] = run;
 }
 
-__global__ __launch_bounds__(256) void blocked_pack_kernel(int64_t n, int64_t batch, int64_t nparts,
-                                                           const float *__restrict__ yb,
-                                                           const int32_t *__restrict__ poff,
-                                                           const int64_t *__restrict__ row_ptr,
-                                                           int32_t *__restrict__ out_col, float *__restrict__ out_val) {
-    __shared__ float tiles[4][64 * kTileLd];
-    const int lane = threadIdx.x & 63;
-    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int64_t nchunks = (batch + kBW - 1) / kBW;
-    if (w >= nchunks * nparts) return;
-    float *tile = tiles[threadIdx.x >> 6];
-    const int64_t c = w / nparts, part = w % nparts;
-    const int64_t a0 = part * kPackR, a1 = min(n, a0 + kPackR);
-    // where each sample's survivors of this part start (lane s holds sample s's position)
-    int64_t pos = 0;
-    if (lane < kBW && c * kBW + lane < batch) pos = row_ptr[c * kBW + lane] + poff[part * batch + c * kBW + lane];
-    for (int64_t a = a0; a < a1; a += 64) {
-        const int64_t j = a + lane;
-        float v[kBW];
-        load_tile(yb, c, n, a, a1, tile, lane, v);
-#pragma unroll
-        for (int s = 0; s < kBW; ++s) {
-            if (c * kBW + s >= batch) break;  // uniform: samples past the batch end hold no output
-            const bool keep = v[s] != 0.0f;
+constexpr int kPackThreads = 1024;
+constexpr int kPackLd = kPackR + 1;  // LDS pitch (floats) of one sample's values in the transposed part
+constexpr size_t kPackLds = (size_t)kBW * kPackLd * sizeof(float) + (size_t)(kPackThreads / 64) * kPackR * 8;
+
+__global__ __launch_bounds__(kPackThreads) void blocked_pack_kernel(int64_t n, int64_t batch, int64_t nparts,
+                                                                    const float *__restrict__ yb,
+                                                                    const int32_t *__restrict__ poff,
+                                                                    const int64_t *__restrict__ row_ptr,
+                                                                    int32_t *__restrict__ out_col,
+                                                                    float *__restrict__ out_val) {
+    extern __shared__ __align__(16) float pack_lds[];
+    float *in = pack_lds;  // [kBW][kPackLd]: sample s's value of neuron a0 + j at s * kPackLd + j
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int32_t *scol = reinterpret_cast<int32_t *>(pack_lds + kBW * kPackLd) + wave * 2 * kPackR;
+    float *sval = reinterpret_cast<float *>(scol + kPackR);
+    const int64_t c = blockIdx.x / nparts, part = blockIdx.x % nparts;
+    const int64_t a0 = part * kPackR;
+    const int rows = (int)(n - a0 < kPackR ? n - a0 : kPackR);
+    // the part's rows (32 samples each, 128 bytes) as 16-byte pieces, coalesced; rows past n read as zero
+    const float4 *src = reinterpret_cast<const float4 *>(yb + (c * n + a0) * kBW);
+    for (int t = tid; t < kPackR * (kBW / 4); t += kPackThreads) {
+        const int row = t / (kBW / 4), q = (t % (kBW / 4)) * 4;
+        float4 f = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row < rows) f = src[t];
+        in[(q + 0) * kPackLd + row] = f.x;
+        in[(q + 1) * kPackLd + row] = f.y;
+        in[(q + 2) * kPackLd + row] = f.z;
+        in[(q + 3) * kPackLd + row] = f.w;
+    }
+    __syncthreads();
+    for (int s = wave; s < kBW; s += kPackThreads / 64) {
+        const int64_t r = c * kBW + s;
+        if (r >= batch) break;  // uniform in the wave; later samples are past the end too
+        int cnt = 0;
+        for (int j0 = 0; j0 < kPackR; j0 += 64) {
+            const float v = in[s * kPackLd + j0 + lane];
+            const bool keep = v != 0.0f;
             const uint64_t m = __ballot(keep);
-            const int64_t base = __shfl(pos, s);
             if (keep) {
-                const int64_t o = base + lane_rank(m);
-                out_col[o] = (int32_t)j;
-                out_val[o] = v[s];
+                const int o = cnt + lane_rank(m);
+                scol[o] = (int32_t)(a0 + j0 + lane);
+                sval[o] = v;
             }
-            if (lane == s) pos += __popcll(m);
+            cnt += __popcll(m);
         }
+        wave_lds_sync();
+        const int64_t base = row_ptr[r] + poff[part * batch + r];
+        // entry e goes to base + e; the lanes start at the 128-byte line holding base, so each store
+        // instruction covers two whole lines
+        const int lead = (int)(base & 31);
+        for (int e = lane - lead; e < cnt; e += 64) {
+            if (e >= 0) {
+                out_col[base + e] = scol[e];
+                out_val[base + e] = sval[e];
+            }
+        }
+        wave_lds_sync();  // the run's LDS area is rewritten for the wave's next sample
     }
 }
 
@@ -774,7 +803,23 @@ hipError_t launch_blocked_to_csr(int64_t n, int64_t batch, const float *yb, int3
     if (e != hipSuccess) return e;
     e = launch_exclusive_scan_i32_to_i64(batch, cnt, row_ptr, scan_tmp, s);
     if (e != hipSuccess) return e;
-    blocked_pack_kernel<<<(unsigned)blocks, 256, 0, s>>>(n, batch, nparts, yb, pcnt, row_ptr, out_col, out_val);
+    // the pack's LDS exceeds the default dynamic limit: raise it once per device (bit d of attr_devices;
+    // devices beyond 63 set it on every call)
+    static std::atomic<unsigned long long> attr_devices{0};
+    int dev = 0;
+    e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const unsigned long long bit = dev >= 0 && dev < 64 ? 1ull << dev : 0ull;
+    if (!bit || !(attr_devices.load(std::memory_order_acquire) & bit)) {
+        e = hipFuncSetAttribute((const void *)blocked_pack_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)kPackLds);
+        if (e != hipSuccess) return e;
+        attr_devices.fetch_or(bit, std::memory_order_release);
+    }
+    const int64_t groups = blocked_chunks(batch) * nparts;
+    if (groups > 0x7fffffffLL) return hipErrorInvalidValue;
+    blocked_pack_kernel<<<(unsigned)groups, kPackThreads, kPackLds, s>>>(n, batch, nparts, yb, pcnt, row_ptr, out_col,
+                                                                        out_val);
     return hipGetLastError();
 }
 
