@@ -756,10 +756,11 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
 // short (a few products per thread), so what bounds it is the chain of dependent loads: the sample's entry,
 // its fan-out row's window offsets, the segment itself, each a round trip to memory.  Here every load is
 // issued at least one window before its value is read.  Workgroup g takes the samples g, g + G, g + 2G, ...
-// of the list (G workgroups).  Every window issues the same loads in the same order: the entries of its own
-// segment beyond the buffered ones; the first kPipePre entries of the next window's segment (in the last
-// window, of the next sample's first window) into the other of two register buffers; the fan-out row starts
-// and window offsets of the next sample's entries (read a window earlier); the next sample's entries.  The
+// of the list (G workgroups).  Every window issues the same loads in the same order: at its start the
+// entries of its own segment beyond the buffered ones (the address unit has nothing else queued then);
+// after its products the first kPipePre entries of the next window's segment (in the last window, of the
+// next sample's first window) into the other of two register buffers, the fan-out row starts and window
+// offsets of the next sample's entries (read a window earlier), and the next sample's entries.  The
 // last two are real in one window each (the entries in the first, the rows in the second, kept from the
 // third on) and read one shared address in the others, so the instruction stream, and with it the count of
 // loads issued after each one, is the same in every window (each wait is for its own load only) while the
@@ -894,20 +895,11 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
         const int32_t lo = E.so[0], len = E.ok ? E.so[1] - lo : 0;
         const Edge *row = w + E.rb + lo;
         if (win == 2) N = T;  // the next sample's rows, loaded in the second window
-        // the loads of every window, in this order (see above)
+        // this window's entries beyond the buffered ones (the other loads follow the products)
         EdgePair rem[kPipeRem / 2];
 #pragma unroll
         for (int u = 0; u < kPipeRem / 2; ++u)
             rem[u] = *reinterpret_cast<const EdgePair *>(kPipePre + 2 * u < len ? row + kPipePre + 2 * u : w);
-        {
-            const bool nx = last && has_next;
-            const int64_t rb = last ? N.rb : E.rb;
-            const int32_t plo = last ? N.so[0] : E.so[1];
-            const int32_t plen = (last ? (nx && N.ok) : E.ok) ? (last ? N.so[1] : E.so[2]) - plo : 0;
-            prefetch(rb, plo, plen, pb);
-        }
-        entry_rows(nxt, ni, ny, T, win == 1);
-        entry_load(nxt, ni, ny, win == 0);
         // the products of this window's segment (buffered ones four at a time)
         const bool mine_any = len > 0;
 #pragma unroll
@@ -956,6 +948,16 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
             }
             add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
         }
+        // the next window's (or sample's) buffered entries and the next sample's rows and entries
+        {
+            const bool nx = last && has_next;
+            const int64_t rb = last ? N.rb : E.rb;
+            const int32_t plo = last ? N.so[0] : E.so[1];
+            const int32_t plen = (last ? (nx && N.ok) : E.ok) ? (last ? N.so[1] : E.so[2]) - plo : 0;
+            prefetch(rb, plo, plen, pb);
+        }
+        entry_rows(nxt, ni, ny, T, win == 1);
+        entry_load(nxt, ni, ny, win == 0);
         if (mine_any) any = 1;
         __syncthreads();
         const bool touched = any != 0;
