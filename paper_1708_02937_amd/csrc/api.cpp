@@ -759,6 +759,13 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
     }
     int32_t kd = k1;
     int cur = 0;  // slot buffer that receives the next sparse layer's output
+    // An empty activation stays empty through every layer whose untouched columns stay zero (every b_j <= 0,
+    // or the bias on the pattern only).  After the 1st, 2nd, 4th, 8th ... sparse layer, when at least
+    // kEmptyCheckLayers such layers follow, the host reads the layer's output count (one synchronisation) and
+    // stops at an empty output, which is then Y_{k1} (the deep sparse network dies out this way after its
+    // second layer; the rest would cost launches only).
+    constexpr int32_t kEmptyCheckLayers = 8;
+    int64_t next_check = 1;
     for (int32_t k = k0; k < k1; ++k) {
         const Layer &l = net->layers[(size_t)k];
         if (!net->bias_pattern && 4 * l.pos_bias >= n) {
@@ -789,6 +796,21 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         const double full = (double)batch * (double)n;
         nnz_hi = (l.bias_nonpos || net->bias_pattern) ? std::min(full, nnz_hi * (double)l.max_fanout) : full;
         exact = false;
+        if (k - k0 + 1 == next_check) {
+            next_check *= 2;
+            bool stays_empty = k1 - k - 1 >= kEmptyCheckLayers;
+            for (int32_t j = k + 1; stays_empty && j < k1; ++j)
+                stays_empty = net->layers[(size_t)j].bias_nonpos || net->bias_pattern;
+            if (stays_empty) {
+                unsigned long long got = 0;
+                SDNN_HIP(hipMemcpyAsync(&got, net->d_stats + sdnn::kSpgemmStats * (k - k0) + sdnn::kSpgemmStatNnz,
+                                        sizeof(got), hipMemcpyDeviceToHost, s));
+                SDNN_HIP(hipStreamSynchronize(s));
+                nnz_hi = (double)got;
+                exact = true;
+                if (got == 0) break;  // Y_{k+1} is empty, and so is every later activation
+            }
+        }
     }
     int last = 0, outb;  // slot buffer holding Y_{k1}, and the buffer the packed CSR goes to
     bool packed = false;  // the CSR is already in buffer outb

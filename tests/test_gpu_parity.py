@@ -700,6 +700,40 @@ def test_config4_scaled(sd):
     parity.compare(p, run_csr(sd, p))
 
 
+@pytest.mark.parametrize("case", ["dies", "survives", "positive_bias_later"])
+def test_csr_forward_stops_at_empty_activation(sd, case):
+    """forward_csr checks the output count after its 1st, 2nd, 4th ... sparse layer when at least 8 later
+    layers keep an empty activation empty, and stops at an empty one.  The deep sparse recipe dies out after
+    its second layer (the loop must stop there, with the oracle's empty Y_L); a denser net with non-positive
+    biases keeps its entries (checked, no stop); one layer with positive biases among the later ones rules
+    the check out.  Every case against the oracle."""
+    import torch
+
+    if case == "dies":
+        p = make_config(4, n=32768, L=20, batch=300)
+    else:
+        p = tiny_random(75, 1500, 12, 120, w_density=0.02, y_density=0.05, bias_lo=-0.02, bias_hi=0.0)
+        if case == "positive_bias_later":
+            p.layers[9] = Layer(p.layers[9].row_ptr, p.layers[9].col, p.layers[9].val,
+                                np.full(p.n, 0.01, np.float32))
+    net = sd.net_from_problem(p)
+    y = tuple(torch.from_numpy(a).cuda() for a in p.y0_as_csr())
+    net.set_profiling(True)
+    rp, c, v = net.forward_csr(*y)
+    torch.cuda.synchronize()
+    layers_run = sum(1 for _, name, _ in net.read_profile() if name == "spgemm_layer")
+    net.set_profiling(False)
+    got = (rp.cpu().numpy(), c.cpu().numpy(), v.cpu().numpy())
+    net.free()
+    _say("stop at empty activation", case, layers_run)
+    parity.compare(p, got)
+    if case == "dies":
+        assert got[0][-1] == 0 and layers_run == 2
+    else:
+        assert got[0][-1] > 0
+        assert layers_run <= p.L
+
+
 def test_config4_layer0_bit_exact_all_rows(sd, config4):
     """Deep sparse, full size, the live layer: weights are exactly 1/16 and inputs binary, so every
     pre-activation is c/16 + b with an integer count c; c/16 is exact and the only rounding is the one to
