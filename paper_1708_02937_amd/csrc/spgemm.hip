@@ -880,6 +880,12 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
     int win = 0;
     int64_t written = 0;
     bool has_next = false;
+    // samples of more than kThreads entries: thread t also takes entry t + kThreads, loaded at the sample's
+    // first window and read window by window without the pipeline (one round trip per window)
+    double y2 = 0.0;
+    int64_t rb2 = 0;
+    int32_t so2[kPipeWin + 1] = {0, 0, 0, 0, 0};
+    bool ok2 = false;
 
     auto step = [&](EdgePair(&cb)[kPipePre / 2], EdgePair(&pb)[kPipePre / 2]) -> bool {
         const int64_t c0 = (int64_t)win * kTile;
@@ -892,6 +898,28 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
             if (has_next && ((s + 1) & 63) == 0) load_refs(s + 1);
             nxt = has_next ? sample_at(s + 1) : cur;
         }
+        const bool two = cur.ylen > kThreads;  // uniform
+        if (two && win == 0) {
+            const int64_t t2 = tid + (int64_t)kThreads;
+            ok2 = false;
+            y2 = 0.0;
+            rb2 = 0;
+            if (t2 < cur.ylen) {
+                const int32_t i2 = in_col[cur.yb + t2];
+                const float v2 = in_val[cur.yb + t2];
+                if (i2 >= 0 && i2 < n) {
+                    ok2 = true;
+                    y2 = (double)v2;
+                    rb2 = w_ptr[i2];
+                    const int32_t *sg = w_seg + (int64_t)i2 * (nwin + 1);
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) so2[t] = sg[t];
+                    so2[4] = sg[nwin == 4 ? 4 : 3];
+                } else {
+                    atomicOr(err, 1u);
+                }
+            }
+        }
         const int32_t lo = E.so[0], len = E.ok ? E.so[1] - lo : 0;
         const Edge *row = w + E.rb + lo;
         if (win == 2) N = T;  // the next sample's rows, loaded in the second window
@@ -901,7 +929,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
         for (int u = 0; u < kPipeRem / 2; ++u)
             rem[u] = *reinterpret_cast<const EdgePair *>(kPipePre + 2 * u < len ? row + kPipePre + 2 * u : w);
         // the products of this window's segment (buffered ones four at a time)
-        const bool mine_any = len > 0;
+        bool mine_any = len > 0;
 #pragma unroll
         for (int h = 0; h < kPipePre; h += 4) {
             int col[4];
@@ -947,6 +975,29 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
                 v[u] = E.y * (double)ed.w;
             }
             add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
+        }
+        if (two) {
+            // the second entry's segment of this window
+            const int32_t len2 = ok2 ? so2[1] - so2[0] : 0;
+            const Edge *row2 = w + rb2 + so2[0];
+            mine_any |= len2 > 0;
+            for (int e = 0; e < len2; e += 4) {
+                EdgePair ep[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+                    ep[u] = *reinterpret_cast<const EdgePair *>(e + 2 * u < len2 ? row2 + e + 2 * u : w);
+                int col[4];
+                double v[4];
+                bool ok[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const Edge &ed = ep[u >> 1].e[u & 1];
+                    ok[u] = e + u < len2;
+                    col[u] = ed.idx - (int)c0;
+                    v[u] = y2 * (double)ed.w;
+                }
+                add_products(acc, bits, col, v, ok, mark_all && y2 != 0.0, !mark_all, zero_below);
+            }
         }
         // the next window's (or sample's) buffered entries and the next sample's rows and entries
         {
@@ -1011,7 +1062,10 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
         __syncthreads();
         if (!last) {
 #pragma unroll
-            for (int t = 0; t < kPipeWin; ++t) E.so[t] = E.so[t + 1];
+            for (int t = 0; t < kPipeWin; ++t) {
+                E.so[t] = E.so[t + 1];
+                so2[t] = so2[t + 1];
+            }
             ++win;
             return true;
         }
@@ -1256,7 +1310,10 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     // segments of at most ~16 entries are walked lane by lane, longer ones by half-waves
     const int lane_segments = (w_seg || nwin == 1) && per_win <= 16.0 ? 1 : 0;
     const int64_t small_len = spgemm_small_len(n, max_fanout);
-    const int64_t resident_len = lane_segments ? (int64_t)kRes * kThreads : 0;
+    // the pipelined instance: three or four windows, and only marked columns leave them; it also takes
+    // samples of up to 2 * kThreads entries (a second entry per thread, loaded without the pipeline)
+    const bool pipe = w_seg && nwin >= 3 && nwin <= kPipeWin && w_nnz > 0 && (pattern || zero_below >= 0.0);
+    const int64_t resident_len = lane_segments ? (int64_t)(pipe ? 2 : kRes) * kThreads : 0;
     spgemm_plan_kernel<<<(unsigned)((batch + 255) / 256), 256, 0, s>>>(
         n, batch, in_row_ptr, in_cnt, in_col, in_val, only_touched, small_len, resident_len, out_cnt, lists, stats,
         err);
@@ -1272,8 +1329,6 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
         if (e != hipSuccess) return e;
     }
     const int64_t grid = batch < num_cu ? batch : num_cu;
-    // the pipelined instance: three or four windows, and only marked columns leave them
-    const bool pipe = w_seg && nwin >= 3 && nwin <= kPipeWin && w_nnz > 0 && (pattern || zero_below >= 0.0);
     if (resident_len > 0 && pipe) {
         spgemm_pipe_kernel<<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
             n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, zero_below, pattern,
