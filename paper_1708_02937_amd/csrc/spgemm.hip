@@ -13,7 +13,8 @@
 // the workgroup kernel below, where one persistent workgroup per CU takes chunks of the list from a device
 // counter (every workgroup leaves once the counter passes the last chunk).  Samples of at most 1024 entries
 // keep them in registers (one per thread); with three or four windows and only marked columns to read, they
-// go to a pipelined instance that loads every window's data a window ahead (described at that kernel).
+// go to a pipelined instance that loads every window's data a window ahead (described at that kernel), which
+// also takes samples of up to 2048 entries.
 //
 // The epilogue visits the window in column order: z = acc + b_j, h(z), one rounding to fp32, and the
 // entries that are not zero (Sec. II.E: zeros are not stored) are compacted with a wave prefix sum of
@@ -765,7 +766,8 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
 // third on) and read one shared address in the others, so the instruction stream, and with it the count of
 // loads issued after each one, is the same in every window (each wait is for its own load only) while the
 // memory requests stay those the sample needs.  Lanes with nothing to load read w[0] and ignore it (the
-// layer has at least one weight).
+// layer has at least one weight).  Samples of up to 2 * kThreads entries give each thread a second entry,
+// read without the pipeline (its offsets at the sample's first window, its segment in every window).
 constexpr int kPipeWin = 4;   // accumulator windows (n <= 4 * 16384)
 constexpr int kPipePre = 8;   // entries of a window's segment loaded a window ahead
 constexpr int kPipeRem = 8;   // entries beyond those, loaded at the start of their window
