@@ -353,13 +353,15 @@ __device__ __forceinline__ int acc_pos(int col) {
 // sum exceeds zero_below was pushed across it by some addition; that addition reads the previous sum back and
 // marks the column, and only marked columns can survive.  The thread's add rounds like the LDS unit's, so no
 // crossing goes unmarked; a column that crosses and falls back is marked and dropped by the epilogue.
-template <int K>
+template <int K, bool kLinear = false>
 __device__ __forceinline__ void add_products(double *acc, uint32_t *bits, const int (&col)[K], const double (&v)[K],
                                              const bool (&ok)[K], bool mark_all, bool cross, double zero_below) {
+    // kLinear: column c of the window at position c (instances without the dense epilogue)
+    auto at = [](int c) { return kLinear ? c : acc_pos(c); };
     if (cross) {
         double old[K];
 #pragma unroll
-        for (int u = 0; u < K; ++u) old[u] = ok[u] ? atomicAdd(&acc[acc_pos(col[u])], v[u]) : 0.0;
+        for (int u = 0; u < K; ++u) old[u] = ok[u] ? atomicAdd(&acc[at(col[u])], v[u]) : 0.0;
 #pragma unroll
         for (int u = 0; u < K; ++u)
             if (ok[u] && old[u] <= zero_below && old[u] + v[u] > zero_below)
@@ -368,7 +370,7 @@ __device__ __forceinline__ void add_products(double *acc, uint32_t *bits, const 
 #pragma unroll
         for (int u = 0; u < K; ++u)
             if (ok[u]) {
-                atomicAdd(&acc[acc_pos(col[u])], v[u]);
+                atomicAdd(&acc[at(col[u])], v[u]);
                 if (mark_all) atomicOr(&bits[col[u] >> 5], 1u << (col[u] & 31));
             }
     }
@@ -944,7 +946,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
                 col[u] = ed.idx - (int)c0;
                 v[u] = E.y * (double)ed.w;
             }
-            add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
+            add_products<4, true>(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
         }
 #pragma unroll
         for (int h = 0; h < kPipeRem; h += 4) {
@@ -958,7 +960,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
                 col[u] = ed.idx - (int)c0;
                 v[u] = E.y * (double)ed.w;
             }
-            add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
+            add_products<4, true>(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
         }
         // rare: segments longer than kPipePre + kPipeRem
         for (int e = kPipePre + kPipeRem; e < len; e += 4) {
@@ -976,7 +978,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
                 col[u] = ed.idx - (int)c0;
                 v[u] = E.y * (double)ed.w;
             }
-            add_products(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
+            add_products<4, true>(acc, bits, col, v, ok, mark_all && E.y != 0.0, !mark_all, zero_below);
         }
         if (two) {
             // the second entry's segment of this window
@@ -998,7 +1000,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
                     col[u] = ed.idx - (int)c0;
                     v[u] = y2 * (double)ed.w;
                 }
-                add_products(acc, bits, col, v, ok, mark_all && y2 != 0.0, !mark_all, zero_below);
+                add_products<4, true>(acc, bits, col, v, ok, mark_all && y2 != 0.0, !mark_all, zero_below);
             }
         }
         // the next window's (or sample's) buffered entries and the next sample's rows and entries
@@ -1021,7 +1023,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
             int keep = 0;
             for (uint32_t m = word; m; m &= m - 1) {
                 const int col = tid * 32 + __builtin_ctz(m);
-                const double a = acc[acc_pos(col)];
+                const double a = acc[col];
                 keep += a > zero_below && activate(a + (double)bias[c0 + col], ymax) != 0.0f;
             }
             int incl = keep;
@@ -1042,9 +1044,9 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
             int64_t pos = cur.r * n + written + off + incl - keep;
             for (uint32_t m = word; m; m &= m - 1) {
                 const int col = tid * 32 + __builtin_ctz(m);
-                const double a = acc[acc_pos(col)];
+                const double a = acc[col];
                 const float f = a > zero_below ? activate(a + (double)bias[c0 + col], ymax) : 0.0f;
-                if (mark_all) acc[acc_pos(col)] = 0.0;
+                if (mark_all) acc[col] = 0.0;
                 if (f != 0.0f) {
                     out_col[pos] = (int32_t)(c0 + col);
                     out_val[pos] = f;
@@ -1053,15 +1055,19 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
             }
             if (tid < nw) bits[tid] = 0u;
             written += tot;
+            if (tid == 0) any = 0;  // every thread read it before the scan's barrier
+            if (!mark_all) {
+                // crossing marks leave the other sums in place.  Wave v read only the marked columns of its
+                // bitmap words, columns 2048 v .. 2048 v + 2047: once its reads are done it clears that
+                // range itself with 16-byte stores, so no workgroup barrier sits between reads and clear
+                wave_lds_sync();
+                if (wave * 64 * 32 < width0) {
+                    double2 *acc2 = reinterpret_cast<double2 *>(acc) + wave * 64 * 16;
+                    for (int t = lane; t < 64 * 16; t += 64) acc2[t] = make_double2(0.0, 0.0);
+                }
+            }
         }
-        __syncthreads();
-        if (tid == 0) any = 0;
-        if (!mark_all && touched) {
-            // crossing marks leave the other sums in place: clear the window with 16-byte stores
-            double2 *acc2 = reinterpret_cast<double2 *>(acc);
-            for (int t = tid; t < width0 / 2; t += kThreads) acc2[t] = make_double2(0.0, 0.0);
-        }
-        __syncthreads();
+        __syncthreads();  // the window's epilogue is done before the next window's products
         if (!last) {
 #pragma unroll
             for (int t = 0; t < kPipeWin; ++t) {
