@@ -151,7 +151,7 @@ __device__ __forceinline__ double xor_lanes(double v, int lane) {
 // One stage (block size KK, distance J) of a bitonic sort of 64 * P (key, value) pairs held by a wave, lane
 // l holding elements l * P .. l * P + P - 1: distances below P stay inside a lane, the others exchange with
 // lane l ^ (J / P).  Equal keys keep their places within each compared pair, so every element survives.
-template <int P, int KK, int J>
+template <int P, int KK, int J, bool kVals>
 __device__ __forceinline__ void bitonic_stages(int32_t (&k)[P], double (&v)[P], int lane) {
     if constexpr (J >= P) {
         constexpr int LJ = J / P;
@@ -160,12 +160,12 @@ __device__ __forceinline__ void bitonic_stages(int32_t (&k)[P], double (&v)[P], 
         for (int r = 0; r < P; ++r) {
             const bool up = ((lane * P + r) & KK) == 0;
             const int32_t pk = xor_lanes<LJ>(k[r], lane);
-            const double pv = xor_lanes<LJ>(v[r], lane);
             const bool take = (lower == up) ? pk < k[r] : pk > k[r];
-            if (take) {
-                k[r] = pk;
-                v[r] = pv;
+            if constexpr (kVals) {
+                const double pv = xor_lanes<LJ>(v[r], lane);
+                if (take) v[r] = pv;
             }
+            if (take) k[r] = pk;
         }
     } else {
 #pragma unroll
@@ -177,35 +177,45 @@ __device__ __forceinline__ void bitonic_stages(int32_t (&k)[P], double (&v)[P], 
                     const int32_t tk = k[r];
                     k[r] = k[r2];
                     k[r2] = tk;
-                    const double tv = v[r];
-                    v[r] = v[r2];
-                    v[r2] = tv;
+                    if constexpr (kVals) {
+                        const double tv = v[r];
+                        v[r] = v[r2];
+                        v[r2] = tv;
+                    }
                 }
             }
         }
     }
-    if constexpr (J > 1) bitonic_stages<P, KK, J / 2>(k, v, lane);
+    if constexpr (J > 1) bitonic_stages<P, KK, J / 2, kVals>(k, v, lane);
 }
-template <int P, int KK>
+template <int P, int KK, bool kVals>
 __device__ __forceinline__ void bitonic_blocks(int32_t (&k)[P], double (&v)[P], int lane) {
-    bitonic_stages<P, KK, KK / 2>(k, v, lane);
-    if constexpr (KK < 64 * P) bitonic_blocks<P, KK * 2>(k, v, lane);
+    bitonic_stages<P, KK, KK / 2, kVals>(k, v, lane);
+    if constexpr (KK < 64 * P) bitonic_blocks<P, KK * 2, kVals>(k, v, lane);
 }
 
-// Bitonic sort by key of the 64 * P pairs in keys/vals (one wave), in registers.
+// Bitonic sort by key of the 64 * P (key, value) pairs in keys/vals (one wave), in registers, with one
+// 32-bit word per pair in the network: (key << 9) | position (keys below 2^22 - 1, at most 512 pairs;
+// 0x7fffffff pads), the values fetched by position afterwards.  Words are unique (equal keys keep their
+// order of position), and an exchange moves one register instead of three.
 template <int P>
-__device__ __forceinline__ void wave_sort_pairs(int32_t *keys, double *vals, int lane) {
+__device__ __forceinline__ void wave_sort_packed(int32_t *keys, double *vals, int lane) {
+    static_assert(64 * P <= 512, "nine position bits");
     int32_t k[P];
     double v[P];
 #pragma unroll
     for (int r = 0; r < P; ++r) {
-        k[r] = keys[lane * P + r];
-        v[r] = vals[lane * P + r];
+        const int e = lane * P + r;
+        const int32_t c = keys[e];
+        k[r] = c == 0x7fffffff ? c : (int32_t)(((uint32_t)c << 9) | (uint32_t)e);
     }
-    bitonic_blocks<P, 2>(k, v, lane);
+    bitonic_blocks<P, 2, false>(k, v, lane);
+#pragma unroll
+    for (int r = 0; r < P; ++r) v[r] = k[r] == 0x7fffffff ? 0.0 : vals[k[r] & 511];
+    wave_lds_sync();  // every lane has read the values at their old places
 #pragma unroll
     for (int r = 0; r < P; ++r) {
-        keys[lane * P + r] = k[r];
+        keys[lane * P + r] = k[r] == 0x7fffffff ? 0x7fffffff : (int32_t)((uint32_t)k[r] >> 9);
         vals[lane * P + r] = v[r];
     }
 }
@@ -276,13 +286,13 @@ __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
         for (int e = total + lane; e < size; e += 64) keys[e] = 0x7fffffff;
         wave_lds_sync();
         // bitonic sort of (key, value) pairs by key over [0, size): in registers up to 512 pairs (more would
-        // cost the kernel's occupancy), through LDS beyond
-        if (size <= 512) {
+        // cost the kernel's occupancy; columns below 2^22 - 1), through LDS otherwise
+        if (size <= 512 && n < (1 << 22)) {
             switch (size) {
-                case 64: wave_sort_pairs<1>(keys, vals, lane); break;
-                case 128: wave_sort_pairs<2>(keys, vals, lane); break;
-                case 256: wave_sort_pairs<4>(keys, vals, lane); break;
-                default: wave_sort_pairs<8>(keys, vals, lane); break;
+                case 64: wave_sort_packed<1>(keys, vals, lane); break;
+                case 128: wave_sort_packed<2>(keys, vals, lane); break;
+                case 256: wave_sort_packed<4>(keys, vals, lane); break;
+                default: wave_sort_packed<8>(keys, vals, lane); break;
             }
         } else {
             for (int k = 2; k <= size; k <<= 1) {
