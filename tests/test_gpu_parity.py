@@ -141,11 +141,13 @@ def test_paper_grid_points(sd, arm, m, S):
 
 @pytest.mark.parametrize("seed,n,L,batch,wd,yd", [(61, 300, 3, 40, 0.02, 0.05), (62, 3000, 2, 257, 0.003, 0.015),
                                                   (63, 40000, 2, 24, 0.0002, 0.0012), (64, 500, 3, 64, 0.05, 0.3),
-                                                  (65, 2000, 2, 100, 0.016, 0.1), (72, 40000, 2, 700, 0.0002, 0.008)])
+                                                  (65, 2000, 2, 100, 0.016, 0.1), (72, 40000, 2, 700, 0.0002, 0.008),
+                                                  (73, 40000, 2, 300, 0.0002, 0.0275)])
 def test_pattern_bias_csr_path(sd, seed, n, L, batch, wd, yd):
     """SDNN_BIAS_PATTERN with positive biases through the CSR path: small-sample and workgroup SpGEMM
-    (one and three windows; the last case gives the pipelined instance several samples per workgroup), and
-    the density-driven switch to dense activations (denser cases)."""
+    (one and three windows; the last two cases give the pipelined instance several samples per workgroup,
+    the last one samples of about 1100 entries, two per thread), and the density-driven switch to dense
+    activations (denser cases)."""
     p = tiny_random(seed, n, L, batch, w_density=wd, y_density=yd, bias_lo=-0.2, bias_hi=0.6,
                     explicit_zeros=seed % 2 == 1, ymax=[math.inf, 2.0][seed % 2])
     _say("pattern csr", seed, n, L, batch)
