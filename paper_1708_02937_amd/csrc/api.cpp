@@ -66,6 +66,7 @@ struct Layer {
     const float *val = nullptr;
     const float *bias = nullptr;
     bool bias_nonpos = true;
+    bool bias_uniform = false;  // every b_j has the same bits
     int64_t pos_bias = 0;      // neurons with b_j > 0
     double zero_below = -INFINITY;  // every b_j <= 0: -max_j b_j (a sum at most this is zero after h), else -inf
     int32_t max_fanout = 0;    // longest fan-out row of W_k
@@ -452,10 +453,10 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
     SDNN_ON_DEVICE(net);
 
     // 1. validate on the device
-    SDNN_HIP(hipMemsetAsync(net->d_flags, 0, 3 * sizeof(uint32_t), s));
+    SDNN_HIP(hipMemsetAsync(net->d_flags, 0, 4 * sizeof(uint32_t), s));
     SDNN_HIP(sdnn::launch_validate_layer(n, nnz, row_ptr, col_idx, val, bias, net->d_flags, s));
-    uint32_t fl[3] = {0, 0, 0};
-    SDNN_HIP(hipMemcpyAsync(fl, net->d_flags, 3 * sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    uint32_t fl[4] = {0, 0, 0, 0};
+    SDNN_HIP(hipMemcpyAsync(fl, net->d_flags, 4 * sizeof(uint32_t), hipMemcpyDeviceToHost, s));
     SDNN_HIP(hipStreamSynchronize(s));
     const uint32_t flags = fl[0];
     if (flags & 1u)
@@ -485,6 +486,8 @@ sdnn_status sdnn_net_set_layer(sdnn_net net, int32_t k, int64_t nnz, const int64
         float bmax;
         std::memcpy(&bmax, &u, sizeof(bmax));
         nl.zero_below = nl.bias_nonpos ? -(double)bmax : -INFINITY;
+        // fl[3] holds the complement of the smallest key: equal keys mean every b_j has the same bits
+        nl.bias_uniform = ~fl[3] == key;
     }
     nl.w_pack = at<Edge>(base, lp.w_pack);
     nl.fan_ptr = at<int64_t>(base, lp.fan_ptr);
@@ -788,7 +791,8 @@ sdnn_status sdnn_forward_csr(sdnn_net net, int32_t k0, int32_t k1, int64_t batch
         SDNN_HIP(prof_begin(net, k, sdnn::kKernSpgemm, &pr));
         SDNN_HIP(sdnn::launch_spgemm_layer(n, batch, first ? y_row_ptr : nullptr, first ? nullptr : w.cnt[cur ^ 1],
                                            first ? y_col : w.col[cur ^ 1], first ? y_val : w.val[cur ^ 1], l.row_ptr,
-                                           l.w_seg, l.w_pack, l.nnz, l.max_fanout, l.bias, l.bias_nonpos ? 1 : 0, l.zero_below,
+                                           l.w_seg, l.w_pack, l.nnz, l.max_fanout, l.bias, l.bias_nonpos ? 1 : 0,
+                                           l.bias_uniform ? 1 : 0, l.zero_below,
                                            net->bias_pattern, net->ymax, w.cnt[cur], w.col[cur], w.val[cur], w.lists,
                                            net->d_stats + sdnn::kSpgemmStats * (k - k0), net->d_flags, net->num_cu, s));
         SDNN_HIP(prof_end(net, pr));

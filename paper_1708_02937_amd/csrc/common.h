@@ -117,12 +117,13 @@ constexpr int kSpgemmStats = 8;
 constexpr int kSpgemmStatNnz = 2;
 // pattern != 0: the bias and h apply only on the structural pattern of Y_k W_k.  zero_below: a sum z with
 // z <= zero_below gives h(z + b_j) = 0 for every j (-max_j b_j when every b_j <= 0, else -infinity), so the
-// epilogues read no bias for such a column.
+// epilogues read no bias for such a column.  bias_uniform != 0: every b_j equals bias[0].
 hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const int32_t *w_seg,
                                const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
-                               double zero_below, int pattern, double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val,
-                               int32_t *lists, unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s);
+                               int bias_uniform, double zero_below, int pattern, double ymax, int32_t *out_cnt,
+                               int32_t *out_col, float *out_val, int32_t *lists, unsigned long long *stats, uint32_t *err,
+                               int num_cu, hipStream_t s);
 // Y^T (n x batch at row pitch ld) from sparse rows; tmp (batch x n floats, may be null) stages them batch-major.
 hipError_t launch_densify(int64_t n, int64_t batch, int64_t ld, const int64_t *in_row_ptr, const int32_t *in_cnt,
                           const int32_t *in_col, const float *in_val, float *yt, float *tmp, uint32_t *err,

@@ -18,19 +18,27 @@ constexpr uint32_t kFlagValue = 2u;    // non-finite weight or bias
 constexpr uint32_t kFlagPosBias = 4u;  // some bias > 0 (informational)
 
 // flags[2] receives the largest bias as an order-preserving key (bits of a negative float complemented, of a
-// positive one with the sign bit set: unsigned order is float order), one atomic per wave.
+// positive one with the sign bit set: unsigned order is float order), flags[3] the complement of the smallest
+// key (so that both start from zero), one atomic each per wave.
 __global__ void validate_layer_kernel(int64_t n, int64_t nnz, const int64_t *__restrict__ row_ptr,
                                       const int32_t *__restrict__ col, const float *__restrict__ val,
                                       const float *__restrict__ bias, uint32_t *flags) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    uint32_t key = 0u;
+    uint32_t key = 0u, nkey = 0u;
     if (i < n) {
         const uint32_t u = __float_as_uint(bias[i]);
         key = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+        nkey = ~key;
     }
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) key = max(key, (uint32_t)__shfl_xor((int)key, off));
-    if ((threadIdx.x & 63) == 0) atomicMax(&flags[2], key);
+    for (int off = 32; off >= 1; off >>= 1) {
+        key = max(key, (uint32_t)__shfl_xor((int)key, off));
+        nkey = max(nkey, (uint32_t)__shfl_xor((int)nkey, off));
+    }
+    if ((threadIdx.x & 63) == 0) {
+        atomicMax(&flags[2], key);
+        atomicMax(&flags[3], nkey);
+    }
     if (i >= n) return;
     uint32_t f = 0;
     const int64_t b = row_ptr[i], e = row_ptr[i + 1];

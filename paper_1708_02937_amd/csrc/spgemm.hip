@@ -226,6 +226,8 @@ __device__ __forceinline__ void wave_sort_packed(int32_t *keys, double *vals, in
 // bitonic network held in registers, then each run of equal columns is summed, biased, activated and rounded once, and the
 // survivors are compacted in column order with a ballot.  Only touched columns can survive when
 // b_j <= 0 or when the bias applies only on the structural pattern, so nothing else is visited.
+// kUniformBias: every b_j is the same value, read once from bias[0] (no bias load per run).
+template <bool kUniformBias>
 __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
     int64_t n, int64_t batch, const int64_t *__restrict__ in_row_ptr, const int32_t *__restrict__ in_cnt,
     const int32_t *__restrict__ in_col, const float *__restrict__ in_val, const int64_t *__restrict__ w_ptr,
@@ -238,6 +240,7 @@ __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
     int32_t *keys = keys_all[wave];
     double *vals = vals_all[wave];
     const int64_t count = (int64_t)stats[kStatSmall];
+    const double b_uni = kUniformBias ? (double)bias[0] : 0.0;
     const int64_t stride = (int64_t)gridDim.x * kSmallWaves;
     for (int64_t q = (int64_t)blockIdx.x * kSmallWaves + wave; q < count; q += stride) {
         const int64_t r = list[q];
@@ -327,7 +330,7 @@ __global__ __launch_bounds__(kSmallWaves * 64) void spgemm_small_kernel(
                 if (e == 0 || keys[e - 1] != key) {
                     double z = 0.0;
                     for (int u = e; u < total && keys[u] == key; ++u) z += vals[u];
-                    f = z > zero_below ? activate(z + (double)bias[key], ymax) : 0.0f;
+                    f = z > zero_below ? activate(z + (kUniformBias ? b_uni : (double)bias[key]), ymax) : 0.0f;
                 }
             }
             const bool keep = f != 0.0f;
@@ -780,6 +783,8 @@ __global__ __launch_bounds__(kThreads) void spgemm_row_kernel(
 // memory requests stay those the sample needs.  Lanes with nothing to load read w[0] and ignore it (the
 // layer has at least one weight).  Samples of up to 2 * kThreads entries give each thread a second entry,
 // read without the pipeline (its offsets at the sample's first window, its segment in every window).
+// kUniformBias: every b_j is the same value, read once from bias[0], so the epilogue issues no load of its own
+// (a bias load there would also wait for the prefetch issued before it).
 constexpr int kPipeWin = 4;   // accumulator windows (n <= 4 * 16384)
 constexpr int kPipePre = 8;   // entries of a window's segment loaded a window ahead
 constexpr int kPipeRem = 8;   // entries beyond those, loaded at the start of their window
@@ -801,6 +806,7 @@ struct PipeEntry {
     bool ok;
 };
 
+template <bool kUniformBias>
 __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
     int64_t n, int64_t batch, int nwin, const int64_t *__restrict__ in_row_ptr, const int32_t *__restrict__ in_cnt,
     const int32_t *__restrict__ in_col, const float *__restrict__ in_val, const int64_t *__restrict__ w_ptr,
@@ -821,6 +827,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
     for (int t = tid; t < kBitWords; t += kThreads) bits[t] = 0u;
     if (tid == 0) any = 0;
     const int32_t *res = list + 2 * batch;
+    const double b_uni = kUniformBias ? (double)bias[0] : 0.0;
 
     // the samples' rows, 64 at a time: lane l of every wave holds sample s0 + l of this workgroup
     int32_t ref_r = 0, ref_len = 0;
@@ -1034,7 +1041,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
             for (uint32_t m = word; m; m &= m - 1) {
                 const int col = tid * 32 + __builtin_ctz(m);
                 const double a = acc[col];
-                keep += a > zero_below && activate(a + (double)bias[c0 + col], ymax) != 0.0f;
+                keep += a > zero_below && activate(a + (kUniformBias ? b_uni : (double)bias[c0 + col]), ymax) != 0.0f;
             }
             int incl = keep;
 #pragma unroll
@@ -1055,7 +1062,7 @@ __global__ __launch_bounds__(kThreads) void spgemm_pipe_kernel(
             for (uint32_t m = word; m; m &= m - 1) {
                 const int col = tid * 32 + __builtin_ctz(m);
                 const double a = acc[col];
-                const float f = a > zero_below ? activate(a + (double)bias[c0 + col], ymax) : 0.0f;
+                const float f = a > zero_below ? activate(a + (kUniformBias ? b_uni : (double)bias[c0 + col]), ymax) : 0.0f;
                 if (mark_all) acc[col] = 0.0;
                 if (f != 0.0f) {
                     out_col[pos] = (int32_t)(c0 + col);
@@ -1300,8 +1307,9 @@ int64_t spgemm_small_len(int64_t n, int32_t max_fanout) {
 hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_ptr, const int32_t *in_cnt,
                                const int32_t *in_col, const float *in_val, const int64_t *w_ptr, const int32_t *w_seg,
                                const Edge *w, int64_t w_nnz, int32_t max_fanout, const float *bias, int bias_nonpos,
-                               double zero_below, int pattern, double ymax, int32_t *out_cnt, int32_t *out_col, float *out_val,
-                               int32_t *lists, unsigned long long *stats, uint32_t *err, int num_cu, hipStream_t s) {
+                               int bias_uniform, double zero_below, int pattern, double ymax, int32_t *out_cnt,
+                               int32_t *out_col, float *out_val, int32_t *lists, unsigned long long *stats, uint32_t *err,
+                               int num_cu, hipStream_t s) {
     if (batch == 0) return hipSuccess;
     const int only_touched = bias_nonpos || pattern;
     if (batch > 0x7fffffffLL) return hipErrorInvalidValue;
@@ -1314,7 +1322,7 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     const unsigned long long bit = dev >= 0 && dev < 64 ? 1ull << dev : 0ull;
     if (!bit || !(attr_devices.load(std::memory_order_acquire) & bit)) {
         for (const void *f : {(const void *)spgemm_row_kernel<true>, (const void *)spgemm_row_kernel<false>,
-                              (const void *)spgemm_pipe_kernel}) {
+                              (const void *)spgemm_pipe_kernel<true>, (const void *)spgemm_pipe_kernel<false>}) {
             hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
                                                (int)((size_t)kTile * sizeof(double)));
             if (e != hipSuccess) return e;
@@ -1340,17 +1348,28 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     if (only_touched) {
         // enough waves to cover every CU several times; each wave strides through the small list
         const int64_t waves = (batch < (int64_t)num_cu * 16 ? batch : (int64_t)num_cu * 16);
-        spgemm_small_kernel<<<(unsigned)((waves + kSmallWaves - 1) / kSmallWaves), kSmallWaves * 64, 0, s>>>(
-            n, batch, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w, bias, zero_below, ymax, lists, stats, out_cnt,
-            out_col, out_val, err);
+        const unsigned blocks = (unsigned)((waves + kSmallWaves - 1) / kSmallWaves);
+        if (bias_uniform)
+            spgemm_small_kernel<true><<<blocks, kSmallWaves * 64, 0, s>>>(
+                n, batch, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w, bias, zero_below, ymax, lists, stats, out_cnt,
+                out_col, out_val, err);
+        else
+            spgemm_small_kernel<false><<<blocks, kSmallWaves * 64, 0, s>>>(
+                n, batch, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w, bias, zero_below, ymax, lists, stats, out_cnt,
+                out_col, out_val, err);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     const int64_t grid = batch < num_cu ? batch : num_cu;
     if (resident_len > 0 && pipe) {
-        spgemm_pipe_kernel<<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
-            n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, zero_below, pattern,
-            sparse_limit, ymax, lists, stats, out_cnt, out_col, out_val, err);
+        if (bias_uniform)
+            spgemm_pipe_kernel<true><<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
+                n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, zero_below, pattern,
+                sparse_limit, ymax, lists, stats, out_cnt, out_col, out_val, err);
+        else
+            spgemm_pipe_kernel<false><<<(unsigned)grid, kThreads, spgemm_lds_bytes(n), s>>>(
+                n, batch, nwin, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w_seg, w, bias, zero_below, pattern,
+                sparse_limit, ymax, lists, stats, out_cnt, out_col, out_val, err);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     } else if (resident_len > 0) {

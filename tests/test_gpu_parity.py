@@ -498,7 +498,8 @@ def test_small_sample_sort_sizes(sd):
                                                      (40000, (4, 24), (450, 1000), (-1.0, -2.0, -3.0), 160),
                                                      (3000, (30, 50), (60, 300), (-1.0, -2.0), 160),
                                                      (40000, (4, 24), (300, 900), (0.0, -1.0), 1100),
-                                                     (60000, (4, 24), (400, 1000), (-1.0, -2.0), 1500)])
+                                                     (60000, (4, 24), (400, 1000), (-1.0, -2.0), 1500),
+                                                     (40000, (4, 24), (20, 1000), (-2.0,), 400)])
 def test_spgemm_crossing_marks(sd, n, fan, lens, biases, batch):
     """Every b_j <= 0 and samples too long for the bitmap epilogue: the scatter marks the columns whose sum
     rises above -max_j b_j and the epilogue reads only those.  Weights of both signs make sums cross the
@@ -509,7 +510,8 @@ def test_spgemm_crossing_marks(sd, n, fan, lens, biases, batch):
     input sparse enough to stay on the SpGEMM; a threshold of 0 comes from b_j = 0.  With three or four
     windows the register-resident samples take the pipelined instance; the two larger batches give each
     workgroup several samples in turn, mixing samples short enough for the bitmap epilogue with longer
-    ones (all rows compared bit for bit, in blocks)."""
+    ones (all rows compared bit for bit, in blocks).  A single bias value takes the instances that read b
+    once instead of per column."""
     rng = np.random.default_rng(17 + n + fan[0] + batch)
     layers = []
     for _ in range(2):
