@@ -132,6 +132,8 @@ def kernel_sources(kernel):
         return ["blocked.hip", "common.h"]
     if kernel.startswith("gemm"):
         return ["gemm.hip", "common.h"]
+    if kernel.startswith("spgemm"):
+        return ["spgemm.hip", "common.h"]
     return ["spmm.hip", "common.h"]
 
 

@@ -129,6 +129,16 @@ def test_source_hash_ignores_comments_only():
     assert bench._code_only(a) != bench._code_only("int x = 2; int y;")
 
 
+def test_kernel_sources_name_the_file_that_defines_the_kernel():
+    """A counter summary is current only while the file holding its kernel is unchanged."""
+    csrc = os.path.join(os.path.dirname(bench.__file__), "paper_1708_02937_amd", "csrc")
+    for kernel in ("spmm_blocked_kernel", "spmm_slots_kernel", "spmm_fanin_kernel", "spmm_narrow_kernel",
+                   "gemm_dense_layer_kernel", "spgemm_pipe_kernel", "spgemm_small_kernel"):
+        src = bench.kernel_sources(kernel)
+        text = open(os.path.join(csrc, src[0]), encoding="utf-8").read()
+        assert f"void {kernel}(" in text or f"void {kernel}<" in text or f" {kernel}(" in text, (kernel, src)
+
+
 def test_kernel_split_and_roofline_from_profile_records():
     """The dominant kernel's roofline and HBM fields from profiling-log records: algorithmic bytes per launch
     (averaged over the launches' layers) divided by the average launch time."""
