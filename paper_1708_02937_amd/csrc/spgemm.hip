@@ -1346,9 +1346,23 @@ hipError_t launch_spgemm_layer(int64_t n, int64_t batch, const int64_t *in_row_p
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (only_touched) {
-        // enough waves to cover every CU several times; each wave strides through the small list
-        const int64_t waves = (batch < (int64_t)num_cu * 16 ? batch : (int64_t)num_cu * 16);
-        const unsigned blocks = (unsigned)((waves + kSmallWaves - 1) / kSmallWaves);
+        // each wave strides through the small list (a static share), so launch no more workgroups than the
+        // CUs hold at once (the LDS areas bound it to 3 per CU): a workgroup that had to wait for another to
+        // finish would start its whole share late
+        static std::atomic<int> per_cu_cache[2] = {{0}, {0}};
+        int per_cu = per_cu_cache[bias_uniform ? 1 : 0].load(std::memory_order_relaxed);
+        if (per_cu <= 0) {
+            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu,
+                bias_uniform ? (const void *)spgemm_small_kernel<true> : (const void *)spgemm_small_kernel<false>,
+                kSmallWaves * 64, 0);
+            if (e != hipSuccess) return e;
+            if (per_cu < 1) per_cu = 1;
+            per_cu_cache[bias_uniform ? 1 : 0].store(per_cu, std::memory_order_relaxed);
+        }
+        const int64_t want = (batch + kSmallWaves - 1) / kSmallWaves;
+        const int64_t cap = (int64_t)num_cu * per_cu;
+        const unsigned blocks = (unsigned)(want < cap ? want : cap);
         if (bias_uniform)
             spgemm_small_kernel<true><<<blocks, kSmallWaves * 64, 0, s>>>(
                 n, batch, in_row_ptr, in_cnt, in_col, in_val, w_ptr, w, bias, zero_below, ymax, lists, stats, out_cnt,
