@@ -154,6 +154,20 @@ def test_pattern_bias_csr_path(sd, seed, n, L, batch, wd, yd):
     parity.compare(p, run_csr(sd, p, bias_mode=1), bias_mode=1)
 
 
+@pytest.mark.parametrize("seed,n,L,batch,wd,yd,b", [(74, 40000, 2, 300, 0.0002, 0.0275, 0.25),
+                                                    (75, 3000, 2, 257, 0.003, 0.015, 0.25),
+                                                    (76, 40000, 2, 200, 0.0002, 0.008, -0.1)])
+def test_uniform_bias_csr_path(sd, seed, n, L, batch, wd, yd, b):
+    """One bias value for every neuron (read once by the small-sample and pipelined SpGEMM instances), on
+    the structural pattern (a positive b) and everywhere (a negative b, so sums are cut at -b)."""
+    pattern = 1 if b > 0 else 0
+    p = tiny_random(seed, n, L, batch, w_density=wd, y_density=yd, bias_lo=b, bias_hi=b,
+                    ymax=[math.inf, 2.0][seed % 2])
+    assert np.all(p.layers[0].bias == np.float32(b))
+    _say("uniform bias csr", seed, n, L, batch, b)
+    parity.compare(p, run_csr(sd, p, bias_mode=pattern), bias_mode=pattern)
+
+
 @pytest.mark.parametrize("seed,n,L,batch,d,yd", [(66, 200, 2, 130, 0.05, 0.3), (67, 1400, 2, 260, 0.95, 0.001),
                                                  (68, 333, 3, 3, 0.1, 0.5), (69, 4100, 1, 2048, 0.002, 0.01),
                                                  (71, 2000, 2, 516, 0.7, 0.002)])
